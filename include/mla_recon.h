@@ -1,0 +1,158 @@
+/*
+ * mla_recon.h -- C ABI of the MI355X (gfx950) end-to-end functional-reconstruction step.
+ *
+ * One converted multi-head-latent-attention (MLA) layer is trained to reproduce the
+ * post-output-projection response of the frozen original GQA/MHA layer on calibration
+ * hidden states ("Beyond KV Reconstruction: Functional Reconstruction for MLA Draft
+ * Models in Speculative Decoding", Sec. 4.1, Eq. 11).  One step is four calls, all
+ * enqueued on the caller's HIP stream:
+ *
+ *   mla_recon_teacher_fwd  A_orig = W_O . GQA(h)                       (Eq. 1-4, Sec. 4.1)
+ *   mla_recon_student_fwd  A_MLA  = W_O . MLA(h)                       (Eq. 5, Sec. 4)
+ *   mla_recon_loss         L = ||M (A_MLA - sg[A_orig])||^2 / (D sum M), dL/dA_MLA (Eq. 11)
+ *   mla_recon_bwd          dL/d{W_DQ, W_UQ, [W_DKV; W_KR], W_UK, W_UV}  (Sec. 4: only the
+ *                          converter-introduced query and KV projections are trained;
+ *                          W_O and the teacher are frozen; h is data)
+ *
+ * Conventions shared by every call
+ *  - Pointers named h, W*, A_*, dA, mask, loss, inv_freq, dW* and ws are DEVICE pointers
+ *    owned by the caller; `cfg` and the small structs below are HOST pointers read during
+ *    the call only.  The library never allocates or frees memory on these paths and
+ *    keeps no state between calls except the thread-local last-error text and the
+ *    optional timing instrumentation below.
+ *  - Matrices are row-major; a weight W[out, in] maps x -> W x (a row of activations
+ *    X[tokens, in] maps to X W^T).  Tokens are flattened as n = b*T + t.
+ *  - Storage dtype (cfg->dtype): MLA_BF16 -> h, all weights and dA are bf16 (raw 16-bit
+ *    patterns); MLA_FP32 (check mode) -> they are fp32.  A_t, A_s, loss, inv_freq and all
+ *    weight gradients are fp32 in both modes.  Arithmetic accumulates in fp32.
+ *  - RoPE (Sec. 3.1): rotate-half pairs (p, p + d/2) of a head are rotated by the angle
+ *    t * inv_freq[p], t = 0 .. T-1 restarting in every sequence.  Both logits use
+ *    cfg->softmax_scale (1/sqrt(d_k) of the teacher, as in Eq. 2 and Eq. 8).
+ *  - Causal attention includes the diagonal (Eq. 3, u <= t); sequences never attend to
+ *    each other.  The mask M enters only the loss (Eq. 11).
+ *  - Every call validates all arguments before enqueueing anything; on error it returns a
+ *    negative mla_status, enqueues nothing and sets mla_recon_last_error().  On success it
+ *    returns MLA_OK after only enqueueing work (no host synchronisation).
+ *  - Workspace: ws must be at least mla_recon_workspace_size(cfg) bytes, 256-byte aligned.
+ *    mla_recon_student_fwd stores the activations mla_recon_bwd needs in ws, so the same
+ *    ws, unmodified, must be passed from student_fwd to bwd.  teacher_fwd and loss only
+ *    use scratch parts of ws that student_fwd/bwd do not keep.
+ *  - Calls that share one ws (or overlapping outputs) must not run concurrently.
+ */
+#ifndef MLA_RECON_H
+#define MLA_RECON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MLA_OK = 0,
+  MLA_ERR_INVALID_ARG = -1,  /* NULL required pointer, bad dimension or grouping        */
+  MLA_ERR_UNSUPPORTED = -2,  /* valid for the method but not for these kernels          */
+  MLA_ERR_WORKSPACE = -3,    /* ws too small or misaligned                              */
+  MLA_ERR_HIP = -4           /* a HIP runtime call or launch failed                     */
+} mla_status;
+
+typedef enum { MLA_BF16 = 0, MLA_FP32 = 1 } mla_dtype;
+
+/* Layer shape.  Teacher (Eq. 1): D = hidden, H query heads, G KV groups (G == H is MHA),
+ * head width d_k (keys and values).  Student (Eq. 5 + decoupled RoPE): query latent rank
+ * r_q (0 = no query factorisation: q = W_UQ h), KV latent rank r_kv, per-head logit width
+ * d_nope + d_rope, value width d_k, G_kv groups of non-positional keys/values and G_r
+ * positional keys k^PE (head i uses group i / (H/G_kv) and rope key i / (H/G_r)).
+ * Requirements: all sizes >= 1 except q_rank, nope_dim >= 0; H % G == H % G_kv == H % G_r
+ * == 0; d_k and d_rope even; hidden, head_dim, q_rank, kv_rank, nope_dim, rope_dim
+ * multiples of 8.  The bf16 kernels additionally support d_k in {64, 128},
+ * d_nope + d_rope in {64, 96, 128, 192}, and seq a multiple of 64 (MLA_ERR_UNSUPPORTED
+ * otherwise). */
+typedef struct {
+  int32_t batch, seq, hidden;               /* B, T, D                                    */
+  int32_t n_heads, n_kv_groups, head_dim;   /* H, G, d_k                                  */
+  int32_t q_rank, kv_rank;                  /* r_q (0 allowed), r_kv                      */
+  int32_t nope_dim, rope_dim;               /* d_nope (0 allowed), d_rope                 */
+  int32_t s_kv_groups, s_rope_groups;       /* G_kv, G_r                                  */
+  float softmax_scale;                      /* multiplies both teacher and student logits */
+  int32_t dtype;                            /* mla_dtype                                  */
+} mla_recon_cfg;
+
+/* Frozen original block.  Wq [H*d_k, D], Wk and Wv [G*d_k, D] (group g owns rows
+ * g*d_k .. g*d_k+d_k-1, head i owns rows i*d_k ..), Wo [D, H*d_k].  inv_freq: fp32
+ * [d_k/2], the RoPE inverse frequency of each rotate-half pair. */
+typedef struct {
+  const void *Wq, *Wk, *Wv, *Wo;
+  const float *inv_freq;
+} mla_teacher_w;
+
+/* Converted MLA block.  Wdq [r_q, D] (NULL iff q_rank == 0); Wuq [H*(d_nope+d_rope),
+ * r_q or D], each head's rows ordered non-positional then rotary; Wdkv_kr
+ * [r_kv + G_r*d_rope, D] = W^DKV stacked over the positional-key projection W^KR;
+ * Wuk [G_kv*d_nope, r_kv]; Wuv [G_kv*d_k, r_kv].  inv_freq: fp32 [G_r, d_rope/2]. */
+typedef struct {
+  const void *Wdq, *Wuq, *Wdkv_kr, *Wuk, *Wuv;
+  const float *inv_freq;
+} mla_student_w;
+
+/* Weight gradients, fp32, same shapes as the weights; overwritten, not accumulated.
+ * A NULL pointer leaves that projection frozen (its gradient is not computed). */
+typedef struct {
+  float *dWdq, *dWuq, *dWdkv_kr, *dWuk, *dWuv;
+} mla_student_grads;
+
+/* Bytes of workspace the four calls need for `cfg` (0 if cfg is invalid). */
+size_t mla_recon_workspace_size(const mla_recon_cfg *cfg);
+
+/* Teacher forward (Eq. 1-4 and the frozen W_O, Sec. 4.1).
+ * h [B, T, D] (storage dtype); writes A_t [B, T, D] fp32 = the post-W_O attention
+ * output of the original block.  Uses only scratch regions of ws. */
+int mla_recon_teacher_fwd(const mla_recon_cfg *cfg, const void *h, const mla_teacher_w *w,
+                          float *A_t, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* Student forward (Eq. 5; low-rank query; decoupled RoPE; Eq. 2-4; the teacher's W_O).
+ * h [B, T, D]; Wo = the teacher's [D, H*d_k] (frozen, shared); writes A_s [B, T, D]
+ * fp32 and keeps the activations the backward needs in ws. */
+int mla_recon_student_fwd(const mla_recon_cfg *cfg, const void *h, const mla_student_w *w,
+                          const void *Wo, float *A_s, void *ws, size_t ws_bytes,
+                          void *hip_stream);
+
+/* Eq. 11 on one minibatch (all B*T tokens flattened) and its gradient.
+ * A_s, A_t [B, T, D] fp32; mask [B, T] uint8 (nonzero = valid) or NULL = all valid.
+ * Writes loss[0] = L = sum(M (A_s - A_t))^2 / (D sum M), loss[1] = the relative error
+ * sum(M (A_s - A_t))^2 / sum(M A_t)^2 (device fp32 [2]), and dA [B, T, D] (storage
+ * dtype) = 2 M (A_s - A_t) / (D sum M).  An all-invalid mask gives L = 0 and dA = 0.
+ * The reduction order is fixed: results are bitwise reproducible.  dA may be NULL
+ * (loss only). */
+int mla_recon_loss(const mla_recon_cfg *cfg, const float *A_s, const float *A_t,
+                   const uint8_t *mask, float *loss, void *dA, void *ws, size_t ws_bytes,
+                   void *hip_stream);
+
+/* Backward of L through the student (Sec. 4: stop-gradient on the teacher, W_O frozen,
+ * no gradient for h).  dA [B, T, D] (storage dtype) is dL/dA_s, e.g. from
+ * mla_recon_loss; h, w and Wo must be the ones given to the preceding student_fwd, and
+ * ws must still hold what it stored.  Writes the requested gradients (fp32). */
+int mla_recon_bwd(const mla_recon_cfg *cfg, const void *h, const mla_student_w *w,
+                  const void *Wo, const void *dA, const mla_student_grads *grads, void *ws,
+                  size_t ws_bytes, void *hip_stream);
+
+/* Text of the last error on the calling thread ("" if none). */
+const char *mla_recon_last_error(void);
+
+/* ---- timing instrumentation (not part of the method) --------------------------------
+ * When enabled for a kernel class, every launch of that class made by the calls above is
+ * bracketed by a pair of HIP events recorded on the launch stream.  mla_recon_prof_read
+ * waits for those events, returns the summed kernel time (ms), the launch count and the
+ * algorithmic FLOPs and HBM bytes those launches account for, and clears the record.
+ * Classes: 0 GEMM, 1 attention forward, 2 attention backward, 3 loss, 4 elementwise
+ * (RoPE, reductions, conversions).  Up to 4096 launches are recorded per class. */
+int mla_recon_prof_enable(int kernel_class, int on);
+int mla_recon_prof_read(int kernel_class, double *total_ms, int64_t *launches,
+                        double *alg_flops, double *alg_bytes);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MLA_RECON_H */

@@ -1,0 +1,148 @@
+"""ctypes binding of libmlarecon.so (include/mla_recon.h).
+
+Argument marshalling only: every function forwards raw device pointers, sizes and the
+HIP stream handle to the C ABI of the same name and raises on a non-zero status.  No
+computation of the reconstruction step happens in Python.  The library must have been
+built (``python -m paper_2607_27269_amd.build``); importing this module fails loudly
+otherwise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmlarecon.so")
+
+MLA_OK = 0
+MLA_ERR_INVALID_ARG = -1
+MLA_ERR_UNSUPPORTED = -2
+MLA_ERR_WORKSPACE = -3
+MLA_ERR_HIP = -4
+MLA_BF16 = 0
+MLA_FP32 = 1
+
+KC_GEMM, KC_ATTN_FWD, KC_ATTN_BWD, KC_LOSS, KC_ELEM = range(5)
+KCLASS_NAMES = {KC_GEMM: "gemm", KC_ATTN_FWD: "attn_fwd", KC_ATTN_BWD: "attn_bwd",
+                KC_LOSS: "loss", KC_ELEM: "elementwise"}
+
+
+class MlaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"mla_recon error {code}: {msg}")
+        self.code = code
+
+
+class Cfg(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("seq", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("n_heads", ctypes.c_int32), ("n_kv_groups", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("q_rank", ctypes.c_int32),
+                ("kv_rank", ctypes.c_int32), ("nope_dim", ctypes.c_int32),
+                ("rope_dim", ctypes.c_int32), ("s_kv_groups", ctypes.c_int32),
+                ("s_rope_groups", ctypes.c_int32), ("softmax_scale", ctypes.c_float),
+                ("dtype", ctypes.c_int32)]
+
+
+class TeacherW(ctypes.Structure):
+    _fields_ = [("Wq", ctypes.c_void_p), ("Wk", ctypes.c_void_p), ("Wv", ctypes.c_void_p),
+                ("Wo", ctypes.c_void_p), ("inv_freq", ctypes.c_void_p)]
+
+
+class StudentW(ctypes.Structure):
+    _fields_ = [("Wdq", ctypes.c_void_p), ("Wuq", ctypes.c_void_p), ("Wdkv_kr", ctypes.c_void_p),
+                ("Wuk", ctypes.c_void_p), ("Wuv", ctypes.c_void_p), ("inv_freq", ctypes.c_void_p)]
+
+
+class StudentGrads(ctypes.Structure):
+    _fields_ = [("dWdq", ctypes.c_void_p), ("dWuq", ctypes.c_void_p),
+                ("dWdkv_kr", ctypes.c_void_p), ("dWuk", ctypes.c_void_p),
+                ("dWuv", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2607_27269_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+        P = ctypes.POINTER
+        L.mla_recon_workspace_size.argtypes = [P(Cfg)]
+        L.mla_recon_workspace_size.restype = sz
+        L.mla_recon_teacher_fwd.argtypes = [P(Cfg), vp, P(TeacherW), vp, vp, sz, vp]
+        L.mla_recon_student_fwd.argtypes = [P(Cfg), vp, P(StudentW), vp, vp, vp, sz, vp]
+        L.mla_recon_loss.argtypes = [P(Cfg), vp, vp, vp, vp, vp, vp, sz, vp]
+        L.mla_recon_bwd.argtypes = [P(Cfg), vp, P(StudentW), vp, vp, P(StudentGrads), vp, sz, vp]
+        for f in ("mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
+                  "mla_recon_bwd", "mla_recon_prof_enable", "mla_recon_prof_read"):
+            getattr(L, f).restype = i32
+        L.mla_recon_last_error.argtypes = []
+        L.mla_recon_last_error.restype = ctypes.c_char_p
+        L.mla_recon_prof_enable.argtypes = [i32, i32]
+        L.mla_recon_prof_read.argtypes = [i32, P(ctypes.c_double), P(ctypes.c_int64),
+                                          P(ctypes.c_double), P(ctypes.c_double)]
+        _lib = L
+    return _lib
+
+
+def _check(rc: int):
+    if rc != MLA_OK:
+        raise MlaError(rc, lib().mla_recon_last_error().decode())
+
+
+def mla_recon_last_error() -> str:
+    return lib().mla_recon_last_error().decode()
+
+
+last_error = mla_recon_last_error
+
+
+def make_cfg(c) -> Cfg:
+    """Cfg from a configs.LayerConfig (or any object with the same attributes)."""
+    return Cfg(c.batch, c.seq, c.hidden, c.n_heads, c.n_kv_groups, c.head_dim, c.q_rank,
+               c.kv_rank, c.nope_dim, c.rope_dim, c.s_kv_groups, c.s_rope_groups,
+               float(c.softmax_scale), MLA_FP32 if c.dtype == "fp32" else MLA_BF16)
+
+
+def mla_recon_workspace_size(cfg: Cfg) -> int:
+    return int(lib().mla_recon_workspace_size(ctypes.byref(cfg)))
+
+
+def mla_recon_teacher_fwd(cfg: Cfg, h: int, w: TeacherW, A_t: int, ws: int, ws_bytes: int,
+                          stream: int) -> None:
+    _check(lib().mla_recon_teacher_fwd(ctypes.byref(cfg), h, ctypes.byref(w), A_t, ws,
+                                       ws_bytes, stream))
+
+
+def mla_recon_student_fwd(cfg: Cfg, h: int, w: StudentW, Wo: int, A_s: int, ws: int,
+                          ws_bytes: int, stream: int) -> None:
+    _check(lib().mla_recon_student_fwd(ctypes.byref(cfg), h, ctypes.byref(w), Wo, A_s, ws,
+                                       ws_bytes, stream))
+
+
+def mla_recon_loss(cfg: Cfg, A_s: int, A_t: int, mask: int | None, loss: int, dA: int | None,
+                   ws: int, ws_bytes: int, stream: int) -> None:
+    _check(lib().mla_recon_loss(ctypes.byref(cfg), A_s, A_t, mask, loss, dA, ws, ws_bytes,
+                                stream))
+
+
+def mla_recon_bwd(cfg: Cfg, h: int, w: StudentW, Wo: int, dA: int, grads: StudentGrads,
+                  ws: int, ws_bytes: int, stream: int) -> None:
+    _check(lib().mla_recon_bwd(ctypes.byref(cfg), h, ctypes.byref(w), Wo, dA,
+                               ctypes.byref(grads), ws, ws_bytes, stream))
+
+
+def mla_recon_prof_enable(kclass: int, on: bool) -> None:
+    _check(lib().mla_recon_prof_enable(kclass, 1 if on else 0))
+
+
+def mla_recon_prof_read(kclass: int):
+    ms, n = ctypes.c_double(), ctypes.c_int64()
+    fl, by = ctypes.c_double(), ctypes.c_double()
+    _check(lib().mla_recon_prof_read(kclass, ctypes.byref(ms), ctypes.byref(n),
+                                     ctypes.byref(fl), ctypes.byref(by)))
+    return dict(ms=ms.value, launches=n.value, flops=fl.value, bytes=by.value)

@@ -1,0 +1,469 @@
+// C ABI of the reconstruction step: argument validation, workspace layout and the launch
+// sequence of each call (teacher forward, student forward, Eq. 11 loss, backward).
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <mutex>
+#include <vector>
+
+#include "../../include/mla_recon.h"
+#include "kernels.h"
+#include "simt.h"
+
+namespace mla {
+
+// ---------------------------------------------------------------------------------------
+// last error
+// ---------------------------------------------------------------------------------------
+static thread_local char g_err[512] = "";
+
+static int fail(int code, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                     \
+  do {                                                                                    \
+    hipError_t e_ = (expr);                                                               \
+    if (e_ != hipSuccess)                                                                 \
+      return fail(MLA_ERR_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));            \
+  } while (0)
+
+// ---------------------------------------------------------------------------------------
+// timing instrumentation
+// ---------------------------------------------------------------------------------------
+struct ProfClass {
+  bool on = false;
+  std::vector<hipEvent_t> ev;  // 2 per launch
+  int used = 0;
+  double flops = 0.0, bytes = 0.0;
+};
+static ProfClass g_prof[KC_COUNT];
+static std::mutex g_prof_mu;
+static constexpr int PROF_MAX = 4096;
+
+void prof_begin(int k, hipStream_t s) {
+  ProfClass& p = g_prof[k];
+  if (!p.on || p.used >= PROF_MAX) return;
+  (void)hipEventRecord(p.ev[2 * p.used], s);
+}
+
+void prof_end(int k, hipStream_t s, double flops, double bytes) {
+  ProfClass& p = g_prof[k];
+  if (!p.on || p.used >= PROF_MAX) return;
+  (void)hipEventRecord(p.ev[2 * p.used + 1], s);
+  p.used++;
+  p.flops += flops;
+  p.bytes += bytes;
+}
+
+// ---------------------------------------------------------------------------------------
+// configuration checks and workspace layout
+// ---------------------------------------------------------------------------------------
+struct Dims {
+  int64_t B, T, N, D, H, G, dk, rq, rkv, dn, dr, dqk, dv, Gkv, Gr, kv_out;
+  DType t;
+  size_t ts;
+};
+
+static Dims dims_of(const mla_recon_cfg* c) {
+  Dims d;
+  d.B = c->batch; d.T = c->seq; d.N = d.B * d.T; d.D = c->hidden;
+  d.H = c->n_heads; d.G = c->n_kv_groups; d.dk = c->head_dim;
+  d.rq = c->q_rank; d.rkv = c->kv_rank; d.dn = c->nope_dim; d.dr = c->rope_dim;
+  d.dqk = d.dn + d.dr; d.dv = d.dk; d.Gkv = c->s_kv_groups; d.Gr = c->s_rope_groups;
+  d.kv_out = d.rkv + d.Gr * d.dr;
+  d.t = c->dtype == MLA_FP32 ? DT_F32 : DT_BF16;
+  d.ts = dsize(d.t);
+  return d;
+}
+
+static bool attn_supported(const Dims& d, int dqk, int dv) {
+  return attn_simt_supported(dqk, dv);
+}
+
+static int check_cfg(const mla_recon_cfg* c) {
+  if (!c) return fail(MLA_ERR_INVALID_ARG, "cfg is NULL");
+  if (c->batch < 1 || c->seq < 1 || c->hidden < 1 || c->n_heads < 1 || c->n_kv_groups < 1 ||
+      c->head_dim < 1 || c->kv_rank < 1 || c->rope_dim < 1 || c->s_kv_groups < 1 ||
+      c->s_rope_groups < 1 || c->q_rank < 0 || c->nope_dim < 0)
+    return fail(MLA_ERR_INVALID_ARG, "non-positive dimension in cfg");
+  if (c->dtype != MLA_BF16 && c->dtype != MLA_FP32)
+    return fail(MLA_ERR_INVALID_ARG, "unknown dtype %d", c->dtype);
+  if (c->n_heads % c->n_kv_groups || c->n_heads % c->s_kv_groups || c->n_heads % c->s_rope_groups)
+    return fail(MLA_ERR_INVALID_ARG, "n_heads must be a multiple of n_kv_groups, s_kv_groups and s_rope_groups");
+  if (c->head_dim % 2 || c->rope_dim % 2)
+    return fail(MLA_ERR_INVALID_ARG, "head_dim and rope_dim must be even");
+  if (!(c->softmax_scale > 0.f) || c->softmax_scale > 1e30f)
+    return fail(MLA_ERR_INVALID_ARG, "softmax_scale must be positive and finite");
+  if (c->hidden % 8 || c->head_dim % 8 || c->q_rank % 8 || c->kv_rank % 8 || c->nope_dim % 8 ||
+      c->rope_dim % 8)
+    return fail(MLA_ERR_INVALID_ARG, "hidden, head_dim, q_rank, kv_rank, nope_dim, rope_dim must be multiples of 8");
+  if (c->s_kv_groups % c->s_rope_groups)
+    return fail(MLA_ERR_UNSUPPORTED, "s_kv_groups must be a multiple of s_rope_groups");
+  Dims d = dims_of(c);
+  if ((double)d.N * d.H * d.dqk >= 9.0e18)
+    return fail(MLA_ERR_INVALID_ARG, "problem too large");
+  if (!attn_supported(d, (int)d.dk, (int)d.dk))
+    return fail(MLA_ERR_UNSUPPORTED, "teacher head_dim %d not supported by the attention kernels", c->head_dim);
+  if (!attn_supported(d, (int)d.dqk, (int)d.dv))
+    return fail(MLA_ERR_UNSUPPORTED, "student logit width %d with value width %d not supported", (int)d.dqk, (int)d.dv);
+  return MLA_OK;
+}
+
+static size_t al(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct Layout {
+  // teacher scratch
+  size_t t_cos, t_sin, t_qkv, t_o;
+  // student state kept from student_fwd to bwd
+  size_t s_cos, s_sin, s_cq, s_q, s_ckv, s_knope, s_v, s_o, s_lse;
+  // backward scratch
+  size_t b_do, b_delta, b_dqacc, b_dq, b_dkv, b_dkpe, b_dckv, b_dcq, b_split;
+  size_t b_split_elems;
+  // loss scratch
+  size_t l_scr;
+  size_t total;
+};
+
+static std::vector<Gemm> bwd_gemm_shapes(const Dims& d);
+
+static Layout layout_of(const Dims& d) {
+  Layout L;
+  size_t o = 0;
+  auto take = [&](size_t bytes) { size_t r = o; o += al(bytes); return r; };
+  const size_t ts = d.ts, N = d.N;
+  L.t_cos = take(d.T * (d.dk / 2) * 4);
+  L.t_sin = take(d.T * (d.dk / 2) * 4);
+  L.t_qkv = take(N * (d.H + 2 * d.G) * d.dk * ts);
+  L.t_o = take(N * d.H * d.dk * ts);
+  L.s_cos = take(d.Gr * d.T * (d.dr / 2) * 4);
+  L.s_sin = take(d.Gr * d.T * (d.dr / 2) * 4);
+  L.s_cq = take(N * d.rq * ts);
+  L.s_q = take(N * d.H * d.dqk * ts);
+  L.s_ckv = take(N * d.kv_out * ts);
+  L.s_knope = take(N * d.Gkv * d.dn * ts);
+  L.s_v = take(N * d.Gkv * d.dv * ts);
+  L.s_o = take(N * d.H * d.dv * ts);
+  L.s_lse = take(N * d.H * 4);
+  L.b_do = take(N * d.H * d.dv * ts);
+  L.b_delta = take(N * d.H * 4);
+  L.b_dqacc = take(N * d.H * d.dqk * 4);
+  L.b_dq = take(N * d.H * d.dqk * ts);
+  L.b_dkv = take(N * d.Gkv * (d.dn + d.dv) * ts);
+  L.b_dkpe = take(d.Gkv * N * d.dr * 4);
+  L.b_dckv = take(N * d.kv_out * ts);
+  L.b_dcq = take(N * d.rq * ts);
+  size_t se = 0;
+  for (const Gemm& g : bwd_gemm_shapes(d)) se = std::max(se, gemm_scratch_elems(g));
+  L.b_split_elems = se;
+  L.b_split = take(se * 4);
+  L.l_scr = take(loss_scratch_bytes());
+  L.total = o;
+  return L;
+}
+
+static int check_ws(const mla_recon_cfg* cfg, void* ws, size_t ws_bytes, Layout* L) {
+  *L = layout_of(dims_of(cfg));
+  if (!ws) return fail(MLA_ERR_INVALID_ARG, "workspace is NULL");
+  if ((uintptr_t)ws % 256) return fail(MLA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (ws_bytes < L->total)
+    return fail(MLA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, L->total);
+  return MLA_OK;
+}
+
+static inline char* at(void* ws, size_t off) { return (char*)ws + off; }
+
+static Gemm mk(int M, int N, int K, const void* A, int64_t lda, bool ak, const void* B,
+               int64_t ldb, bool bk, void* C, int64_t ldc, DType in_t, DType c_t,
+               float beta = 0.f) {
+  Gemm g;
+  g.M = M; g.N = N; g.K = K; g.A = A; g.lda = lda; g.a_kmajor = ak; g.B = B; g.ldb = ldb;
+  g.b_kmajor = bk; g.C = C; g.ldc = ldc; g.in_t = in_t; g.c_t = c_t; g.alpha = 1.f; g.beta = beta;
+  return g;
+}
+
+// Shapes (only M, N, K, layouts and types matter) of the backward GEMMs, for scratch sizing.
+static std::vector<Gemm> bwd_gemm_shapes(const Dims& d) {
+  std::vector<Gemm> v;
+  const int N = (int)d.N;
+  v.push_back(mk((int)(d.Gkv * d.dn), (int)d.rkv, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
+  v.push_back(mk((int)(d.Gkv * d.dv), (int)d.rkv, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
+  v.push_back(mk((int)d.kv_out, (int)d.D, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
+  v.push_back(mk((int)(d.H * d.dqk), (int)(d.rq ? d.rq : d.D), N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
+  if (d.rq) v.push_back(mk((int)d.rq, (int)d.D, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
+  return v;
+}
+
+}  // namespace mla
+
+using namespace mla;
+
+// ---------------------------------------------------------------------------------------
+// the C ABI
+// ---------------------------------------------------------------------------------------
+extern "C" {
+
+const char* mla_recon_last_error(void) { return g_err; }
+
+size_t mla_recon_workspace_size(const mla_recon_cfg* cfg) {
+  if (check_cfg(cfg) != MLA_OK) return 0;
+  return layout_of(dims_of(cfg)).total;
+}
+
+int mla_recon_teacher_fwd(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w* w,
+                          float* A_t, void* ws, size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!h || !w || !A_t || !w->Wq || !w->Wk || !w->Wv || !w->Wo || !w->inv_freq)
+    return fail(MLA_ERR_INVALID_ARG, "teacher_fwd: NULL pointer argument");
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  const Dims d = dims_of(cfg);
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int N = (int)d.N, D = (int)d.D, H = (int)d.H, G = (int)d.G, dk = (int)d.dk;
+  const int64_t ld_qkv = (H + 2 * G) * (int64_t)dk;
+  float* cs = (float*)at(ws, L.t_cos);
+  float* sn = (float*)at(ws, L.t_sin);
+  char* qkv = at(ws, L.t_qkv);
+  char* o = at(ws, L.t_o);
+  const size_t ts = d.ts;
+
+  HIP_TRY(rope_tables(w->inv_freq, 1, (int)d.T, dk / 2, cs, sn, s));
+  // Eq. 1: q = W^Q h, k = W^K h, v = W^V h  (columns [Q | K | V] of one buffer)
+  HIP_TRY(gemm(mk(N, H * dk, D, h, D, true, w->Wq, D, true, qkv, ld_qkv, d.t, d.t), nullptr, 0, s));
+  HIP_TRY(gemm(mk(N, G * dk, D, h, D, true, w->Wk, D, true, qkv + (size_t)H * dk * ts, ld_qkv, d.t, d.t), nullptr, 0, s));
+  HIP_TRY(gemm(mk(N, G * dk, D, h, D, true, w->Wv, D, true, qkv + (size_t)(H + G) * dk * ts, ld_qkv, d.t, d.t), nullptr, 0, s));
+  // R_t on queries and keys (Sec. 3.1)
+  HIP_TRY(rope_apply(qkv, d.t, N, (int)d.T, H, ld_qkv, dk, 0, dk / 2, H, cs, sn, s));
+  HIP_TRY(rope_apply(qkv + (size_t)H * dk * ts, d.t, N, (int)d.T, G, ld_qkv, dk, 0, dk / 2, G, cs, sn, s));
+  // Eq. 2-4: causal softmax attention, head i reads KV group i / (H/G)
+  Attn a;
+  a.B = (int)d.B; a.T = (int)d.T; a.H = H; a.dqk = dk; a.dnope = dk; a.dv = dk;
+  a.Q = HeadView{qkv, ld_qkv, dk, 1};
+  a.Ka = HeadView{qkv + (size_t)H * dk * ts, ld_qkv, dk, H / G};
+  a.Kb = HeadView{nullptr, 0, 0, 1};
+  a.V = HeadView{qkv + (size_t)(H + G) * dk * ts, ld_qkv, dk, H / G};
+  a.O = o; a.o_tok = (int64_t)H * dk; a.lse = nullptr; a.scale = cfg->softmax_scale; a.t = d.t;
+  HIP_TRY(attn_fwd(a, s));
+  // the fixed output projection: A = concat_i o_i W_O^T
+  HIP_TRY(gemm(mk(N, D, H * dk, o, (int64_t)H * dk, true, w->Wo, (int64_t)H * dk, true, A_t, D, d.t, DT_F32), nullptr, 0, s));
+  return MLA_OK;
+}
+
+int mla_recon_student_fwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* w,
+                          const void* Wo, float* A_s, void* ws, size_t ws_bytes,
+                          void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!h || !w || !Wo || !A_s || !w->Wuq || !w->Wdkv_kr || !w->Wuv || !w->inv_freq ||
+      (cfg->q_rank > 0 && !w->Wdq) || (cfg->nope_dim > 0 && !w->Wuk))
+    return fail(MLA_ERR_INVALID_ARG, "student_fwd: NULL pointer argument");
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  const Dims d = dims_of(cfg);
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int N = (int)d.N, D = (int)d.D, H = (int)d.H, T = (int)d.T;
+  const int rq = (int)d.rq, rkv = (int)d.rkv, dn = (int)d.dn, dr = (int)d.dr, dqk = (int)d.dqk;
+  const int dv = (int)d.dv, Gkv = (int)d.Gkv, Gr = (int)d.Gr, kv_out = (int)d.kv_out;
+  const size_t ts = d.ts;
+  float* cs = (float*)at(ws, L.s_cos);
+  float* sn = (float*)at(ws, L.s_sin);
+  char* cq = at(ws, L.s_cq);
+  char* q = at(ws, L.s_q);
+  char* ckv = at(ws, L.s_ckv);
+  char* knope = at(ws, L.s_knope);
+  char* v = at(ws, L.s_v);
+  char* o = at(ws, L.s_o);
+  float* lse = (float*)at(ws, L.s_lse);
+
+  HIP_TRY(rope_tables(w->inv_freq, Gr, T, dr / 2, cs, sn, s));
+  // low-rank query: c^Q = W_DQ h, q = W_UQ c^Q  (q = W_UQ h when r_q = 0)
+  const void* qin = h;
+  int qk = D;
+  if (rq > 0) {
+    HIP_TRY(gemm(mk(N, rq, D, h, D, true, w->Wdq, D, true, cq, rq, d.t, d.t), nullptr, 0, s));
+    qin = cq;
+    qk = rq;
+  }
+  HIP_TRY(gemm(mk(N, H * dqk, qk, qin, qk, true, w->Wuq, qk, true, q, (int64_t)H * dqk, d.t, d.t), nullptr, 0, s));
+  // Eq. 5: [c^KV | k^PE] = [W^DKV; W^KR] h, [k^nope; v] = W^UKV c^KV
+  HIP_TRY(gemm(mk(N, kv_out, D, h, D, true, w->Wdkv_kr, D, true, ckv, kv_out, d.t, d.t), nullptr, 0, s));
+  if (dn > 0)
+    HIP_TRY(gemm(mk(N, Gkv * dn, rkv, ckv, kv_out, true, w->Wuk, rkv, true, knope, (int64_t)Gkv * dn, d.t, d.t), nullptr, 0, s));
+  HIP_TRY(gemm(mk(N, Gkv * dv, rkv, ckv, kv_out, true, w->Wuv, rkv, true, v, (int64_t)Gkv * dv, d.t, d.t), nullptr, 0, s));
+  // decoupled RoPE on q^rope (rope group i / (H/G_r)) and on k^PE
+  HIP_TRY(rope_apply(q, d.t, N, T, H, (int64_t)H * dqk, dqk, dn, dr / 2, H / Gr, cs, sn, s));
+  HIP_TRY(rope_apply(ckv, d.t, N, T, Gr, kv_out, dr, rkv, dr / 2, 1, cs, sn, s));
+  // Eq. 2-4 with q = [q^nope; R q^rope], k = [k^nope_{g(i)}; R k^PE_{r(i)}]
+  Attn a;
+  a.B = (int)d.B; a.T = T; a.H = H; a.dqk = dqk; a.dnope = dn; a.dv = dv;
+  a.Q = HeadView{q, (int64_t)H * dqk, dqk, 1};
+  a.Ka = HeadView{knope, (int64_t)Gkv * dn, dn, H / Gkv};
+  a.Kb = HeadView{ckv + (size_t)rkv * ts, kv_out, dr, H / Gr};
+  a.V = HeadView{v, (int64_t)Gkv * dv, dv, H / Gkv};
+  a.O = o; a.o_tok = (int64_t)H * dv; a.lse = lse; a.scale = cfg->softmax_scale; a.t = d.t;
+  HIP_TRY(attn_fwd(a, s));
+  // the teacher's frozen W_O
+  HIP_TRY(gemm(mk(N, D, H * dv, o, (int64_t)H * dv, true, Wo, (int64_t)H * dv, true, A_s, D, d.t, DT_F32), nullptr, 0, s));
+  return MLA_OK;
+}
+
+int mla_recon_loss(const mla_recon_cfg* cfg, const float* A_s, const float* A_t,
+                   const uint8_t* mask, float* loss, void* dA, void* ws, size_t ws_bytes,
+                   void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!A_s || !A_t || !loss) return fail(MLA_ERR_INVALID_ARG, "loss: NULL pointer argument");
+  if (((uintptr_t)A_s | (uintptr_t)A_t) % 16 || (dA && (uintptr_t)dA % 16))
+    return fail(MLA_ERR_INVALID_ARG, "loss: A_s, A_t and dA must be 16-byte aligned");
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  const Dims d = dims_of(cfg);
+  HIP_TRY(recon_loss(A_s, A_t, mask, d.N, (int)d.D, loss, dA, d.t, at(ws, L.l_scr),
+                     (hipStream_t)hip_stream));
+  return MLA_OK;
+}
+
+int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* w,
+                  const void* Wo, const void* dA, const mla_student_grads* gr, void* ws,
+                  size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!h || !w || !Wo || !dA || !gr || !w->Wuq || !w->Wuv || (cfg->q_rank > 0 && !w->Wdq) ||
+      (cfg->nope_dim > 0 && !w->Wuk))
+    return fail(MLA_ERR_INVALID_ARG, "bwd: NULL pointer argument");
+  if (cfg->q_rank == 0 && gr->dWdq)
+    return fail(MLA_ERR_INVALID_ARG, "bwd: dWdq given but q_rank == 0 (no W_DQ)");
+  if (cfg->nope_dim == 0 && gr->dWuk)
+    return fail(MLA_ERR_INVALID_ARG, "bwd: dWuk given but nope_dim == 0 (no W_UK)");
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  const bool need_q = gr->dWuq || gr->dWdq;
+  const bool need_kv = gr->dWuk || gr->dWuv || gr->dWdkv_kr;
+  if (!need_q && !need_kv) return MLA_OK;
+  const Dims d = dims_of(cfg);
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int N = (int)d.N, D = (int)d.D, H = (int)d.H, T = (int)d.T;
+  const int rq = (int)d.rq, rkv = (int)d.rkv, dn = (int)d.dn, dr = (int)d.dr, dqk = (int)d.dqk;
+  const int dv = (int)d.dv, Gkv = (int)d.Gkv, Gr = (int)d.Gr, kv_out = (int)d.kv_out;
+  const size_t ts = d.ts;
+  const DType t = d.t;
+  float* cs = (float*)at(ws, L.s_cos);
+  float* sn = (float*)at(ws, L.s_sin);
+  char* cq = at(ws, L.s_cq);
+  char* q = at(ws, L.s_q);
+  char* ckv = at(ws, L.s_ckv);
+  char* knope = at(ws, L.s_knope);
+  char* v = at(ws, L.s_v);
+  char* o = at(ws, L.s_o);
+  float* lse = (float*)at(ws, L.s_lse);
+  char* dO = at(ws, L.b_do);
+  float* delta = (float*)at(ws, L.b_delta);
+  float* dqacc = (float*)at(ws, L.b_dqacc);
+  char* dq = at(ws, L.b_dq);
+  char* dkv = at(ws, L.b_dkv);
+  float* dkpe = (float*)at(ws, L.b_dkpe);
+  char* dckv = at(ws, L.b_dckv);
+  char* dcq = at(ws, L.b_dcq);
+  float* split = (float*)at(ws, L.b_split);
+  const size_t se = L.b_split_elems;
+  const int64_t ld_dkv = (int64_t)Gkv * (dn + dv);
+
+  // dO = dA W_O  (W_O frozen: no dW_O)
+  HIP_TRY(gemm(mk(N, H * dv, D, dA, D, true, Wo, (int64_t)H * dv, false, dO, (int64_t)H * dv, t, t), nullptr, 0, s));
+  // softmax-attention backward -> dq (rotated), dk^nope, dv, dk^PE partials
+  AttnBwd ab;
+  Attn& a = ab.f;
+  a.B = (int)d.B; a.T = T; a.H = H; a.dqk = dqk; a.dnope = dn; a.dv = dv;
+  a.Q = HeadView{q, (int64_t)H * dqk, dqk, 1};
+  a.Ka = HeadView{knope, (int64_t)Gkv * dn, dn, H / Gkv};
+  a.Kb = HeadView{ckv + (size_t)rkv * ts, kv_out, dr, H / Gr};
+  a.V = HeadView{v, (int64_t)Gkv * dv, dv, H / Gkv};
+  a.O = o; a.o_tok = (int64_t)H * dv; a.lse = lse; a.scale = cfg->softmax_scale; a.t = t;
+  ab.dO = dO; ab.delta = delta; ab.dq_acc = dqacc;
+  ab.dKa = dkv; ab.dka_tok = ld_dkv;
+  ab.dV = dkv + (size_t)Gkv * dn * ts; ab.dv_tok = ld_dkv;
+  ab.dkb_part = dkpe; ab.n_ka_groups = Gkv;
+  HIP_TRY(attn_bwd(ab, s));
+
+  if (need_q) {
+    // dq^rope <- R^T dq^rope
+    HIP_TRY(dq_finish(dqacc, dq, t, N, T, H, dqk, dn, H / Gr, cs, sn, s));
+    const void* qin = rq > 0 ? (const void*)cq : h;
+    const int qk = rq > 0 ? rq : D;
+    // dW_UQ = dq^T c^Q
+    if (gr->dWuq)
+      HIP_TRY(gemm(mk(H * dqk, qk, N, dq, (int64_t)H * dqk, false, qin, qk, false, gr->dWuq, qk, t, DT_F32), split, se, s));
+    if (gr->dWdq) {
+      // dc^Q = dq W_UQ, dW_DQ = dc^Q^T h
+      HIP_TRY(gemm(mk(N, rq, H * dqk, dq, (int64_t)H * dqk, true, w->Wuq, rq, false, dcq, rq, t, t), nullptr, 0, s));
+      HIP_TRY(gemm(mk(rq, D, N, dcq, rq, false, h, D, false, gr->dWdq, D, t, DT_F32), split, se, s));
+    }
+  }
+  if (need_kv) {
+    // Eq. 5 backward: dW_UK = dk^nope^T c^KV, dW_UV = dv^T c^KV
+    if (gr->dWuk && dn > 0)
+      HIP_TRY(gemm(mk(Gkv * dn, rkv, N, dkv, ld_dkv, false, ckv, kv_out, false, gr->dWuk, rkv, t, DT_F32), split, se, s));
+    if (gr->dWuv)
+      HIP_TRY(gemm(mk(Gkv * dv, rkv, N, dkv + (size_t)Gkv * dn * ts, ld_dkv, false, ckv, kv_out, false, gr->dWuv, rkv, t, DT_F32), split, se, s));
+    if (gr->dWdkv_kr) {
+      // dc^KV = dk^nope W_UK + dv W_UV; dk^PE = R^T sum of the head partials
+      if (dn > 0)
+        HIP_TRY(gemm(mk(N, rkv, Gkv * dn, dkv, ld_dkv, true, w->Wuk, rkv, false, dckv, kv_out, t, t), nullptr, 0, s));
+      HIP_TRY(gemm(mk(N, rkv, Gkv * dv, dkv + (size_t)Gkv * dn * ts, ld_dkv, true, w->Wuv, rkv, false, dckv, kv_out, t, t, dn > 0 ? 1.f : 0.f), nullptr, 0, s));
+      HIP_TRY(dkpe_finish(dkpe, dckv + (size_t)rkv * ts, t, kv_out, N, T, Gr, Gkv / Gr, dr, cs, sn, s));
+      // d[W_DKV; W_KR] = [dc^KV | dk^PE]^T h
+      HIP_TRY(gemm(mk(kv_out, D, N, dckv, kv_out, false, h, D, false, gr->dWdkv_kr, D, t, DT_F32), split, se, s));
+    }
+  }
+  return MLA_OK;
+}
+
+int mla_recon_prof_enable(int k, int on) {
+  if (k < 0 || k >= KC_COUNT) return fail(MLA_ERR_INVALID_ARG, "bad kernel class %d", k);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  ProfClass& p = g_prof[k];
+  if (on && p.ev.empty()) {
+    p.ev.resize(2 * PROF_MAX);
+    for (auto& e : p.ev) HIP_TRY(hipEventCreate(&e));
+  }
+  p.on = on != 0;
+  p.used = 0;
+  p.flops = p.bytes = 0.0;
+  return MLA_OK;
+}
+
+int mla_recon_prof_read(int k, double* total_ms, int64_t* launches, double* alg_flops,
+                        double* alg_bytes) {
+  if (k < 0 || k >= KC_COUNT) return fail(MLA_ERR_INVALID_ARG, "bad kernel class %d", k);
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  ProfClass& p = g_prof[k];
+  double ms = 0.0;
+  for (int i = 0; i < p.used; ++i) {
+    HIP_TRY(hipEventSynchronize(p.ev[2 * i + 1]));
+    float e = 0.f;
+    HIP_TRY(hipEventElapsedTime(&e, p.ev[2 * i], p.ev[2 * i + 1]));
+    ms += e;
+  }
+  if (total_ms) *total_ms = ms;
+  if (launches) *launches = p.used;
+  if (alg_flops) *alg_flops = p.flops;
+  if (alg_bytes) *alg_bytes = p.bytes;
+  p.used = 0;
+  p.flops = p.bytes = 0.0;
+  return MLA_OK;
+}
+
+}  // extern "C"

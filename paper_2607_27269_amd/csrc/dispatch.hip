@@ -1,0 +1,52 @@
+// Kernel selection: bf16 storage runs the MFMA kernels, fp32 (check mode) the vector-ALU
+// kernels.  Also owns the per-launch FLOP/byte accounting of the instrumentation.
+#include "common.h"
+#include "kernels.h"
+#include "simt.h"
+
+namespace mla {
+
+size_t gemm_scratch_elems(const Gemm& g) {
+  (void)g;
+  return 0;
+}
+
+hipError_t gemm(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s) {
+  (void)scratch;
+  (void)scratch_elems;
+  if (g.M == 0 || g.N == 0) return hipSuccess;
+  double flops = 2.0 * g.M * g.N * (double)g.K;
+  double bytes = ((double)g.M * g.K + (double)g.N * g.K) * dsize(g.in_t) +
+                 (double)g.M * g.N * dsize(g.c_t) * (g.beta != 0.f ? 2.0 : 1.0);
+  prof_begin(KC_GEMM, s);
+  hipError_t e = gemm_simt(g, s);
+  prof_end(KC_GEMM, s, flops, bytes);
+  return e;
+}
+
+static double causal_pairs(const Attn& a) {
+  return (double)a.B * a.H * (double)a.T * (a.T + 1) / 2.0;
+}
+
+hipError_t attn_fwd(const Attn& a, hipStream_t s) {
+  double flops = 2.0 * causal_pairs(a) * (a.dqk + a.dv);
+  double N = (double)a.B * a.T;
+  double bytes = N * a.H * (a.dqk + a.dv) * dsize(a.t) + N * a.H * (a.lse ? 4.0 : 0.0);
+  prof_begin(KC_ATTN_FWD, s);
+  hipError_t e = attn_fwd_simt(a, s);
+  prof_end(KC_ATTN_FWD, s, flops, bytes);
+  return e;
+}
+
+hipError_t attn_bwd(const AttnBwd& w, hipStream_t s) {
+  const Attn& a = w.f;
+  double flops = 2.0 * causal_pairs(a) * (2.0 * a.dv + 2.0 * a.dqk);
+  double N = (double)a.B * a.T;
+  double bytes = N * a.H * (a.dqk + 2.0 * a.dv) * dsize(a.t) + N * a.H * (8.0 + 4.0 * a.dqk);
+  prof_begin(KC_ATTN_BWD, s);
+  hipError_t e = attn_bwd_simt(w, s);
+  prof_end(KC_ATTN_BWD, s, flops, bytes);
+  return e;
+}
+
+}  // namespace mla

@@ -1,0 +1,295 @@
+// Bandwidth-bound kernels of the reconstruction step: RoPE tables and rotation, the
+// fused Eq. 11 loss + gradient, and the finishing passes of the attention backward.
+// Every kernel reads and writes HBM once, with consecutive lanes on consecutive
+// addresses, and reduces inside a wavefront with cross-lane shuffles.
+#include "common.h"
+#include "kernels.h"
+
+#include <algorithm>
+
+namespace mla {
+
+// ---------------------------------------------------------------------------------------
+// RoPE (Sec. 3.1): R_t rotates rotate-half pair p of a head by t * inv_freq[p].
+// ---------------------------------------------------------------------------------------
+__global__ void rope_table_kernel(const float* __restrict__ inv_freq, int G, int T, int np,
+                                  float* __restrict__ cos_t, float* __restrict__ sin_t) {
+  int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t total = (int64_t)G * T * np;
+  if (idx >= total) return;
+  int p = (int)(idx % np);
+  int t = (int)((idx / np) % T);
+  int g = (int)(idx / ((int64_t)np * T));
+  double ang = (double)t * (double)inv_freq[g * np + p];
+  cos_t[idx] = (float)cos(ang);
+  sin_t[idx] = (float)sin(ang);
+}
+
+hipError_t rope_tables(const float* inv_freq, int G, int T, int npairs, float* cos_t,
+                       float* sin_t, hipStream_t s) {
+  int64_t total = (int64_t)G * T * npairs;
+  if (total == 0) return hipSuccess;
+  prof_begin(KC_ELEM, s);
+  rope_table_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(inv_freq, G, T, npairs,
+                                                                    cos_t, sin_t);
+  prof_end(KC_ELEM, s, 0.0, (double)total * 8.0 + G * npairs * 4.0);
+  return hipGetLastError();
+}
+
+template <typename T, bool INV>
+__global__ void rope_apply_kernel(T* __restrict__ x, int N, int Tseq, int nheads, int64_t tok,
+                                  int64_t head, int off, int np, int div,
+                                  const float* __restrict__ cos_t,
+                                  const float* __restrict__ sin_t) {
+  int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t total = (int64_t)N * nheads * np;
+  if (idx >= total) return;
+  int p = (int)(idx % np);
+  int h = (int)((idx / np) % nheads);
+  int64_t n = idx / ((int64_t)np * nheads);
+  int t = (int)(n % Tseq);
+  int g = h / div;
+  float c = cos_t[((int64_t)g * Tseq + t) * np + p];
+  float sn = sin_t[((int64_t)g * Tseq + t) * np + p];
+  if (INV) sn = -sn;
+  T* base = x + n * tok + (int64_t)h * head + off;
+  float x1 = ld(base + p), x2 = ld(base + p + np);
+  st(base + p, x1 * c - x2 * sn);
+  st(base + p + np, x1 * sn + x2 * c);
+}
+
+hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, int64_t head,
+                      int off, int npairs, int div, const float* cos_t, const float* sin_t,
+                      hipStream_t s) {
+  int64_t total = (int64_t)N * nheads * npairs;
+  if (total == 0) return hipSuccess;
+  unsigned grid = (unsigned)((total + 255) / 256);
+  prof_begin(KC_ELEM, s);
+  if (t == DT_BF16)
+    rope_apply_kernel<bf16_t, false><<<grid, 256, 0, s>>>((bf16_t*)x, N, T, nheads, tok, head,
+                                                          off, npairs, div, cos_t, sin_t);
+  else
+    rope_apply_kernel<float, false><<<grid, 256, 0, s>>>((float*)x, N, T, nheads, tok, head,
+                                                         off, npairs, div, cos_t, sin_t);
+  prof_end(KC_ELEM, s, 0.0, (double)total * 4.0 * dsize(t));
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+// Backward finishing: rotate the rotary gradients back with R^T and cast.
+// ---------------------------------------------------------------------------------------
+template <typename T>
+__global__ void dq_finish_kernel(const float* __restrict__ acc, T* __restrict__ dq, int N,
+                                 int Tseq, int H, int dqk, int dnope, int rdiv,
+                                 const float* __restrict__ cos_t,
+                                 const float* __restrict__ sin_t) {
+  // one thread per (n, i, e) with e < dnope + np: e < dnope copies, else pair e - dnope
+  int np = (dqk - dnope) / 2;
+  int per_head = dnope + np;
+  int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t total = (int64_t)N * H * per_head;
+  if (idx >= total) return;
+  int e = (int)(idx % per_head);
+  int i = (int)((idx / per_head) % H);
+  int64_t n = idx / ((int64_t)per_head * H);
+  const float* a = acc + (n * H + i) * dqk;
+  T* o = dq + (n * H + i) * dqk;
+  if (e < dnope) {
+    st(o + e, a[e]);
+    return;
+  }
+  int p = e - dnope;
+  int t = (int)(n % Tseq);
+  int g = i / rdiv;
+  float c = cos_t[((int64_t)g * Tseq + t) * np + p];
+  float sn = sin_t[((int64_t)g * Tseq + t) * np + p];
+  float x1 = a[dnope + p], x2 = a[dnope + p + np];
+  st(o + dnope + p, x1 * c + x2 * sn);
+  st(o + dnope + p + np, -x1 * sn + x2 * c);
+}
+
+hipError_t dq_finish(const float* dq_acc, void* dq, DType t, int N, int T, int H, int dqk,
+                     int dnope, int rdiv, const float* cos_t, const float* sin_t,
+                     hipStream_t s) {
+  int64_t total = (int64_t)N * H * (dnope + (dqk - dnope) / 2);
+  if (total == 0) return hipSuccess;
+  unsigned grid = (unsigned)((total + 255) / 256);
+  prof_begin(KC_ELEM, s);
+  if (t == DT_BF16)
+    dq_finish_kernel<bf16_t><<<grid, 256, 0, s>>>(dq_acc, (bf16_t*)dq, N, T, H, dqk, dnope,
+                                                  rdiv, cos_t, sin_t);
+  else
+    dq_finish_kernel<float><<<grid, 256, 0, s>>>(dq_acc, (float*)dq, N, T, H, dqk, dnope, rdiv,
+                                                 cos_t, sin_t);
+  prof_end(KC_ELEM, s, 0.0, (double)N * H * dqk * (4.0 + dsize(t)));
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ void dkpe_finish_kernel(const float* __restrict__ part, T* __restrict__ out,
+                                   int64_t out_tok, int N, int Tseq, int Gr, int per, int dr,
+                                   const float* __restrict__ cos_t,
+                                   const float* __restrict__ sin_t) {
+  int np = dr / 2;
+  int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int64_t total = (int64_t)N * Gr * np;
+  if (idx >= total) return;
+  int p = (int)(idx % np);
+  int r = (int)((idx / np) % Gr);
+  int64_t n = idx / ((int64_t)np * Gr);
+  float x1 = 0.f, x2 = 0.f;
+  for (int k = 0; k < per; ++k) {  // fixed order: deterministic
+    const float* src = part + ((int64_t)(r * per + k) * N + n) * dr;
+    x1 += src[p];
+    x2 += src[p + np];
+  }
+  int t = (int)(n % Tseq);
+  float c = cos_t[((int64_t)r * Tseq + t) * np + p];
+  float sn = sin_t[((int64_t)r * Tseq + t) * np + p];
+  T* o = out + n * out_tok + (int64_t)r * dr;
+  st(o + p, x1 * c + x2 * sn);
+  st(o + p + np, -x1 * sn + x2 * c);
+}
+
+hipError_t dkpe_finish(const float* part, void* out, DType t, int64_t out_tok, int N, int T,
+                       int Gr, int per, int drope, const float* cos_t, const float* sin_t,
+                       hipStream_t s) {
+  int64_t total = (int64_t)N * Gr * (drope / 2);
+  if (total == 0) return hipSuccess;
+  unsigned grid = (unsigned)((total + 255) / 256);
+  prof_begin(KC_ELEM, s);
+  if (t == DT_BF16)
+    dkpe_finish_kernel<bf16_t><<<grid, 256, 0, s>>>(part, (bf16_t*)out, out_tok, N, T, Gr, per,
+                                                    drope, cos_t, sin_t);
+  else
+    dkpe_finish_kernel<float><<<grid, 256, 0, s>>>(part, (float*)out, out_tok, N, T, Gr, per,
+                                                   drope, cos_t, sin_t);
+  prof_end(KC_ELEM, s, 0.0, (double)N * Gr * drope * (4.0 * per + dsize(t)));
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+// Eq. 11: L = sum (M (A_s - A_t))^2 / (D sum M), dA = 2 M (A_s - A_t) / (D sum M).
+// Pass 1 counts the valid tokens, pass 2 streams A_s and A_t once (float4 loads), writes
+// dA and leaves one fp64 partial (sse, ref) per workgroup, pass 3 sums the partials in a
+// fixed order.  A fixed grid makes the result bitwise reproducible.
+// ---------------------------------------------------------------------------------------
+static constexpr int LOSS_BLOCKS = 2048;
+static constexpr int LOSS_THREADS = 256;
+
+struct LossScratch {
+  double count;
+  double pad[31];
+  double part[2 * LOSS_BLOCKS];
+};
+
+size_t loss_scratch_bytes() { return sizeof(LossScratch); }
+
+__global__ void mask_count_kernel(const uint8_t* __restrict__ mask, int64_t N,
+                                  LossScratch* __restrict__ ws) {
+  __shared__ double red[16];
+  double c = 0.0;
+  if (mask) {
+    for (int64_t i = threadIdx.x; i < N; i += blockDim.x) c += mask[i] ? 1.0 : 0.0;
+  } else if (threadIdx.x == 0) {
+    c = (double)N;
+  }
+  c = warp_sum_d(c);
+  int w = threadIdx.x / 64, l = threadIdx.x % 64;
+  if (l == 0) red[w] = c;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t = 0.0;
+    for (int i = 0; i < (int)(blockDim.x / 64); ++i) t += red[i];
+    ws->count = t;
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void store4(T* p, float a, float b, float c, float d);
+template <>
+__device__ __forceinline__ void store4<float>(float* p, float a, float b, float c, float d) {
+  *(float4*)p = make_float4(a, b, c, d);
+}
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t* p, float a, float b, float c, float d) {
+  *(u32x2*)p = u32x2{pack2bf(a, b), pack2bf(c, d)};
+}
+
+template <typename T>
+__global__ __launch_bounds__(LOSS_THREADS) void loss_main_kernel(
+    const float* __restrict__ As, const float* __restrict__ At,
+    const uint8_t* __restrict__ mask, int64_t N, int D, T* __restrict__ dA,
+    LossScratch* __restrict__ ws) {
+  __shared__ double red[2][LOSS_THREADS / 64];
+  const double cnt = ws->count;
+  const float g = cnt > 0.0 ? (float)(2.0 / ((double)D * cnt)) : 0.f;
+  const int64_t nvec = N * (int64_t)D / 4;
+  const int dv = D / 4;
+  float sse = 0.f, ref = 0.f;
+  for (int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; v < nvec;
+       v += (int64_t)gridDim.x * blockDim.x) {
+    int64_t n = v / dv;
+    float m = (mask == nullptr || mask[n]) ? 1.f : 0.f;
+    float4 a = ((const float4*)As)[v];
+    float4 b = ((const float4*)At)[v];
+    float e0 = m * (a.x - b.x), e1 = m * (a.y - b.y), e2 = m * (a.z - b.z), e3 = m * (a.w - b.w);
+    sse += e0 * e0 + e1 * e1 + e2 * e2 + e3 * e3;
+    float r0 = m * b.x, r1 = m * b.y, r2 = m * b.z, r3 = m * b.w;
+    ref += r0 * r0 + r1 * r1 + r2 * r2 + r3 * r3;
+    if (dA) store4<T>(dA + v * 4, g * e0, g * e1, g * e2, g * e3);
+  }
+  double s = warp_sum_d((double)sse), r = warp_sum_d((double)ref);
+  int w = threadIdx.x / 64, l = threadIdx.x % 64;
+  if (l == 0) {
+    red[0][w] = s;
+    red[1][w] = r;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double ts = 0.0, tr = 0.0;
+    for (int i = 0; i < LOSS_THREADS / 64; ++i) {
+      ts += red[0][i];
+      tr += red[1][i];
+    }
+    ws->part[2 * blockIdx.x] = ts;
+    ws->part[2 * blockIdx.x + 1] = tr;
+  }
+}
+
+__global__ void loss_final_kernel(const LossScratch* __restrict__ ws, int nblocks, int D,
+                                  float* __restrict__ loss) {
+  if (threadIdx.x != 0) return;
+  double s = 0.0, r = 0.0;
+  for (int i = 0; i < nblocks; ++i) {
+    s += ws->part[2 * i];
+    r += ws->part[2 * i + 1];
+  }
+  double den = (double)D * ws->count;
+  if (den == 0.0) {
+    loss[0] = 0.f;
+    loss[1] = 0.f;
+    return;
+  }
+  loss[0] = (float)(s / den);
+  loss[1] = r > 0.0 ? (float)(s / r) : (s == 0.0 ? 0.f : INFINITY);
+}
+
+hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, int64_t N, int D,
+                      float* loss, void* dA, DType t, void* scratch, hipStream_t s) {
+  LossScratch* ws = (LossScratch*)scratch;
+  int64_t nvec = N * (int64_t)D / 4;
+  int blocks = (int)std::min<int64_t>(LOSS_BLOCKS, std::max<int64_t>(1, (nvec + LOSS_THREADS - 1) / LOSS_THREADS));
+  prof_begin(KC_LOSS, s);
+  mask_count_kernel<<<1, 1024, 0, s>>>(mask, N, ws);
+  if (t == DT_BF16)
+    loss_main_kernel<bf16_t><<<blocks, LOSS_THREADS, 0, s>>>(A_s, A_t, mask, N, D, (bf16_t*)dA, ws);
+  else
+    loss_main_kernel<float><<<blocks, LOSS_THREADS, 0, s>>>(A_s, A_t, mask, N, D, (float*)dA, ws);
+  loss_final_kernel<<<1, 64, 0, s>>>(ws, blocks, D, loss);
+  double bytes = (double)N * D * (8.0 + (dA ? dsize(t) : 0)) + (mask ? N : 0);
+  prof_end(KC_LOSS, s, 0.0, bytes);
+  return hipGetLastError();
+}
+
+}  // namespace mla

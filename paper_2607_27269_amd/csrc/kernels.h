@@ -1,0 +1,90 @@
+// Internal launch interface between the C ABI (api.cpp) and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace mla {
+
+enum DType { DT_BF16 = 0, DT_F32 = 1 };
+inline size_t dsize(DType t) { return t == DT_BF16 ? 2 : 4; }
+
+enum KClass { KC_GEMM = 0, KC_ATTN_FWD = 1, KC_ATTN_BWD = 2, KC_LOSS = 3, KC_ELEM = 4, KC_COUNT = 5 };
+
+// Timing instrumentation hooks (implemented in api.cpp).  prof_end also records the
+// algorithmic FLOPs / bytes of the bracketed launch(es).
+void prof_begin(int kclass, hipStream_t s);
+void prof_end(int kclass, hipStream_t s, double flops, double bytes);
+
+// C[m, n] = alpha * sum_k A(m, k) B(n, k) + beta * C[m, n]
+//   A(m, k) = A[m*lda + k] if a_kmajor else A[k*lda + m]
+//   B(n, k) = B[n*ldb + k] if b_kmajor else B[k*ldb + n]
+struct Gemm {
+  int M, N, K;
+  const void* A; int64_t lda; bool a_kmajor;
+  const void* B; int64_t ldb; bool b_kmajor;
+  void* C; int64_t ldc;
+  DType in_t, c_t;
+  float alpha, beta;
+};
+// Scratch (fp32 elements) a GEMM of this shape needs for split-K partials.
+size_t gemm_scratch_elems(const Gemm& g);
+hipError_t gemm(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s);
+
+// Per-head strided view: element (n, i, d) at ptr[n*tok + (i / div)*head + d].
+struct HeadView {
+  const void* p; int64_t tok; int64_t head; int div;
+};
+
+// Causal attention over B sequences of T tokens, H query heads.  The logit width is
+// dqk; key dims [0, dnope) come from Ka and [dnope, dqk) from Kb (d = dnope + e reads
+// Kb element e).  Q, Ka, Kb, V are already rotated where RoPE applies.
+struct Attn {
+  int B, T, H, dqk, dnope, dv;
+  HeadView Q, Ka, Kb, V;
+  void* O; int64_t o_tok;   // O[n*o_tok + i*dv + d]
+  float* lse;               // [N, H] (natural-log units) or null in the forward
+  float scale;
+  DType t;
+};
+hipError_t attn_fwd(const Attn& a, hipStream_t s);
+
+struct AttnBwd {
+  Attn f;                    // forward operands; f.O and f.lse are inputs here
+  const void* dO;            // [N, H*dv], row stride H*dv
+  float* delta;              // scratch [N, H]
+  float* dq_acc;             // [N, H, dqk] fp32 (fully overwritten)
+  void* dKa; int64_t dka_tok;  // [N, ...]: group g's d_nope grads at dKa[n*dka_tok + g*dnope]
+  void* dV;  int64_t dv_tok;   // group g's value grads at dV[n*dv_tok + g*dv]
+  float* dkb_part;           // [Gka, N, dqk - dnope] fp32 partial grads of the Kb part per Ka group
+  int n_ka_groups;           // number of Ka groups (heads i / f.Ka.div)
+};
+hipError_t attn_bwd(const AttnBwd& a, hipStream_t s);
+
+// RoPE -------------------------------------------------------------------------------
+// cos/sin tables [G][T][npairs] fp32 from inv_freq [G][npairs] fp32 (angles in fp64).
+hipError_t rope_tables(const float* inv_freq, int G, int T, int npairs, float* cos_t,
+                       float* sin_t, hipStream_t s);
+// In-place rotation of x[n*tok + h*head + off + {p, p + npairs}] for heads h < nheads,
+// tokens n < N (position n % T), with the tables of group h / div.  inverse: R^T.
+hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, int64_t head,
+                      int off, int npairs, int div, const float* cos_t, const float* sin_t,
+                      hipStream_t s);
+
+// Backward finishing ----------------------------------------------------------------------
+// dq[n, i, :] = dq_acc with the rotary block [dnope, dqk) rotated back by R^T (tables of
+// rope group i / rdiv), written in storage dtype with row stride H*dqk.
+hipError_t dq_finish(const float* dq_acc, void* dq, DType t, int N, int T, int H, int dqk,
+                     int dnope, int rdiv, const float* cos_t, const float* sin_t, hipStream_t s);
+// dk^PE of rope group r = R^T sum of the partials of Ka groups r*per .. r*per+per-1,
+// written to out[n*out_tok + r*drope + e] in storage dtype.
+hipError_t dkpe_finish(const float* part, void* out, DType t, int64_t out_tok, int N, int T,
+                       int Gr, int per, int drope, const float* cos_t, const float* sin_t,
+                       hipStream_t s);
+
+// Loss (Eq. 11) -------------------------------------------------------------------------
+// scratch: at least loss_scratch_bytes(); loss[0] = L, loss[1] = relative error.
+size_t loss_scratch_bytes();
+hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, int64_t N, int D,
+                      float* loss, void* dA, DType t, void* scratch, hipStream_t s);
+
+}  // namespace mla

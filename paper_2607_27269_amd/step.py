@@ -1,0 +1,114 @@
+"""Device buffers and call sequence of one reconstruction step (torch for memory/streams).
+
+``DeviceStep`` uploads a synthetic workload once (hidden states, frozen teacher, student
+weights, mask) and owns the outputs (A_t, A_s, loss, dA, gradients) and the workspace.
+Its methods forward the tensors' device pointers and the current HIP stream to the C
+ABI; all arithmetic happens in the library's kernels.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import _lib as L
+from . import synth
+
+
+def _dev_tensor(x: np.ndarray, dtype: str, device) -> torch.Tensor:
+    if dtype == "bf16":
+        bits = synth.bf16_bits(x).view(np.int16)
+        return torch.from_numpy(np.ascontiguousarray(bits)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(device)
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+class DeviceStep:
+    def __init__(self, wl: "synth.Workload", device: str = "cuda:0", grads: tuple = None):
+        if not torch.cuda.is_available():
+            raise RuntimeError("DeviceStep needs a ROCm GPU")
+        L.lib()  # fail loudly if the HIP library is not built
+        cfg = wl.cfg
+        self.cfg = cfg
+        self.dtype = cfg.dtype
+        self.device = torch.device(device)
+        self.ccfg = L.make_cfg(cfg)
+        dev = self.device
+        up = lambda a: None if a is None else _dev_tensor(a, self.dtype, dev)
+        B, T, D = cfg.batch, cfg.seq, cfg.hidden
+        self.h = up(wl.h.reshape(B * T, D))
+        self.Wq, self.Wk, self.Wv, self.Wo = up(wl.Wq), up(wl.Wk), up(wl.Wv), up(wl.Wo)
+        self.inv_freq_t = torch.from_numpy(wl.inv_freq_t.astype(np.float32)).to(dev)
+        self.Wdq, self.Wuq, self.Wdkv_kr = up(wl.Wdq), up(wl.Wuq), up(wl.Wdkv_kr)
+        self.Wuk, self.Wuv = up(wl.Wuk), up(wl.Wuv)
+        self.inv_freq_s = torch.from_numpy(np.ascontiguousarray(wl.inv_freq_s, np.float32)).to(dev)
+        self.mask = torch.from_numpy(np.ascontiguousarray(wl.mask.reshape(-1))).to(dev)
+        tdt = torch.bfloat16 if self.dtype == "bf16" else torch.float32
+        self.A_t = torch.zeros(B * T, D, dtype=torch.float32, device=dev)
+        self.A_s = torch.zeros(B * T, D, dtype=torch.float32, device=dev)
+        self.loss_buf = torch.zeros(2, dtype=torch.float32, device=dev)
+        self.dA = torch.zeros(B * T, D, dtype=tdt, device=dev)
+        want = grads or ("dWdq", "dWuq", "dWdkv_kr", "dWuk", "dWuv")
+        self.grads = {}
+        for name, W in (("dWdq", self.Wdq), ("dWuq", self.Wuq), ("dWdkv_kr", self.Wdkv_kr),
+                        ("dWuk", self.Wuk), ("dWuv", self.Wuv)):
+            if W is not None and name in want:
+                self.grads[name] = torch.full(tuple(W.shape), float("nan"), dtype=torch.float32,
+                                              device=dev)
+        self.ws_bytes = L.mla_recon_workspace_size(self.ccfg)
+        if self.ws_bytes == 0:
+            raise L.MlaError(L.MLA_ERR_INVALID_ARG, L.last_error())
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)
+        self.tw = L.TeacherW(_ptr(self.Wq), _ptr(self.Wk), _ptr(self.Wv), _ptr(self.Wo),
+                             _ptr(self.inv_freq_t))
+        self.sw = L.StudentW(_ptr(self.Wdq), _ptr(self.Wuq), _ptr(self.Wdkv_kr), _ptr(self.Wuk),
+                             _ptr(self.Wuv), _ptr(self.inv_freq_s))
+        self.sg = L.StudentGrads(*[_ptr(self.grads.get(n)) for n in
+                                   ("dWdq", "dWuq", "dWdkv_kr", "dWuk", "dWuv")])
+
+    @property
+    def stream(self) -> int:
+        return torch.cuda.current_stream(self.device).cuda_stream
+
+    def teacher_fwd(self):
+        L.mla_recon_teacher_fwd(self.ccfg, _ptr(self.h), self.tw, _ptr(self.A_t),
+                                _ptr(self.ws), self.ws_bytes, self.stream)
+
+    def student_fwd(self):
+        L.mla_recon_student_fwd(self.ccfg, _ptr(self.h), self.sw, _ptr(self.Wo), _ptr(self.A_s),
+                                _ptr(self.ws), self.ws_bytes, self.stream)
+
+    def loss(self, A_s=None, A_t=None, mask=True, dA=True):
+        A_s = self.A_s if A_s is None else A_s
+        A_t = self.A_t if A_t is None else A_t
+        L.mla_recon_loss(self.ccfg, _ptr(A_s), _ptr(A_t), _ptr(self.mask) if mask else None,
+                         _ptr(self.loss_buf), _ptr(self.dA) if dA else None, _ptr(self.ws),
+                         self.ws_bytes, self.stream)
+
+    def bwd(self, dA=None):
+        dA = self.dA if dA is None else dA
+        L.mla_recon_bwd(self.ccfg, _ptr(self.h), self.sw, _ptr(self.Wo), _ptr(dA), self.sg,
+                        _ptr(self.ws), self.ws_bytes, self.stream)
+
+    def step(self):
+        """One whole step: teacher forward, student forward, Eq. 11, backward."""
+        self.teacher_fwd()
+        self.student_fwd()
+        self.loss()
+        self.bwd()
+
+    def upload(self, x: np.ndarray, dtype: str | None = None) -> torch.Tensor:
+        return _dev_tensor(x, dtype or self.dtype, self.device)
+
+    def results(self) -> dict:
+        torch.cuda.synchronize(self.device)
+        B, T, D = self.cfg.batch, self.cfg.seq, self.cfg.hidden
+        out = dict(A_t=self.A_t.double().cpu().numpy().reshape(B, T, D),
+                   A_s=self.A_s.double().cpu().numpy().reshape(B, T, D),
+                   loss=float(self.loss_buf[0]), rel=float(self.loss_buf[1]),
+                   dA=self.dA.double().cpu().numpy().reshape(B, T, D))
+        for k, v in self.grads.items():
+            out[k] = v.double().cpu().numpy()
+        return out

@@ -1,0 +1,105 @@
+"""The C ABI library: symbols, workspace sizing and argument validation (no GPU needed).
+
+Every check here returns before the library touches the GPU: validation happens before
+any launch, so these calls are safe on a machine without a device.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2607_27269_amd import _lib as L
+from paper_2607_27269_amd import configs
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mla_recon.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(L.LIB_PATH),
+                                reason="libmlarecon.so not built (run __graft_entry__.build())")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mla_recon_\w+)\s*\(", text)))
+
+
+def test_exports_every_declared_function():
+    names = header_functions()
+    assert {"mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
+            "mla_recon_bwd", "mla_recon_workspace_size", "mla_recon_last_error"} <= set(names)
+    lib = ctypes.CDLL(L.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_python_binding_names_match_header():
+    for n in header_functions():
+        assert hasattr(L, n), n
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2, 3, 4])
+def test_workspace_size_positive(idx):
+    c = L.make_cfg(configs.get(idx))
+    ws = L.mla_recon_workspace_size(c)
+    assert ws > 0 and ws % 256 == 0
+    # monotone in the number of tokens
+    c2 = L.make_cfg(configs.shrink(configs.get(idx), batch=1, seq=64))
+    assert L.mla_recon_workspace_size(c2) < ws
+
+
+def bad(**kw):
+    base = configs.shrink(configs.get(1), batch=1, seq=64)
+    return L.make_cfg(base.replace(**kw))
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_heads=15), L.MLA_ERR_INVALID_ARG),        # H % G != 0
+    (dict(rope_dim=36), L.MLA_ERR_INVALID_ARG),       # not a multiple of 8
+    (dict(head_dim=60), L.MLA_ERR_INVALID_ARG),
+    (dict(batch=0), L.MLA_ERR_INVALID_ARG),
+    (dict(q_rank=-8), L.MLA_ERR_INVALID_ARG),
+    (dict(s_rope_groups=7, n_heads=14), L.MLA_ERR_UNSUPPORTED),   # G_kv % G_r != 0
+])
+def test_invalid_configs_rejected(kw, code):
+    c = bad(**kw)
+    assert L.mla_recon_workspace_size(c) == 0
+    w = L.TeacherW(1, 1, 1, 1, 1)
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_teacher_fwd(c, 1, w, 1, 256, 1 << 40, None)
+    assert e.value.code == code
+    assert L.last_error()
+
+
+def test_null_pointers_and_small_workspace_rejected():
+    cfg = configs.shrink(configs.get(1), batch=1, seq=64)
+    c = L.make_cfg(cfg)
+    ws = L.mla_recon_workspace_size(c)
+    w = L.TeacherW(1, 1, 1, 1, 1)
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_teacher_fwd(c, None, w, 1, 256, ws, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_teacher_fwd(c, 1, w, 1, 256, ws - 1, None)
+    assert e.value.code == L.MLA_ERR_WORKSPACE
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_teacher_fwd(c, 1, w, 1, 257, ws, None)     # misaligned
+    assert e.value.code == L.MLA_ERR_WORKSPACE
+    sw = L.StudentW(None, 1, 1, 1, 1, 1)                           # W_DQ missing, q_rank > 0
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_student_fwd(c, 1, sw, 1, 1, 256, ws, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_loss(c, 1, 1, None, None, None, 256, ws, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
+    g = L.StudentGrads(1, None, None, None, None)
+    c0 = L.make_cfg(cfg.replace(q_rank=0))
+    with pytest.raises(L.MlaError) as e:   # dW_DQ requested without a W_DQ
+        L.mla_recon_bwd(c0, 1, L.StudentW(None, 1, 1, 1, 1, 1), 1, 1, g, 256, 1 << 40, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
+
+
+def test_prof_class_validation():
+    with pytest.raises(L.MlaError):
+        L.mla_recon_prof_read(99)

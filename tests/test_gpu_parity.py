@@ -1,0 +1,86 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Inputs are seeded synthetic workloads (paper_2607_27269_amd.synth) shaped like the five
+layer configurations, shortened to sizes the oracle finishes in seconds while still
+spanning several attention/GEMM tiles and a ragged tail.  Right-padding masks exercise
+Eq. 11's M.  Tolerances: 2e-2 relative (Frobenius) for bf16 outputs and gradients, 1e-5
+in the fp32 check mode, 1e-3 relative on the loss.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from paper_2607_27269_amd import configs, synth
+from parity_util import LOSS_TOL, TOL, compare, oracle_step, rel_err
+
+pytestmark = pytest.mark.gpu
+
+GRADS = ("dWdq", "dWuq", "dWdkv_kr", "dWuk", "dWuv")
+
+CASES = {
+    # name: (config index, batch, seq, valid lengths or None)
+    "cfg0_full_fp32": (0, 2, 64, None),
+    "cfg0_ragged_fp32": (0, 2, 77, [77, 40]),
+    "cfg0_bf16": (0, 2, 64, None),
+    "cfg1_ragged": (1, 2, 200, [200, 131]),
+    "cfg2_short": (2, 1, 192, None),
+    "cfg3_short": (3, 1, 136, [100]),
+    "cfg4_short": (4, 1, 130, None),
+}
+
+
+def make_case(name):
+    idx, B, T, lengths = CASES[name]
+    cfg = configs.shrink(configs.get(idx), batch=B, seq=T)
+    if name == "cfg0_bf16":
+        cfg = cfg.replace(dtype="bf16")
+    return cfg, synth.make_workload(cfg, lengths=lengths)
+
+
+@pytest.mark.parametrize("name", list(CASES))
+def test_step_parity(name):
+    from paper_2607_27269_amd.step import DeviceStep
+    print(f"[parity] case={name}", flush=True)
+    cfg, wl = make_case(name)
+    ref = oracle_step(wl)
+    dev = DeviceStep(wl)
+    dev.step()
+    out = dev.results()
+    tol = TOL[cfg.dtype]
+    errs = compare(out, ref, ("A_t", "A_s") + GRADS, tol, label=f"{name}: ")
+    assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
+    assert abs(out["rel"] - ref["rel"]) <= LOSS_TOL * abs(ref["rel"]), (out["rel"], ref["rel"])
+    print(f"[parity] {name} loss={out['loss']:.6e} ref={ref['loss']:.6e} errs={errs}", flush=True)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_loss_kernel_parity(dtype):
+    """Eq. 11 kernel alone on seeded A_s, A_t with a ragged mask (oracle in fp64)."""
+    import torch
+    from paper_2607_27269_amd.step import DeviceStep
+    import oracle as O
+    cfg = configs.shrink(configs.get(1), batch=3, seq=333).replace(dtype=dtype)
+    wl = synth.make_workload(cfg, lengths=[333, 200, 0])
+    dev = DeviceStep(wl)
+    As, At = synth.random_outputs(cfg, seed=11, dtype="fp32")
+    tA_s = dev.upload(As.reshape(-1, cfg.hidden), "fp32")
+    tA_t = dev.upload(At.reshape(-1, cfg.hidden), "fp32")
+    dev.loss(tA_s, tA_t)
+    torch.cuda.synchronize()
+    L, rel, dA = O.recon_loss(As, At, wl.mask)
+    got = dev.loss_buf.double().cpu().numpy()
+    assert abs(got[0] - L) <= 1e-6 * L and abs(got[1] - rel) <= 1e-6 * rel
+    gdA = dev.dA.double().cpu().numpy().reshape(dA.shape)
+    assert rel_err(gdA, dA) <= (4e-3 if dtype == "bf16" else 1e-6)
+    assert not gdA[2].any() and not gdA[1, 200:].any()        # masked rows: zero gradient
+    # the same inputs twice: bitwise identical (fixed reduction order)
+    first = dev.loss_buf.clone()
+    dev.loss(tA_s, tA_t)
+    torch.cuda.synchronize()
+    assert torch.equal(first, dev.loss_buf)
+    # all-invalid mask
+    dev.mask.zero_()
+    dev.loss(tA_s, tA_t)
+    torch.cuda.synchronize()
+    assert float(dev.loss_buf[0]) == 0.0 and not dev.dA.any()
