@@ -2,24 +2,22 @@
 // kernels.  Also owns the per-launch FLOP/byte accounting of the instrumentation.
 #include "common.h"
 #include "kernels.h"
+#include "mfma.h"
 #include "simt.h"
 
 namespace mla {
 
 size_t gemm_scratch_elems(const Gemm& g) {
-  (void)g;
-  return 0;
+  return g.in_t == DT_BF16 ? gemm_mfma_scratch_elems(g) : 0;
 }
 
 hipError_t gemm(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s) {
-  (void)scratch;
-  (void)scratch_elems;
   if (g.M == 0 || g.N == 0) return hipSuccess;
   double flops = 2.0 * g.M * g.N * (double)g.K;
   double bytes = ((double)g.M * g.K + (double)g.N * g.K) * dsize(g.in_t) +
                  (double)g.M * g.N * dsize(g.c_t) * (g.beta != 0.f ? 2.0 : 1.0);
   prof_begin(KC_GEMM, s);
-  hipError_t e = gemm_simt(g, s);
+  hipError_t e = g.in_t == DT_BF16 ? gemm_mfma(g, scratch, scratch_elems, s) : gemm_simt(g, s);
   prof_end(KC_GEMM, s, flops, bytes);
   return e;
 }

@@ -1,0 +1,8 @@
+// bf16 matrix-core (MFMA) kernels for gfx950; see gemm_mfma.hip and attn_mfma.hip.
+#pragma once
+#include "kernels.h"
+
+namespace mla {
+size_t gemm_mfma_scratch_elems(const Gemm& g);
+hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s);
+}  // namespace mla

@@ -1,0 +1,104 @@
+"""GPU parity at the full layer sizes, in the launch configuration the benchmark times.
+
+The oracle cannot evaluate a whole full-size step in a test's time budget, so each check
+uses a property that pins the full-size launch to what the oracle can compute:
+
+* causality (Eq. 3): row t of A_orig / A_MLA depends only on tokens 0..t of its sequence,
+  so the first `tc` rows of sequence 0 equal the oracle's output on that prefix, and the
+  rows of the last sequence equal the oracle run on that one sequence (last rows sampled);
+* the backward is linear in dA: with an upstream gradient that is non-zero only on the
+  first `tc` tokens of sequence 0, every weight gradient equals the oracle's gradient of
+  the prefix problem (the other tokens contribute exact zeros);
+* Eq. 11 on seeded (A_s, A_t) pairs of full size against the oracle's loss.
+"""
+import numpy as np
+import pytest
+
+import oracle as O
+from paper_2607_27269_amd import configs, synth
+from parity_util import TOL, compare, rel_err
+
+pytestmark = pytest.mark.gpu
+
+GRADS = ("dWdq", "dWuq", "dWdkv_kr", "dWuk", "dWuv")
+
+
+def prefix_workload(wl, b, tc):
+    """The same layer restricted to sequence b, tokens 0..tc-1."""
+    import copy
+    w = copy.copy(wl)
+    w.cfg = wl.cfg.replace(batch=1, seq=tc)
+    w.h = wl.h[b:b + 1, :tc]
+    w.mask = np.ones((1, tc), dtype=np.uint8)
+    return w
+
+
+def oracle_fwd(w):
+    c = w.cfg
+    A_t = O.teacher_forward(w.h, w.Wq, w.Wk, w.Wv, w.Wo, w.inv_freq_t, c.n_heads, c.n_kv_groups,
+                            c.softmax_scale)
+    A_s, cache = O.student_forward(w.h, w.Wdq, w.Wuq, w.Wdkv_kr, w.Wuk, w.Wuv, w.Wo, w.inv_freq_s,
+                                   n_heads=c.n_heads, s_kv_groups=c.s_kv_groups,
+                                   s_rope_groups=c.s_rope_groups, nope_dim=c.nope_dim,
+                                   rope_dim=c.rope_dim, scale=c.softmax_scale)
+    return A_t, A_s, cache
+
+
+@pytest.mark.parametrize("idx", [3, 4, 1, 2])
+def test_fullsize_step(idx):
+    import torch
+    from paper_2607_27269_amd.step import DeviceStep
+    cfg = configs.get(idx)
+    print(f"[fullsize] config {idx} {cfg.name} B={cfg.batch} T={cfg.seq}", flush=True)
+    wl = synth.make_workload(cfg)
+    dev = DeviceStep(wl)
+    dev.teacher_fwd()
+    dev.student_fwd()
+    tc = 192
+    # sparse upstream gradient on the first tc tokens of sequence 0
+    rows = [(0, t) for t in range(tc)]
+    dA = synth.random_upstream(cfg, seed=5, dtype=cfg.dtype, rows=rows, scale=1e-4)
+    dev.bwd(dev.upload(dA.reshape(-1, cfg.hidden)))
+    out = dev.results()
+    B, T = cfg.batch, cfg.seq
+    tol = TOL[cfg.dtype]
+
+    # prefix of sequence 0: forward rows and every gradient
+    pw = prefix_workload(wl, 0, tc)
+    A_t, A_s, cache = oracle_fwd(pw)
+    compare(dict(A_t=out["A_t"][0, :tc], A_s=out["A_s"][0, :tc]), dict(A_t=A_t[0], A_s=A_s[0]),
+            ("A_t", "A_s"), tol, label=f"cfg{idx} prefix: ")
+    g = O.student_backward(cache, dA[0:1, :tc])
+    errs = compare(out, g, GRADS, tol, label=f"cfg{idx} grads: ")
+    print(f"[fullsize] cfg{idx} grad errs {errs}", flush=True)
+
+    # the whole last sequence: sampled rows including the final tokens
+    lw = prefix_workload(wl, B - 1, T)
+    A_t, A_s, _ = oracle_fwd(lw)
+    rows = np.r_[0, 1, 63, 64, 65, 1000, T // 2, T - 130, T - 65, T - 64, T - 2, T - 1]
+    e = compare(dict(A_t=out["A_t"][B - 1, rows], A_s=out["A_s"][B - 1, rows]),
+                dict(A_t=A_t[0, rows], A_s=A_s[0, rows]), ("A_t", "A_s"), tol,
+                label=f"cfg{idx} last seq: ")
+    print(f"[fullsize] cfg{idx} last-seq errs {e}", flush=True)
+    del dev
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("idx", [3])
+def test_fullsize_loss(idx):
+    import torch
+    from paper_2607_27269_amd.step import DeviceStep
+    cfg = configs.get(idx)
+    wl = synth.make_workload(cfg, lengths=[cfg.seq, cfg.seq - 1, 1000, cfg.seq])
+    dev = DeviceStep(wl)
+    As, At = synth.random_outputs(cfg, seed=3, dtype="fp32")
+    dev.loss(dev.upload(As.reshape(-1, cfg.hidden), "fp32"), dev.upload(At.reshape(-1, cfg.hidden), "fp32"))
+    torch.cuda.synchronize()
+    L, rel, dA = O.recon_loss(As, At, wl.mask)
+    got = dev.loss_buf.double().cpu().numpy()
+    assert abs(got[0] - L) <= 1e-5 * L, (got[0], L)
+    assert abs(got[1] - rel) <= 1e-5 * rel, (got[1], rel)
+    gdA = dev.dA.double().cpu().numpy().reshape(dA.shape)
+    assert rel_err(gdA, dA) <= 4e-3
+    del dev
+    torch.cuda.empty_cache()
