@@ -1,0 +1,157 @@
+"""Benchmark of the end-to-end functional-reconstruction step on one MI355X.
+
+One step = teacher forward + student forward + Eq. 11 loss + backward to the five
+converter-introduced projections, on one calibration minibatch of synthetic hidden states
+resident in HBM.  Default workload: the Llama-3-8B-shaped layer (B=4, T=4096, D=4096,
+H=32, G=8, d_k=128; student r_q=1536, r_kv=512, d_nope=128, d_rope=64).
+
+Prints one JSON line: calibration tokens/s per layer (B*T / step time), the fraction of
+the bf16 MFMA peak reached by the whole step, the roofline of the dominant kernel class
+(timed with HIP events on the launch stream inside the timed region), and the float64
+CPU oracle timed on a bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--config", type=int, default=3)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-seq", type=int, default=2048, help="oracle sample: tokens of one sequence")
+    return p.parse_args()
+
+
+def cpu_baseline(cfg, wl, seq):
+    """The float64 oracle on one sequence of `seq` tokens of the same layer."""
+    import numpy as np
+
+    import oracle as O
+    c = cfg
+    h = wl.h[0:1, :seq]
+    mask = np.ones((1, seq), dtype=np.uint8)
+    t0 = time.perf_counter()
+    A_t = O.teacher_forward(h, wl.Wq, wl.Wk, wl.Wv, wl.Wo, wl.inv_freq_t, c.n_heads,
+                            c.n_kv_groups, c.softmax_scale)
+    A_s, cache = O.student_forward(h, wl.Wdq, wl.Wuq, wl.Wdkv_kr, wl.Wuk, wl.Wuv, wl.Wo,
+                                   wl.inv_freq_s, n_heads=c.n_heads, s_kv_groups=c.s_kv_groups,
+                                   s_rope_groups=c.s_rope_groups, nope_dim=c.nope_dim,
+                                   rope_dim=c.rope_dim, scale=c.softmax_scale)
+    _, _, dA = O.recon_loss(A_s, A_t, mask)
+    O.student_backward(cache, dA)
+    dt = time.perf_counter() - t0
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count()
+    threads = int(os.environ.get("OMP_NUM_THREADS", cores))
+    return {"value": seq / dt, "unit": "tokens/s", "cores": min(cores, threads), "kind": "oracle",
+            "sample": f"1 sequence x {seq} tokens of the {cfg.name} layer (full widths), "
+                      f"teacher fwd + student fwd + Eq. 11 + backward, float64 numpy; {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: the reconstruction step is not sharded across "
+              "GPUs (layers are independent); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2607_27269_amd import _lib as L
+    from paper_2607_27269_amd import configs, synth
+    from paper_2607_27269_amd.step import DeviceStep
+
+    cfg = configs.get(args.config)
+    wl = synth.make_workload(cfg)
+    dev = DeviceStep(wl)
+    for _ in range(args.warmup):
+        dev.step()
+    torch.cuda.synchronize()
+
+    classes = list(L.KCLASS_NAMES)
+    for k in classes:
+        L.mla_recon_prof_enable(k, True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        dev.step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / args.steps
+    prof = {L.KCLASS_NAMES[k]: L.mla_recon_prof_read(k) for k in classes}
+    for k in classes:
+        L.mla_recon_prof_enable(k, False)
+
+    # same loop without instrumentation (event overhead check)
+    start.record()
+    for _ in range(args.steps):
+        dev.step()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_plain = start.elapsed_time(stop) / args.steps
+
+    loss = float(dev.loss_buf[0])
+    tokens = cfg.tokens
+    flops = cfg.total_flops()
+    tok_s = tokens / (ms / 1e3)
+    dom = max(prof, key=lambda k: prof[k]["ms"])
+    p = prof[dom]
+    bound = "mfma" if p["flops"] > 0 else "hbm"
+    if bound == "mfma":
+        achieved = p["flops"] / (p["ms"] / 1e3) / 1e12
+        peak, unit = PEAK_BF16_TFLOPS, "TFLOP/s"
+    else:
+        achieved = p["bytes"] / (p["ms"] / 1e3) / 1e9
+        peak, unit = PEAK_HBM_GBS, "GB/s"
+    kernel_share = {k: round(v["ms"] / args.steps, 4) for k, v in prof.items()}
+    out = {
+        "metric": "calibration tokens/sec per layer (fwd+bwd recon)",
+        "value": round(tok_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}: B={cfg.batch} T={cfg.seq} D={cfg.hidden} "
+                               f"H={cfg.n_heads} G={cfg.n_kv_groups} d_k={cfg.head_dim}; student "
+                               f"r_q={cfg.q_rank} r_kv={cfg.kv_rank} d_nope={cfg.nope_dim} "
+                               f"d_rope={cfg.rope_dim} G_kv={cfg.s_kv_groups} G_r={cfg.s_rope_groups}",
+                   "global_batch": cfg.batch, "seq_len": cfg.seq, "parallelism": "none (1 GPU)"},
+        "mfma_peak_frac": round(flops / (ms / 1e3) / (PEAK_BF16_TFLOPS * 1e12), 4),
+        "alg_gflop_per_step": round(flops / 1e9, 1),
+        "ms_per_step_uninstrumented": round(ms_plain, 4),
+        "kernel_ms_per_step": kernel_share,
+        "roofline": {"kernel": dom, "bound": bound, "achieved": round(achieved, 2),
+                     "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
+                     "traffic": None,
+                     "launches_per_step": p["launches"] / args.steps},
+        "loss": loss,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(cfg, wl, min(args.cpu_seq, cfg.seq))
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -12,6 +12,7 @@
 
 #include "../../include/mla_recon.h"
 #include "kernels.h"
+#include "mfma.h"
 #include "simt.h"
 
 namespace mla {
@@ -86,7 +87,7 @@ static Dims dims_of(const mla_recon_cfg* c) {
 }
 
 static bool attn_supported(const Dims& d, int dqk, int dv) {
-  return attn_simt_supported(dqk, dv);
+  return attn_simt_supported(dqk, dv) || (d.t == DT_BF16 && attn_mfma_supported(dqk, dv));
 }
 
 static int check_cfg(const mla_recon_cfg* c) {

@@ -31,7 +31,8 @@ hipError_t attn_fwd(const Attn& a, hipStream_t s) {
   double N = (double)a.B * a.T;
   double bytes = N * a.H * (a.dqk + a.dv) * dsize(a.t) + N * a.H * (a.lse ? 4.0 : 0.0);
   prof_begin(KC_ATTN_FWD, s);
-  hipError_t e = attn_fwd_simt(a, s);
+  hipError_t e = a.t == DT_BF16 && attn_mfma_supported(a.dqk, a.dv) ? attn_fwd_mfma(a, s)
+                                                                    : attn_fwd_simt(a, s);
   prof_end(KC_ATTN_FWD, s, flops, bytes);
   return e;
 }
