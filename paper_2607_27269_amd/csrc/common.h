@@ -71,3 +71,32 @@ __device__ __forceinline__ int xcd_remap(int pid, int nwg) {
 }
 
 }  // namespace mla
+
+namespace mla {
+
+// gfx950 LDS transpose read (ds_read_b64_tr_b16).  Inside each group of 16 lanes, lane r
+// supplies the address of 4 consecutive 16-bit elements; lane j of the group receives
+// element (j % 4) of the rows supplied by lanes j/4, j/4 + 4, j/4 + 8, j/4 + 12.  With
+// lane r pointing at row k0 + r/4, columns n0 + 4(r%4) of a [k][n] (n-contiguous) LDS
+// matrix, lane j receives column n0 + j, rows k0 .. k0+3: a transposed 4 x 16 block.
+__device__ __forceinline__ u32x2 lds_read_tr4(const bf16_t* p) {
+  typedef short i16x4 __attribute__((ext_vector_type(4)));
+  i16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) i16x4*)p);
+  return __builtin_bit_cast(u32x2, v);
+}
+
+// MFMA 32x32x16 operand (lane: row/column m0 + lane%32, 8 k-values) read from an LDS
+// matrix stored [k][m] with row stride ld.  The lane's k-slots 0..3 are rows klo..klo+3,
+// slots 4..7 rows khi..khi+3, where klo / khi may differ between the two lane halves.
+__device__ __forceinline__ bf16x8 lds_operand_tr(const bf16_t* base, int ld, int m0, int klo,
+                                                 int khi) {
+  const int lane = threadIdx.x & 63;
+  const int g = lane >> 4, r = lane & 15;
+  const int n0 = m0 + 16 * (g & 1) + 4 * (r & 3);
+  u32x2 lo = lds_read_tr4(base + (klo + (r >> 2)) * ld + n0);
+  u32x2 hi = lds_read_tr4(base + (khi + (r >> 2)) * ld + n0);
+  u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+  return __builtin_bit_cast(bf16x8, w);
+}
+
+}  // namespace mla

@@ -43,7 +43,8 @@ hipError_t attn_bwd(const AttnBwd& w, hipStream_t s) {
   double N = (double)a.B * a.T;
   double bytes = N * a.H * (a.dqk + 2.0 * a.dv) * dsize(a.t) + N * a.H * (8.0 + 4.0 * a.dqk);
   prof_begin(KC_ATTN_BWD, s);
-  hipError_t e = attn_bwd_simt(w, s);
+  hipError_t e = a.t == DT_BF16 && attn_mfma_supported(a.dqk, a.dv) ? attn_bwd_mfma(w, s)
+                                                                    : attn_bwd_simt(w, s);
   prof_end(KC_ATTN_BWD, s, flops, bytes);
   return e;
 }
