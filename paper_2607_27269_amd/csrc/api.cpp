@@ -10,7 +10,7 @@
 #include <mutex>
 #include <vector>
 
-#include "../../include/mla_recon.h"
+#include "mla_recon.h"
 #include "kernels.h"
 #include "mfma.h"
 #include "simt.h"

@@ -1,0 +1,278 @@
+// Causal softmax attention (Eq. 2-4) on gfx950 matrix cores, bf16 operands, fp32 softmax.
+//
+// Forward.  A workgroup (8 wavefronts) owns 256 queries of one (sequence, head); each
+// wavefront owns 32 of them.  Keys/values stream through LDS 64 at a time (double
+// buffered, the next tile's global loads in flight during the current tile's math).
+// The logits are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: the
+// query is the MFMA column, so every lane owns one query and the online-softmax state
+// (running max m, running sum l, the output row O^T) of that query lives in that lane.
+// The accumulator layout of S^T is then reused directly as the B operand of
+// O^T = V^T P^T (the key order inside one MFMA K-step is permuted identically on the
+// V^T side), so P never leaves registers.  V stays [key][d_v] in LDS and its transposed
+// operand comes from gfx950's transposing LDS read.  Softmax runs in base 2 with the
+// logit scale folded into one FMA, and the output is only rescaled when the running
+// maximum grows by more than 2^8 (P stays <= 2^8 otherwise).
+// Tiles entirely above the causal diagonal are skipped per wavefront; only diagonal tiles
+// are masked.  The key of head i is [Ka_{i/div_a} ; Kb_{i/div_b}] (non-positional part
+// from one buffer, rotary part from another), which serves both the teacher
+// (Ka = full key) and the MLA student (k^nope of the KV group, k^PE of the rope group).
+#include "attn_common.h"
+#include "mfma.h"
+
+namespace mla {
+namespace attn {
+namespace {
+
+// K and V tiles of BKV keys, staged global -> registers -> LDS in their natural
+// [key][dim] layout (16-byte chunks).  Source addresses are formed once per workgroup and
+// advanced by one tile per step; only the ragged last tile checks the sequence end.
+template <int DQK, int DV, int NTHR>
+struct KVStage {
+  static constexpr int KCH = BKV * (DQK / 8);
+  static constexpr int KPER = (KCH + NTHR - 1) / NTHR;
+  static constexpr int VCH = BKV * (DV / 8);
+  static constexpr int VPER = (VCH + NTHR - 1) / NTHR;
+  static constexpr int LDK = DQK + KPAD;
+  static constexpr int LDV = DV + 16;  // 4 rows x 32 B of a transposing read hit distinct banks
+  u32x4 k[KPER];
+  u32x4 v[VPER];
+  const bf16_t* ksrc[KPER];
+  const bf16_t* vsrc[VPER];
+  int64_t kstr[KPER];
+  int krow[KPER], vrow[VPER];
+
+  __device__ __forceinline__ void init(const AttnDev& a, int b, int i) {
+    const int ga = i / a.ka_div, gb = i / a.kb_div, gv = i / a.v_div;
+#pragma unroll
+    for (int it = 0; it < KPER; ++it) {
+      const int c = min((int)threadIdx.x + it * NTHR, KCH - 1);
+      const int key = c / (DQK / 8), dc = (c % (DQK / 8)) * 8;
+      const int64_t n = (int64_t)b * a.T + key;
+      krow[it] = key;
+      const bool nope = dc < a.dnope;
+      kstr[it] = nope ? a.ka_tok : a.kb_tok;
+      ksrc[it] = nope ? a.Ka + n * a.ka_tok + (int64_t)ga * a.ka_head + dc
+                      : a.Kb + n * a.kb_tok + (int64_t)gb * a.kb_head + (dc - a.dnope);
+    }
+#pragma unroll
+    for (int it = 0; it < VPER; ++it) {
+      const int c = min((int)threadIdx.x + it * NTHR, VCH - 1);
+      const int key = c / (DV / 8), dc = (c % (DV / 8)) * 8;
+      vrow[it] = key;
+      vsrc[it] = a.V + ((int64_t)b * a.T + key) * a.v_tok + (int64_t)gv * a.v_head + dc;
+    }
+  }
+
+  // tile starting at key j0 (a multiple of BKV)
+  __device__ __forceinline__ void load(const AttnDev& a, int j0) {
+    const bool full = j0 + BKV <= a.T;
+#pragma unroll
+    for (int it = 0; it < KPER; ++it) {
+      u32x4 val = {0u, 0u, 0u, 0u};
+      const bool in = KCH % NTHR == 0 || (int)threadIdx.x + it * NTHR < KCH;
+      if (in && (full || j0 + krow[it] < a.T)) val = *(const u32x4*)(ksrc[it] + (int64_t)j0 * kstr[it]);
+      k[it] = val;
+    }
+#pragma unroll
+    for (int it = 0; it < VPER; ++it) {
+      u32x4 val = {0u, 0u, 0u, 0u};
+      const bool in = VCH % NTHR == 0 || (int)threadIdx.x + it * NTHR < VCH;
+      if (in && (full || j0 + vrow[it] < a.T)) val = *(const u32x4*)(vsrc[it] + (int64_t)j0 * a.v_tok);
+      v[it] = val;
+    }
+  }
+
+  __device__ __forceinline__ void store(bf16_t* ks, bf16_t* vs) const {
+#pragma unroll
+    for (int it = 0; it < KPER; ++it) {
+      const int c = (int)threadIdx.x + it * NTHR;
+      if (KCH % NTHR == 0 || c < KCH)
+        *(u32x4*)(ks + (c / (DQK / 8)) * LDK + (c % (DQK / 8)) * 8) = k[it];
+    }
+#pragma unroll
+    for (int it = 0; it < VPER; ++it) {
+      const int c = (int)threadIdx.x + it * NTHR;
+      if (VCH % NTHR == 0 || c < VCH)
+        *(u32x4*)(vs + (c / (DV / 8)) * LDV + (c % (DV / 8)) * 8) = v[it];
+    }
+  }
+};
+
+constexpr int FWD_WAVES = 8;
+constexpr int FWD_BQ = 32 * FWD_WAVES;   // queries per workgroup
+constexpr float RESCALE_SLACK = 8.f;     // log2 units the running reference max may lag
+
+template <int DQK, int DV, bool LSE>
+__global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a) {
+  using Stage = KVStage<DQK, DV, 64 * FWD_WAVES>;
+  constexpr int LDK = Stage::LDK, LDV = Stage::LDV;
+  constexpr int KS = BKV * LDK;
+  constexpr int VS = BKV * LDV;
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (KS + VS)];
+  constexpr int NKK = DQK / 16;  // MFMA K-steps of the logits
+  constexpr int NC = DV / 32;    // 32-row tiles of O^T
+
+  // work item: XCD-aware remap so that the query blocks of neighbouring heads (which share
+  // K/V) run on one XCD; heavy (late) query blocks first inside each head
+  const int nwork = a.B * a.H * a.nqb;
+  const int pid = xcd_remap(blockIdx.x, nwork);
+  const int bh = pid / a.nqb;
+  const int qb = a.nqb - 1 - pid % a.nqb;
+  const int b = bh / a.H, i = bh % a.H;
+  const int q0 = qb * FWD_BQ;
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  const int qw0 = q0 + wave * 32;
+  const int my_q = qw0 + col;
+  const int64_t nq = (int64_t)b * a.T + min(my_q, a.T - 1);
+
+  // this lane's query, as MFMA B operand fragments (d = 16 kk + 8 half + 0..7)
+  bf16x8 qf[NKK];
+  {
+    const bf16_t* qp = a.Q + nq * a.q_tok + (int64_t)i * a.q_head + 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
+  }
+
+  f32x16 acc_o[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc_o[c][e] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int kend = min(a.T, q0 + FWD_BQ);
+  const int nkb = (kend + BKV - 1) / BKV;
+  Stage st;
+  st.init(a, b, i);
+  st.load(a, 0);
+  st.store(smem, smem + KS);
+  __syncthreads();
+
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int cur = kb & 1;
+    const int j0 = kb * BKV;
+    if (kb + 1 < nkb) st.load(a, j0 + BKV);
+    const bf16_t* ks = smem + cur * (KS + VS);
+    const bf16_t* vs = ks + KS;
+    if (j0 <= qw0 + 31) {  // wave-uniform: some key of this tile is visible to the wave
+      f32x16 s[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) s[t][e] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              *(const bf16x8*)(ks + (32 * t + col) * LDK + 16 * kk + 8 * half), qf[kk], s[t], 0, 0, 0);
+      // causal mask on diagonal tiles; tile max of this lane's query (raw logits)
+      const bool diag = j0 + BKV - 1 > qw0;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          if (diag) {
+            const int key = j0 + 32 * t + 8 * (e >> 2) + 4 * half + (e & 3);
+            if (key > my_q) s[t][e] = -INFINITY;
+          }
+          mx = fmaxf(mx, s[t][e]);
+        }
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.sl2;
+      // lazy rescale: the reference max moves only when a tile max exceeds it by more
+      // than RESCALE_SLACK (so P <= 2^RESCALE_SLACK); wave-uniform branch
+      if (__ballot(mx > m_run + RESCALE_SLACK) != 0) {
+        const float m_new = fmaxf(m_run, mx);
+        const float corr = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
+        m_run = m_new;
+        l_run *= corr;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc_o[c][e] *= corr;
+      }
+      const float m_use = m_run == -INFINITY ? 0.f : m_run;
+      // P = 2^(s sl2 - m), packed to bf16 as the B operand of O^T = V^T P^T
+      bf16x8 pf[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        u32x4 w;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[u >> 1][8 * (u & 1) + 2 * q], a.sl2, -m_use));
+          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[u >> 1][8 * (u & 1) + 2 * q + 1], a.sl2, -m_use));
+          l_run += p0 + p1;
+          w[q] = pack2bf(p0, p1);
+        }
+        pf[u] = __builtin_bit_cast(bf16x8, w);
+      }
+      // O^T += V^T P^T; K-step u covers keys 32(u/2) + 16(u%2) + {4h..4h+3, 8+4h..8+4h+3}
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int klo = 32 * (u >> 1) + 16 * (u & 1) + 4 * half;
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+          acc_o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(vs, LDV, 32 * c, klo, klo + 8),
+                                                             pf[u], acc_o[c], 0, 0, 0);
+      }
+    }
+    if (kb + 1 < nkb) {
+      bf16_t* nxt = smem + (cur ^ 1) * (KS + VS);
+      st.store(nxt, nxt + KS);
+    }
+    __syncthreads();
+  }
+
+  // normalise and store: lane holds query my_q, d = 32c + 8(e/4) + 4 half + e%4
+  const float l = l_run + __shfl_xor(l_run, 32, 64);
+  if (my_q >= a.T) return;
+  const float inv = 1.f / l;
+  bf16_t* op = a.O + ((int64_t)b * a.T + my_q) * a.o_tok + (int64_t)i * DV + 4 * half;
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      u32x2 w = {pack2bf(acc_o[c][4 * g] * inv, acc_o[c][4 * g + 1] * inv),
+                 pack2bf(acc_o[c][4 * g + 2] * inv, acc_o[c][4 * g + 3] * inv)};
+      *(u32x2*)(op + 32 * c + 8 * g) = w;
+    }
+  if (LSE && half == 0) a.lse[((int64_t)b * a.T + my_q) * a.H + i] = (m_run + __log2f(l)) * LN2;
+}
+
+template <int DQK, int DV>
+hipError_t fwd_launch(const Attn& at, hipStream_t s) {
+  AttnDev d = to_dev(at);
+  d.nqb = (at.T + FWD_BQ - 1) / FWD_BQ;
+  const int nwork = d.B * d.H * d.nqb;
+  if (at.lse)
+    attn_fwd_mfma_kernel<DQK, DV, true><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
+  else
+    attn_fwd_mfma_kernel<DQK, DV, false><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
+  return hipGetLastError();
+}
+
+
+}  // namespace
+
+bool supported(int dqk, int dv) {
+#define X(a_, b_) if (dqk == a_ && dv == b_) return true;
+  MLA_MFMA_SHAPES(X)
+#undef X
+  return false;
+}
+
+}  // namespace attn
+
+bool attn_mfma_supported(int dqk, int dv) { return attn::supported(dqk, dv); }
+
+hipError_t attn_fwd_mfma(const Attn& a, hipStream_t s) {
+#define X(a_, b_) if (a.dqk == a_ && a.dv == b_) return attn::fwd_launch<a_, b_>(a, s);
+  MLA_MFMA_SHAPES(X)
+#undef X
+  return hipErrorInvalidValue;
+}
+
+}  // namespace mla

@@ -36,42 +36,59 @@ hipError_t rope_tables(const float* inv_freq, int G, int T, int npairs, float* c
   return hipGetLastError();
 }
 
-template <typename T, bool INV>
+template <typename T> struct Vec4;
+template <> struct Vec4<float> {
+  static __device__ __forceinline__ f32x4 load(const float* p) { return *(const f32x4*)p; }
+  static __device__ __forceinline__ void store(float* p, f32x4 v) { *(f32x4*)p = v; }
+};
+template <> struct Vec4<bf16_t> {
+  static __device__ __forceinline__ f32x4 load(const bf16_t* p) {
+    u32x2 w = *(const u32x2*)p;
+    return f32x4{__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
+                 __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u)};
+  }
+  static __device__ __forceinline__ void store(bf16_t* p, f32x4 v) {
+    *(u32x2*)p = u32x2{pack2bf(v[0], v[1]), pack2bf(v[2], v[3])};
+  }
+};
+
+// in-place rotation of pairs (p, p + np), 4 consecutive pairs per thread
+template <typename T>
 __global__ void rope_apply_kernel(T* __restrict__ x, int N, int Tseq, int nheads, int64_t tok,
                                   int64_t head, int off, int np, int div,
                                   const float* __restrict__ cos_t,
                                   const float* __restrict__ sin_t) {
+  const int nq = np / 4;
   int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  int64_t total = (int64_t)N * nheads * np;
+  int64_t total = (int64_t)N * nheads * nq;
   if (idx >= total) return;
-  int p = (int)(idx % np);
-  int h = (int)((idx / np) % nheads);
-  int64_t n = idx / ((int64_t)np * nheads);
+  int p = (int)(idx % nq) * 4;
+  int h = (int)((idx / nq) % nheads);
+  int64_t n = idx / ((int64_t)nq * nheads);
   int t = (int)(n % Tseq);
   int g = h / div;
-  float c = cos_t[((int64_t)g * Tseq + t) * np + p];
-  float sn = sin_t[((int64_t)g * Tseq + t) * np + p];
-  if (INV) sn = -sn;
+  const int64_t ti = ((int64_t)g * Tseq + t) * np + p;
+  f32x4 c = *(const f32x4*)(cos_t + ti), sn = *(const f32x4*)(sin_t + ti);
   T* base = x + n * tok + (int64_t)h * head + off;
-  float x1 = ld(base + p), x2 = ld(base + p + np);
-  st(base + p, x1 * c - x2 * sn);
-  st(base + p + np, x1 * sn + x2 * c);
+  f32x4 x1 = Vec4<T>::load(base + p), x2 = Vec4<T>::load(base + p + np);
+  Vec4<T>::store(base + p, x1 * c - x2 * sn);
+  Vec4<T>::store(base + p + np, x1 * sn + x2 * c);
 }
 
 hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, int64_t head,
                       int off, int npairs, int div, const float* cos_t, const float* sin_t,
                       hipStream_t s) {
-  int64_t total = (int64_t)N * nheads * npairs;
+  int64_t total = (int64_t)N * nheads * (npairs / 4);
   if (total == 0) return hipSuccess;
   unsigned grid = (unsigned)((total + 255) / 256);
   prof_begin(KC_ELEM, s);
   if (t == DT_BF16)
-    rope_apply_kernel<bf16_t, false><<<grid, 256, 0, s>>>((bf16_t*)x, N, T, nheads, tok, head,
-                                                          off, npairs, div, cos_t, sin_t);
+    rope_apply_kernel<bf16_t><<<grid, 256, 0, s>>>((bf16_t*)x, N, T, nheads, tok, head, off,
+                                                   npairs, div, cos_t, sin_t);
   else
-    rope_apply_kernel<float, false><<<grid, 256, 0, s>>>((float*)x, N, T, nheads, tok, head,
-                                                         off, npairs, div, cos_t, sin_t);
-  prof_end(KC_ELEM, s, 0.0, (double)total * 4.0 * dsize(t));
+    rope_apply_kernel<float><<<grid, 256, 0, s>>>((float*)x, N, T, nheads, tok, head, off,
+                                                  npairs, div, cos_t, sin_t);
+  prof_end(KC_ELEM, s, 0.0, (double)N * nheads * npairs * 4.0 * dsize(t));
   return hipGetLastError();
 }
 
@@ -83,9 +100,10 @@ __global__ void dq_finish_kernel(const float* __restrict__ acc, T* __restrict__ 
                                  int Tseq, int H, int dqk, int dnope, int rdiv,
                                  const float* __restrict__ cos_t,
                                  const float* __restrict__ sin_t) {
-  // one thread per (n, i, e) with e < dnope + np: e < dnope copies, else pair e - dnope
-  int np = (dqk - dnope) / 2;
-  int per_head = dnope + np;
+  // one thread per 4 elements: chunks [0, dnope/4) copy, chunks [dnope/4, +np/4) rotate
+  // 4 pairs (p .. p+3, p+np .. p+np+3) back with R^T
+  const int np = (dqk - dnope) / 2;
+  const int per_head = dnope / 4 + np / 4;
   int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t total = (int64_t)N * H * per_head;
   if (idx >= total) return;
@@ -94,24 +112,24 @@ __global__ void dq_finish_kernel(const float* __restrict__ acc, T* __restrict__ 
   int64_t n = idx / ((int64_t)per_head * H);
   const float* a = acc + (n * H + i) * dqk;
   T* o = dq + (n * H + i) * dqk;
-  if (e < dnope) {
-    st(o + e, a[e]);
+  if (e < dnope / 4) {
+    Vec4<T>::store(o + 4 * e, *(const f32x4*)(a + 4 * e));
     return;
   }
-  int p = e - dnope;
+  int p = 4 * (e - dnope / 4);
   int t = (int)(n % Tseq);
   int g = i / rdiv;
-  float c = cos_t[((int64_t)g * Tseq + t) * np + p];
-  float sn = sin_t[((int64_t)g * Tseq + t) * np + p];
-  float x1 = a[dnope + p], x2 = a[dnope + p + np];
-  st(o + dnope + p, x1 * c + x2 * sn);
-  st(o + dnope + p + np, -x1 * sn + x2 * c);
+  const int64_t ti = ((int64_t)g * Tseq + t) * np + p;
+  f32x4 c = *(const f32x4*)(cos_t + ti), sn = *(const f32x4*)(sin_t + ti);
+  f32x4 x1 = *(const f32x4*)(a + dnope + p), x2 = *(const f32x4*)(a + dnope + p + np);
+  Vec4<T>::store(o + dnope + p, x1 * c + x2 * sn);
+  Vec4<T>::store(o + dnope + p + np, x2 * c - x1 * sn);
 }
 
 hipError_t dq_finish(const float* dq_acc, void* dq, DType t, int N, int T, int H, int dqk,
                      int dnope, int rdiv, const float* cos_t, const float* sin_t,
                      hipStream_t s) {
-  int64_t total = (int64_t)N * H * (dnope + (dqk - dnope) / 2);
+  int64_t total = (int64_t)N * H * (dnope / 4 + (dqk - dnope) / 8);
   if (total == 0) return hipSuccess;
   unsigned grid = (unsigned)((total + 255) / 256);
   prof_begin(KC_ELEM, s);
@@ -257,14 +275,29 @@ __global__ __launch_bounds__(LOSS_THREADS) void loss_main_kernel(
   }
 }
 
-__global__ void loss_final_kernel(const LossScratch* __restrict__ ws, int nblocks, int D,
-                                  float* __restrict__ loss) {
-  if (threadIdx.x != 0) return;
+__global__ __launch_bounds__(256) void loss_final_kernel(const LossScratch* __restrict__ ws,
+                                                         int nblocks, int D,
+                                                         float* __restrict__ loss) {
+  // thread t sums partials t, t+256, ... in order; then a fixed tree over the 256 threads
+  __shared__ double red[2][256];
   double s = 0.0, r = 0.0;
-  for (int i = 0; i < nblocks; ++i) {
+  for (int i = threadIdx.x; i < nblocks; i += 256) {
     s += ws->part[2 * i];
     r += ws->part[2 * i + 1];
   }
+  red[0][threadIdx.x] = s;
+  red[1][threadIdx.x] = r;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) {
+      red[0][threadIdx.x] += red[0][threadIdx.x + w];
+      red[1][threadIdx.x] += red[1][threadIdx.x + w];
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x != 0) return;
+  s = red[0][0];
+  r = red[1][0];
   double den = (double)D * ws->count;
   if (den == 0.0) {
     loss[0] = 0.f;
@@ -286,7 +319,7 @@ hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, i
     loss_main_kernel<bf16_t><<<blocks, LOSS_THREADS, 0, s>>>(A_s, A_t, mask, N, D, (bf16_t*)dA, ws);
   else
     loss_main_kernel<float><<<blocks, LOSS_THREADS, 0, s>>>(A_s, A_t, mask, N, D, (float*)dA, ws);
-  loss_final_kernel<<<1, 64, 0, s>>>(ws, blocks, D, loss);
+  loss_final_kernel<<<1, 256, 0, s>>>(ws, blocks, D, loss);
   double bytes = (double)N * D * (8.0 + (dA ? dsize(t) : 0)) + (mask ? N : 0);
   prof_end(KC_LOSS, s, 0.0, bytes);
   return hipGetLastError();

@@ -172,18 +172,20 @@ __global__ __launch_bounds__(64) void attn_fwd_simt_kernel(Attn a) {
 template <typename T>
 __global__ void attn_delta_kernel(const void* dO_, const void* O_, int64_t o_tok, int64_t N,
                                   int H, int dv, float* __restrict__ delta) {
-  // one wavefront per (n, i)
-  int64_t row = (int64_t)blockIdx.x * (blockDim.x / 64) + threadIdx.x / 64;
-  int lane = threadIdx.x % 64;
-  if (row >= N * H) return;
-  int64_t n = row / H;
-  int i = (int)(row % H);
+  // 16 lanes per (n, i) row, each lane a strided set of elements; reduce within 16 lanes
+  int64_t row = (int64_t)blockIdx.x * (blockDim.x / 16) + threadIdx.x / 16;
+  int sub = threadIdx.x % 16;
+  bool ok = row < N * H;
+  int64_t n = ok ? row / H : 0;
+  int i = ok ? (int)(row % H) : 0;
   const T* dO = (const T*)dO_ + n * (int64_t)H * dv + (int64_t)i * dv;
   const T* O = (const T*)O_ + n * o_tok + (int64_t)i * dv;
   float s = 0.f;
-  for (int d = lane; d < dv; d += 64) s += ld(dO + d) * ld(O + d);
-  s = warp_sum(s);
-  if (lane == 0) delta[row] = s;
+  if (ok)
+    for (int d = sub; d < dv; d += 16) s += ld(dO + d) * ld(O + d);
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) s += __shfl_xor(s, o, 64);
+  if (ok && sub == 0) delta[row] = s;
 }
 
 template <typename T, int DQK, int DV>
@@ -309,7 +311,7 @@ template <typename T>
 hipError_t delta_launch(const AttnBwd& w, hipStream_t s) {
   const Attn& a = w.f;
   int64_t rows = (int64_t)a.B * a.T * a.H;
-  attn_delta_kernel<T><<<(unsigned)((rows + 3) / 4), 256, 0, s>>>(w.dO, a.O, a.o_tok,
+  attn_delta_kernel<T><<<(unsigned)((rows + 15) / 16), 256, 0, s>>>(w.dO, a.O, a.o_tok,
                                                                   (int64_t)a.B * a.T, a.H, a.dv,
                                                                   w.delta);
   return hipGetLastError();
