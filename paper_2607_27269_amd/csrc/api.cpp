@@ -384,7 +384,7 @@ int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* 
 
   // dO = dA W_O  (W_O frozen: no dW_O)
   HIP_TRY(gemm(mk(N, H * dv, D, dA, D, true, Wo, (int64_t)H * dv, false, dO, (int64_t)H * dv, t, t), nullptr, 0, s));
-  // softmax-attention backward -> dq (rotated), dk^nope, dv, dk^PE partials
+  // softmax-attention backward -> dq (rotary block rotated back), dk^nope, dv, dk^PE partials
   AttnBwd ab;
   Attn& a = ab.f;
   a.B = (int)d.B; a.T = T; a.H = H; a.dqk = dqk; a.dnope = dn; a.dv = dv;
@@ -394,14 +394,13 @@ int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* 
   a.V = HeadView{v, (int64_t)Gkv * dv, dv, H / Gkv};
   a.O = o; a.o_tok = (int64_t)H * dv; a.lse = lse; a.scale = cfg->softmax_scale; a.t = t;
   ab.dO = dO; ab.delta = delta; ab.dq_acc = dqacc;
+  ab.dq = dq; ab.rdiv = H / Gr; ab.cos_t = cs; ab.sin_t = sn;
   ab.dKa = dkv; ab.dka_tok = ld_dkv;
   ab.dV = dkv + (size_t)Gkv * dn * ts; ab.dv_tok = ld_dkv;
   ab.dkb_part = dkpe; ab.n_ka_groups = Gkv;
   HIP_TRY(attn_bwd(ab, s));
 
   if (need_q) {
-    // dq^rope <- R^T dq^rope
-    HIP_TRY(dq_finish(dqacc, dq, t, N, T, H, dqk, dn, H / Gr, cs, sn, s));
     const void* qin = rq > 0 ? (const void*)cq : h;
     const int qk = rq > 0 ? rq : D;
     // dW_UQ = dq^T c^Q

@@ -1,4 +1,23 @@
 // Causal softmax attention backward (gradients of Eq. 2-4) on gfx950 matrix cores.
+//
+//   P = exp(S - lse) (recomputed from the forward's log-sum-exp), dV = P^T dO,
+//   dP = dO V^T, dS = P (dP - delta) with delta = rowsum(dO . O),
+//   dQ = scale dS K, dK = scale dS^T Q.
+//
+// Two kernels, each sized so that its accumulators stay in registers:
+//
+// * dK/dV: a workgroup owns 128 keys of one (sequence, KV group); each of its 4
+//   wavefronts owns 32 keys (K staged once in LDS, V held as MFMA B-operand fragments) and walks
+//   every head of the group and every 64-query block at or after its keys.  S = Q K^T and
+//   dP = dO V^T put the key in the MFMA column, so the accumulators of P and dS are
+//   directly the B operands of dV^T += dO^T P and dK^T += Q^T dS; dO^T and Q^T come from
+//   the natural [query][dim] LDS tiles through gfx950's transposing LDS read.  The rotary
+//   part of dK is summed over the group's heads and left as an fp32 partial per group
+//   (the positional key may be shared by several groups).
+// * dQ: laid out like the forward (a lane owns one query; 4 wavefronts x 32 queries):
+//   S^T = K Q^T, dP^T = V dO^T, and dQ^T += K^T dS^T with K^T read transposed from the
+//   [key][dim] tile; dQ is written once in bf16 (no fp32 buffer, no atomics), then its
+//   rotary block is rotated back with R^T.
 #include "attn_common.h"
 #include "mfma.h"
 #include "simt.h"
@@ -7,26 +26,18 @@ namespace mla {
 namespace attn {
 namespace {
 
-// ---------------------------------------------------------------------------------------
-// Backward.  A workgroup owns 128 keys of one (sequence, Ka group) and walks every head of
-// the group and every query block of 64 at or after its keys.  Each wavefront owns 32
-// keys: S = Q K^T and dP = dO V^T are computed with the key as the MFMA column, so the
-// accumulator layout of P and dS is directly the B operand of dV^T += dO^T P and
-// dK^T += Q^T dS (gradients of keys/values accumulate in registers over all heads and
-// query blocks).  dO^T and Q^T operands are read from the natural [query][dim] LDS tiles
-// with gfx950's transposing LDS read.  dS goes through LDS once ([key][query]) so that
-// dQ = dS K for the 64 x d_qk query tile can be split across the four wavefronts; the
-// per-workgroup partial dQ is added to an fp32 accumulator with hardware float atomics.
-// P = 2^(S log2e scale - lse log2e) reuses the forward's log-sum-exp.
-// ---------------------------------------------------------------------------------------
-constexpr int BKB = 128;  // keys per workgroup
-constexpr int BQB = 64;   // queries per iteration
+constexpr int BKB = 128;  // keys per dK/dV workgroup
+constexpr int BQB = 64;   // queries per dK/dV step
+constexpr int DQ_BQ = 128;  // queries per dQ workgroup
 
 struct BwdDev {
   AttnDev f;
   const bf16_t* dO;      // [N][H*dv]
   const float* delta;    // [N][H]
-  float* dq_acc;         // [N][H][dqk]
+  bf16_t* dq;            // [N][H*dqk]
+  int rdiv;
+  const float* cos_t;
+  const float* sin_t;
   bf16_t* dKa; int64_t dka_tok;
   bf16_t* dV; int64_t dv_tok;
   float* dkb_part;       // [G][N][dqk - dnope]
@@ -34,24 +45,32 @@ struct BwdDev {
   float scale;
 };
 
+// ---------------------------------------------------------------------------------------
+// dK / dV
+// ---------------------------------------------------------------------------------------
 template <int DQK, int DV>
-struct BwdStage {
+struct QStage {
+  static constexpr int LDQ = ld_of(DQK);
+  static constexpr int LDO = ld_of(DV);
   static constexpr int QCH = BQB * (DQK / 8);
   static constexpr int QPER = (QCH + 255) / 256;
   static constexpr int OCH = BQB * (DV / 8);
   static constexpr int OPER = (OCH + 255) / 256;
+  static constexpr int QS = BQB * LDQ, OS = BQB * LDO;
+  static constexpr int BUF = QS + OS + 2 * BQB * 2;  // bf16 elements incl. lse2, delta
   u32x4 q[QPER];
   u32x4 o[OPER];
   float stat;
 
   __device__ __forceinline__ void load(const BwdDev& w, int b, int i, int q0) {
     const AttnDev& a = w.f;
+    const bool full = q0 + BQB <= a.T;
 #pragma unroll
     for (int it = 0; it < QPER; ++it) {
       const int c = threadIdx.x + it * 256;
       const int r = c / (DQK / 8), dc = (c % (DQK / 8)) * 8;
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (c < QCH && q0 + r < a.T)
+      if ((QCH % 256 == 0 || c < QCH) && (full || q0 + r < a.T))
         v = *(const u32x4*)(a.Q + ((int64_t)b * a.T + q0 + r) * a.q_tok + (int64_t)i * a.q_head + dc);
       q[it] = v;
     }
@@ -60,47 +79,43 @@ struct BwdStage {
       const int c = threadIdx.x + it * 256;
       const int r = c / (DV / 8), dc = (c % (DV / 8)) * 8;
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (c < OCH && q0 + r < a.T)
+      if ((OCH % 256 == 0 || c < OCH) && (full || q0 + r < a.T))
         v = *(const u32x4*)(w.dO + ((int64_t)b * a.T + q0 + r) * ((int64_t)a.H * DV) + (int64_t)i * DV + dc);
       o[it] = v;
     }
-    const int t = threadIdx.x & 63;
-    const int q = q0 + t;
+    const int q = q0 + (threadIdx.x & 63);
     if (threadIdx.x < 64)
       stat = q < a.T ? a.lse[((int64_t)b * a.T + q) * a.H + i] * LOG2E : INFINITY;
     else if (threadIdx.x < 128)
       stat = q < a.T ? w.delta[((int64_t)b * a.T + q) * a.H + i] : 0.f;
   }
 
-  __device__ __forceinline__ void store(bf16_t* Qs, bf16_t* dOs, float* st) const {
+  __device__ __forceinline__ void store(bf16_t* buf) const {
+    bf16_t* Qs = buf;
+    bf16_t* dOs = buf + QS;
+    float* st = (float*)(buf + QS + OS);
 #pragma unroll
     for (int it = 0; it < QPER; ++it) {
       const int c = threadIdx.x + it * 256;
-      if (c < QCH) *(u32x4*)(Qs + (c / (DQK / 8)) * (DQK + KPAD) + (c % (DQK / 8)) * 8) = q[it];
+      if (QCH % 256 == 0 || c < QCH) *(u32x4*)(Qs + (c / (DQK / 8)) * LDQ + (c % (DQK / 8)) * 8) = q[it];
     }
 #pragma unroll
     for (int it = 0; it < OPER; ++it) {
       const int c = threadIdx.x + it * 256;
-      if (c < OCH) *(u32x4*)(dOs + (c / (DV / 8)) * (DV + KPAD) + (c % (DV / 8)) * 8) = o[it];
+      if (OCH % 256 == 0 || c < OCH) *(u32x4*)(dOs + (c / (DV / 8)) * LDO + (c % (DV / 8)) * 8) = o[it];
     }
     if (threadIdx.x < 128) st[threadIdx.x] = stat;
   }
 };
 
 template <int DQK, int DV>
-__global__ __launch_bounds__(256) void attn_bwd_mfma_kernel(BwdDev w) {
-  const AttnDev& a = w.f;
-  constexpr int LDK = DQK + KPAD, LDO = DV + KPAD, LDT = BQB + 16;
+__global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
+  using Stage = QStage<DQK, DV>;
+  constexpr int LDQ = Stage::LDQ, LDO = Stage::LDO;
   constexpr int NKK = DQK / 16, NVK = DV / 16;
   constexpr int NCK = DQK / 32, NCV = DV / 32;
-  constexpr int SM = BKB * LDK + BQB * LDK + BQB * LDO + BKB * LDT;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[SM + 2 * BQB * 2];
-  bf16_t* Ks = smem;
-  bf16_t* Qs = Ks + BKB * LDK;
-  bf16_t* dOs = Qs + BQB * LDK;
-  bf16_t* dSt = dOs + BQB * LDO;
-  float* st_lse = (float*)(dSt + BKB * LDT);
-  float* st_dl = st_lse + BQB;
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * Stage::BUF + BKB * ld_of(DQK)];
+  const AttnDev& a = w.f;
 
   const int nbg = a.B * w.G;
   const int kb = blockIdx.x / nbg;  // early key blocks (the most query blocks) first
@@ -114,7 +129,9 @@ __global__ __launch_bounds__(256) void attn_bwd_mfma_kernel(BwdDev w) {
   const int my_key = kw0 + col;
   const int i0 = g * hpg;
 
-  // keys of this block into LDS ([key][d]); this wave's values as B operand fragments
+  // keys of this workgroup in LDS ([key][d], read as B operand fragments each step); this
+  // lane's value as B operand fragments in registers (col = key, k = 16 kk + 8 half + 0..7)
+  bf16_t* Ks = smem + 2 * Stage::BUF;
   {
     constexpr int KCH = BKB * (DQK / 8);
     const int ga = i0 / a.ka_div, gb = i0 / a.kb_div;
@@ -124,19 +141,20 @@ __global__ __launch_bounds__(256) void attn_bwd_mfma_kernel(BwdDev w) {
       u32x4 val = {0u, 0u, 0u, 0u};
       if (j < a.T) {
         const int64_t n = (int64_t)b * a.T + j;
-        const bf16_t* src = dc < a.dnope
-                                ? a.Ka + n * a.ka_tok + (int64_t)ga * a.ka_head + dc
-                                : a.Kb + n * a.kb_tok + (int64_t)gb * a.kb_head + (dc - a.dnope);
+        const bf16_t* src = dc < a.dnope ? a.Ka + n * a.ka_tok + (int64_t)ga * a.ka_head + dc
+                                         : a.Kb + n * a.kb_tok + (int64_t)gb * a.kb_head + (dc - a.dnope);
         val = *(const u32x4*)src;
       }
-      *(u32x4*)(Ks + key * LDK + dc) = val;
+      *(u32x4*)(Ks + key * LDQ + dc) = val;
     }
   }
+  const bf16_t* krow = Ks + (32 * wave + col) * LDQ + 8 * half;
   bf16x8 vf[NVK];
   {
-    const int gv = i0 / a.v_div;
     const int jj = min(my_key, a.T - 1);
-    const bf16_t* vp = a.V + ((int64_t)b * a.T + jj) * a.v_tok + (int64_t)gv * a.v_head + 8 * half;
+    const int64_t n = (int64_t)b * a.T + jj;
+    const int gv = i0 / a.v_div;
+    const bf16_t* vp = a.V + n * a.v_tok + (int64_t)gv * a.v_head + 8 * half;
 #pragma unroll
     for (int kk = 0; kk < NVK; ++kk) {
       u32x4 v = *(const u32x4*)(vp + 16 * kk);
@@ -159,43 +177,45 @@ __global__ __launch_bounds__(256) void attn_bwd_mfma_kernel(BwdDev w) {
   const int nqb = (a.T + BQB - 1) / BQB;
   const int nper = nqb - qb0;
   const int niter = hpg * nper;
-  BwdStage<DQK, DV> stg;
+  Stage stg;
   if (niter > 0) {
     stg.load(w, b, i0, qb0 * BQB);
-    stg.store(Qs, dOs, st_lse);
+    stg.store(smem);
   }
   __syncthreads();
 
   for (int it = 0; it < niter; ++it) {
-    const int i = i0 + it / nper;
     const int q0 = (qb0 + it % nper) * BQB;
+    const bf16_t* Qs = smem + (it & 1) * Stage::BUF;
+    const bf16_t* dOs = Qs + Stage::QS;
+    const float* st_lse = (const float*)(dOs + Stage::OS);
+    const float* st_dl = st_lse + BQB;
     if (it + 1 < niter) stg.load(w, b, i0 + (it + 1) / nper, (qb0 + (it + 1) % nper) * BQB);
 
-    const bool active = kw0 <= min(q0 + BQB - 1, a.T - 1);
-    bf16_t* dst_row = dSt + (32 * wave + col) * LDT + 4 * half;
-    if (active) {
+    if (kw0 <= min(q0 + BQB - 1, a.T - 1)) {  // wave-uniform: some pair is visible
       f32x16 sp[2], dp[2];
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
+      for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
         for (int e = 0; e < 16; ++e) { sp[qt][e] = 0.f; dp[qt][e] = 0.f; }
-        const bf16_t* qrow = Qs + (32 * qt + col) * LDK + 8 * half;
-        const bf16_t* krow = Ks + (32 * wave + col) * LDK + 8 * half;
 #pragma unroll
-        for (int kk = 0; kk < NKK; ++kk)
-          sp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(qrow + 16 * kk),
-                                                          *(const bf16x8*)(krow + 16 * kk), sp[qt], 0, 0, 0);
-        const bf16_t* orow = dOs + (32 * qt + col) * LDO + 8 * half;
+      for (int kk = 0; kk < NKK; ++kk) {
+        const bf16x8 kf = *(const bf16x8*)(krow + 16 * kk);
 #pragma unroll
-        for (int kk = 0; kk < NVK; ++kk)
-          dp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(orow + 16 * kk), vf[kk],
-                                                          dp[qt], 0, 0, 0);
+        for (int qt = 0; qt < 2; ++qt)
+          sp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              *(const bf16x8*)(Qs + (32 * qt + col) * LDQ + 16 * kk + 8 * half), kf, sp[qt], 0, 0, 0);
       }
+#pragma unroll
+      for (int kk = 0; kk < NVK; ++kk)
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+          dp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              *(const bf16x8*)(dOs + (32 * qt + col) * LDO + 16 * kk + 8 * half), vf[kk], dp[qt], 0, 0, 0);
       // P = 2^(S sl2 - lse2), dS = P (dP - delta); rows q = q0 + 32 qt + 8(e/4) + 4 half + e%4
       const bool diag = kw0 + 31 > q0;
-      bf16x8 pf[4], sf[4];
 #pragma unroll
-      for (int qt = 0; qt < 2; ++qt) {
+      for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
         for (int e4 = 0; e4 < 4; ++e4) {
           const int qr = 32 * qt + 8 * e4 + 4 * half;
@@ -204,17 +224,13 @@ __global__ __launch_bounds__(256) void attn_bwd_mfma_kernel(BwdDev w) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int e = 4 * e4 + r;
-            float p = __builtin_amdgcn_exp2f(sp[qt][e] * a.sl2 - l2[r]);
+            float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sp[qt][e], a.sl2, -l2[r]));
             if (diag && my_key > q0 + qr + r) p = 0.f;
             sp[qt][e] = p;
             dp[qt][e] = p * (dp[qt][e] - dl[r]);
           }
-          // dS^T to LDS: row = this lane's key, 4 consecutive queries
-          u32x2 wv = {pack2bf(dp[qt][4 * e4], dp[qt][4 * e4 + 1]),
-                      pack2bf(dp[qt][4 * e4 + 2], dp[qt][4 * e4 + 3])};
-          *(u32x2*)(dst_row + 32 * qt + 8 * e4) = wv;
         }
-      }
+      // dV^T += dO^T P,  dK^T += Q^T dS   (K-step u: queries 32(u/2) + 16(u%2) + {4h.., 8+4h..})
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
         u32x4 wp, wd;
@@ -223,52 +239,19 @@ __global__ __launch_bounds__(256) void attn_bwd_mfma_kernel(BwdDev w) {
           wp[q] = pack2bf(sp[u >> 1][8 * (u & 1) + 2 * q], sp[u >> 1][8 * (u & 1) + 2 * q + 1]);
           wd[q] = pack2bf(dp[u >> 1][8 * (u & 1) + 2 * q], dp[u >> 1][8 * (u & 1) + 2 * q + 1]);
         }
-        pf[u] = __builtin_bit_cast(bf16x8, wp);
-        sf[u] = __builtin_bit_cast(bf16x8, wd);
-      }
-      // dV^T += dO^T P,  dK^T += Q^T dS   (K-step u: queries 32(u/2) + 16(u%2) + {4h.., 8+4h..})
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
+        const bf16x8 pf = __builtin_bit_cast(bf16x8, wp), sf = __builtin_bit_cast(bf16x8, wd);
         const int klo = 32 * (u >> 1) + 16 * (u & 1) + 4 * half;
 #pragma unroll
         for (int c = 0; c < NCV; ++c)
           dv[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(dOs, LDO, 32 * c, klo, klo + 8),
-                                                         pf[u], dv[c], 0, 0, 0);
+                                                         pf, dv[c], 0, 0, 0);
 #pragma unroll
         for (int c = 0; c < NCK; ++c)
-          dk[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(Qs, LDK, 32 * c, klo, klo + 8),
-                                                         sf[u], dk[c], 0, 0, 0);
-      }
-    } else {
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) *(u32x2*)(dst_row + 32 * qt + 8 * e4) = u32x2{0u, 0u};
-    }
-    __syncthreads();
-    if (it + 1 < niter) stg.store(Qs, dOs, st_lse);
-
-    // dQ (64 x DQK) = dS (64 x 128 keys) K (128 x DQK): 2 * DQK/32 tiles over 4 wavefronts
-    constexpr int NT = 2 * NCK;
-    for (int tau = wave; tau < NT; tau += 4) {
-      const int qt = tau / NCK, dt = tau % NCK;
-      f32x16 acc;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) acc[e] = 0.f;
-#pragma unroll
-      for (int ks = 0; ks < BKB / 16; ++ks) {
-        const int klo = 16 * ks + 8 * half;
-        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(dSt, LDT, 32 * qt, klo, klo + 4),
-                                                      lds_operand_tr(Ks, LDK, 32 * dt, klo, klo + 4),
-                                                      acc, 0, 0, 0);
-      }
-      float* dqp = w.dq_acc + (int64_t)i * DQK + 32 * dt + col;
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int q = q0 + 32 * qt + 8 * (e >> 2) + 4 * half + (e & 3);
-        if (q < a.T) unsafeAtomicAdd(dqp + ((int64_t)b * a.T + q) * ((int64_t)a.H * DQK), acc[e] * w.scale);
+          dk[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(Qs, LDQ, 32 * c, klo, klo + 8),
+                                                         sf, dk[c], 0, 0, 0);
       }
     }
+    if (it + 1 < niter) stg.store(smem + ((it + 1) & 1) * Stage::BUF);
     __syncthreads();
   }
 
@@ -284,26 +267,144 @@ __global__ __launch_bounds__(256) void attn_bwd_mfma_kernel(BwdDev w) {
       u32x2 wv = {pack2bf(dv[c][4 * e4], dv[c][4 * e4 + 1]), pack2bf(dv[c][4 * e4 + 2], dv[c][4 * e4 + 3])};
       *(u32x2*)(w.dV + n * w.dv_tok + (int64_t)g * DV + d) = wv;
     }
+  const float sc = w.scale;
 #pragma unroll
   for (int c = 0; c < NCK; ++c)
 #pragma unroll
     for (int e4 = 0; e4 < 4; ++e4) {
       const int d = 32 * c + 8 * e4 + 4 * half;
-      const float s = w.scale;
       if (d < a.dnope) {
-        u32x2 wv = {pack2bf(s * dk[c][4 * e4], s * dk[c][4 * e4 + 1]),
-                    pack2bf(s * dk[c][4 * e4 + 2], s * dk[c][4 * e4 + 3])};
+        u32x2 wv = {pack2bf(sc * dk[c][4 * e4], sc * dk[c][4 * e4 + 1]),
+                    pack2bf(sc * dk[c][4 * e4 + 2], sc * dk[c][4 * e4 + 3])};
         *(u32x2*)(w.dKa + n * w.dka_tok + (int64_t)g * a.dnope + d) = wv;
       } else {
-        f32x4 v = {s * dk[c][4 * e4], s * dk[c][4 * e4 + 1], s * dk[c][4 * e4 + 2], s * dk[c][4 * e4 + 3]};
+        f32x4 v = {sc * dk[c][4 * e4], sc * dk[c][4 * e4 + 1], sc * dk[c][4 * e4 + 2], sc * dk[c][4 * e4 + 3]};
         *(f32x4*)(w.dkb_part + ((int64_t)g * ((int64_t)a.B * a.T) + n) * dr + (d - a.dnope)) = v;
       }
     }
 }
 
-__global__ void zero_f32_kernel(float* __restrict__ p, int64_t n4) {
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n4) ((f32x4*)p)[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+// ---------------------------------------------------------------------------------------
+// dQ
+// ---------------------------------------------------------------------------------------
+template <int DQK, int DV>
+__global__ __launch_bounds__(256) void attn_dq_mfma_kernel(BwdDev w) {
+  using Stage = KVStage<DQK, DV, 256>;
+  constexpr int LDK = Stage::LDK, LDV = Stage::LDV;
+  constexpr int KS = BKV * LDK, VS = BKV * LDV;
+  constexpr int NKK = DQK / 16, NVK = DV / 16, NCK = DQK / 32;
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (KS + VS)];
+  const AttnDev& a = w.f;
+
+  const int nqb = (a.T + DQ_BQ - 1) / DQ_BQ;
+  const int nwork = a.B * a.H * nqb;
+  const int pid = xcd_remap(blockIdx.x, nwork);
+  const int bh = pid / nqb;
+  const int qb = nqb - 1 - pid % nqb;
+  const int b = bh / a.H, i = bh % a.H;
+  const int q0 = qb * DQ_BQ;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  const int qw0 = q0 + 32 * wave;
+  const int my_q = qw0 + col;
+  const bool qvalid = my_q < a.T;
+  const int64_t nq = (int64_t)b * a.T + min(my_q, a.T - 1);
+
+  // this lane's query and output gradient as B operand fragments (col = query)
+  bf16x8 qf[NKK], of[NVK];
+  {
+    const bf16_t* qp = a.Q + nq * a.q_tok + (int64_t)i * a.q_head + 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
+    const bf16_t* op = w.dO + nq * ((int64_t)a.H * DV) + (int64_t)i * DV + 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < NVK; ++kk) of[kk] = *(const bf16x8*)(op + 16 * kk);
+  }
+  const float lse2 = qvalid ? a.lse[nq * a.H + i] * LOG2E : INFINITY;
+  const float dlt = qvalid ? w.delta[nq * a.H + i] : 0.f;
+
+  f32x16 dq[NCK];
+#pragma unroll
+  for (int c = 0; c < NCK; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) dq[c][e] = 0.f;
+
+  const int kend = min(a.T, q0 + DQ_BQ);
+  const int nkb = (kend + BKV - 1) / BKV;
+  Stage st;
+  st.init(a, b, i);
+  st.load(a, 0);
+  st.store(smem, smem + KS);
+  __syncthreads();
+
+  for (int kb = 0; kb < nkb; ++kb) {
+    const int cur = kb & 1;
+    const int j0 = kb * BKV;
+    if (kb + 1 < nkb) st.load(a, j0 + BKV);
+    const bf16_t* ks = smem + cur * (KS + VS);
+    const bf16_t* vs = ks + KS;
+    if (j0 <= qw0 + 31) {
+      f32x16 s[2], dp[2];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) { s[t][e] = 0.f; dp[t][e] = 0.f; }
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              *(const bf16x8*)(ks + (32 * t + col) * LDK + 16 * kk + 8 * half), qf[kk], s[t], 0, 0, 0);
+#pragma unroll
+      for (int kk = 0; kk < NVK; ++kk)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+          dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              *(const bf16x8*)(vs + (32 * t + col) * LDV + 16 * kk + 8 * half), of[kk], dp[t], 0, 0, 0);
+      const bool diag = j0 + BKV - 1 > qw0;
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][e], a.sl2, -lse2));
+          if (diag && j0 + 32 * t + 8 * (e >> 2) + 4 * half + (e & 3) > my_q) p = 0.f;
+          dp[t][e] = p * (dp[t][e] - dlt);
+        }
+      // dQ^T += K^T dS^T; K-step u covers keys 32(u/2) + 16(u%2) + {4h.., 8+4h..}
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        u32x4 wd;
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          wd[q] = pack2bf(dp[u >> 1][8 * (u & 1) + 2 * q], dp[u >> 1][8 * (u & 1) + 2 * q + 1]);
+        const bf16x8 sf = __builtin_bit_cast(bf16x8, wd);
+        const int klo = 32 * (u >> 1) + 16 * (u & 1) + 4 * half;
+#pragma unroll
+        for (int c = 0; c < NCK; ++c)
+          dq[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(ks, LDK, 32 * c, klo, klo + 8),
+                                                         sf, dq[c], 0, 0, 0);
+      }
+    }
+    if (kb + 1 < nkb) {
+      bf16_t* nxt = smem + (cur ^ 1) * (KS + VS);
+      st.store(nxt, nxt + KS);
+    }
+    __syncthreads();
+  }
+
+  // epilogue: rows d = 32c + 8(e/4) + 4 half + e%4 of this lane's query (the rotary block is
+  // rotated back by the caller's R^T pass)
+  if (!qvalid) return;
+  const float sc = w.scale;
+  bf16_t* dst = w.dq + nq * ((int64_t)a.H * DQK) + (int64_t)i * DQK + 4 * half;
+#pragma unroll
+  for (int c = 0; c < NCK; ++c)
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4) {
+      u32x2 wv = {pack2bf(sc * dq[c][4 * e4], sc * dq[c][4 * e4 + 1]),
+                  pack2bf(sc * dq[c][4 * e4 + 2], sc * dq[c][4 * e4 + 3])};
+      *(u32x2*)(dst + 32 * c + 8 * e4) = wv;
+    }
 }
 
 template <int DQK, int DV>
@@ -311,15 +412,23 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   const Attn& at = wb.f;
   BwdDev w;
   w.f = to_dev(at);
-  w.dO = (const bf16_t*)wb.dO; w.delta = wb.delta; w.dq_acc = wb.dq_acc;
+  w.dO = (const bf16_t*)wb.dO; w.delta = wb.delta;
+  w.dq = (bf16_t*)wb.dq; w.rdiv = wb.rdiv; w.cos_t = wb.cos_t; w.sin_t = wb.sin_t;
   w.dKa = (bf16_t*)wb.dKa; w.dka_tok = wb.dka_tok;
   w.dV = (bf16_t*)wb.dV; w.dv_tok = wb.dv_tok;
   w.dkb_part = wb.dkb_part; w.G = wb.n_ka_groups; w.scale = at.scale;
-  const int64_t n4 = (int64_t)at.B * at.T * at.H * DQK / 4;
-  zero_f32_kernel<<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(wb.dq_acc, n4);
   const int nkb = (at.T + BKB - 1) / BKB;
-  attn_bwd_mfma_kernel<DQK, DV><<<nkb * at.B * w.G, 256, 0, s>>>(w);
-  return hipGetLastError();
+  attn_dkdv_mfma_kernel<DQK, DV><<<nkb * at.B * w.G, 256, 0, s>>>(w);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int nqb = (at.T + DQ_BQ - 1) / DQ_BQ;
+  attn_dq_mfma_kernel<DQK, DV><<<nqb * at.B * at.H, 256, 0, s>>>(w);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // rotary block of dQ back to the pre-rotation basis: R^T
+  const int np = (DQK - at.dnope) / 2;
+  return rope_apply(wb.dq, DT_BF16, at.B * at.T, at.T, at.H, (int64_t)at.H * DQK, DQK, at.dnope,
+                    np, wb.rdiv, wb.cos_t, wb.sin_t, s, true);
 }
 
 }  // namespace

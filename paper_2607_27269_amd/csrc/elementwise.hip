@@ -57,7 +57,7 @@ template <typename T>
 __global__ void rope_apply_kernel(T* __restrict__ x, int N, int Tseq, int nheads, int64_t tok,
                                   int64_t head, int off, int np, int div,
                                   const float* __restrict__ cos_t,
-                                  const float* __restrict__ sin_t) {
+                                  const float* __restrict__ sin_t, float sgn) {
   const int nq = np / 4;
   int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t total = (int64_t)N * nheads * nq;
@@ -68,7 +68,7 @@ __global__ void rope_apply_kernel(T* __restrict__ x, int N, int Tseq, int nheads
   int t = (int)(n % Tseq);
   int g = h / div;
   const int64_t ti = ((int64_t)g * Tseq + t) * np + p;
-  f32x4 c = *(const f32x4*)(cos_t + ti), sn = *(const f32x4*)(sin_t + ti);
+  f32x4 c = *(const f32x4*)(cos_t + ti), sn = *(const f32x4*)(sin_t + ti) * sgn;
   T* base = x + n * tok + (int64_t)h * head + off;
   f32x4 x1 = Vec4<T>::load(base + p), x2 = Vec4<T>::load(base + p + np);
   Vec4<T>::store(base + p, x1 * c - x2 * sn);
@@ -77,17 +77,18 @@ __global__ void rope_apply_kernel(T* __restrict__ x, int N, int Tseq, int nheads
 
 hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, int64_t head,
                       int off, int npairs, int div, const float* cos_t, const float* sin_t,
-                      hipStream_t s) {
+                      hipStream_t s, bool inverse) {
+  const float sgn = inverse ? -1.f : 1.f;
   int64_t total = (int64_t)N * nheads * (npairs / 4);
   if (total == 0) return hipSuccess;
   unsigned grid = (unsigned)((total + 255) / 256);
   prof_begin(KC_ELEM, s);
   if (t == DT_BF16)
     rope_apply_kernel<bf16_t><<<grid, 256, 0, s>>>((bf16_t*)x, N, T, nheads, tok, head, off,
-                                                   npairs, div, cos_t, sin_t);
+                                                   npairs, div, cos_t, sin_t, sgn);
   else
     rope_apply_kernel<float><<<grid, 256, 0, s>>>((float*)x, N, T, nheads, tok, head, off,
-                                                  npairs, div, cos_t, sin_t);
+                                                  npairs, div, cos_t, sin_t, sgn);
   prof_end(KC_ELEM, s, 0.0, (double)N * nheads * npairs * 4.0 * dsize(t));
   return hipGetLastError();
 }

@@ -52,7 +52,11 @@ struct AttnBwd {
   Attn f;                    // forward operands; f.O and f.lse are inputs here
   const void* dO;            // [N, H*dv], row stride H*dv
   float* delta;              // scratch [N, H]
-  float* dq_acc;             // [N, H, dqk] fp32 (fully overwritten)
+  float* dq_acc;             // scratch [N, H, dqk] fp32 (vector-ALU path)
+  void* dq;                  // out [N, H*dqk]: dQ with the rotary block [dnope, dqk) rotated
+  int rdiv;                  //   back by R^T using the tables of rope group i / rdiv
+  const float* cos_t;        //   ([G_r][T][(dqk-dnope)/2] fp32)
+  const float* sin_t;
   void* dKa; int64_t dka_tok;  // [N, ...]: group g's d_nope grads at dKa[n*dka_tok + g*dnope]
   void* dV;  int64_t dv_tok;   // group g's value grads at dV[n*dv_tok + g*dv]
   float* dkb_part;           // [Gka, N, dqk - dnope] fp32 partial grads of the Kb part per Ka group
@@ -65,10 +69,11 @@ hipError_t attn_bwd(const AttnBwd& a, hipStream_t s);
 hipError_t rope_tables(const float* inv_freq, int G, int T, int npairs, float* cos_t,
                        float* sin_t, hipStream_t s);
 // In-place rotation of x[n*tok + h*head + off + {p, p + npairs}] for heads h < nheads,
-// tokens n < N (position n % T), with the tables of group h / div.  inverse: R^T.
+// tokens n < N (position n % T), with the tables of group h / div; R^T when inverse.
+// npairs must be a multiple of 4.
 hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, int64_t head,
                       int off, int npairs, int div, const float* cos_t, const float* sin_t,
-                      hipStream_t s);
+                      hipStream_t s, bool inverse = false);
 
 // Backward finishing ----------------------------------------------------------------------
 // dq[n, i, :] = dq_acc with the rotary block [dnope, dqk) rotated back by R^T (tables of

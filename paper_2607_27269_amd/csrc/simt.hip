@@ -337,7 +337,10 @@ static hipError_t simt_bwd_launch(const AttnBwd& w, hipStream_t s) {
   attn_dq_simt_kernel<T, DQK, DV><<<gq, 64, 0, s>>>(w);
   dim3 gk((a.T + 63) / 64, w.n_ka_groups, a.B);
   attn_dkv_simt_kernel<T, DQK, DV><<<gk, 64, 0, s>>>(w);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return dq_finish(w.dq_acc, w.dq, a.t, a.B * a.T, a.T, a.H, DQK, a.dnope, w.rdiv, w.cos_t,
+                   w.sin_t, s);
 }
 
 #define MLA_SIMT_SHAPES(X) \
