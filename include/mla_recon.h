@@ -66,9 +66,10 @@ typedef enum { MLA_BF16 = 0, MLA_FP32 = 1 } mla_dtype;
  * positional keys k^PE (head i uses group i / (H/G_kv) and rope key i / (H/G_r)).
  * Requirements: all sizes >= 1 except q_rank, nope_dim >= 0; H % G == H % G_kv == H % G_r
  * == 0; d_k and d_rope even; hidden, head_dim, q_rank, kv_rank, nope_dim, rope_dim
- * multiples of 8.  The bf16 kernels additionally support d_k in {64, 128},
- * d_nope + d_rope in {64, 96, 128, 192}, and seq a multiple of 64 (MLA_ERR_UNSUPPORTED
- * otherwise). */
+ * multiples of 8; G_kv a multiple of G_r.  Attention widths: the teacher's (d_k, d_k) and
+ * the student's (d_nope + d_rope, d_k) must be one of (64,64), (96,64), (128,64),
+ * (128,128), (192,128) (matrix-core kernels) or, through the vector-ALU kernels, (64,32),
+ * (32,32), (16,16), (12,8), (8,8); MLA_ERR_UNSUPPORTED otherwise.  Any seq >= 1. */
 typedef struct {
   int32_t batch, seq, hidden;               /* B, T, D                                    */
   int32_t n_heads, n_kv_groups, head_dim;   /* H, G, d_k                                  */
@@ -145,7 +146,9 @@ const char *mla_recon_last_error(void);
  * bracketed by a pair of HIP events recorded on the launch stream.  mla_recon_prof_read
  * waits for those events, returns the summed kernel time (ms), the launch count and the
  * algorithmic FLOPs and HBM bytes those launches account for, and clears the record.
- * Classes: 0 GEMM, 1 attention forward, 2 attention backward, 3 loss, 4 elementwise
+ * Classes: 0 GEMM C = A B^T, 1 GEMM with B N-contiguous, 2 GEMM with both operands
+ * M/N-contiguous (weight gradients), 3 attention forward, 4 attention backward dK/dV,
+ * 5 attention backward dQ, 6 loss, 7 elementwise
  * (RoPE, reductions, conversions).  Up to 4096 launches are recorded per class. */
 int mla_recon_prof_enable(int kernel_class, int on);
 int mla_recon_prof_read(int kernel_class, double *total_ms, int64_t *launches,

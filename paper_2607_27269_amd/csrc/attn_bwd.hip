@@ -417,12 +417,25 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   w.dKa = (bf16_t*)wb.dKa; w.dka_tok = wb.dka_tok;
   w.dV = (bf16_t*)wb.dV; w.dv_tok = wb.dv_tok;
   w.dkb_part = wb.dkb_part; w.G = wb.n_ka_groups; w.scale = at.scale;
+  const double pairs = attn_causal_pairs(at);
+  const double N = (double)at.B * at.T;
+  // dK/dV kernel: algorithmic dV = P^T dO, dP = dO V^T, dK = dS^T Q; reads Q, dO, K, V,
+  // lse, delta once, writes dK, dV
+  prof_begin(KC_ATTN_DKDV, s);
+  hipError_t e = attn_delta(wb, s);
+  if (e != hipSuccess) return e;
   const int nkb = (at.T + BKB - 1) / BKB;
   attn_dkdv_mfma_kernel<DQK, DV><<<nkb * at.B * w.G, 256, 0, s>>>(w);
-  hipError_t e = hipGetLastError();
+  prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV + DQK),
+           N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 4.0 + N * at.H * 8.0);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // dQ kernel: algorithmic dQ = dS K
+  prof_begin(KC_ATTN_DQ, s);
   const int nqb = (at.T + DQ_BQ - 1) / DQ_BQ;
   attn_dq_mfma_kernel<DQK, DV><<<nqb * at.B * at.H, 256, 0, s>>>(w);
+  prof_end(KC_ATTN_DQ, s, 2.0 * pairs * DQK,
+           N * at.H * (2.0 * DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   // rotary block of dQ back to the pre-rotation basis: R^T
@@ -442,10 +455,6 @@ hipError_t bwd_dispatch(const AttnBwd& w, hipStream_t s) {
 
 }  // namespace attn
 
-hipError_t attn_bwd_mfma(const AttnBwd& w, hipStream_t s) {
-  hipError_t e = attn_delta(w, s);
-  if (e != hipSuccess) return e;
-  return attn::bwd_dispatch(w, s);
-}
+hipError_t attn_bwd_mfma(const AttnBwd& w, hipStream_t s) { return attn::bwd_dispatch(w, s); }
 
 }  // namespace mla

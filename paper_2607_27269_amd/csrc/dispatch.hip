@@ -16,9 +16,10 @@ hipError_t gemm(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t
   double flops = 2.0 * g.M * g.N * (double)g.K;
   double bytes = ((double)g.M * g.K + (double)g.N * g.K) * dsize(g.in_t) +
                  (double)g.M * g.N * dsize(g.c_t) * (g.beta != 0.f ? 2.0 : 1.0);
-  prof_begin(KC_GEMM, s);
+  const int kc = g.a_kmajor ? (g.b_kmajor ? KC_GEMM_NT : KC_GEMM_NN) : KC_GEMM_TN;
+  prof_begin(kc, s);
   hipError_t e = g.in_t == DT_BF16 ? gemm_mfma(g, scratch, scratch_elems, s) : gemm_simt(g, s);
-  prof_end(KC_GEMM, s, flops, bytes);
+  prof_end(kc, s, flops, bytes);
   return e;
 }
 
@@ -39,14 +40,17 @@ hipError_t attn_fwd(const Attn& a, hipStream_t s) {
 
 hipError_t attn_bwd(const AttnBwd& w, hipStream_t s) {
   const Attn& a = w.f;
+  if (a.t == DT_BF16 && attn_mfma_supported(a.dqk, a.dv)) return attn_bwd_mfma(w, s);
+  // vector-ALU path: one bracket for the whole backward
   double flops = 2.0 * causal_pairs(a) * (2.0 * a.dv + 2.0 * a.dqk);
   double N = (double)a.B * a.T;
   double bytes = N * a.H * (a.dqk + 2.0 * a.dv) * dsize(a.t) + N * a.H * (8.0 + 4.0 * a.dqk);
-  prof_begin(KC_ATTN_BWD, s);
-  hipError_t e = a.t == DT_BF16 && attn_mfma_supported(a.dqk, a.dv) ? attn_bwd_mfma(w, s)
-                                                                    : attn_bwd_simt(w, s);
-  prof_end(KC_ATTN_BWD, s, flops, bytes);
+  prof_begin(KC_ATTN_DKDV, s);
+  hipError_t e = attn_bwd_simt(w, s);
+  prof_end(KC_ATTN_DKDV, s, flops, bytes);
   return e;
 }
+
+double attn_causal_pairs(const Attn& a) { return causal_pairs(a); }
 
 }  // namespace mla

@@ -8,7 +8,18 @@ namespace mla {
 enum DType { DT_BF16 = 0, DT_F32 = 1 };
 inline size_t dsize(DType t) { return t == DT_BF16 ? 2 : 4; }
 
-enum KClass { KC_GEMM = 0, KC_ATTN_FWD = 1, KC_ATTN_BWD = 2, KC_LOSS = 3, KC_ELEM = 4, KC_COUNT = 5 };
+// Timing classes: one per kernel family (a GEMM layout, an attention kernel, ...).
+enum KClass {
+  KC_GEMM_NT = 0,      // C = A B^T, both operands K-contiguous (projections)
+  KC_GEMM_NN = 1,      // B N-contiguous (data gradients)
+  KC_GEMM_TN = 2,      // both operands M/N-contiguous (weight gradients, split-K)
+  KC_ATTN_FWD = 3,     // causal attention forward
+  KC_ATTN_DKDV = 4,    // attention backward: dK, dV (plus the delta row term)
+  KC_ATTN_DQ = 5,      // attention backward: dQ (plus its R^T pass)
+  KC_LOSS = 6,         // Eq. 11 loss and gradient
+  KC_ELEM = 7,         // RoPE tables / rotation, dk^PE finishing, split-K reduction
+  KC_COUNT = 8
+};
 
 // Timing instrumentation hooks (implemented in api.cpp).  prof_end also records the
 // algorithmic FLOPs / bytes of the bracketed launch(es).
@@ -63,6 +74,8 @@ struct AttnBwd {
   int n_ka_groups;           // number of Ka groups (heads i / f.Ka.div)
 };
 hipError_t attn_bwd(const AttnBwd& a, hipStream_t s);
+// (sequence, head, query, key) pairs with key <= query: B H T (T+1) / 2
+double attn_causal_pairs(const Attn& a);
 
 // RoPE -------------------------------------------------------------------------------
 // cos/sin tables [G][T][npairs] fp32 from inv_freq [G][npairs] fp32 (angles in fp64).
