@@ -2,21 +2,24 @@
 //
 //   C[m, n] = alpha * sum_k A(m, k) B(n, k) + beta * C[m, n]
 //
-// Either operand may be K-contiguous ("k-major": a row of the weight / activation) or
+// Either operand may be K-contiguous ("k-major": rows of a weight or of activations) or
 // M/N-contiguous (the transposed operand of the weight-gradient and data-gradient
-// products).  A workgroup of 4 wavefronts owns a BM x BN output tile and walks K in
-// BK = 64 slices that are staged in LDS as [row][k] with k contiguous, the layout the MFMA
-// operand registers want (8 consecutive k per lane).  M/N-contiguous operands are
-// transposed on the way in: a thread loads an 8 (k) x 8 (m) block with eight 16-byte
-// loads, transposes it in registers and writes eight 16-byte rows.  LDS is double
-// buffered: the next slice's global loads are in flight while the current one feeds the
-// matrix cores.  Rows are padded by 16 bytes so the 16-byte operand reads of a wavefront
-// hit distinct banks.  Workgroup ids are remapped so that neighbouring tiles (which share
-// A row panels or B column panels) run on the same XCD and hit its L2.  Weight gradients
-// reduce over all tokens (K up to 1e5) and have few output tiles: they are split along K
-// into fp32 partials that a second kernel sums in a fixed order (deterministic).
+// products).  A workgroup owns a BM x BN output tile and walks K in BK = 64 slices staged
+// in LDS in the operand's natural layout: k-major tiles as [row][k] (16-byte operand reads,
+// 8 consecutive k per lane) and m-major tiles as [k][row], whose operands come from
+// gfx950's transposing LDS read.  Both give the same k order inside an MFMA step, so the
+// two kinds mix freely.  LDS is double buffered: the next slice's global loads are in
+// flight while the current one feeds the matrix cores; row strides are padded so that the
+// operand reads of a wavefront hit distinct banks.  Large problems use 256 x 256 tiles on
+// 8 wavefronts (128 x 64 each), which halves the LDS bytes per MFMA compared with
+// 128 x 128 tiles on 4 wavefronts (64 x 64 each), used for small problems.  Workgroup
+// ids are remapped so that neighbouring tiles (sharing A row panels or B column panels)
+// run on one XCD and hit its L2.  Weight gradients reduce over all tokens (K up to 1e5)
+// and have few output tiles: they are split along K into fp32 partials that a second
+// kernel sums in a fixed order (deterministic).
 #include "common.h"
 #include "kernels.h"
+#include "mfma.h"
 
 #include <algorithm>
 
@@ -25,11 +28,9 @@ namespace mla {
 namespace {
 
 constexpr int BK = 64;
-constexpr int PADK = BK + 8;  // LDS row length in bf16 elements (144 bytes)
-constexpr int NTHR = 256;
 
 struct GemmDev {
-  int M, N, K;        // K here is the K range of one split
+  int M, N;
   const bf16_t* A; int64_t lda;
   const bf16_t* B; int64_t ldb;
   void* C; int64_t ldc;
@@ -39,21 +40,37 @@ struct GemmDev {
   int ktotal;
 };
 
+// row stride (elements) of an m-major [k][ROWS] tile: 4 rows x 32 B of a transposing read
+// on distinct banks
+constexpr int mm_ld(int rows) {
+  for (int p = 8; p <= 64; p += 8) {
+    const int r = ((rows + p) / 2) % 64;
+    if (r == 12 || r == 28 || r == 36 || r == 52) return rows + p;
+  }
+  return rows + 8;
+}
+constexpr int KM_LD = BK + 8;  // k-major [row][k] tile: 144-byte rows
+
 // ---- global -> register staging -------------------------------------------------------
-// k-major tile: ROWS x BK, 16-byte chunks, chunk c -> row c / 8, k-chunk c % 8
-template <int ROWS>
-struct KMajorLoader {
+template <bool KMAJOR, int ROWS, int NTHR>
+struct Loader;
+
+// k-major tile: ROWS x BK, chunk c -> row c / 8, k-chunk c % 8
+template <int ROWS, int NTHR>
+struct Loader<true, ROWS, NTHR> {
   static constexpr int CHUNKS = ROWS * (BK / 8);
-  static constexpr int PER = (CHUNKS + NTHR - 1) / NTHR;
+  static constexpr int PER = CHUNKS / NTHR;
+  static constexpr int ELEMS = ROWS * KM_LD;
+  static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
   u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
                                        int rows_valid, int k0, int kend) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      int c = threadIdx.x + i * NTHR;
-      int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
+      const int c = threadIdx.x + i * NTHR;
+      const int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (c < CHUNKS && row < rows_valid && k0 + kc < kend)
+      if (row < rows_valid && k0 + kc < kend)
         v = *(const u32x4*)(p + (int64_t)(row0 + row) * ld + k0 + kc);
       r[i] = v;
     }
@@ -61,67 +78,51 @@ struct KMajorLoader {
   __device__ __forceinline__ void store(bf16_t* lds) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      int c = threadIdx.x + i * NTHR;
-      if (c < CHUNKS) {
-        int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
-        *(u32x4*)(lds + row * PADK + kc) = r[i];
-      }
+      const int c = threadIdx.x + i * NTHR;
+      *(u32x4*)(lds + (c / (BK / 8)) * KM_LD + (c % (BK / 8)) * 8) = r[i];
     }
+  }
+  // operand fragment: rows row0 + lane%32, k = 16 kk + 8 half + 0..7
+  static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
+    const int lane = threadIdx.x & 63;
+    return *(const bf16x8*)(lds + (row0 + (lane & 31)) * KM_LD + 16 * kk + 8 * (lane >> 5));
   }
 };
 
-// m-major tile (global [k][m]): 8 x 8 blocks, block b -> m-block b % (ROWS/8), k-block b / (ROWS/8)
-template <int ROWS>
-struct MMajorLoader {
-  static constexpr int MB = ROWS / 8;
-  static constexpr int BLOCKS = MB * (BK / 8);
-  static constexpr int PER = (BLOCKS + NTHR - 1) / NTHR;
-  u32x4 r[PER][8];
+// m-major tile (global [k][row]): BK x ROWS, chunk c -> k-row c / (ROWS/8), row-chunk c % (ROWS/8)
+template <int ROWS, int NTHR>
+struct Loader<false, ROWS, NTHR> {
+  static constexpr int LD = mm_ld(ROWS);
+  static constexpr int CPR = ROWS / 8;
+  static constexpr int CHUNKS = BK * CPR;
+  static constexpr int PER = CHUNKS / NTHR;
+  static constexpr int ELEMS = BK * LD;
+  static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
+  u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
                                        int rows_valid, int k0, int kend) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      int b = threadIdx.x + i * NTHR;
-      int mb = (b % MB) * 8, kb = (b / MB) * 8;
-      bool ok = b < BLOCKS && mb < rows_valid;
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (ok && k0 + kb + j < kend)
-          v = *(const u32x4*)(p + (int64_t)(k0 + kb + j) * ld + row0 + mb);
-        r[i][j] = v;
-      }
+      const int c = threadIdx.x + i * NTHR;
+      const int kr = c / CPR, rc = (c % CPR) * 8;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (rc < rows_valid && k0 + kr < kend)
+        v = *(const u32x4*)(p + (int64_t)(k0 + kr) * ld + row0 + rc);
+      r[i] = v;
     }
   }
   __device__ __forceinline__ void store(bf16_t* lds) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      int b = threadIdx.x + i * NTHR;
-      if (b >= BLOCKS) continue;
-      int mb = (b % MB) * 8, kb = (b / MB) * 8;
-      // transpose the 8 (k) x 8 (m) block: row mm of the output holds k = 0..7 of m = mm
-#pragma unroll
-      for (int mm = 0; mm < 8; ++mm) {
-        const int w = mm >> 1, sh = (mm & 1) * 16;
-        u32x4 o;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          uint32_t lo = (r[i][2 * q][w] >> sh) & 0xffffu;
-          uint32_t hi = (r[i][2 * q + 1][w] >> sh) & 0xffffu;
-          o[q] = lo | (hi << 16);
-        }
-        *(u32x4*)(lds + (mb + mm) * PADK + kb) = o;
-      }
+      const int c = threadIdx.x + i * NTHR;
+      *(u32x4*)(lds + (c / CPR) * LD + (c % CPR) * 8) = r[i];
     }
   }
+  static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
+    const int klo = 16 * kk + 8 * ((threadIdx.x & 63) >> 5);
+    return lds_operand_tr(lds, LD, row0, klo, klo + 4);
+  }
 };
-
-template <bool KMAJOR, int ROWS>
-struct Loader;
-template <int ROWS>
-struct Loader<true, ROWS> : KMajorLoader<ROWS> {};
-template <int ROWS>
-struct Loader<false, ROWS> : MMajorLoader<ROWS> {};
 
 template <typename TC>
 __device__ __forceinline__ void store_out(TC* p, float v);
@@ -132,11 +133,14 @@ __device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) { *p = f2b
 
 // ---- the kernel --------------------------------------------------------------------------
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC>
-__global__ __launch_bounds__(NTHR) void gemm_mfma_kernel(GemmDev g) {
-  static_assert(WM * WN == 4, "4 wavefronts");
+__global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
+  constexpr int NTHR = 64 * WM * WN;
   constexpr int TM = BM / WM / 32;  // 32x32 MFMA tiles per wave along M
   constexpr int TN = BN / WN / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t lds[2][(BM + BN) * PADK];
+  using LA = Loader<AK, BM, NTHR>;
+  using LB = Loader<BKM, BN, NTHR>;
+  constexpr int STAGE = LA::ELEMS + LB::ELEMS;
+  __shared__ __attribute__((aligned(16))) bf16_t lds[2 * STAGE];
 
   const int ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
   const int ntiles = ntm * ntn;
@@ -165,15 +169,15 @@ __global__ __launch_bounds__(NTHR) void gemm_mfma_kernel(GemmDev g) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
 
-  Loader<AK, BM> la;
-  Loader<BKM, BN> lb;
+  LA la;
+  LB lb;
   const int mvalid = g.M - m0, nvalid = g.N - n0;
   const int nk = (kend - kbeg + BK - 1) / BK;
   if (nk > 0) {
     la.load(g.A, g.lda, m0, mvalid, kbeg, kend);
     lb.load(g.B, g.ldb, n0, nvalid, kbeg, kend);
-    la.store(lds[0]);
-    lb.store(lds[0] + BM * PADK);
+    la.store(lds);
+    lb.store(lds + LA::ELEMS);
   }
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
@@ -182,18 +186,15 @@ __global__ __launch_bounds__(NTHR) void gemm_mfma_kernel(GemmDev g) {
       la.load(g.A, g.lda, m0, mvalid, kbeg + (kt + 1) * BK, kend);
       lb.load(g.B, g.ldb, n0, nvalid, kbeg + (kt + 1) * BK, kend);
     }
-    const bf16_t* As = lds[cur];
-    const bf16_t* Bs = lds[cur] + BM * PADK;
+    const bf16_t* As = lds + cur * STAGE;
+    const bf16_t* Bs = As + LA::ELEMS;
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      const int koff = kk * 16 + (lane >> 5) * 8;
       bf16x8 af[TM], bfr[TN];
 #pragma unroll
-      for (int i = 0; i < TM; ++i)
-        af[i] = *(const bf16x8*)(As + (wrow0 + i * 32 + (lane & 31)) * PADK + koff);
+      for (int i = 0; i < TM; ++i) af[i] = LA::frag(As, wrow0 + i * 32, kk);
 #pragma unroll
-      for (int j = 0; j < TN; ++j)
-        bfr[j] = *(const bf16x8*)(Bs + (wcol0 + j * 32 + (lane & 31)) * PADK + koff);
+      for (int j = 0; j < TN; ++j) bfr[j] = LB::frag(Bs, wcol0 + j * 32, kk);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -201,8 +202,9 @@ __global__ __launch_bounds__(NTHR) void gemm_mfma_kernel(GemmDev g) {
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
     if (kt + 1 < nk) {
-      la.store(lds[cur ^ 1]);
-      lb.store(lds[cur ^ 1] + BM * PADK);
+      bf16_t* nxt = lds + (cur ^ 1) * STAGE;
+      la.store(nxt);
+      lb.store(nxt + LA::ELEMS);
     }
     __syncthreads();
   }
@@ -247,28 +249,52 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits,
   store_out<TC>(c, v);
 }
 
-constexpr int TILE_M = 128, TILE_N = 128;
+// tile shape: 256 x 256 on 8 wavefronts when that still yields enough workgroups
+struct Plan {
+  bool big;
+  int bm, bn, splits, kchunk;
+};
 
-int choose_splits(const Gemm& g) {
-  const int tiles = ((g.M + TILE_M - 1) / TILE_M) * ((g.N + TILE_N - 1) / TILE_N);
-  if (tiles >= 512 || g.K < 4 * BK * 8) return 1;
-  int want = (768 + tiles - 1) / tiles;
-  int maxs = g.K / (BK * 8);  // keep at least 512 k per split
-  return std::max(1, std::min(want, maxs));
+Plan plan_of(const Gemm& g, bool allow_split) {
+  Plan p;
+  const int t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
+  const int t128 = ((g.M + 127) / 128) * ((g.N + 127) / 128);
+  // a 256-tile wastes work on ragged edges; use it when the padded area stays small
+  const double waste = (double)((g.M + 255) / 256 * 256) * ((g.N + 255) / 256 * 256) /
+                       ((double)((g.M + 127) / 128 * 128) * ((g.N + 127) / 128 * 128));
+  const bool splittable = allow_split && g.K >= 8 * BK * 8;
+  p.big = waste < 1.15 && (t256 >= 192 || splittable);
+  p.bm = p.bn = p.big ? 256 : 128;
+  const int tiles = p.big ? t256 : t128;
+  p.splits = 1;
+  if (splittable && tiles < 512) {
+    const int want = (512 + tiles - 1) / tiles;
+    const int maxs = g.K / (BK * 8);  // at least 512 k per split
+    p.splits = std::max(1, std::min(want, maxs));
+  }
+  int kchunk = (g.K + p.splits - 1) / p.splits;
+  kchunk = (kchunk + BK - 1) / BK * BK;
+  p.kchunk = std::max(kchunk, BK);
+  p.splits = (g.K + p.kchunk - 1) / p.kchunk;
+  if (p.splits < 1) p.splits = 1;
+  return p;
 }
 
 template <bool AK, bool BKM, typename TC>
-void launch(const GemmDev& d, int splits, hipStream_t s) {
-  const int tiles = ((d.M + TILE_M - 1) / TILE_M) * ((d.N + TILE_N - 1) / TILE_N);
-  dim3 grid(tiles, splits);
-  gemm_mfma_kernel<TILE_M, TILE_N, 2, 2, AK, BKM, TC><<<grid, NTHR, 0, s>>>(d);
+void launch(const GemmDev& d, const Plan& p, hipStream_t s) {
+  const int tiles = ((d.M + p.bm - 1) / p.bm) * ((d.N + p.bn - 1) / p.bn);
+  dim3 grid(tiles, p.splits);
+  if (p.big)
+    gemm_mfma_kernel<256, 256, 2, 4, AK, BKM, TC><<<grid, 512, 0, s>>>(d);
+  else
+    gemm_mfma_kernel<128, 128, 2, 2, AK, BKM, TC><<<grid, 256, 0, s>>>(d);
 }
 
 }  // namespace
 
 size_t gemm_mfma_scratch_elems(const Gemm& g) {
-  int sp = choose_splits(g);
-  return sp > 1 ? (size_t)sp * g.M * g.N : 0;
+  Plan p = plan_of(g, true);
+  return p.splits > 1 ? (size_t)p.splits * g.M * g.N : 0;
 }
 
 hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s) {
@@ -277,32 +303,28 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   d.A = (const bf16_t*)g.A; d.lda = g.lda;
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = g.beta;
-  int splits = choose_splits(g);
-  if (splits > 1 && (scratch == nullptr || scratch_elems < (size_t)splits * g.M * g.N))
-    splits = 1;
-  int kchunk = (g.K + splits - 1) / splits;
-  kchunk = (kchunk + BK - 1) / BK * BK;
-  splits = (g.K + kchunk - 1) / kchunk;
-  d.kchunk = kchunk;
-  d.K = kchunk;
-  d.part = splits > 1 ? scratch : nullptr;
+  Plan p = plan_of(g, true);
+  if (p.splits > 1 && (scratch == nullptr || scratch_elems < (size_t)p.splits * g.M * g.N))
+    p = plan_of(g, false);
+  d.kchunk = p.kchunk;
+  d.part = p.splits > 1 ? scratch : nullptr;
   const bool f32 = g.c_t == DT_F32;
 #define L_(AK, BK_)                                                                     \
   if (g.a_kmajor == AK && g.b_kmajor == BK_) {                                          \
-    if (f32) launch<AK, BK_, float>(d, splits, s);                                      \
-    else launch<AK, BK_, bf16_t>(d, splits, s);                                         \
+    if (f32) launch<AK, BK_, float>(d, p, s);                                           \
+    else launch<AK, BK_, bf16_t>(d, p, s);                                              \
   }
   L_(true, true) else L_(true, false) else L_(false, false) else L_(false, true)
 #undef L_
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || splits == 1) return e;
+  if (e != hipSuccess || p.splits == 1) return e;
   int64_t total = (int64_t)g.M * g.N;
   unsigned grid = (unsigned)((total + 255) / 256);
   if (f32)
-    splitk_reduce_kernel<float><<<grid, 256, 0, s>>>(scratch, splits, g.M, g.N, (float*)g.C, g.ldc,
-                                                     g.alpha, g.beta);
+    splitk_reduce_kernel<float><<<grid, 256, 0, s>>>(scratch, p.splits, g.M, g.N, (float*)g.C,
+                                                     g.ldc, g.alpha, g.beta);
   else
-    splitk_reduce_kernel<bf16_t><<<grid, 256, 0, s>>>(scratch, splits, g.M, g.N, (bf16_t*)g.C,
+    splitk_reduce_kernel<bf16_t><<<grid, 256, 0, s>>>(scratch, p.splits, g.M, g.N, (bf16_t*)g.C,
                                                       g.ldc, g.alpha, g.beta);
   return hipGetLastError();
 }
