@@ -31,10 +31,10 @@ KCLASS_KERNELS = {"gemm_nt": "gemm_mfma_kernel<..., true, true, ...>",
                   "gemm_nn": "gemm_mfma_kernel<..., true, false, ...>",
                   "gemm_tn": "gemm_mfma_kernel<..., false, false, float> + splitk_reduce_kernel",
                   "attn_fwd": "attn_fwd_mfma_kernel",
-                  "attn_bwd_dkdv": "attn_delta_kernel + attn_dkdv_mfma_kernel",
+                  "attn_bwd_dkdv": "attn_dkdv_mfma_kernel",
                   "attn_bwd_dq": "attn_dq_mfma_kernel",
                   "loss": "mask_count_kernel + loss_main_kernel + loss_final_kernel",
-                  "elementwise": "rope_table_kernel, rope_apply_kernel, dkpe_finish_kernel"}
+                  "elementwise": "rope_table_kernel, rope_apply_kernel, attn_delta_kernel, dkpe_finish_kernel"}
 
 
 class MlaError(RuntimeError):

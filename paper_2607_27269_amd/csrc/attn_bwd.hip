@@ -419,11 +419,13 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   w.dkb_part = wb.dkb_part; w.G = wb.n_ka_groups; w.scale = at.scale;
   const double pairs = attn_causal_pairs(at);
   const double N = (double)at.B * at.T;
-  // dK/dV kernel: algorithmic dV = P^T dO, dP = dO V^T, dK = dS^T Q; reads Q, dO, K, V,
-  // lse, delta once, writes dK, dV
-  prof_begin(KC_ATTN_DKDV, s);
+  // delta = rowsum(dO . O), then the dK/dV kernel: algorithmic dV = P^T dO, dP = dO V^T,
+  // dK = dS^T Q; reads Q, dO, K, V, lse, delta once, writes dK, dV
+  prof_begin(KC_ELEM, s);
   hipError_t e = attn_delta(wb, s);
+  prof_end(KC_ELEM, s, 0.0, N * at.H * (2.0 * DV * 2.0 + 4.0));
   if (e != hipSuccess) return e;
+  prof_begin(KC_ATTN_DKDV, s);
   const int nkb = (at.T + BKB - 1) / BKB;
   attn_dkdv_mfma_kernel<DQK, DV><<<nkb * at.B * w.G, 256, 0, s>>>(w);
   prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV + DQK),

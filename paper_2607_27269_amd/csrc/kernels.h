@@ -14,10 +14,10 @@ enum KClass {
   KC_GEMM_NN = 1,      // B N-contiguous (data gradients)
   KC_GEMM_TN = 2,      // both operands M/N-contiguous (weight gradients, split-K)
   KC_ATTN_FWD = 3,     // causal attention forward
-  KC_ATTN_DKDV = 4,    // attention backward: dK, dV (plus the delta row term)
-  KC_ATTN_DQ = 5,      // attention backward: dQ (plus its R^T pass)
+  KC_ATTN_DKDV = 4,    // attention backward: dK, dV
+  KC_ATTN_DQ = 5,      // attention backward: dQ
   KC_LOSS = 6,         // Eq. 11 loss and gradient
-  KC_ELEM = 7,         // RoPE tables / rotation, dk^PE finishing, split-K reduction
+  KC_ELEM = 7,         // RoPE tables / rotation, softmax-backward row term, dk^PE finishing
   KC_COUNT = 8
 };
 
