@@ -40,14 +40,15 @@ struct GemmDev {
   int ktotal;
 };
 
-// row stride (elements) of an m-major [k][ROWS] tile: 4 rows x 32 B of a transposing read
-// on distinct banks
+// row stride (elements) of an m-major [k][ROWS] tile, read only through the transposing
+// read (32 lanes cover 4 consecutive rows x 64 bytes): a stride of 16 or 48 banks modulo
+// 64 puts the 4 rows on disjoint banks
 constexpr int mm_ld(int rows) {
   for (int p = 8; p <= 64; p += 8) {
     const int r = ((rows + p) / 2) % 64;
-    if (r == 12 || r == 28 || r == 36 || r == 52) return rows + p;
+    if (r == 16 || r == 48) return rows + p;
   }
-  return rows + 8;
+  return rows + 32;
 }
 constexpr int KM_LD = BK + 8;  // k-major [row][k] tile: 144-byte rows
 
