@@ -52,58 +52,40 @@ template <int DQK, int DV>
 struct QStage {
   static constexpr int LDQ = ld_of(DQK);
   static constexpr int LDO = ld_of(DV);
-  static constexpr int QCH = BQB * (DQK / 8);
-  static constexpr int QPER = (QCH + 255) / 256;
-  static constexpr int OCH = BQB * (DV / 8);
-  static constexpr int OPER = (OCH + 255) / 256;
-  static constexpr int QS = BQB * LDQ, OS = BQB * LDO;
+  using QT = DmaTile<BQB, DQK, LDQ, 4>;
+  using OT = DmaTile<BQB, DV, LDO, 4>;
+  static constexpr int QS = QT::ALLOC, OS = OT::ALLOC;
   static constexpr int BUF = QS + OS + 2 * BQB * 2;  // bf16 elements incl. lse2, delta
-  u32x4 q[QPER];
-  u32x4 o[OPER];
+  QT qt;
+  OT ot;
   float stat;
 
-  __device__ __forceinline__ void load(const BwdDev& w, int b, int i, int q0) {
-    const AttnDev& a = w.f;
-    const bool full = q0 + BQB <= a.T;
-#pragma unroll
-    for (int it = 0; it < QPER; ++it) {
-      const int c = threadIdx.x + it * 256;
-      const int r = c / (DQK / 8), dc = (c % (DQK / 8)) * 8;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if ((QCH % 256 == 0 || c < QCH) && (full || q0 + r < a.T))
-        v = *(const u32x4*)(a.Q + ((int64_t)b * a.T + q0 + r) * a.q_tok + (int64_t)i * a.q_head + dc);
-      q[it] = v;
-    }
-#pragma unroll
-    for (int it = 0; it < OPER; ++it) {
-      const int c = threadIdx.x + it * 256;
-      const int r = c / (DV / 8), dc = (c % (DV / 8)) * 8;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if ((OCH % 256 == 0 || c < OCH) && (full || q0 + r < a.T))
-        v = *(const u32x4*)(w.dO + ((int64_t)b * a.T + q0 + r) * ((int64_t)a.H * DV) + (int64_t)i * DV + dc);
-      o[it] = v;
-    }
-    const int q = q0 + (threadIdx.x & 63);
-    if (threadIdx.x < 64)
-      stat = q < a.T ? a.lse[((int64_t)b * a.T + q) * a.H + i] * LOG2E : INFINITY;
-    else if (threadIdx.x < 128)
-      stat = q < a.T ? w.delta[((int64_t)b * a.T + q) * a.H + i] : 0.f;
+  __device__ __forceinline__ void init() {
+    qt.init();
+    ot.init();
   }
 
-  __device__ __forceinline__ void store(bf16_t* buf) const {
-    bf16_t* Qs = buf;
-    bf16_t* dOs = buf + QS;
+  // queries q0 .. q0+BQB-1 of head i into buf (rows past the end load the last valid row;
+  // their lse is +inf so they carry zero probability)
+  __device__ __forceinline__ void issue(const BwdDev& w, int b, int i, int q0, bf16_t* buf) {
+    const AttnDev& a = w.f;
+    const int last = a.T - 1;
+    const int64_t n0 = (int64_t)b * a.T;
+    const bf16_t* qb = a.Q + n0 * a.q_tok + (int64_t)i * a.q_head;
+    const bf16_t* ob = w.dO + n0 * ((int64_t)a.H * DV) + (int64_t)i * DV;
+    qt.issue(buf, [&](int r, int c) { return qb + (int64_t)min(q0 + r, last) * a.q_tok + c; });
+    ot.issue(buf + QS, [&](int r, int c) {
+      return ob + (int64_t)min(q0 + r, last) * ((int64_t)a.H * DV) + c;
+    });
+    const int q = q0 + (threadIdx.x & 63);
+    if (threadIdx.x < 64)
+      stat = q < a.T ? a.lse[(n0 + q) * a.H + i] * LOG2E : INFINITY;
+    else if (threadIdx.x < 128)
+      stat = q < a.T ? w.delta[(n0 + q) * a.H + i] : 0.f;
+  }
+
+  __device__ __forceinline__ void store_stats(bf16_t* buf) const {
     float* st = (float*)(buf + QS + OS);
-#pragma unroll
-    for (int it = 0; it < QPER; ++it) {
-      const int c = threadIdx.x + it * 256;
-      if (QCH % 256 == 0 || c < QCH) *(u32x4*)(Qs + (c / (DQK / 8)) * LDQ + (c % (DQK / 8)) * 8) = q[it];
-    }
-#pragma unroll
-    for (int it = 0; it < OPER; ++it) {
-      const int c = threadIdx.x + it * 256;
-      if (OCH % 256 == 0 || c < OCH) *(u32x4*)(dOs + (c / (DV / 8)) * LDO + (c % (DV / 8)) * 8) = o[it];
-    }
     if (threadIdx.x < 128) st[threadIdx.x] = stat;
   }
 };
@@ -114,7 +96,7 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
   constexpr int LDQ = Stage::LDQ, LDO = Stage::LDO;
   constexpr int NKK = DQK / 16, NVK = DV / 16;
   constexpr int NCK = DQK / 32, NCV = DV / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * Stage::BUF + BKB * ld_of(DQK)];
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * Stage::BUF + BKB * ld_of(DQK)];
   const AttnDev& a = w.f;
 
   const int nbg = a.B * w.G;
@@ -178,10 +160,12 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
   const int nper = nqb - qb0;
   const int niter = hpg * nper;
   Stage stg;
+  stg.init();
   if (niter > 0) {
-    stg.load(w, b, i0, qb0 * BQB);
-    stg.store(smem);
+    stg.issue(w, b, i0, qb0 * BQB, smem);
+    stg.store_stats(smem);
   }
+  wait_all();
   __syncthreads();
 
   for (int it = 0; it < niter; ++it) {
@@ -190,7 +174,8 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
     const bf16_t* dOs = Qs + Stage::QS;
     const float* st_lse = (const float*)(dOs + Stage::OS);
     const float* st_dl = st_lse + BQB;
-    if (it + 1 < niter) stg.load(w, b, i0 + (it + 1) / nper, (qb0 + (it + 1) % nper) * BQB);
+    if (it + 1 < niter)
+      stg.issue(w, b, i0 + (it + 1) / nper, (qb0 + (it + 1) % nper) * BQB, smem + ((it + 1) & 1) * Stage::BUF);
 
     if (kw0 <= min(q0 + BQB - 1, a.T - 1)) {  // wave-uniform: some pair is visible
       f32x16 sp[2], dp[2];
@@ -251,7 +236,8 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
                                                          sf, dk[c], 0, 0, 0);
       }
     }
-    if (it + 1 < niter) stg.store(smem + ((it + 1) & 1) * Stage::BUF);
+    if (it + 1 < niter) stg.store_stats(smem + ((it + 1) & 1) * Stage::BUF);
+    wait_all();
     __syncthreads();
   }
 
@@ -289,11 +275,11 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
 // ---------------------------------------------------------------------------------------
 template <int DQK, int DV>
 __global__ __launch_bounds__(256) void attn_dq_mfma_kernel(BwdDev w) {
-  using Stage = KVStage<DQK, DV, 256>;
+  using Stage = KVStage<DQK, DV, 4>;
   constexpr int LDK = Stage::LDK, LDV = Stage::LDV;
-  constexpr int KS = BKV * LDK, VS = BKV * LDV;
+  constexpr int KS = Stage::KS, VS = Stage::VS;
   constexpr int NKK = DQK / 16, NVK = DV / 16, NCK = DQK / 32;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (KS + VS)];
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * (KS + VS)];
   const AttnDev& a = w.f;
 
   const int nqb = (a.T + DQ_BQ - 1) / DQ_BQ;
@@ -333,14 +319,17 @@ __global__ __launch_bounds__(256) void attn_dq_mfma_kernel(BwdDev w) {
   const int nkb = (kend + BKV - 1) / BKV;
   Stage st;
   st.init(a, b, i);
-  st.load(a, 0);
-  st.store(smem, smem + KS);
+  st.issue(0, smem, smem + KS);
+  wait_all();
   __syncthreads();
 
   for (int kb = 0; kb < nkb; ++kb) {
     const int cur = kb & 1;
     const int j0 = kb * BKV;
-    if (kb + 1 < nkb) st.load(a, j0 + BKV);
+    if (kb + 1 < nkb) {
+      bf16_t* nxt = smem + (cur ^ 1) * (KS + VS);
+      st.issue(j0 + BKV, nxt, nxt + KS);
+    }
     const bf16_t* ks = smem + cur * (KS + VS);
     const bf16_t* vs = ks + KS;
     if (j0 <= qw0 + 31) {
@@ -385,10 +374,7 @@ __global__ __launch_bounds__(256) void attn_dq_mfma_kernel(BwdDev w) {
                                                          sf, dq[c], 0, 0, 0);
       }
     }
-    if (kb + 1 < nkb) {
-      bf16_t* nxt = smem + (cur ^ 1) * (KS + VS);
-      st.store(nxt, nxt + KS);
-    }
+    wait_all();
     __syncthreads();
   }
 

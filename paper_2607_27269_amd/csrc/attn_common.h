@@ -50,81 +50,95 @@ inline AttnDev to_dev(const Attn& a) {
   return d;
 }
 
-// K and V tiles of BKV keys, staged global -> registers -> LDS in their natural
-// [key][dim] layout (16-byte chunks).  Source addresses are formed once per workgroup and
-// advanced by one tile per step; only the ragged last tile checks the sequence end.
-template <int DQK, int DV, int NTHR>
-struct KVStage {
-  static constexpr int KCH = BKV * (DQK / 8);
-  static constexpr int KPER = (KCH + NTHR - 1) / NTHR;
-  static constexpr int VCH = BKV * (DV / 8);
-  static constexpr int VPER = (VCH + NTHR - 1) / NTHR;
-  static constexpr int LDK = ld_of(DQK);
-  static constexpr int LDV = ld_of(DV);
-  u32x4 k[KPER];
-  u32x4 v[VPER];
-  const bf16_t* ksrc[KPER];
-  const bf16_t* vsrc[VPER];
-  int64_t kstr[KPER];
-  int krow[KPER], vrow[VPER];
+// Direct global -> LDS copy (gfx950 global_load_lds_dwordx4) of a [ROWS][D] bf16 tile into
+// a padded LDS tile with row stride LD.  The tile's LDS bytes are cut into 1 KB blocks; a
+// wavefront fills one block per instruction (lane l writes 16 bytes at block + 16 l) and
+// chooses each lane's global source so that the block matches the padded layout.  Lanes
+// that land on row padding, or past the last row inside the final block, load a valid
+// chunk of the tile that is never read.  Nothing passes through registers; completion is
+// awaited with a counter wait before the workgroup barrier that publishes the tile.
+template <int ROWS, int D, int LD, int NW>
+struct DmaTile {
+  static constexpr int BYTES = ROWS * LD * 2;
+  static constexpr int NBLK = (BYTES + 1023) / 1024;
+  static constexpr int PER = (NBLK + NW - 1) / NW;
+  static constexpr int ALLOC = NBLK * 512;  // bf16 elements reserved in LDS
+  short row[PER], col[PER];
 
-  __device__ __forceinline__ void init(const AttnDev& a, int b, int i) {
-    const int ga = i / a.ka_div, gb = i / a.kb_div, gv = i / a.v_div;
+  __device__ __forceinline__ void init() {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int it = 0; it < KPER; ++it) {
-      const int c = min((int)threadIdx.x + it * NTHR, KCH - 1);
-      const int key = c / (DQK / 8), dc = (c % (DQK / 8)) * 8;
-      const int64_t n = (int64_t)b * a.T + key;
-      krow[it] = key;
-      const bool nope = dc < a.dnope;
-      kstr[it] = nope ? a.ka_tok : a.kb_tok;
-      ksrc[it] = nope ? a.Ka + n * a.ka_tok + (int64_t)ga * a.ka_head + dc
-                      : a.Kb + n * a.kb_tok + (int64_t)gb * a.kb_head + (dc - a.dnope);
-    }
-#pragma unroll
-    for (int it = 0; it < VPER; ++it) {
-      const int c = min((int)threadIdx.x + it * NTHR, VCH - 1);
-      const int key = c / (DV / 8), dc = (c % (DV / 8)) * 8;
-      vrow[it] = key;
-      vsrc[it] = a.V + ((int64_t)b * a.T + key) * a.v_tok + (int64_t)gv * a.v_head + dc;
+    for (int p = 0; p < PER; ++p) {
+      const int b = wave + p * NW;
+      const int e = (b * 1024 + 16 * lane) / 2;
+      int r = e / LD, c = e % LD;
+      if (c >= D) c = 0;
+      if (r >= ROWS) r = ROWS - 1;
+      row[p] = (short)r;
+      col[p] = (short)c;
     }
   }
-
-  // tile starting at key j0 (a multiple of BKV)
-  __device__ __forceinline__ void load(const AttnDev& a, int j0) {
-    const bool full = j0 + BKV <= a.T;
+  // src(row, col) -> global address of the 16-byte chunk at (row, col) of this tile
+  template <class F>
+  __device__ __forceinline__ void issue(bf16_t* lds, F src) const {
+    const int wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int it = 0; it < KPER; ++it) {
-      u32x4 val = {0u, 0u, 0u, 0u};
-      const bool in = KCH % NTHR == 0 || (int)threadIdx.x + it * NTHR < KCH;
-      if (in && (full || j0 + krow[it] < a.T)) val = *(const u32x4*)(ksrc[it] + (int64_t)j0 * kstr[it]);
-      k[it] = val;
-    }
-#pragma unroll
-    for (int it = 0; it < VPER; ++it) {
-      u32x4 val = {0u, 0u, 0u, 0u};
-      const bool in = VCH % NTHR == 0 || (int)threadIdx.x + it * NTHR < VCH;
-      if (in && (full || j0 + vrow[it] < a.T)) val = *(const u32x4*)(vsrc[it] + (int64_t)j0 * a.v_tok);
-      v[it] = val;
-    }
-  }
-
-  __device__ __forceinline__ void store(bf16_t* ks, bf16_t* vs) const {
-#pragma unroll
-    for (int it = 0; it < KPER; ++it) {
-      const int c = (int)threadIdx.x + it * NTHR;
-      if (KCH % NTHR == 0 || c < KCH)
-        *(u32x4*)(ks + (c / (DQK / 8)) * LDK + (c % (DQK / 8)) * 8) = k[it];
-    }
-#pragma unroll
-    for (int it = 0; it < VPER; ++it) {
-      const int c = (int)threadIdx.x + it * NTHR;
-      if (VCH % NTHR == 0 || c < VCH)
-        *(u32x4*)(vs + (c / (DV / 8)) * LDV + (c % (DV / 8)) * 8) = v[it];
+    for (int p = 0; p < PER; ++p) {
+      const int b = wave + p * NW;
+      if (NBLK % NW == 0 || b < NBLK)
+        __builtin_amdgcn_global_load_lds((const void*)src(row[p], col[p]),
+                                         (__attribute__((address_space(3))) void*)(lds + b * 512),
+                                         16, 0, 0);
     }
   }
 };
 
+// all outstanding memory operations of this wavefront (incl. LDS DMA) complete
+__device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
+
+// K and V tiles of BKV keys streamed straight into padded [key][dim] LDS tiles.  Keys at or
+// past the sequence end load the last valid key (finite data; such keys are causally
+// masked or carry zero probability).
+template <int DQK, int DV, int NW>
+struct KVStage {
+  static constexpr int LDK = ld_of(DQK);
+  static constexpr int LDV = ld_of(DV);
+  using KT = DmaTile<BKV, DQK, LDK, NW>;
+  using VT = DmaTile<BKV, DV, LDV, NW>;
+  static constexpr int KS = KT::ALLOC;  // LDS elements of the K tile
+  static constexpr int VS = VT::ALLOC;
+  KT kt;
+  VT vt;
+  const bf16_t* ka;   // key rows of this (sequence, head): element (n, d) at ka + n*ka_tok + d
+  const bf16_t* kb;
+  const bf16_t* vb;
+  int64_t ka_tok, kb_tok, v_tok;
+  int dnope, T;
+
+  __device__ __forceinline__ void init(const AttnDev& a, int b, int i) {
+    kt.init();
+    vt.init();
+    const int64_t n0 = (int64_t)b * a.T;
+    ka = a.Ka + n0 * a.ka_tok + (int64_t)(i / a.ka_div) * a.ka_head;
+    kb = a.Kb + n0 * a.kb_tok + (int64_t)(i / a.kb_div) * a.kb_head - a.dnope;
+    vb = a.V + n0 * a.v_tok + (int64_t)(i / a.v_div) * a.v_head;
+    ka_tok = a.ka_tok; kb_tok = a.kb_tok; v_tok = a.v_tok;
+    dnope = a.dnope; T = a.T;
+  }
+
+  // keys j0 .. j0+BKV-1 into (ks, vs)
+  __device__ __forceinline__ void issue(int j0, bf16_t* ks, bf16_t* vs) const {
+    const int last = T - 1;
+    kt.issue(ks, [&](int r, int c) {
+      const int64_t n = min(j0 + r, last);
+      return c < dnope ? ka + n * ka_tok + c : kb + n * kb_tok + c;
+    });
+    vt.issue(vs, [&](int r, int c) {
+      const int64_t n = min(j0 + r, last);
+      return vb + n * v_tok + c;
+    });
+  }
+};
 
 }  // namespace attn
 }  // namespace mla

@@ -1,8 +1,9 @@
 // Causal softmax attention (Eq. 2-4) on gfx950 matrix cores, bf16 operands, fp32 softmax.
 //
 // Forward.  A workgroup (8 wavefronts) owns 256 queries of one (sequence, head); each
-// wavefront owns 32 of them.  Keys/values stream through LDS 64 at a time (double
-// buffered, the next tile's global loads in flight during the current tile's math).
+// wavefront owns 32 of them.  Keys/values stream through LDS 64 at a time, double
+// buffered and copied straight from HBM into LDS (the next tile's copy is in flight
+// during the current tile's math).
 // The logits are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: the
 // query is the MFMA column, so every lane owns one query and the online-softmax state
 // (running max m, running sum l, the output row O^T) of that query lives in that lane.
@@ -29,11 +30,10 @@ constexpr float RESCALE_SLACK = 8.f;     // log2 units the running reference max
 
 template <int DQK, int DV, bool LSE>
 __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a) {
-  using Stage = KVStage<DQK, DV, 64 * FWD_WAVES>;
+  using Stage = KVStage<DQK, DV, FWD_WAVES>;
   constexpr int LDK = Stage::LDK, LDV = Stage::LDV;
-  constexpr int KS = BKV * LDK;
-  constexpr int VS = BKV * LDV;
-  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (KS + VS)];
+  constexpr int KS = Stage::KS, VS = Stage::VS;
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * (KS + VS)];
   constexpr int NKK = DQK / 16;  // MFMA K-steps of the logits
   constexpr int NC = DV / 32;    // 32-row tiles of O^T
 
@@ -71,14 +71,17 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   const int nkb = (kend + BKV - 1) / BKV;
   Stage st;
   st.init(a, b, i);
-  st.load(a, 0);
-  st.store(smem, smem + KS);
+  st.issue(0, smem, smem + KS);
+  wait_all();
   __syncthreads();
 
   for (int kb = 0; kb < nkb; ++kb) {
     const int cur = kb & 1;
     const int j0 = kb * BKV;
-    if (kb + 1 < nkb) st.load(a, j0 + BKV);
+    if (kb + 1 < nkb) {
+      bf16_t* nxt = smem + (cur ^ 1) * (KS + VS);
+      st.issue(j0 + BKV, nxt, nxt + KS);
+    }
     const bf16_t* ks = smem + cur * (KS + VS);
     const bf16_t* vs = ks + KS;
     if (j0 <= qw0 + 31) {  // wave-uniform: some key of this tile is visible to the wave
@@ -144,10 +147,7 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
                                                              pf[u], acc_o[c], 0, 0, 0);
       }
     }
-    if (kb + 1 < nkb) {
-      bf16_t* nxt = smem + (cur ^ 1) * (KS + VS);
-      st.store(nxt, nxt + KS);
-    }
+    wait_all();
     __syncthreads();
   }
 
