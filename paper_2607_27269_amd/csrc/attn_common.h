@@ -50,52 +50,6 @@ inline AttnDev to_dev(const Attn& a) {
   return d;
 }
 
-// Direct global -> LDS copy (gfx950 global_load_lds_dwordx4) of a [ROWS][D] bf16 tile into
-// a padded LDS tile with row stride LD.  The tile's LDS bytes are cut into 1 KB blocks; a
-// wavefront fills one block per instruction (lane l writes 16 bytes at block + 16 l) and
-// chooses each lane's global source so that the block matches the padded layout.  Lanes
-// that land on row padding, or past the last row inside the final block, load a valid
-// chunk of the tile that is never read.  Nothing passes through registers; completion is
-// awaited with a counter wait before the workgroup barrier that publishes the tile.
-template <int ROWS, int D, int LD, int NW>
-struct DmaTile {
-  static constexpr int BYTES = ROWS * LD * 2;
-  static constexpr int NBLK = (BYTES + 1023) / 1024;
-  static constexpr int PER = (NBLK + NW - 1) / NW;
-  static constexpr int ALLOC = NBLK * 512;  // bf16 elements reserved in LDS
-  short row[PER], col[PER];
-
-  __device__ __forceinline__ void init() {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int b = wave + p * NW;
-      const int e = (b * 1024 + 16 * lane) / 2;
-      int r = e / LD, c = e % LD;
-      if (c >= D) c = 0;
-      if (r >= ROWS) r = ROWS - 1;
-      row[p] = (short)r;
-      col[p] = (short)c;
-    }
-  }
-  // src(row, col) -> global address of the 16-byte chunk at (row, col) of this tile
-  template <class F>
-  __device__ __forceinline__ void issue(bf16_t* lds, F src) const {
-    const int wave = threadIdx.x >> 6;
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int b = wave + p * NW;
-      if (NBLK % NW == 0 || b < NBLK)
-        __builtin_amdgcn_global_load_lds((const void*)src(row[p], col[p]),
-                                         (__attribute__((address_space(3))) void*)(lds + b * 512),
-                                         16, 0, 0);
-    }
-  }
-};
-
-// all outstanding memory operations of this wavefront (incl. LDS DMA) complete
-__device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
-
 // K and V tiles of BKV keys streamed straight into padded [key][dim] LDS tiles.  Keys at or
 // past the sequence end load the last valid key (finite data; such keys are causally
 // masked or carry zero probability).

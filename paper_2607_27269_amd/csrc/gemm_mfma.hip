@@ -8,8 +8,9 @@
 // in LDS in the operand's natural layout: k-major tiles as [row][k] (16-byte operand reads,
 // 8 consecutive k per lane) and m-major tiles as [k][row], whose operands come from
 // gfx950's transposing LDS read.  Both give the same k order inside an MFMA step, so the
-// two kinds mix freely.  LDS is double buffered: the next slice's global loads are in
-// flight while the current one feeds the matrix cores; row strides are padded so that the
+// two kinds mix freely.  LDS is double buffered: full K slices are copied straight from
+// HBM into LDS (global_load_lds) while the current slice feeds the matrix cores; a ragged
+// last slice goes through registers with zero fill.  Row strides are padded so that the
 // operand reads of a wavefront hit distinct banks.  Large problems use 256 x 256 tiles on
 // 8 wavefronts (128 x 64 each), which halves the LDS bytes per MFMA compared with
 // 128 x 128 tiles on 4 wavefronts (64 x 64 each), used for small problems.  Workgroup
@@ -61,7 +62,7 @@ template <int ROWS, int NTHR>
 struct Loader<true, ROWS, NTHR> {
   static constexpr int CHUNKS = ROWS * (BK / 8);
   static constexpr int PER = CHUNKS / NTHR;
-  static constexpr int ELEMS = ROWS * KM_LD;
+  static constexpr int ELEMS = ((ROWS * KM_LD * 2 + 1023) / 1024) * 512;  // whole 1 KB blocks
   static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
   u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
@@ -83,6 +84,15 @@ struct Loader<true, ROWS, NTHR> {
       *(u32x4*)(lds + (c / (BK / 8)) * KM_LD + (c % (BK / 8)) * 8) = r[i];
     }
   }
+  // full k-slice straight from HBM into LDS (rows past the end repeat the last row;
+  // their outputs are not stored)
+  using Dma = DmaTile<ROWS, BK, KM_LD, NTHR / 64>;
+  __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
+                                      int row0, int rows_valid, int k0, bf16_t* lds) const {
+    const bf16_t* base = p + (int64_t)row0 * ld + k0;
+    const int rl = rows_valid - 1;
+    t.issue(lds, [&](int r, int c) { return base + (int64_t)min(r, rl) * ld + c; });
+  }
   // operand fragment: rows row0 + lane%32, k = 16 kk + 8 half + 0..7
   static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
     const int lane = threadIdx.x & 63;
@@ -97,7 +107,7 @@ struct Loader<false, ROWS, NTHR> {
   static constexpr int CPR = ROWS / 8;
   static constexpr int CHUNKS = BK * CPR;
   static constexpr int PER = CHUNKS / NTHR;
-  static constexpr int ELEMS = BK * LD;
+  static constexpr int ELEMS = ((BK * LD * 2 + 1023) / 1024) * 512;  // whole 1 KB blocks
   static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
   u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
@@ -118,6 +128,13 @@ struct Loader<false, ROWS, NTHR> {
       const int c = threadIdx.x + i * NTHR;
       *(u32x4*)(lds + (c / CPR) * LD + (c % CPR) * 8) = r[i];
     }
+  }
+  using Dma = DmaTile<BK, ROWS, LD, NTHR / 64>;
+  __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
+                                      int row0, int rows_valid, int k0, bf16_t* lds) const {
+    const bf16_t* base = p + (int64_t)k0 * ld + row0;
+    const int cl = rows_valid - 8;
+    t.issue(lds, [&](int r, int c) { return base + (int64_t)r * ld + min(c, cl); });
   }
   static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
     const int klo = 16 * kk + 8 * ((threadIdx.x & 63) >> 5);
@@ -141,7 +158,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
   using LA = Loader<AK, BM, NTHR>;
   using LB = Loader<BKM, BN, NTHR>;
   constexpr int STAGE = LA::ELEMS + LB::ELEMS;
-  __shared__ __attribute__((aligned(16))) bf16_t lds[2 * STAGE];
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * STAGE];
 
   const int ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
   const int ntiles = ntm * ntn;
@@ -172,21 +189,32 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
 
   LA la;
   LB lb;
+  typename LA::Dma da;
+  typename LB::Dma db;
+  da.init();
+  db.init();
   const int mvalid = g.M - m0, nvalid = g.N - n0;
   const int nk = (kend - kbeg + BK - 1) / BK;
-  if (nk > 0) {
-    la.load(g.A, g.lda, m0, mvalid, kbeg, kend);
-    lb.load(g.B, g.ldb, n0, nvalid, kbeg, kend);
-    la.store(lds);
-    lb.store(lds + LA::ELEMS);
-  }
+  const int nfull = (kend - kbeg) / BK;  // slices copied straight to LDS; a ragged last
+                                         // slice goes through registers with zero fill
+  auto stage = [&](int kt, bf16_t* dst) {
+    const int k0 = kbeg + kt * BK;
+    if (kt < nfull) {
+      la.dma(da, g.A, g.lda, m0, mvalid, k0, dst);
+      lb.dma(db, g.B, g.ldb, n0, nvalid, k0, dst + LA::ELEMS);
+    } else {
+      la.load(g.A, g.lda, m0, mvalid, k0, kend);
+      lb.load(g.B, g.ldb, n0, nvalid, k0, kend);
+      la.store(dst);
+      lb.store(dst + LA::ELEMS);
+    }
+  };
+  if (nk > 0) stage(0, lds);
+  wait_all();
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
-    if (kt + 1 < nk) {
-      la.load(g.A, g.lda, m0, mvalid, kbeg + (kt + 1) * BK, kend);
-      lb.load(g.B, g.ldb, n0, nvalid, kbeg + (kt + 1) * BK, kend);
-    }
+    if (kt + 1 < nk) stage(kt + 1, lds + (cur ^ 1) * STAGE);
     const bf16_t* As = lds + cur * STAGE;
     const bf16_t* Bs = As + LA::ELEMS;
 #pragma unroll
@@ -202,11 +230,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
         for (int j = 0; j < TN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
     }
-    if (kt + 1 < nk) {
-      bf16_t* nxt = lds + (cur ^ 1) * STAGE;
-      la.store(nxt);
-      lb.store(nxt + LA::ELEMS);
-    }
+    wait_all();
     __syncthreads();
   }
 
