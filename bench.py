@@ -34,7 +34,85 @@ def parse():
     p.add_argument("--config", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-seq", type=int, default=4096, help="oracle sample: tokens of one sequence")
+    p.add_argument("--calib-copy-mb", type=int, default=0,
+                   help="run one device-to-device copy of this many MiB first (HBM counter calibration)")
+    p.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                   help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) "
+                        "of a --calib-copy-mb run into per-class HBM bytes per launch; print JSON")
     return p.parse_args()
+
+
+# kernel-name fragments of each timing class, as rocprofv3 reports them
+CLASS_PATTERNS = {
+    "gemm_nt": ("gemm_mfma_kernel<", ", true, true,"),
+    "gemm_nn": ("gemm_mfma_kernel<", ", true, false,"),
+    "gemm_tn": ("gemm_mfma_kernel<", ", false, false,"),
+    "attn_fwd": ("attn_fwd_mfma_kernel<",),
+    "attn_bwd_dkdv": ("attn_dkdv_mfma_kernel<",),
+    "attn_bwd_dq": ("attn_dq_mfma_kernel<",),
+    "loss": ("loss_main_kernel<",),
+}
+# sources whose change invalidates stored counter readings
+TRAFFIC_SOURCES = ["paper_2607_27269_amd/csrc/gemm_mfma.hip", "paper_2607_27269_amd/csrc/attn_fwd.hip",
+                   "paper_2607_27269_amd/csrc/attn_bwd.hip", "paper_2607_27269_amd/csrc/attn_common.h",
+                   "paper_2607_27269_amd/csrc/common.h", "paper_2607_27269_amd/csrc/elementwise.hip",
+                   "paper_2607_27269_amd/csrc/api.cpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+
+
+def sources_digest():
+    import hashlib
+    h = hashlib.sha1()
+    for f in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def summarize_traffic(fetch_csv, write_csv, copy_mb):
+    """HBM bytes per launch of each timing class from FETCH_SIZE / WRITE_SIZE (KiB per
+    dispatch), each scaled so that the calibration copy reads and writes copy_mb MiB."""
+    import csv
+    def read(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        per = {}
+        for r in rows:
+            key = (r["Dispatch_Id"], r["Kernel_Name"])
+            per[key] = per.get(key, 0.0) + float(r["Counter_Value"]) * 1024.0
+        return per
+    fetch, write = read(fetch_csv, "FETCH_SIZE"), read(write_csv, "WRITE_SIZE")
+    known = copy_mb * 1024.0 * 1024.0
+    def copy_value(d):
+        # the calibration copy is the largest non-library dispatch named like a copy
+        cands = [v for (i, n), v in d.items() if "copy" in n.lower() or "Copy" in n]
+        return max(cands) if cands else None
+    fc, wc = copy_value(fetch), copy_value(write)
+    out = {"copy_mb": copy_mb, "fetch_scale": known / fc if fc else None,
+           "write_scale": known / wc if wc else None, "classes": {}}
+    for cls, pats in CLASS_PATTERNS.items():
+        fv = [v for (i, n), v in fetch.items() if all(p in n for p in pats)]
+        wv = [v for (i, n), v in write.items() if all(p in n for p in pats)]
+        if not fv or not wv or not fc or not wc:
+            continue
+        out["classes"][cls] = {"launches": len(fv),
+                               "bytes_per_launch": (sum(fv) * out["fetch_scale"] + sum(wv) * out["write_scale"]) / len(fv),
+                               "read_bytes_per_launch": sum(fv) * out["fetch_scale"] / len(fv),
+                               "write_bytes_per_launch": sum(wv) * out["write_scale"] / len(wv)}
+    out["sources_sha1"] = sources_digest()
+    return out
+
+
+def stored_traffic(cls):
+    """Counter-derived HBM bytes per launch for `cls`, if taken on the current sources."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            t = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    if t.get("sources_sha1") != sources_digest():
+        return None
+    c = t.get("classes", {}).get(cls)
+    return None if c is None else c["bytes_per_launch"]
 
 
 def cpu_baseline(cfg, wl, seq):
@@ -67,6 +145,9 @@ def cpu_baseline(cfg, wl, seq):
 
 def main():
     args = parse()
+    if args.summarize_traffic:
+        print(json.dumps(summarize_traffic(*args.summarize_traffic, args.calib_copy_mb or 1024), indent=1))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the reconstruction step is not sharded across "
               "GPUs (layers are independent); run with --gpus 1", file=sys.stderr)
@@ -76,6 +157,15 @@ def main():
     from paper_2607_27269_amd import _lib as L
     from paper_2607_27269_amd import configs, synth
     from paper_2607_27269_amd.step import DeviceStep
+
+    if args.calib_copy_mb:
+        n = args.calib_copy_mb * 1024 * 1024 // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
 
     cfg = configs.get(args.config)
     wl = synth.make_workload(cfg)
@@ -148,7 +238,7 @@ def main():
         "kernel_ms_per_step": kernel_share,
         "roofline": {"kernel": f"{dom}: {L.KCLASS_KERNELS[dom]}", "bound": bound, "achieved": round(achieved, 2),
                      "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
-                     "traffic": None,
+                     "traffic": stored_traffic(dom),
                      "launches_per_step": p["launches"] / args.steps},
         "loss": loss,
     }

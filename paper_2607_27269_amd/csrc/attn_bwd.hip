@@ -8,7 +8,7 @@
 //
 // * dK/dV: a workgroup owns 128 keys of one (sequence, KV group); each of its 4
 //   wavefronts owns 32 keys (K staged once in LDS, V held as MFMA B-operand fragments) and walks
-//   every head of the group and every 64-query block at or after its keys.  S = Q K^T and
+//   every 64-query block at or after its keys (last block first) and every head of the group.  S = Q K^T and
 //   dP = dO V^T put the key in the MFMA column, so the accumulators of P and dS are
 //   directly the B operands of dV^T += dO^T P and dK^T += Q^T dS; dO^T and Q^T come from
 //   the natural [query][dim] LDS tiles through gfx950's transposing LDS read.  The rotary
@@ -161,21 +161,26 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
   const int niter = hpg * nper;
   Stage stg;
   stg.init();
+  // step it -> (query block, head): query blocks in descending order with the group's heads
+  // innermost, so that all key blocks of a (sequence, group) stream the same Q/dO tile at
+  // the same time and share it through L2
+  auto q_of = [&](int it) { return (nqb - 1 - it / hpg) * BQB; };
+  auto h_of = [&](int it) { return i0 + it % hpg; };
   if (niter > 0) {
-    stg.issue(w, b, i0, qb0 * BQB, smem);
+    stg.issue(w, b, h_of(0), q_of(0), smem);
     stg.store_stats(smem);
   }
   wait_all();
   __syncthreads();
 
   for (int it = 0; it < niter; ++it) {
-    const int q0 = (qb0 + it % nper) * BQB;
+    const int q0 = q_of(it);
     const bf16_t* Qs = smem + (it & 1) * Stage::BUF;
     const bf16_t* dOs = Qs + Stage::QS;
     const float* st_lse = (const float*)(dOs + Stage::OS);
     const float* st_dl = st_lse + BQB;
     if (it + 1 < niter)
-      stg.issue(w, b, i0 + (it + 1) / nper, (qb0 + (it + 1) % nper) * BQB, smem + ((it + 1) & 1) * Stage::BUF);
+      stg.issue(w, b, h_of(it + 1), q_of(it + 1), smem + ((it + 1) & 1) * Stage::BUF);
 
     if (kw0 <= min(q0 + BQB - 1, a.T - 1)) {  // wave-uniform: some pair is visible
       f32x16 sp[2], dp[2];
