@@ -106,6 +106,19 @@ __device__ __forceinline__ bf16x8 lds_operand_tr(const bf16_t* base, int ld, int
 // that land on row padding, or past the last row inside the final block, load a valid
 // chunk of the tile that is never read.  Nothing passes through registers; completion is
 // awaited with a counter wait before the workgroup barrier that publishes the tile.
+//
+// The copy is issued from inline assembly: with a global_load_lds in flight the compiler's
+// counter bookkeeping cannot tell which LDS results are ready and waits for all of them
+// (lgkmcnt(0)) before each use, which serialises the operand reads of the next MFMA step
+// with the current one.  Out of its sight, the copies are awaited explicitly (wait_all,
+// itself inline assembly so that it is never relaxed) before the barrier that publishes
+// the tile.  m0 holds the wavefront's LDS destination; lane l writes 16 bytes at m0 + 16 l.
+__device__ __forceinline__ void dma16(const bf16_t* gsrc, bf16_t* lds_dst) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)lds_dst);
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gsrc), "{m0}"(l) : "memory");
+}
+
 template <int ROWS, int D, int LD, int NW>
 struct DmaTile {
   static constexpr int BYTES = ROWS * LD * 2;
@@ -135,14 +148,14 @@ struct DmaTile {
     for (int p = 0; p < PER; ++p) {
       const int b = wave + p * NW;
       if (NBLK % NW == 0 || b < NBLK)
-        __builtin_amdgcn_global_load_lds((const void*)src(row[p], col[p]),
-                                         (__attribute__((address_space(3))) void*)(lds + b * 512),
-                                         16, 0, 0);
+        dma16(src(row[p], col[p]), lds + b * 512);
     }
   }
 };
 
 // all outstanding memory operations of this wavefront (incl. LDS DMA) complete
-__device__ __forceinline__ void wait_all() { __builtin_amdgcn_s_waitcnt(0); }
+__device__ __forceinline__ void wait_all() {
+  asm volatile("s_waitcnt vmcnt(0) expcnt(0) lgkmcnt(0)" : : : "memory");
+}
 
 }  // namespace mla

@@ -10,7 +10,11 @@
 // gfx950's transposing LDS read.  Both give the same k order inside an MFMA step, so the
 // two kinds mix freely.  LDS is double buffered: full K slices are copied straight from
 // HBM into LDS (global_load_lds) while the current slice feeds the matrix cores; a ragged
-// last slice goes through registers with zero fill.  Row strides are padded so that the
+// last slice goes through registers with zero fill.  Operand fragments are double buffered
+// in registers as well: the LDS reads of the next 16-wide k step are in flight while the
+// matrix cores work on the current one, and the first step of the next slice is read
+// right after the barrier that publishes it.  The epilogue stages each 32-row strip of a
+// wavefront's tile in LDS and writes it back with 16-byte (fp32) or 8-byte (bf16) stores.  Row strides are padded so that the
 // operand reads of a wavefront hit distinct banks.  Large problems use 256 x 256 tiles on
 // 8 wavefronts (128 x 64 each), which halves the LDS bytes per MFMA compared with
 // 128 x 128 tiles on 4 wavefronts (64 x 64 each), used for small problems.  Workgroup
@@ -149,6 +153,29 @@ __device__ __forceinline__ void store_out<float>(float* p, float v) { *p = v; }
 template <>
 __device__ __forceinline__ void store_out<bf16_t>(bf16_t* p, float v) { *p = f2bf(v); }
 
+// four consecutive outputs: alpha * v + beta * C
+template <typename TC>
+__device__ __forceinline__ void store4(TC* p, f32x4 v, float alpha, float beta);
+template <>
+__device__ __forceinline__ void store4<float>(float* p, f32x4 v, float alpha, float beta) {
+  f32x4 o = v * alpha;
+  if (beta != 0.f) o += beta * *(const f32x4*)p;
+  *(f32x4*)p = o;
+}
+template <>
+__device__ __forceinline__ void store4<bf16_t>(bf16_t* p, f32x4 v, float alpha, float beta) {
+  f32x4 o = v * alpha;
+  if (beta != 0.f) {
+    const u32x2 c = *(const u32x2*)p;
+    o[0] += beta * bf2f((bf16_t)(c[0] & 0xffff)); o[1] += beta * bf2f((bf16_t)(c[0] >> 16));
+    o[2] += beta * bf2f((bf16_t)(c[1] & 0xffff)); o[3] += beta * bf2f((bf16_t)(c[1] >> 16));
+  }
+  u32x2 w;
+  w[0] = (uint32_t)f2bf(o[0]) | ((uint32_t)f2bf(o[1]) << 16);
+  w[1] = (uint32_t)f2bf(o[2]) | ((uint32_t)f2bf(o[3]) << 16);
+  *(u32x2*)p = w;
+}
+
 // ---- the kernel --------------------------------------------------------------------------
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
@@ -212,46 +239,87 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
   if (nk > 0) stage(0, lds);
   wait_all();
   __syncthreads();
+  // fragments of one 16-wide k step, double buffered in registers: the reads of step
+  // kk + 1 are issued before the matrix ops of step kk
+  bf16x8 af[2][TM], bfr[2][TN];
+  auto load_frags = [&](const bf16_t* As, int kk, bf16x8* a, bf16x8* b) {
+    const bf16_t* Bs = As + LA::ELEMS;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) a[i] = LA::frag(As, wrow0 + i * 32, kk);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) b[j] = LB::frag(Bs, wcol0 + j * 32, kk);
+  };
+  auto mma = [&](const bf16x8* a, const bf16x8* b) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  };
+  if (nk > 0) load_frags(lds, 0, af[0], bfr[0]);
   for (int kt = 0; kt < nk; ++kt) {
     const int cur = kt & 1;
     if (kt + 1 < nk) stage(kt + 1, lds + (cur ^ 1) * STAGE);
     const bf16_t* As = lds + cur * STAGE;
-    const bf16_t* Bs = As + LA::ELEMS;
 #pragma unroll
     for (int kk = 0; kk < BK / 16; ++kk) {
-      bf16x8 af[TM], bfr[TN];
-#pragma unroll
-      for (int i = 0; i < TM; ++i) af[i] = LA::frag(As, wrow0 + i * 32, kk);
-#pragma unroll
-      for (int j = 0; j < TN; ++j) bfr[j] = LB::frag(Bs, wcol0 + j * 32, kk);
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+      if (kk + 1 < BK / 16) {
+        load_frags(As, kk + 1, af[(kk + 1) & 1], bfr[(kk + 1) & 1]);
+      } else {
+        // next slice: its copy must have landed and every wave must be done with this one
+        wait_all();
+        __syncthreads();
+        if (kt + 1 < nk) load_frags(lds + (cur ^ 1) * STAGE, 0, af[0], bfr[0]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mma(af[kk & 1], bfr[kk & 1]);
+      __builtin_amdgcn_sched_barrier(0);
     }
-    wait_all();
-    __syncthreads();
   }
 
-  // epilogue: lane holds column (lane % 32) and rows 8*(e/4) + 4*(lane/32) + e%4 of a tile
+  // epilogue: each wavefront stages one 32-row strip of its tile at a time in a private
+  // LDS region (the main loop's last barrier has retired every operand read) and writes
+  // it back row by row, 4 consecutive columns per lane.  In the MFMA result a lane holds
+  // column lane % 32 and rows 8 (e / 4) + 4 (lane / 32) + e % 4 of each 32 x 32 block.
+  constexpr int WTN = BN / WN;              // columns of the wave tile
+  constexpr int SLD = WTN + 8;              // strip row stride (floats)
+  static_assert(NTHR / 64 * 32 * SLD * 4 <= (int)sizeof(lds), "epilogue strip too large");
+  float* strip = (float*)lds + wave * 32 * SLD;
+  TC* C = (TC*)g.C;
+  const bool vec = (g.ldc % 4) == 0;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-      const int n = n0 + wcol0 + j * 32 + (lane & 31);
-      if (n >= g.N) continue;
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int m = m0 + wrow0 + i * 32 + (e >> 2) * 8 + (lane >> 5) * 4 + (e & 3);
-        if (m >= g.M) continue;
-        if (g.part) {
-          g.part[((int64_t)split * g.M + m) * g.N + n] = acc[i][j][e];
+      for (int e = 0; e < 16; ++e)
+        strip[((e >> 2) * 8 + (lane >> 5) * 4 + (e & 3)) * SLD + j * 32 + (lane & 31)] =
+            acc[i][j][e];
+    constexpr int CPR = WTN / 4;            // float4 chunks per strip row
+#pragma unroll
+    for (int it = 0; it < 32 * CPR / 64; ++it) {
+      const int c = it * 64 + lane;
+      const int r = c / CPR, col = (c % CPR) * 4;
+      const int m = m0 + wrow0 + i * 32 + r, n = n0 + wcol0 + col;
+      if (m >= g.M || n >= g.N) continue;
+      const f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+      if (g.part) {
+        float* p = g.part + ((int64_t)split * g.M + m) * g.N + n;
+        if (n + 4 <= g.N && (g.N % 4) == 0) {
+          *(f32x4*)p = v;
         } else {
-          TC* c = (TC*)g.C + (int64_t)m * g.ldc + n;
-          float v = g.alpha * acc[i][j][e];
-          if (g.beta != 0.f) v += g.beta * ld(c);
-          store_out<TC>(c, v);
+          for (int q = 0; q < 4 && n + q < g.N; ++q) p[q] = v[q];
+        }
+        continue;
+      }
+      TC* p = C + (int64_t)m * g.ldc + n;
+      if (vec && n + 4 <= g.N) {
+        store4<TC>(p, v, g.alpha, g.beta);
+      } else {
+        for (int q = 0; q < 4 && n + q < g.N; ++q) {
+          float x = g.alpha * v[q];
+          if (g.beta != 0.f) x += g.beta * ld(p + q);
+          store_out<TC>(p + q, x);
         }
       }
     }
