@@ -49,7 +49,8 @@ CLASS_PATTERNS = {
     "gemm_tn": ("gemm_mfma_kernel<", ", false, false,"),
     "attn_fwd": ("attn_fwd_mfma_kernel<",),
     "attn_bwd_dkdv": ("attn_dkdv_mfma_kernel<",),
-    "attn_bwd_dq": ("attn_dq_mfma_kernel<",),
+    "attn_bwd_dq": ("attn_ds_gemm_kernel<", ", false, false,"),
+    "attn_bwd_dk": ("attn_ds_gemm_kernel<", ", true, false,"),
     "loss": ("loss_main_kernel<",),
 }
 # sources whose change invalidates stored counter readings

@@ -147,9 +147,10 @@ const char *mla_recon_last_error(void);
  * waits for those events, returns the summed kernel time (ms), the launch count and the
  * algorithmic FLOPs and HBM bytes those launches account for, and clears the record.
  * Classes: 0 GEMM C = A B^T, 1 GEMM with B N-contiguous, 2 GEMM with both operands
- * M/N-contiguous (weight gradients), 3 attention forward, 4 attention backward dK/dV,
- * 5 attention backward dQ, 6 loss, 7 elementwise
- * (RoPE, reductions, conversions).  Up to 4096 launches are recorded per class. */
+ * M/N-contiguous (weight gradients), 3 attention forward, 4 attention backward dK/dV
+ * (dV only, plus the stored dS^T, when class 8 runs), 5 attention backward dQ, 6 loss,
+ * 7 elementwise (RoPE, reductions, conversions), 8 attention backward dK as a GEMM over
+ * the stored dS^T.  Up to 4096 launches are recorded per class. */
 int mla_recon_prof_enable(int kernel_class, int on);
 int mla_recon_prof_read(int kernel_class, double *total_ms, int64_t *launches,
                         double *alg_flops, double *alg_bytes);

@@ -22,19 +22,22 @@ MLA_ERR_HIP = -4
 MLA_BF16 = 0
 MLA_FP32 = 1
 
-KC_GEMM_NT, KC_GEMM_NN, KC_GEMM_TN, KC_ATTN_FWD, KC_ATTN_DKDV, KC_ATTN_DQ, KC_LOSS, KC_ELEM = range(8)
+(KC_GEMM_NT, KC_GEMM_NN, KC_GEMM_TN, KC_ATTN_FWD, KC_ATTN_DKDV, KC_ATTN_DQ, KC_LOSS, KC_ELEM,
+ KC_ATTN_DK) = range(9)
 KCLASS_NAMES = {KC_GEMM_NT: "gemm_nt", KC_GEMM_NN: "gemm_nn", KC_GEMM_TN: "gemm_tn",
                 KC_ATTN_FWD: "attn_fwd", KC_ATTN_DKDV: "attn_bwd_dkdv", KC_ATTN_DQ: "attn_bwd_dq",
-                KC_LOSS: "loss", KC_ELEM: "elementwise"}
+                KC_LOSS: "loss", KC_ELEM: "elementwise", KC_ATTN_DK: "attn_bwd_dk"}
 # kernel function(s) behind each timing class (as rocprofv3 names them)
 KCLASS_KERNELS = {"gemm_nt": "gemm_mfma_kernel<..., true, true, ...>",
                   "gemm_nn": "gemm_mfma_kernel<..., true, false, ...>",
                   "gemm_tn": "gemm_mfma_kernel<..., false, false, float> + splitk_reduce_kernel",
                   "attn_fwd": "attn_fwd_mfma_kernel",
                   "attn_bwd_dkdv": "attn_dkdv_mfma_kernel",
-                  "attn_bwd_dq": "attn_dq_mfma_kernel",
+                  "attn_bwd_dq": "attn_ds_gemm_kernel<..., false, false, ...> (or attn_dq_mfma_kernel)",
+                  "attn_bwd_dk": "attn_ds_gemm_kernel<..., true, false, float>",
                   "loss": "mask_count_kernel + loss_main_kernel + loss_final_kernel",
-                  "elementwise": "rope_table_kernel, rope_apply_kernel, attn_delta_kernel, dkpe_finish_kernel"}
+                  "elementwise": "rope_table_kernel, rope_apply_kernel, attn_delta_kernel, dkpe_finish_kernel, "
+                                 "kcat_kernel, dk_split_kernel"}
 
 
 class MlaError(RuntimeError):

@@ -127,7 +127,8 @@ struct Layout {
   // student state kept from student_fwd to bwd
   size_t s_cos, s_sin, s_cq, s_q, s_ckv, s_knope, s_v, s_o, s_lse;
   // backward scratch
-  size_t b_do, b_delta, b_dqacc, b_dq, b_dkv, b_dkpe, b_dckv, b_dcq, b_split;
+  size_t b_do, b_delta, b_dqacc, b_dq, b_dkv, b_dkpe, b_dckv, b_dcq, b_split, b_ds, b_kcat, b_dktmp;
+  size_t b_ds_bytes;
   size_t b_split_elems;
   // loss scratch
   size_t l_scr;
@@ -156,12 +157,16 @@ static Layout layout_of(const Dims& d) {
   L.s_lse = take(N * d.H * 4);
   L.b_do = take(N * d.H * d.dv * ts);
   L.b_delta = take(N * d.H * 4);
-  L.b_dqacc = take(N * d.H * d.dqk * 4);
+  L.b_dqacc = take(d.t == DT_F32 ? N * d.H * d.dqk * 4 : 0);
   L.b_dq = take(N * d.H * d.dqk * ts);
   L.b_dkv = take(N * d.Gkv * (d.dn + d.dv) * ts);
   L.b_dkpe = take(d.Gkv * N * d.dr * 4);
   L.b_dckv = take(N * d.kv_out * ts);
   L.b_dcq = take(N * d.rq * ts);
+  L.b_ds_bytes = attn_bwd_ds_bytes((int)d.B, (int)d.H, (int)d.T, (int)d.dqk, (int)d.dv, d.t);
+  L.b_ds = take(L.b_ds_bytes);
+  L.b_kcat = take(L.b_ds_bytes ? N * d.Gkv * d.dqk * ts : 0);
+  L.b_dktmp = take(L.b_ds_bytes ? N * d.Gkv * d.dqk * 4 : 0);
   size_t se = 0;
   for (const Gemm& g : bwd_gemm_shapes(d)) se = std::max(se, gemm_scratch_elems(g));
   L.b_split_elems = se;
@@ -398,6 +403,9 @@ int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* 
   ab.dKa = dkv; ab.dka_tok = ld_dkv;
   ab.dV = dkv + (size_t)Gkv * dn * ts; ab.dv_tok = ld_dkv;
   ab.dkb_part = dkpe; ab.n_ka_groups = Gkv;
+  ab.dsT = L.b_ds_bytes ? at(ws, L.b_ds) : nullptr;
+  ab.kcat = L.b_ds_bytes ? at(ws, L.b_kcat) : nullptr;
+  ab.dk_tmp = L.b_ds_bytes ? (float*)at(ws, L.b_dktmp) : nullptr;
   HIP_TRY(attn_bwd(ab, s));
 
   if (need_q) {

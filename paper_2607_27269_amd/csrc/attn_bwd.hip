@@ -14,10 +14,16 @@
 //   the natural [query][dim] LDS tiles through gfx950's transposing LDS read.  The rotary
 //   part of dK is summed over the group's heads and left as an fp32 partial per group
 //   (the positional key may be shared by several groups).
-// * dQ: laid out like the forward (a lane owns one query; 4 wavefronts x 32 queries):
-//   S^T = K Q^T, dP^T = V dO^T, and dQ^T += K^T dS^T with K^T read transposed from the
-//   [key][dim] tile; dQ is written once in bf16 (no fp32 buffer, no atomics), then its
-//   rotary block is rotated back with R^T.
+//   With a dS^T buffer given, the kernel also stores dS^T in bf16 (the 8-byte groups of
+//   4 consecutive queries it already packs for the dK product), zeros included wherever
+//   the dQ product below reads a masked pair.
+// * dQ, preferred: dQ = scale dS K as a batched causal GEMM (one batch entry per
+//   (sequence, head)) over the stored dS^T and the keys gathered per group into one
+//   [token][group][dqk] tensor; no recomputation of S or dP.
+// * dQ, when no dS^T buffer fits: a kernel laid out like the forward (a lane owns one
+//   query; 4 wavefronts x 32 queries): S^T = K Q^T, dP^T = V dO^T, and dQ^T += K^T dS^T
+//   with K^T read transposed from the [key][dim] tile, written once in bf16.
+// Either way the rotary block of dQ is then rotated back with R^T.
 #include "attn_common.h"
 #include "mfma.h"
 #include "simt.h"
@@ -43,7 +49,14 @@ struct BwdDev {
   float* dkb_part;       // [G][N][dqk - dnope]
   int G;                 // Ka groups
   float scale;
+  bf16_t* dsT;           // [B*H][T][ds_ld] when ds_on
+  int64_t ds_ld;
+  int ds_on;
 };
+
+// dS^T tile rows a dQ GEMM row tile reads: queries from the start of the 256-query tile
+// that holds the key (the GEMM's row tile) to the end
+constexpr int DQ_TILE = 256;
 
 // ---------------------------------------------------------------------------------------
 // dK / dV
@@ -90,7 +103,8 @@ struct QStage {
   }
 };
 
-template <int DQK, int DV>
+// WITH_DK = false: dK is left to the GEMM over the stored dS^T (no dK accumulators here)
+template <int DQK, int DV, bool WITH_DK>
 __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
   using Stage = QStage<DQK, DV>;
   constexpr int LDQ = Stage::LDQ, LDO = Stage::LDO;
@@ -130,6 +144,21 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
       *(u32x4*)(Ks + key * LDQ + dc) = val;
     }
   }
+  // dS^T rows of this workgroup's keys: the queries in [tile start, k0) precede every key
+  // here, so their entries are zeros that no step below writes
+  const int zq0 = k0 / DQ_TILE * DQ_TILE;
+  if (w.ds_on && zq0 < k0) {
+    const int nz = k0 - zq0;                       // multiple of 128
+    const int cpr = nz / 8;                        // 16-byte chunks per key row
+    const int kr = min(BKB, a.T - k0);
+    for (int h = 0; h < hpg; ++h) {
+      bf16_t* plane = w.dsT + ((int64_t)b * a.H + i0 + h) * a.T * w.ds_ld;
+      for (int c = threadIdx.x; c < kr * cpr; c += 256) {
+        const int r = c / cpr, q = zq0 + (c % cpr) * 8;
+        *(u32x4*)(plane + (int64_t)(k0 + r) * w.ds_ld + q) = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  }
   const bf16_t* krow = Ks + (32 * wave + col) * LDQ + 8 * half;
   bf16x8 vf[NVK];
   {
@@ -145,9 +174,10 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
     }
   }
 
-  f32x16 dk[NCK], dv[NCV];
+  constexpr int NCKA = WITH_DK ? NCK : 1;
+  f32x16 dk[NCKA], dv[NCV];
 #pragma unroll
-  for (int c = 0; c < NCK; ++c)
+  for (int c = 0; c < NCKA; ++c)
 #pragma unroll
     for (int e = 0; e < 16; ++e) dk[c][e] = 0.f;
 #pragma unroll
@@ -182,6 +212,11 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
     if (it + 1 < niter)
       stg.issue(w, b, h_of(it + 1), q_of(it + 1), smem + ((it + 1) & 1) * Stage::BUF);
 
+    // this lane's dS^T row segment for the block: queries q0 + 4 half + {0..3, 8..11, ...}
+    // (a wave-uniform plane base and a 32-bit lane offset)
+    bf16_t* dsplane = w.ds_on ? w.dsT + ((int64_t)b * a.H + h_of(it)) * a.T * w.ds_ld : nullptr;
+    const uint32_t dsoff = (uint32_t)my_key * (uint32_t)w.ds_ld + (uint32_t)(q0 + 4 * half);
+    const bool dsrow = dsplane != nullptr && my_key < a.T;
     if (kw0 <= min(q0 + BQB - 1, a.T - 1)) {  // wave-uniform: some pair is visible
       f32x16 sp[2], dp[2];
 #pragma unroll
@@ -220,6 +255,16 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
             dp[qt][e] = p * (dp[qt][e] - dl[r]);
           }
         }
+      // dS^T in bf16: element e of tile qt is query 32 qt + 8 (e/4) + 4 half + e%4
+      if (dsrow) {
+#pragma unroll
+        for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+          for (int e4 = 0; e4 < 4; ++e4)
+            st_global8(dsplane + dsoff + (32 * qt + 8 * e4),
+                       u32x2{pack2bf(dp[qt][4 * e4], dp[qt][4 * e4 + 1]),
+                             pack2bf(dp[qt][4 * e4 + 2], dp[qt][4 * e4 + 3])});
+      }
       // dV^T += dO^T P,  dK^T += Q^T dS   (K-step u: queries 32(u/2) + 16(u%2) + {4h.., 8+4h..})
 #pragma unroll
       for (int u = 0; u < 4; ++u) {
@@ -235,11 +280,17 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
         for (int c = 0; c < NCV; ++c)
           dv[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(dOs, LDO, 32 * c, klo, klo + 8),
                                                          pf, dv[c], 0, 0, 0);
+        if constexpr (WITH_DK) {
 #pragma unroll
-        for (int c = 0; c < NCK; ++c)
-          dk[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(Qs, LDQ, 32 * c, klo, klo + 8),
-                                                         sf, dk[c], 0, 0, 0);
+          for (int c = 0; c < NCK; ++c)
+            dk[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                lds_operand_tr(Qs, LDQ, 32 * c, klo, klo + 8), sf, dk[c], 0, 0, 0);
+        }
       }
+    } else if (dsrow) {
+      // every key of this wavefront follows every query of the block: zeros
+#pragma unroll
+      for (int o = 0; o < BQB; o += 8) st_global8(dsplane + dsoff + o, u32x2{0u, 0u});
     }
     if (it + 1 < niter) stg.store_stats(smem + ((it + 1) & 1) * Stage::BUF);
     wait_all();
@@ -258,9 +309,10 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
       u32x2 wv = {pack2bf(dv[c][4 * e4], dv[c][4 * e4 + 1]), pack2bf(dv[c][4 * e4 + 2], dv[c][4 * e4 + 3])};
       *(u32x2*)(w.dV + n * w.dv_tok + (int64_t)g * DV + d) = wv;
     }
+  if constexpr (!WITH_DK) return;
   const float sc = w.scale;
 #pragma unroll
-  for (int c = 0; c < NCK; ++c)
+  for (int c = 0; c < NCKA; ++c)
 #pragma unroll
     for (int e4 = 0; e4 < 4; ++e4) {
       const int d = 32 * c + 8 * e4 + 4 * half;
@@ -398,6 +450,45 @@ __global__ __launch_bounds__(256) void attn_dq_mfma_kernel(BwdDev w) {
     }
 }
 
+// kcat[n][g][d] = the logit key of Ka group g at token n: d < dnope from Ka, the rest from
+// Kb (rope group of the group's first head); 8 elements per thread
+__global__ void kcat_kernel(AttnDev a, int G, int DQK, bf16_t* __restrict__ out) {
+  const int cpr = DQK / 8;
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = (int64_t)a.B * a.T * G * cpr;
+  if (c >= total) return;
+  const int d = (int)(c % cpr) * 8;
+  const int64_t ng = c / cpr;
+  const int g = (int)(ng % G);
+  const int64_t n = ng / G;
+  const int i = g * (a.H / G);
+  const bf16_t* src = d < a.dnope
+                          ? a.Ka + n * a.ka_tok + (int64_t)(i / a.ka_div) * a.ka_head + d
+                          : a.Kb + n * a.kb_tok + (int64_t)(i / a.kb_div) * a.kb_head + (d - a.dnope);
+  *(u32x4*)(out + ng * DQK + d) = *(const u32x4*)src;
+}
+
+// dK of the GEMM ([N][G][DQK] fp32) split into the layouts the caller expects: the first
+// dnope dims in bf16 at dKa[n*dka_tok + g*dnope + d], the rest as the per-group fp32
+// partials dkb_part[g][n][d - dnope]; 4 elements per thread
+__global__ void dk_split_kernel(const float* __restrict__ dk, int64_t N, int G, int DQK,
+                                int dnope, bf16_t* __restrict__ dKa, int64_t dka_tok,
+                                float* __restrict__ dkb_part) {
+  const int cpr = DQK / 4;
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= N * G * cpr) return;
+  const int d = (int)(c % cpr) * 4;
+  const int64_t ng = c / cpr;
+  const int g = (int)(ng % G);
+  const int64_t n = ng / G;
+  const f32x4 v = *(const f32x4*)(dk + ng * DQK + d);
+  if (d < dnope) {
+    *(u32x2*)(dKa + n * dka_tok + (int64_t)g * dnope + d) = u32x2{pack2bf(v[0], v[1]), pack2bf(v[2], v[3])};
+  } else {
+    *(f32x4*)(dkb_part + ((int64_t)g * N + n) * (DQK - dnope) + (d - dnope)) = v;
+  }
+}
+
 template <int DQK, int DV>
 hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   const Attn& at = wb.f;
@@ -408,6 +499,10 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   w.dKa = (bf16_t*)wb.dKa; w.dka_tok = wb.dka_tok;
   w.dV = (bf16_t*)wb.dV; w.dv_tok = wb.dv_tok;
   w.dkb_part = wb.dkb_part; w.G = wb.n_ka_groups; w.scale = at.scale;
+  const bool ds_path = wb.dsT != nullptr && wb.kcat != nullptr && wb.dk_tmp != nullptr;
+  w.dsT = (bf16_t*)wb.dsT;
+  w.ds_on = ds_path ? 1 : 0;
+  w.ds_ld = attn_ds_ld(at.T);
   const double pairs = attn_causal_pairs(at);
   const double N = (double)at.B * at.T;
   // delta = rowsum(dO . O), then the dK/dV kernel: algorithmic dV = P^T dO, dP = dO V^T,
@@ -416,20 +511,83 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   hipError_t e = attn_delta(wb, s);
   prof_end(KC_ELEM, s, 0.0, N * at.H * (2.0 * DV * 2.0 + 4.0));
   if (e != hipSuccess) return e;
-  prof_begin(KC_ATTN_DKDV, s);
   const int nkb = (at.T + BKB - 1) / BKB;
-  attn_dkdv_mfma_kernel<DQK, DV><<<nkb * at.B * w.G, 256, 0, s>>>(w);
-  prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV + DQK),
-           N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 4.0 + N * at.H * 8.0);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  // dQ kernel: algorithmic dQ = dS K
-  prof_begin(KC_ATTN_DQ, s);
-  const int nqb = (at.T + DQ_BQ - 1) / DQ_BQ;
-  attn_dq_mfma_kernel<DQK, DV><<<nqb * at.B * at.H, 256, 0, s>>>(w);
-  prof_end(KC_ATTN_DQ, s, 2.0 * pairs * DQK,
-           N * at.H * (2.0 * DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0);
-  e = hipGetLastError();
+  const int hpg = at.H / w.G;
+  if (ds_path) {
+    // dV (and dS^T) from the fused kernel: algorithmic dV = P^T dO, dP = dO V^T
+    prof_begin(KC_ATTN_DKDV, s);
+    attn_dkdv_mfma_kernel<DQK, DV, false><<<nkb * at.B * w.G, 256, 0, s>>>(w);
+    prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV),
+             N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0 +
+                 pairs * 2.0);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // dK = scale dS^T Q per (sequence, group), the group's heads stacked along K:
+    // algorithmic dS read once, Q read once, dK written once (fp32)
+    {
+      Gemm g;
+      g.M = at.T; g.N = DQK; g.K = at.T;
+      g.A = wb.dsT; g.lda = w.ds_ld; g.a_kmajor = true;
+      g.B = at.Q.p; g.ldb = at.Q.tok; g.b_kmajor = false;
+      g.C = wb.dk_tmp; g.ldc = (int64_t)w.G * DQK;
+      g.in_t = DT_BF16; g.c_t = DT_F32; g.alpha = at.scale; g.beta = 0.f;
+      GemmBatch bt;
+      bt.nbatch = at.B * w.G; bt.zdiv = w.G; bt.bdiv = 1; bt.mstore = at.T;
+      bt.rev = 1; bt.kgroups = hpg;
+      bt.sA = (int64_t)hpg * at.T * w.ds_ld; bt.sAk = (int64_t)at.T * w.ds_ld;
+      bt.sB1 = (int64_t)at.T * at.Q.tok; bt.sB2 = (int64_t)hpg * at.Q.head; bt.sBk = at.Q.head;
+      bt.sC1 = (int64_t)at.T * w.G * DQK; bt.sC2 = DQK;
+      prof_begin(KC_ATTN_DK, s);
+      e = gemm_mfma_causal(g, bt, s);
+      prof_end(KC_ATTN_DK, s, 2.0 * pairs * DQK, pairs * 2.0 + N * at.H * DQK * 2.0 + N * w.G * DQK * 4.0);
+      if (e != hipSuccess) return e;
+      prof_begin(KC_ELEM, s);
+      const int64_t chunks = (int64_t)at.B * at.T * w.G * (DQK / 4);
+      dk_split_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(
+          wb.dk_tmp, (int64_t)at.B * at.T, w.G, DQK, at.dnope, w.dKa, w.dka_tok, w.dkb_part);
+      prof_end(KC_ELEM, s, 0.0, N * w.G * DQK * 4.0 * 2.0);
+      e = hipGetLastError();
+      if (e != hipSuccess) return e;
+    }
+    // keys of each group gathered into one operand, then dQ = scale dS K per (sequence,
+    // head): algorithmic dS read once, K read once per head, dQ written once
+    prof_begin(KC_ELEM, s);
+    const int64_t chunks = (int64_t)at.B * at.T * w.G * (DQK / 8);
+    kcat_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(w.f, w.G, DQK, (bf16_t*)wb.kcat);
+    prof_end(KC_ELEM, s, 0.0, N * w.G * DQK * 2.0 * 2.0);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    Gemm g;
+    g.M = (int)w.ds_ld; g.N = DQK; g.K = at.T;
+    g.A = wb.dsT; g.lda = w.ds_ld; g.a_kmajor = false;
+    g.B = wb.kcat; g.ldb = (int64_t)w.G * DQK; g.b_kmajor = false;
+    g.C = wb.dq; g.ldc = (int64_t)at.H * DQK;
+    g.in_t = DT_BF16; g.c_t = DT_BF16; g.alpha = at.scale; g.beta = 0.f;
+    GemmBatch bt;
+    bt.nbatch = at.B * at.H; bt.zdiv = at.H; bt.bdiv = at.H / w.G; bt.mstore = at.T;
+    bt.sA = (int64_t)at.T * w.ds_ld;
+    bt.sB1 = (int64_t)at.T * w.G * DQK; bt.sB2 = DQK;
+    bt.sC1 = (int64_t)at.T * at.H * DQK; bt.sC2 = DQK;
+    bt.rev = 0; bt.kgroups = 1; bt.sAk = bt.sBk = 0;
+    prof_begin(KC_ATTN_DQ, s);
+    e = gemm_mfma_causal(g, bt, s);
+    prof_end(KC_ATTN_DQ, s, 2.0 * pairs * DQK,
+             pairs * 2.0 + N * at.H * DQK * 2.0 * 2.0);
+  } else {
+    prof_begin(KC_ATTN_DKDV, s);
+    attn_dkdv_mfma_kernel<DQK, DV, true><<<nkb * at.B * w.G, 256, 0, s>>>(w);
+    prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV + DQK),
+             N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 4.0 + N * at.H * 8.0);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // dQ kernel: algorithmic dQ = dS K
+    prof_begin(KC_ATTN_DQ, s);
+    const int nqb = (at.T + DQ_BQ - 1) / DQ_BQ;
+    attn_dq_mfma_kernel<DQK, DV><<<nqb * at.B * at.H, 256, 0, s>>>(w);
+    prof_end(KC_ATTN_DQ, s, 2.0 * pairs * DQK,
+             N * at.H * (2.0 * DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0);
+    e = hipGetLastError();
+  }
   if (e != hipSuccess) return e;
   // rotary block of dQ back to the pre-rotation basis: R^T
   const int np = (DQK - at.dnope) / 2;
@@ -449,5 +607,10 @@ hipError_t bwd_dispatch(const AttnBwd& w, hipStream_t s) {
 }  // namespace attn
 
 hipError_t attn_bwd_mfma(const AttnBwd& w, hipStream_t s) { return attn::bwd_dispatch(w, s); }
+
+int64_t attn_ds_ld(int T) { return ((int64_t)T + 63) / 64 * 64; }
+size_t attn_ds_bytes(int B, int H, int T) {
+  return (size_t)B * H * (size_t)T * (size_t)attn_ds_ld(T) * 2;
+}
 
 }  // namespace mla

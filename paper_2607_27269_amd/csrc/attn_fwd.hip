@@ -1,9 +1,12 @@
 // Causal softmax attention (Eq. 2-4) on gfx950 matrix cores, bf16 operands, fp32 softmax.
 //
 // Forward.  A workgroup (8 wavefronts) owns 256 queries of one (sequence, head); each
-// wavefront owns 32 of them.  Keys/values stream through LDS 64 at a time, double
-// buffered and copied straight from HBM into LDS (the next tile's copy is in flight
-// during the current tile's math).
+// wavefront owns 32 of them.  Keys/values stream through a ring of three LDS stages, 64
+// keys at a time, copied straight from HBM into LDS.  The loop is software-pipelined in
+// blocks of 32 keys: while the vector ALUs exponentiate the logits of one block, the matrix
+// cores already compute the logits of the next (the second half of the tile, or the first
+// half of tile kb + 1, whose keys are resident), then O is updated with the block's values;
+// tile kb + 2 is in flight meanwhile.
 // The logits are computed transposed, S^T = K Q^T, with v_mfma_f32_32x32x16_bf16: the
 // query is the MFMA column, so every lane owns one query and the online-softmax state
 // (running max m, running sum l, the output row O^T) of that query lives in that lane.
@@ -33,7 +36,8 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   using Stage = KVStage<DQK, DV, FWD_WAVES>;
   constexpr int LDK = Stage::LDK, LDV = Stage::LDV;
   constexpr int KS = Stage::KS, VS = Stage::VS;
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * (KS + VS)];
+  constexpr int NST = 3;  // K/V ring: tile kb (V in use), kb + 1 (K in use), kb + 2 (landing)
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[NST * (KS + VS)];
   constexpr int NKK = DQK / 16;  // MFMA K-steps of the logits
   constexpr int NC = DV / 32;    // 32-row tiles of O^T
 
@@ -69,84 +73,98 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
 
   const int kend = min(a.T, q0 + FWD_BQ);
   const int nkb = (kend + BKV - 1) / BKV;
+  // tiles this wavefront sees (a prefix: the causal diagonal cuts its queries last)
+  const int nvis = min(nkb, (qw0 + 31) / BKV + 1);
   Stage st;
   st.init(a, b, i);
   st.issue(0, smem, smem + KS);
+  if (nkb > 1) st.issue(BKV, smem + (KS + VS), smem + (KS + VS) + KS);
   wait_all();
   __syncthreads();
 
+  // S^T of 32 keys (rows of ks) against this lane's query
+  auto logits = [&](const bf16_t* ks, f32x16& s) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s[e] = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          *(const bf16x8*)(ks + col * LDK + 16 * kk + 8 * half), qf[kk], s, 0, 0, 0);
+  };
+
+  // Half h (32 keys) of tile kb, its logits in sc: the softmax of this half runs while the
+  // matrix cores compute the logits of the next half (into sn: the other half of this
+  // tile, or the first half of tile kb + 1, whose keys are resident; past the last tile
+  // they come from a stale but finite stage and are not used), then O^T += V^T P^T.
+  auto step = [&](int kb, int h, f32x16& sc, f32x16& sn) {
+    const int j0 = kb * BKV + 32 * h;
+    const bf16_t* ksn = h == 0 ? smem + (kb % NST) * (KS + VS) + 32 * LDK
+                               : smem + ((kb + 1) % NST) * (KS + VS);
+    const bf16_t* vs = smem + (kb % NST) * (KS + VS) + KS;
+    // causal mask on diagonal halves; max of this lane's query (raw logits)
+    const bool diag = j0 + 31 > qw0;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      if (diag) {
+        const int key = j0 + 8 * (e >> 2) + 4 * half + (e & 3);
+        if (key > my_q) sc[e] = -INFINITY;
+      }
+      mx = fmaxf(mx, sc[e]);
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.sl2;
+    // lazy rescale: the reference max moves only when a block max exceeds it by more
+    // than RESCALE_SLACK (so P <= 2^RESCALE_SLACK); wave-uniform branch
+    if (__ballot(mx > m_run + RESCALE_SLACK) != 0) {
+      const float m_new = fmaxf(m_run, mx);
+      const float corr = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
+      m_run = m_new;
+      l_run *= corr;
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc_o[c][e] *= corr;
+    }
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
+    logits(ksn, sn);
+    // P = 2^(s sl2 - m), packed to bf16 as the B operand of O^T = V^T P^T
+    bf16x8 pf[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      u32x4 w;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[8 * u + 2 * q], a.sl2, -m_use));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[8 * u + 2 * q + 1], a.sl2, -m_use));
+        l_run += p0 + p1;
+        w[q] = pack2bf(p0, p1);
+      }
+      pf[u] = __builtin_bit_cast(bf16x8, w);
+    }
+    // O^T += V^T P^T; K-step u covers keys 32 h + 16 u + {4h'..4h'+3, 8+4h'..8+4h'+3}
+    // (h' = the lane half)
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int klo = 32 * h + 16 * u + 4 * half;
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        acc_o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(vs, LDV, 32 * c, klo, klo + 8),
+                                                           pf[u], acc_o[c], 0, 0, 0);
+    }
+  };
+
+  f32x16 sa, sb;
+  if (nvis > 0) logits(smem, sa);
   for (int kb = 0; kb < nkb; ++kb) {
-    const int cur = kb & 1;
-    const int j0 = kb * BKV;
-    if (kb + 1 < nkb) {
-      bf16_t* nxt = smem + (cur ^ 1) * (KS + VS);
-      st.issue(j0 + BKV, nxt, nxt + KS);
+    if (kb + 2 < nkb) {
+      bf16_t* nxt = smem + ((kb + 2) % NST) * (KS + VS);
+      st.issue((kb + 2) * BKV, nxt, nxt + KS);
     }
-    const bf16_t* ks = smem + cur * (KS + VS);
-    const bf16_t* vs = ks + KS;
-    if (j0 <= qw0 + 31) {  // wave-uniform: some key of this tile is visible to the wave
-      f32x16 s[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s[t][e] = 0.f;
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              *(const bf16x8*)(ks + (32 * t + col) * LDK + 16 * kk + 8 * half), qf[kk], s[t], 0, 0, 0);
-      // causal mask on diagonal tiles; tile max of this lane's query (raw logits)
-      const bool diag = j0 + BKV - 1 > qw0;
-      float mx = -INFINITY;
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          if (diag) {
-            const int key = j0 + 32 * t + 8 * (e >> 2) + 4 * half + (e & 3);
-            if (key > my_q) s[t][e] = -INFINITY;
-          }
-          mx = fmaxf(mx, s[t][e]);
-        }
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.sl2;
-      // lazy rescale: the reference max moves only when a tile max exceeds it by more
-      // than RESCALE_SLACK (so P <= 2^RESCALE_SLACK); wave-uniform branch
-      if (__ballot(mx > m_run + RESCALE_SLACK) != 0) {
-        const float m_new = fmaxf(m_run, mx);
-        const float corr = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
-        m_run = m_new;
-        l_run *= corr;
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-          for (int e = 0; e < 16; ++e) acc_o[c][e] *= corr;
-      }
-      const float m_use = m_run == -INFINITY ? 0.f : m_run;
-      // P = 2^(s sl2 - m), packed to bf16 as the B operand of O^T = V^T P^T
-      bf16x8 pf[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        u32x4 w;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[u >> 1][8 * (u & 1) + 2 * q], a.sl2, -m_use));
-          const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[u >> 1][8 * (u & 1) + 2 * q + 1], a.sl2, -m_use));
-          l_run += p0 + p1;
-          w[q] = pack2bf(p0, p1);
-        }
-        pf[u] = __builtin_bit_cast(bf16x8, w);
-      }
-      // O^T += V^T P^T; K-step u covers keys 32(u/2) + 16(u%2) + {4h..4h+3, 8+4h..8+4h+3}
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int klo = 32 * (u >> 1) + 16 * (u & 1) + 4 * half;
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-          acc_o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(vs, LDV, 32 * c, klo, klo + 8),
-                                                             pf[u], acc_o[c], 0, 0, 0);
-      }
+    if (kb < nvis) {  // wave-uniform
+      step(kb, 0, sa, sb);
+      step(kb, 1, sb, sa);
     }
+    // tile kb + 2 has landed and nobody reads tile kb's stage any more
     wait_all();
     __syncthreads();
   }

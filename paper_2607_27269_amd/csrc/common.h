@@ -113,17 +113,21 @@ __device__ __forceinline__ bf16x8 lds_operand_tr(const bf16_t* base, int ld, int
 // with the current one.  Out of its sight, the copies are awaited explicitly (wait_all,
 // itself inline assembly so that it is never relaxed) before the barrier that publishes
 // the tile.  m0 holds the wavefront's LDS destination; lane l writes 16 bytes at m0 + 16 l.
+// (The low 32 bits of a generic pointer into LDS are the LDS byte address.)
 __device__ __forceinline__ void dma16(const bf16_t* gsrc, bf16_t* lds_dst) {
-  const uint32_t l = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16_t*)lds_dst);
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_dst);
   asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gsrc), "{m0}"(l) : "memory");
 }
 
-template <int ROWS, int D, int LD, int NW>
+// With EXACT, every wavefront issues the same number (PER) of copies: the block count is
+// padded to a multiple of the wavefront count (the extra blocks land in reserved LDS), so
+// that a counter wait can name how many copies of later tiles may still be in flight.
+template <int ROWS, int D, int LD, int NW, bool EXACT = false>
 struct DmaTile {
   static constexpr int BYTES = ROWS * LD * 2;
-  static constexpr int NBLK = (BYTES + 1023) / 1024;
-  static constexpr int PER = (NBLK + NW - 1) / NW;
+  static constexpr int NBLK0 = (BYTES + 1023) / 1024;
+  static constexpr int PER = (NBLK0 + NW - 1) / NW;
+  static constexpr int NBLK = EXACT ? PER * NW : NBLK0;
   static constexpr int ALLOC = NBLK * 512;  // bf16 elements reserved in LDS
   short row[PER], col[PER];
 
@@ -152,6 +156,24 @@ struct DmaTile {
     }
   }
 };
+
+// 8-byte store through an explicitly global pointer (no generic-address handling)
+__device__ __forceinline__ void st_global8(bf16_t* p, u32x2 v) {
+  *(__attribute__((address_space(1))) u32x2*)p = v;
+}
+
+// at most N vector-memory operations of this wavefront (e.g. LDS DMA copies of later
+// tiles) still in flight
+template <int N>
+__device__ __forceinline__ void wait_vm() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+// LDS operations of this wavefront complete, then a workgroup barrier (no memory fence:
+// global copies are awaited with wait_vm)
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory");
+}
 
 // all outstanding memory operations of this wavefront (incl. LDS DMA) complete
 __device__ __forceinline__ void wait_all() {

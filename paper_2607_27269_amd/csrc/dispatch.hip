@@ -53,4 +53,10 @@ hipError_t attn_bwd(const AttnBwd& w, hipStream_t s) {
 
 double attn_causal_pairs(const Attn& a) { return causal_pairs(a); }
 
+size_t attn_bwd_ds_bytes(int B, int H, int T, int dqk, int dv, DType t) {
+  if (t != DT_BF16 || !attn_mfma_supported(dqk, dv)) return 0;
+  const size_t b = attn_ds_bytes(B, H, T);
+  return b <= ((size_t)16 << 30) ? b : 0;
+}
+
 }  // namespace mla

@@ -32,7 +32,11 @@ namespace mla {
 
 namespace {
 
-constexpr int BK = 64;
+constexpr int BK = 64;  // K granule of split-K chunks (and the slice of the small tiles)
+// slice depth, LDS ring depth and wavefront grid of the 256 x 256 tiles (measured on the
+// step's shapes: deeper rings of 32-deep slices and 4-wavefront grids of 128 x 128 were
+// slower)
+constexpr int GBK = 64, GNST = 2, GWM = 2, GWN = 4;
 
 struct GemmDev {
   int M, N;
@@ -43,6 +47,14 @@ struct GemmDev {
   float alpha, beta;
   int kchunk;         // K elements per split (multiple of BK)
   int ktotal;
+  int mstore;         // rows of C written (M is the row count operand A may be read at)
+  // batched causal mode (causal != 0): workgroup z of nbatch works on A + z sA,
+  // B + (z / zdiv) sB1 + ((z % zdiv) / bdiv) sB2, C + (z / zdiv) sC1 + (z % zdiv) sC2; the
+  // K range of an M tile ends at its last row (entries with k > m are zero) or, with rev,
+  // starts at its first row (entries with k < m are zero); it is walked kgroups times, the
+  // j-th time on A + j sAk and B + j sBk (a sum over stacked operands)
+  int causal, rev, nbatch, zdiv, bdiv, kgroups;
+  int64_t sA, sB1, sB2, sC1, sC2, sAk, sBk;
 };
 
 // row stride (elements) of an m-major [k][ROWS] tile, read only through the transposing
@@ -55,18 +67,19 @@ constexpr int mm_ld(int rows) {
   }
   return rows + 32;
 }
-constexpr int KM_LD = BK + 8;  // k-major [row][k] tile: 144-byte rows
-
 // ---- global -> register staging -------------------------------------------------------
-template <bool KMAJOR, int ROWS, int NTHR>
+template <bool KMAJOR, int ROWS, int NTHR, int BK>
 struct Loader;
 
-// k-major tile: ROWS x BK, chunk c -> row c / 8, k-chunk c % 8
-template <int ROWS, int NTHR>
-struct Loader<true, ROWS, NTHR> {
+// k-major tile: ROWS x BK, chunk c -> row c / (BK/8), k-chunk c % (BK/8); rows padded by 8
+// elements (BK = 64: 144-byte rows, BK = 32: 80-byte rows; conflict-free operand reads)
+template <int ROWS, int NTHR, int BK>
+struct Loader<true, ROWS, NTHR, BK> {
+  static constexpr int KM_LD = BK + 8;
   static constexpr int CHUNKS = ROWS * (BK / 8);
   static constexpr int PER = CHUNKS / NTHR;
-  static constexpr int ELEMS = ((ROWS * KM_LD * 2 + 1023) / 1024) * 512;  // whole 1 KB blocks
+  using Dma = DmaTile<ROWS, BK, KM_LD, NTHR / 64, true>;
+  static constexpr int ELEMS = Dma::ALLOC;  // whole 1 KB blocks, a multiple per wavefront
   static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
   u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
@@ -90,7 +103,6 @@ struct Loader<true, ROWS, NTHR> {
   }
   // full k-slice straight from HBM into LDS (rows past the end repeat the last row;
   // their outputs are not stored)
-  using Dma = DmaTile<ROWS, BK, KM_LD, NTHR / 64>;
   __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
     const bf16_t* base = p + (int64_t)row0 * ld + k0;
@@ -105,13 +117,14 @@ struct Loader<true, ROWS, NTHR> {
 };
 
 // m-major tile (global [k][row]): BK x ROWS, chunk c -> k-row c / (ROWS/8), row-chunk c % (ROWS/8)
-template <int ROWS, int NTHR>
-struct Loader<false, ROWS, NTHR> {
+template <int ROWS, int NTHR, int BK>
+struct Loader<false, ROWS, NTHR, BK> {
   static constexpr int LD = mm_ld(ROWS);
   static constexpr int CPR = ROWS / 8;
   static constexpr int CHUNKS = BK * CPR;
   static constexpr int PER = CHUNKS / NTHR;
-  static constexpr int ELEMS = ((BK * LD * 2 + 1023) / 1024) * 512;  // whole 1 KB blocks
+  using Dma = DmaTile<BK, ROWS, LD, NTHR / 64, true>;
+  static constexpr int ELEMS = Dma::ALLOC;  // whole 1 KB blocks, a multiple per wavefront
   static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
   u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
@@ -133,7 +146,6 @@ struct Loader<false, ROWS, NTHR> {
       *(u32x4*)(lds + (c / CPR) * LD + (c % CPR) * 8) = r[i];
     }
   }
-  using Dma = DmaTile<BK, ROWS, LD, NTHR / 64>;
   __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
     const bf16_t* base = p + (int64_t)k0 * ld + row0;
@@ -177,30 +189,57 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, f32x4 v, float alpha, 
 }
 
 // ---- the kernel --------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC>
-__global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST>
+__device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   constexpr int NTHR = 64 * WM * WN;
   constexpr int TM = BM / WM / 32;  // 32x32 MFMA tiles per wave along M
   constexpr int TN = BN / WN / 32;
-  using LA = Loader<AK, BM, NTHR>;
-  using LB = Loader<BKM, BN, NTHR>;
+  constexpr int KK = BK / 16;       // MFMA k-steps per slice
+  using LA = Loader<AK, BM, NTHR, BK>;
+  using LB = Loader<BKM, BN, NTHR, BK>;
   constexpr int STAGE = LA::ELEMS + LB::ELEMS;
-  __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * STAGE];
+  constexpr int D = LA::Dma::PER + LB::Dma::PER;  // copies per wavefront per slice
+  static_assert(NST >= 2 && NST <= 4 && (NST - 2) * D < 64, "stages / counter range");
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
 
   const int ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
   const int ntiles = ntm * ntn;
-  // XCD-aware remap, then group 8 row panels together for L2 reuse
-  int pid = xcd_remap(blockIdx.x, ntiles);
-  const int GROUP = 8;
-  int group = pid / (GROUP * ntn);
-  int first = group * GROUP;
-  int gsz = min(ntm - first, GROUP);
-  int tm = first + (pid % (GROUP * ntn)) % gsz;
-  int tn = (pid % (GROUP * ntn)) / gsz;
+  int tm, tn;
+  const bf16_t* gA = g.A;
+  const bf16_t* gB = g.B;
+  TC* C = (TC*)g.C;
+  if (g.causal) {
+    // the longest K ranges (last row tiles) of every batch entry first; batch entry z runs
+    // on XCD z % 8, so its B panel stays in one L2
+    const int pid = blockIdx.x;
+    const int per = g.nbatch * ntn;
+    tm = g.rev ? pid / per : ntm - 1 - pid / per;
+    const int z = pid % per % g.nbatch;
+    tn = pid % per / g.nbatch;
+    const int z1 = z / g.zdiv, z2 = z % g.zdiv;
+    gA += z * g.sA;
+    gB += z1 * g.sB1 + (z2 / g.bdiv) * g.sB2;
+    C += z1 * g.sC1 + z2 * g.sC2;
+  } else {
+    // XCD-aware remap, then group 8 row panels together for L2 reuse
+    const int pid = xcd_remap(blockIdx.x, ntiles);
+    const int GROUP = 8;
+    const int group = pid / (GROUP * ntn);
+    const int first = group * GROUP;
+    const int gsz = min(ntm - first, GROUP);
+    tm = first + (pid % (GROUP * ntn)) % gsz;
+    tn = (pid % (GROUP * ntn)) / gsz;
+  }
   const int m0 = tm * BM, n0 = tn * BN;
   const int split = blockIdx.y;
-  const int kbeg = split * g.kchunk;
-  const int kend = min(g.ktotal, kbeg + g.kchunk);
+  int kbeg, kend;
+  if (g.causal) {
+    kbeg = g.rev ? m0 : 0;
+    kend = g.rev ? g.ktotal : min(g.ktotal, m0 + BM);
+  } else {
+    kbeg = split * g.kchunk;
+    kend = min(g.ktotal, kbeg + g.kchunk);
+  }
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -221,24 +260,35 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
   da.init();
   db.init();
   const int mvalid = g.M - m0, nvalid = g.N - n0;
-  const int nk = (kend - kbeg + BK - 1) / BK;
+  const int nkg = (kend - kbeg + BK - 1) / BK;  // slices per operand group
+  const int nk = nkg * (g.causal ? g.kgroups : 1);
   const int nfull = (kend - kbeg) / BK;  // slices copied straight to LDS; a ragged last
                                          // slice goes through registers with zero fill
   auto stage = [&](int kt, bf16_t* dst) {
-    const int k0 = kbeg + kt * BK;
-    if (kt < nfull) {
-      la.dma(da, g.A, g.lda, m0, mvalid, k0, dst);
-      lb.dma(db, g.B, g.ldb, n0, nvalid, k0, dst + LA::ELEMS);
+    const int grp = kt / nkg, ks = kt - grp * nkg;
+    const int k0 = kbeg + ks * BK;
+    const bf16_t* pa = gA + grp * g.sAk;
+    const bf16_t* pb = gB + grp * g.sBk;
+    if (ks < nfull) {
+      la.dma(da, pa, g.lda, m0, mvalid, k0, dst);
+      lb.dma(db, pb, g.ldb, n0, nvalid, k0, dst + LA::ELEMS);
     } else {
-      la.load(g.A, g.lda, m0, mvalid, k0, kend);
-      lb.load(g.B, g.ldb, n0, nvalid, k0, kend);
+      la.load(pa, g.lda, m0, mvalid, k0, kend);
+      lb.load(pb, g.ldb, n0, nvalid, k0, kend);
       la.store(dst);
       lb.store(dst + LA::ELEMS);
     }
   };
-  if (nk > 0) stage(0, lds);
-  wait_all();
-  __syncthreads();
+  // slice s waits for its own copies while up to n later slices may still be in flight
+  auto wait_slice = [&](int n) {
+    if constexpr (NST >= 4) {
+      if (n >= 2) { wait_vm<2 * D>(); return; }
+    }
+    if constexpr (NST >= 3) {
+      if (n >= 1) { wait_vm<D>(); return; }
+    }
+    wait_vm<0>();
+  };
   // fragments of one 16-wide k step, double buffered in registers: the reads of step
   // kk + 1 are issued before the matrix ops of step kk
   bf16x8 af[2][TM], bfr[2][TN];
@@ -256,20 +306,28 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
       for (int j = 0; j < TN; ++j)
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   };
+  // ring of NST slices: slices kt + 1 .. kt + NST - 1 are in flight while slice kt feeds the
+  // matrix cores
+#pragma unroll
+  for (int s0 = 0; s0 < NST - 1; ++s0)
+    if (s0 < nk) stage(s0, lds + s0 * STAGE);
+  wait_slice(min(NST - 2, nk - 1));
+  lds_barrier();
   if (nk > 0) load_frags(lds, 0, af[0], bfr[0]);
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) stage(kt + 1, lds + (cur ^ 1) * STAGE);
-    const bf16_t* As = lds + cur * STAGE;
+    const bf16_t* As = lds + (kt % NST) * STAGE;
+    // the stage of slice kt - 1 is free: every wave passed the barrier after its last read
+    if (kt + NST - 1 < nk) stage(kt + NST - 1, lds + ((kt + NST - 1) % NST) * STAGE);
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
-      if (kk + 1 < BK / 16) {
+    for (int kk = 0; kk < KK; ++kk) {
+      if (kk + 1 < KK) {
         load_frags(As, kk + 1, af[(kk + 1) & 1], bfr[(kk + 1) & 1]);
       } else {
-        // next slice: its copy must have landed and every wave must be done with this one
-        wait_all();
-        __syncthreads();
-        if (kt + 1 < nk) load_frags(lds + (cur ^ 1) * STAGE, 0, af[0], bfr[0]);
+        // next slice: its copies must have landed (later ones may still fly) and every
+        // wave must be done reading this one
+        wait_slice(min(NST - 2, nk - 2 - kt));
+        lds_barrier();
+        if (kt + 1 < nk) load_frags(lds + ((kt + 1) % NST) * STAGE, 0, af[0], bfr[0]);
       }
       __builtin_amdgcn_sched_barrier(0);
       mma(af[kk & 1], bfr[kk & 1]);
@@ -285,7 +343,6 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
   constexpr int SLD = WTN + 8;              // strip row stride (floats)
   static_assert(NTHR / 64 * 32 * SLD * 4 <= (int)sizeof(lds), "epilogue strip too large");
   float* strip = (float*)lds + wave * 32 * SLD;
-  TC* C = (TC*)g.C;
   const bool vec = (g.ldc % 4) == 0;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
@@ -301,7 +358,7 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
       const int c = it * 64 + lane;
       const int r = c / CPR, col = (c % CPR) * 4;
       const int m = m0 + wrow0 + i * 32 + r, n = n0 + wcol0 + col;
-      if (m >= g.M || n >= g.N) continue;
+      if (m >= g.mstore || n >= g.N) continue;
       const f32x4 v = *(const f32x4*)(strip + r * SLD + col);
       if (g.part) {
         float* p = g.part + ((int64_t)split * g.M + m) * g.N + n;
@@ -324,6 +381,17 @@ __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
       }
     }
   }
+}
+
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
+  gemm_tile<BM, BN, WM, WN, AK, BKM, TC, BK, NST>(g);
+}
+// the same tile program for the dS products of attention's backward (own name, so that
+// profiles tell them apart)
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST>
+__global__ __launch_bounds__(64 * WM * WN) void attn_ds_gemm_kernel(GemmDev g) {
+  gemm_tile<BM, BN, WM, WN, AK, BKM, TC, BK, NST>(g);
 }
 
 // C = alpha * sum_s part[s] + beta * C, summed in split order
@@ -378,9 +446,9 @@ void launch(const GemmDev& d, const Plan& p, hipStream_t s) {
   const int tiles = ((d.M + p.bm - 1) / p.bm) * ((d.N + p.bn - 1) / p.bn);
   dim3 grid(tiles, p.splits);
   if (p.big)
-    gemm_mfma_kernel<256, 256, 2, 4, AK, BKM, TC><<<grid, 512, 0, s>>>(d);
+    gemm_mfma_kernel<256, 256, GWM, GWN, AK, BKM, TC, GBK, GNST><<<grid, 64 * GWM * GWN, 0, s>>>(d);
   else
-    gemm_mfma_kernel<128, 128, 2, 2, AK, BKM, TC><<<grid, 256, 0, s>>>(d);
+    gemm_mfma_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(d);
 }
 
 }  // namespace
@@ -396,6 +464,9 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   d.A = (const bf16_t*)g.A; d.lda = g.lda;
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = g.beta;
+  d.mstore = g.M;
+  d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
+  d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
   Plan p = plan_of(g, true);
   if (p.splits > 1 && (scratch == nullptr || scratch_elems < (size_t)p.splits * g.M * g.N))
     p = plan_of(g, false);
@@ -420,6 +491,50 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
     splitk_reduce_kernel<bf16_t><<<grid, 256, 0, s>>>(scratch, p.splits, g.M, g.N, (bf16_t*)g.C,
                                                       g.ldc, g.alpha, g.beta);
   return hipGetLastError();
+}
+
+// Batched causal products of attention's backward: dQ = dS K (A = dS^T stored [key][query],
+// M/N-contiguous, bf16 result) and dK = dS^T Q summed over a group's heads (A k-major, fp32
+// result).  BN is the output width rounded up to the supported tile widths.
+template <int BN, int WM, int WN, bool AK, typename TC>
+static void launch_causal(const GemmDev& d, int nbatch, hipStream_t s) {
+  const int ntm = (d.M + 255) / 256, ntn = (d.N + BN - 1) / BN;
+  attn_ds_gemm_kernel<256, BN, WM, WN, AK, false, TC, 64, 2>
+      <<<dim3(ntm * ntn * nbatch, 1), 64 * WM * WN, 0, s>>>(d);
+}
+
+template <bool AK, typename TC>
+static hipError_t dispatch_causal(const GemmDev& d, int nbatch, hipStream_t s) {
+  if (d.N <= 64) launch_causal<64, 4, 2, AK, TC>(d, nbatch, s);
+  else if (d.N <= 96) launch_causal<96, 4, 1, AK, TC>(d, nbatch, s);
+  else if (d.N <= 128) launch_causal<128, 4, 2, AK, TC>(d, nbatch, s);
+  else if (d.N <= 192) launch_causal<192, 4, 2, AK, TC>(d, nbatch, s);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s) {
+  // (an M-contiguous A is read in 8-row chunks)
+  const bool ok = !g.b_kmajor && g.in_t == DT_BF16 && g.beta == 0.f &&
+                  (g.a_kmajor || g.M % 8 == 0) &&
+                  g.N % 32 == 0 && g.lda % 8 == 0 && g.ldb % 8 == 0 && bt.mstore <= g.M &&
+                  bt.kgroups >= 1 && (g.a_kmajor ? (bt.rev && g.c_t == DT_F32)
+                                                 : (!bt.rev && g.c_t == DT_BF16));
+  if (!ok) return hipErrorInvalidValue;
+  GemmDev d;
+  d.M = g.M; d.N = g.N; d.ktotal = g.K;
+  d.A = (const bf16_t*)g.A; d.lda = g.lda;
+  d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
+  d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = 0.f;
+  d.part = nullptr;
+  d.kchunk = (g.K + BK - 1) / BK * BK;
+  d.mstore = bt.mstore;
+  d.causal = 1; d.rev = bt.rev; d.nbatch = bt.nbatch; d.zdiv = bt.zdiv; d.bdiv = bt.bdiv;
+  d.kgroups = bt.kgroups;
+  d.sA = bt.sA; d.sB1 = bt.sB1; d.sB2 = bt.sB2; d.sC1 = bt.sC1; d.sC2 = bt.sC2;
+  d.sAk = bt.sAk; d.sBk = bt.sBk;
+  return g.a_kmajor ? dispatch_causal<true, float>(d, bt.nbatch, s)
+                    : dispatch_causal<false, bf16_t>(d, bt.nbatch, s);
 }
 
 }  // namespace mla

@@ -18,7 +18,8 @@ enum KClass {
   KC_ATTN_DQ = 5,      // attention backward: dQ
   KC_LOSS = 6,         // Eq. 11 loss and gradient
   KC_ELEM = 7,         // RoPE tables / rotation, softmax-backward row term, dk^PE finishing
-  KC_COUNT = 8
+  KC_ATTN_DK = 8,      // attention backward: dK (GEMM over the stored dS^T)
+  KC_COUNT = 9
 };
 
 // Timing instrumentation hooks (implemented in api.cpp).  prof_end also records the
@@ -72,7 +73,21 @@ struct AttnBwd {
   void* dV;  int64_t dv_tok;   // group g's value grads at dV[n*dv_tok + g*dv]
   float* dkb_part;           // [Gka, N, dqk - dnope] fp32 partial grads of the Kb part per Ka group
   int n_ka_groups;           // number of Ka groups (heads i / f.Ka.div)
+  // Optional (matrix-core path): with both set, dS^T is stored in bf16 by the dK/dV kernel
+  // as [B*H][T keys][ds_ld queries] (ds_ld = T rounded up to 64) and dQ = scale dS K is a
+  // batched causal GEMM against the keys gathered as kcat [N][n_ka_groups][dqk].
+  // dK = scale dS^T Q is then a GEMM as well, into dk_tmp before the split into dKa and
+  // dkb_part.
+  void* dsT;                 // attn_ds_bytes(f.B, f.H, f.T) bytes, or null
+  void* kcat;                // N * n_ka_groups * dqk bf16, or null
+  float* dk_tmp;             // N * n_ka_groups * dqk fp32, or null
 };
+// Row stride and size of the stored dS^T of the matrix-core backward.
+int64_t attn_ds_ld(int T);
+size_t attn_ds_bytes(int B, int H, int T);
+// Bytes of dS^T buffer the backward of this attention shape uses (0: dQ is recomputed by
+// its own kernel; the case for the vector-ALU path and when dS^T would exceed 16 GiB).
+size_t attn_bwd_ds_bytes(int B, int H, int T, int dqk, int dv, DType t);
 hipError_t attn_bwd(const AttnBwd& a, hipStream_t s);
 // (sequence, head, query, key) pairs with key <= query: B H T (T+1) / 2
 double attn_causal_pairs(const Attn& a);

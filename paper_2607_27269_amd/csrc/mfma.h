@@ -5,6 +5,17 @@
 namespace mla {
 size_t gemm_mfma_scratch_elems(const Gemm& g);
 hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s);
+// Batch entry z of a batched causal GEMM uses A + z sA, B + (z / zdiv) sB1 +
+// ((z % zdiv) / bdiv) sB2 and C + (z / zdiv) sC1 + (z % zdiv) sC2 (elements).  Row m of C
+// sums k < min(K, end of m's 256-row tile) (rev = 0; A M-contiguous, bf16 C) or
+// k >= start of m's tile (rev = 1; A K-contiguous, fp32 C), so A must hold zeros for the
+// excluded side of the diagonal inside a tile; that K range is summed kgroups times, the
+// j-th on A + j sAk and B + j sBk.  B is N-contiguous; rows m >= mstore are not written.
+struct GemmBatch {
+  int nbatch, zdiv, bdiv, mstore, rev, kgroups;
+  int64_t sA, sB1, sB2, sC1, sC2, sAk, sBk;
+};
+hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s);
 bool attn_mfma_supported(int dqk, int dv);
 hipError_t attn_fwd_mfma(const Attn& a, hipStream_t s);
 hipError_t attn_bwd_mfma(const AttnBwd& w, hipStream_t s);
