@@ -128,6 +128,7 @@ struct Layout {
   size_t s_cos, s_sin, s_cq, s_q, s_ckv, s_knope, s_v, s_o, s_lse;
   // backward scratch
   size_t b_do, b_delta, b_dqacc, b_dq, b_dkv, b_dkpe, b_dckv, b_dcq, b_split, b_ds, b_kcat, b_dktmp;
+  size_t b_statT;
   size_t b_ds_bytes;
   size_t b_split_elems;
   // loss scratch
@@ -167,6 +168,7 @@ static Layout layout_of(const Dims& d) {
   L.b_ds = take(L.b_ds_bytes);
   L.b_kcat = take(L.b_ds_bytes ? N * d.Gkv * d.dqk * ts : 0);
   L.b_dktmp = take(L.b_ds_bytes ? N * d.Gkv * d.dqk * 4 : 0);
+  L.b_statT = take(L.b_ds_bytes ? attn_stats_bytes((int)d.B, (int)d.H, (int)d.T) : 0);
   size_t se = 0;
   for (const Gemm& g : bwd_gemm_shapes(d)) se = std::max(se, gemm_scratch_elems(g));
   L.b_split_elems = se;
@@ -406,6 +408,7 @@ int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* 
   ab.dsT = L.b_ds_bytes ? at(ws, L.b_ds) : nullptr;
   ab.kcat = L.b_ds_bytes ? at(ws, L.b_kcat) : nullptr;
   ab.dk_tmp = L.b_ds_bytes ? (float*)at(ws, L.b_dktmp) : nullptr;
+  ab.statT = L.b_ds_bytes ? (float*)at(ws, L.b_statT) : nullptr;
   HIP_TRY(attn_bwd(ab, s));
 
   if (need_q) {

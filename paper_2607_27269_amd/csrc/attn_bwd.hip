@@ -52,6 +52,9 @@ struct BwdDev {
   bf16_t* dsT;           // [B*H][T][ds_ld] when ds_on
   int64_t ds_ld;
   int ds_on;
+  bf16_t* ds_dummy;      // scratch rows for stores of lanes past the sequence end
+  const float* statT;    // [2][H][B][tpad]: log2-scaled lse, delta (dV kernel)
+  int tpad;
 };
 
 // dS^T tile rows a dQ GEMM row tile reads: queries from the start of the 256-query tile
@@ -61,14 +64,14 @@ constexpr int DQ_TILE = 256;
 // ---------------------------------------------------------------------------------------
 // dK / dV
 // ---------------------------------------------------------------------------------------
-template <int DQK, int DV>
+template <int DQK, int DV, int BQ = BQB>
 struct QStage {
   static constexpr int LDQ = ld_of(DQK);
   static constexpr int LDO = ld_of(DV);
-  using QT = DmaTile<BQB, DQK, LDQ, 4>;
-  using OT = DmaTile<BQB, DV, LDO, 4>;
+  using QT = DmaTile<BQ, DQK, LDQ, 4>;
+  using OT = DmaTile<BQ, DV, LDO, 4>;
   static constexpr int QS = QT::ALLOC, OS = OT::ALLOC;
-  static constexpr int BUF = QS + OS + 2 * BQB * 2;  // bf16 elements incl. lse2, delta
+  static constexpr int BUF = QS + OS + 2 * BQ * 2;  // bf16 elements incl. lse2, delta
   QT qt;
   OT ot;
   float stat;
@@ -78,7 +81,7 @@ struct QStage {
     ot.init();
   }
 
-  // queries q0 .. q0+BQB-1 of head i into buf (rows past the end load the last valid row;
+  // queries q0 .. q0+BQ-1 of head i into buf (rows past the end load the last valid row;
   // their lse is +inf so they carry zero probability)
   __device__ __forceinline__ void issue(const BwdDev& w, int b, int i, int q0, bf16_t* buf) {
     const AttnDev& a = w.f;
@@ -90,16 +93,16 @@ struct QStage {
     ot.issue(buf + QS, [&](int r, int c) {
       return ob + (int64_t)min(q0 + r, last) * ((int64_t)a.H * DV) + c;
     });
-    const int q = q0 + (threadIdx.x & 63);
-    if (threadIdx.x < 64)
+    const int q = q0 + (int)(threadIdx.x % BQ);
+    if (threadIdx.x < BQ)
       stat = q < a.T ? a.lse[(n0 + q) * a.H + i] * LOG2E : INFINITY;
-    else if (threadIdx.x < 128)
+    else if (threadIdx.x < 2 * BQ)
       stat = q < a.T ? w.delta[(n0 + q) * a.H + i] : 0.f;
   }
 
   __device__ __forceinline__ void store_stats(bf16_t* buf) const {
     float* st = (float*)(buf + QS + OS);
-    if (threadIdx.x < 128) st[threadIdx.x] = stat;
+    if (threadIdx.x < 2 * BQ) st[threadIdx.x] = stat;
   }
 };
 
@@ -328,6 +331,272 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
 }
 
 // ---------------------------------------------------------------------------------------
+// dV and dS^T (the path where dK and dQ are GEMMs over the stored dS^T)
+// ---------------------------------------------------------------------------------------
+// A workgroup owns 128 keys of one (sequence, KV group), 32 per wavefront, and walks the
+// group's heads and 32-query blocks.  K and V of the lane's key are B-operand fragments
+// held in registers; only the 32-query Q / dO tiles and their softmax statistics pass
+// through LDS, in a ring of three stages (about 72 KB), so two workgroups share a CU and
+// each block's copy is issued two steps before its use.  Every wavefront issues the same
+// number of copies per stage (the block count is padded) and of dS^T stores per step, so
+// one counter wait names exactly the copies that must have landed.
+constexpr int DV_BQ = 32;
+constexpr int DS_STORES = DV_BQ / 8;  // 8-byte dS^T stores per lane per step
+#ifndef DV_STAGES
+#define DV_STAGES 2
+#endif
+constexpr int DV_NST = DV_STAGES;  // ring depth: copies are issued DV_NST - 1 steps ahead
+
+// [2][H][B][Tpad] fp32: log2-scaled lse (+inf past the sequence end) and delta (0 there)
+__global__ void attn_stats_t_kernel(const float* __restrict__ lse, const float* __restrict__ delta,
+                                    int B, int T, int H, int Tpad, float* __restrict__ out) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t total = 2LL * H * B * Tpad;
+  if (idx >= total) return;
+  const int q = (int)(idx % Tpad);
+  const int64_t r = idx / Tpad;
+  const int b = (int)(r % B);
+  const int h = (int)((r / B) % H);
+  const int part = (int)(r / ((int64_t)B * H));
+  float v;
+  if (q < T) {
+    const int64_t src = ((int64_t)b * T + q) * H + h;
+    v = part == 0 ? lse[src] * LOG2E : delta[src];
+  } else {
+    v = part == 0 ? INFINITY : 0.f;
+  }
+  out[idx] = v;
+}
+
+template <int DQK, int DV>
+struct DvStage {
+  static constexpr int LDQ = ld_of(DQK);
+  static constexpr int LDO = ld_of(DV);
+  static constexpr int NQB = (DV_BQ * LDQ * 2 + 1023) / 1024;  // 1 KB blocks of the Q tile
+  static constexpr int NOB = (DV_BQ * LDO * 2 + 1023) / 1024;  // ... of the dO tile
+  static constexpr int NB = (NQB + NOB + 1 + 3) / 4 * 4;      // + statistics, padded
+  static constexpr int PER = NB / 4;                          // copies per wavefront
+  static constexpr int OFF_O = NQB * 512, OFF_S = (NQB + NOB) * 512;  // bf16 elements
+  static constexpr int ELEMS = NB * 512;
+
+  // block blk = wave + 4 p: its kind is wave-uniform (blk < NQB: Q, < NQB + NOB: dO, then
+  // the statistics block, then padding that re-copies Q row 0 into unused LDS); the lane's
+  // (row, column) inside the block is recomputed at each issue (no registers held)
+  __device__ __forceinline__ void issue(const BwdDev& w, int b, int h, int q0, bf16_t* stage) const {
+    const AttnDev& a = w.f;
+    const int wave = threadIdx.x >> 6;
+    // opaque copy of the lane id: the per-lane coordinates below are recomputed at every
+    // issue instead of being kept live across the loop
+    int lane = threadIdx.x & 63;
+    asm volatile("" : "+v"(lane));
+    const int last = a.T - 1;
+    const int64_t n0 = (int64_t)b * a.T;
+    const bf16_t* qb = a.Q + n0 * a.q_tok + (int64_t)h * a.q_head;
+    const bf16_t* ob = w.dO + n0 * ((int64_t)a.H * DV) + (int64_t)h * DV;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int blk = wave + 4 * p;
+      const bf16_t* src;
+      if (blk < NQB) {
+        const int e = (blk * 1024 + 16 * lane) / 2;
+        const int r = min(e / LDQ, DV_BQ - 1), c0 = e % LDQ, c = c0 < DQK ? c0 : 0;
+        src = qb + (int64_t)min(q0 + r, last) * a.q_tok + c;
+      } else if (blk < NQB + NOB) {
+        const int e = ((blk - NQB) * 1024 + 16 * lane) / 2;
+        const int r = min(e / LDO, DV_BQ - 1), c0 = e % LDO, c = c0 < DV ? c0 : 0;
+        src = ob + (int64_t)min(q0 + r, last) * ((int64_t)a.H * DV) + c;
+      } else if (blk == NQB + NOB) {
+        // lanes 0-7: lse2 of queries q0 + 4 l .. + 3; lanes 8-15: delta; the rest repeat
+        const int part = (lane >> 3) & 1, c = 4 * (lane & 7);
+        src = (const bf16_t*)(w.statT + (((int64_t)part * a.H + h) * a.B + b) * w.tpad + q0 + c);
+      } else {
+        src = qb + (int64_t)min(q0, last) * a.q_tok;
+      }
+      dma16(src, stage + blk * 512);
+    }
+  }
+};
+
+template <int DQK, int DV>
+__global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
+  using Stage = DvStage<DQK, DV>;
+  constexpr int LDQ = Stage::LDQ, LDO = Stage::LDO;
+  constexpr int NKK = DQK / 16, NVK = DV / 16, NCV = DV / 32;
+  constexpr int D = Stage::PER;
+  static_assert(D + 2 * DS_STORES < 64, "counter range");
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[DV_NST * Stage::ELEMS];
+  const AttnDev& a = w.f;
+
+  const int nbg = a.B * w.G;
+  const int kb = blockIdx.x / nbg;  // early key blocks (the most query blocks) first
+  const int bg = blockIdx.x % nbg;
+  const int b = bg / w.G, g = bg % w.G;
+  const int hpg = a.H / w.G;
+  const int k0 = kb * BKB;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, col = lane & 31;
+  const int kw0 = k0 + 32 * wave;
+  const int my_key = kw0 + col;
+  const int i0 = g * hpg;
+
+  // dS^T rows of this workgroup's keys: the queries in [tile start, k0) precede every key
+  // here, so their entries are zeros that no step below writes
+  const int zq0 = k0 / DQ_TILE * DQ_TILE;
+  if (zq0 < k0) {
+    const int nz = k0 - zq0;                       // multiple of 128
+    const int cpr = nz / 8;                        // 16-byte chunks per key row
+    const int kr = min(BKB, a.T - k0);
+    for (int h = 0; h < hpg; ++h) {
+      bf16_t* plane = w.dsT + ((int64_t)b * a.H + i0 + h) * a.T * w.ds_ld;
+      for (int c = threadIdx.x; c < kr * cpr; c += 256) {
+        const int r = c / cpr, q = zq0 + (c % cpr) * 8;
+        *(u32x4*)(plane + (int64_t)(k0 + r) * w.ds_ld + q) = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  }
+
+  // this lane's key and value as B operand fragments (col = key, k = 16 kk + 8 half + 0..7)
+  bf16x8 kf[NKK], vf[NVK];
+  {
+    const int jj = min(my_key, a.T - 1);
+    const int64_t n = (int64_t)b * a.T + jj;
+    const int ga = i0 / a.ka_div, gb = i0 / a.kb_div, gv = i0 / a.v_div;
+#pragma unroll
+    for (int kk = 0; kk < NKK; ++kk) {
+      const int d = 16 * kk + 8 * half;
+      const bf16_t* src = d < a.dnope ? a.Ka + n * a.ka_tok + (int64_t)ga * a.ka_head + d
+                                      : a.Kb + n * a.kb_tok + (int64_t)gb * a.kb_head + (d - a.dnope);
+      kf[kk] = *(const bf16x8*)src;
+    }
+    const bf16_t* vp = a.V + n * a.v_tok + (int64_t)gv * a.v_head + 8 * half;
+#pragma unroll
+    for (int kk = 0; kk < NVK; ++kk) vf[kk] = *(const bf16x8*)(vp + 16 * kk);
+  }
+
+  f32x16 dv[NCV];
+#pragma unroll
+  for (int c = 0; c < NCV; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) dv[c][e] = 0.f;
+
+  const int qb0 = k0 / DV_BQ;
+  const int nqb = (a.T + DV_BQ - 1) / DV_BQ;
+  const int nper = nqb - qb0;
+  const int niter = hpg * nper;  // >= 1
+  Stage stg;
+  // step it -> (query block, head): query blocks in descending order with the group's heads
+  // innermost, so that all key blocks of a (sequence, group) stream the same Q/dO tile at
+  // the same time and share it through L2; steps past the end re-copy the last block
+  auto q_of = [&](int it) { return (nqb - 1 - min(it, niter - 1) / hpg) * DV_BQ; };
+  auto h_of = [&](int it) { return i0 + min(it, niter - 1) % hpg; };
+  auto stage_of = [&](int it) { return smem + (it % DV_NST) * Stage::ELEMS; };
+  bf16_t* scratch = w.ds_dummy + 64 * lane;
+  static_assert(DV_NST == 2 || DV_NST == 3, "ring depth");
+  stg.issue(w, b, h_of(0), q_of(0), stage_of(0));
+  if constexpr (DV_NST == 3) {
+    stg.issue(w, b, h_of(1), q_of(1), stage_of(1));
+    // stand-ins for the stores of step -1, so that every step's wait counts the same
+#pragma unroll
+    for (int j = 0; j < DS_STORES; ++j) st_global8(scratch + 8 * j, u32x2{0u, 0u});
+    wait_vm<D + DS_STORES>();  // stage 0 has landed
+  } else {
+    wait_vm<0>();
+  }
+  lds_barrier();
+
+  for (int it = 0; it < niter; ++it) {
+    const int q0 = q_of(it);
+    const bf16_t* Qs = stage_of(it);
+    const bf16_t* dOs = Qs + Stage::OFF_O;
+    const float* st_lse = (const float*)(Qs + Stage::OFF_S);
+    const float* st_dl = st_lse + DV_BQ;
+    // the stage of step it + DV_NST - 1 (= it - 1) is free: every wave passed the barrier
+    // after reading it
+    stg.issue(w, b, h_of(it + DV_NST - 1), q_of(it + DV_NST - 1), stage_of(it + DV_NST - 1));
+
+    // this lane's dS^T row segment for the block: queries q0 + 4 half + {0..3, 8..11, ...};
+    // lanes past the sequence end write a scratch row instead, so that every wavefront
+    // issues exactly DS_STORES stores per step
+    bf16_t* dsrow = my_key < a.T
+                        ? w.dsT + ((int64_t)b * a.H + h_of(it)) * a.T * w.ds_ld +
+                              (int64_t)my_key * w.ds_ld + q0 + 4 * half
+                        : scratch + 4 * half;
+    if (kw0 <= min(q0 + DV_BQ - 1, a.T - 1)) {  // wave-uniform: some pair is visible
+      f32x16 sp, dp;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) { sp[e] = 0.f; dp[e] = 0.f; }
+#pragma unroll
+      for (int kk = 0; kk < NKK; ++kk)
+        sp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            *(const bf16x8*)(Qs + col * LDQ + 16 * kk + 8 * half), kf[kk], sp, 0, 0, 0);
+#pragma unroll
+      for (int kk = 0; kk < NVK; ++kk)
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            *(const bf16x8*)(dOs + col * LDO + 16 * kk + 8 * half), vf[kk], dp, 0, 0, 0);
+      // P = 2^(S sl2 - lse2), dS = P (dP - delta); rows q = q0 + 8(e/4) + 4 half + e%4
+      // (lse2 = +inf past the sequence end)
+      const bool diag = kw0 + 31 > q0;
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int qr = 8 * e4 + 4 * half;
+        const f32x4 l2 = *(const f32x4*)(st_lse + qr);
+        const f32x4 dl = *(const f32x4*)(st_dl + qr);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int e = 4 * e4 + r;
+          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sp[e], a.sl2, -l2[r]));
+          if (diag && my_key > q0 + qr + r) p = 0.f;
+          sp[e] = p;
+          dp[e] = p * (dp[e] - dl[r]);
+        }
+      }
+      // dS^T in bf16: element e is query 8 (e/4) + 4 half + e%4
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4)
+        st_global8(dsrow + 8 * e4,
+                   u32x2{pack2bf(dp[4 * e4], dp[4 * e4 + 1]), pack2bf(dp[4 * e4 + 2], dp[4 * e4 + 3])});
+      // dV^T += dO^T P   (K-step u: queries 16 u + {4h.., 8+4h..})
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        u32x4 wp;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) wp[q] = pack2bf(sp[8 * u + 2 * q], sp[8 * u + 2 * q + 1]);
+        const bf16x8 pf = __builtin_bit_cast(bf16x8, wp);
+        const int klo = 16 * u + 4 * half;
+#pragma unroll
+        for (int c = 0; c < NCV; ++c)
+          dv[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(dOs, LDO, 32 * c, klo, klo + 8),
+                                                         pf, dv[c], 0, 0, 0);
+      }
+    } else {
+      // every key of this wavefront follows every query of the block: zeros
+#pragma unroll
+      for (int o = 0; o < DV_BQ; o += 8) st_global8(dsrow + o, u32x2{0u, 0u});
+    }
+    // step it + 1's copies have landed; younger are this step's stores and, with three
+    // stages, the stores of step it - 1 and the copies of step it + 2 (counters complete in
+    // issue order)
+    if constexpr (DV_NST == 3)
+      wait_vm<D + 2 * DS_STORES>();
+    else
+      wait_vm<DS_STORES>();
+    lds_barrier();
+  }
+
+  // epilogue: this lane's key; rows d = 32c + 8(e/4) + 4 half + e%4
+  if (my_key >= a.T) return;
+  const int64_t n = (int64_t)b * a.T + my_key;
+#pragma unroll
+  for (int c = 0; c < NCV; ++c)
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4) {
+      const int d = 32 * c + 8 * e4 + 4 * half;
+      u32x2 wv = {pack2bf(dv[c][4 * e4], dv[c][4 * e4 + 1]), pack2bf(dv[c][4 * e4 + 2], dv[c][4 * e4 + 3])};
+      *(u32x2*)(w.dV + n * w.dv_tok + (int64_t)g * DV + d) = wv;
+    }
+}
+
+// ---------------------------------------------------------------------------------------
 // dQ
 // ---------------------------------------------------------------------------------------
 template <int DQK, int DV>
@@ -499,10 +768,14 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   w.dKa = (bf16_t*)wb.dKa; w.dka_tok = wb.dka_tok;
   w.dV = (bf16_t*)wb.dV; w.dv_tok = wb.dv_tok;
   w.dkb_part = wb.dkb_part; w.G = wb.n_ka_groups; w.scale = at.scale;
-  const bool ds_path = wb.dsT != nullptr && wb.kcat != nullptr && wb.dk_tmp != nullptr;
+  const bool ds_path = wb.dsT != nullptr && wb.kcat != nullptr && wb.dk_tmp != nullptr &&
+                       wb.statT != nullptr;
   w.dsT = (bf16_t*)wb.dsT;
   w.ds_on = ds_path ? 1 : 0;
   w.ds_ld = attn_ds_ld(at.T);
+  w.ds_dummy = w.dsT + (ds_path ? (int64_t)at.B * at.H * at.T * w.ds_ld : 0);
+  w.statT = wb.statT;
+  w.tpad = attn_stats_tpad(at.T);
   const double pairs = attn_causal_pairs(at);
   const double N = (double)at.B * at.T;
   // delta = rowsum(dO . O), then the dK/dV kernel: algorithmic dV = P^T dO, dP = dO V^T,
@@ -514,9 +787,17 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   const int nkb = (at.T + BKB - 1) / BKB;
   const int hpg = at.H / w.G;
   if (ds_path) {
-    // dV (and dS^T) from the fused kernel: algorithmic dV = P^T dO, dP = dO V^T
+    // statistics per (head, sequence) in query order, then dV (and dS^T) from the fused
+    // kernel: algorithmic dV = P^T dO, dP = dO V^T
+    prof_begin(KC_ELEM, s);
+    const int64_t nst = 2LL * at.H * at.B * w.tpad;
+    attn_stats_t_kernel<<<(unsigned)((nst + 255) / 256), 256, 0, s>>>(at.lse, wb.delta, at.B, at.T, at.H,
+                                                                      w.tpad, wb.statT);
+    prof_end(KC_ELEM, s, 0.0, nst * 4.0 * 2.0);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
     prof_begin(KC_ATTN_DKDV, s);
-    attn_dkdv_mfma_kernel<DQK, DV, false><<<nkb * at.B * w.G, 256, 0, s>>>(w);
+    attn_dv_mfma_kernel<DQK, DV><<<nkb * at.B * w.G, 256, 0, s>>>(w);
     prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV),
              N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0 +
                  pairs * 2.0);
@@ -609,8 +890,11 @@ hipError_t bwd_dispatch(const AttnBwd& w, hipStream_t s) {
 hipError_t attn_bwd_mfma(const AttnBwd& w, hipStream_t s) { return attn::bwd_dispatch(w, s); }
 
 int64_t attn_ds_ld(int T) { return ((int64_t)T + 63) / 64 * 64; }
+int attn_stats_tpad(int T) { return (T + 31) / 32 * 32; }
+size_t attn_stats_bytes(int B, int H, int T) { return 2ull * H * B * attn_stats_tpad(T) * 4; }
 size_t attn_ds_bytes(int B, int H, int T) {
-  return (size_t)B * H * (size_t)T * (size_t)attn_ds_ld(T) * 2;
+  // + scratch rows: 64 lanes x 64 elements
+  return (size_t)B * H * (size_t)T * (size_t)attn_ds_ld(T) * 2 + 64 * 64 * 2;
 }
 
 }  // namespace mla

@@ -81,10 +81,13 @@ struct AttnBwd {
   void* dsT;                 // attn_ds_bytes(f.B, f.H, f.T) bytes, or null
   void* kcat;                // N * n_ka_groups * dqk bf16, or null
   float* dk_tmp;             // N * n_ka_groups * dqk fp32, or null
+  float* statT;              // attn_stats_bytes(f.B, f.H, f.T), or null
 };
 // Row stride and size of the stored dS^T of the matrix-core backward.
 int64_t attn_ds_ld(int T);
 size_t attn_ds_bytes(int B, int H, int T);
+int attn_stats_tpad(int T);
+size_t attn_stats_bytes(int B, int H, int T);
 // Bytes of dS^T buffer the backward of this attention shape uses (0: dQ is recomputed by
 // its own kernel; the case for the vector-ALU path and when dS^T would exceed 16 GiB).
 size_t attn_bwd_ds_bytes(int B, int H, int T, int dqk, int dv, DType t);
