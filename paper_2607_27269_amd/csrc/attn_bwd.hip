@@ -380,19 +380,47 @@ struct DvStage {
   static constexpr int ELEMS = NB * 512;
 
   // block blk = wave + 4 p: its kind is wave-uniform (blk < NQB: Q, < NQB + NOB: dO, then
-  // the statistics block, then padding that re-copies Q row 0 into unused LDS); the lane's
-  // (row, column) inside the block is recomputed at each issue (no registers held)
+  // the statistics block, then padding that re-copies Q row 0 into unused LDS).  A full
+  // block (all 32 queries inside the sequence) is copied from wave-uniform row bases with
+  // loop-invariant lane offsets; the last, partial block clamps rows to the sequence end.
   __device__ __forceinline__ void issue(const BwdDev& w, int b, int h, int q0, bf16_t* stage) const {
     const AttnDev& a = w.f;
     const int wave = threadIdx.x >> 6;
-    // opaque copy of the lane id: the per-lane coordinates below are recomputed at every
-    // issue instead of being kept live across the loop
+    // opaque copy of the lane id: the lane offsets below are recomputed (32-bit arithmetic)
+    // at every issue instead of being kept live across the loop
     int lane = threadIdx.x & 63;
     asm volatile("" : "+v"(lane));
     const int last = a.T - 1;
     const int64_t n0 = (int64_t)b * a.T;
+    const int64_t o_tok = (int64_t)a.H * DV;
+    const float* sbase = w.statT + ((int64_t)h * a.B + b) * w.tpad + q0;  // lse2 row
+    const uint32_t s_part = (uint32_t)a.H * a.B * w.tpad * 4;          // lse2 -> delta bytes
+    if (q0 + DV_BQ - 1 <= last) {
+      const bf16_t* qrow = a.Q + (n0 + q0) * a.q_tok + (int64_t)h * a.q_head;
+      const bf16_t* orow = w.dO + (n0 + q0) * o_tok + (int64_t)h * DV;
+#pragma unroll
+      for (int p = 0; p < PER; ++p) {
+        const int blk = wave + 4 * p;
+        if (blk < NQB) {
+          const int e = (blk * 1024 + 16 * lane) / 2;
+          const int r = min(e / LDQ, DV_BQ - 1), c0 = e % LDQ, c = c0 < DQK ? c0 : 0;
+          dma16_s(qrow, 2u * (uint32_t)(r * (int)a.q_tok + c), stage + blk * 512);
+        } else if (blk < NQB + NOB) {
+          const int e = ((blk - NQB) * 1024 + 16 * lane) / 2;
+          const int r = min(e / LDO, DV_BQ - 1), c0 = e % LDO, c = c0 < DV ? c0 : 0;
+          dma16_s(orow, 2u * (uint32_t)(r * (int)o_tok + c), stage + blk * 512);
+        } else if (blk == NQB + NOB) {
+          // lanes 0-7: lse2 of queries q0 + 4 l .. + 3; lanes 8-15: delta; the rest repeat
+          const uint32_t off = ((lane >> 3) & 1) * s_part + 16u * (lane & 7);
+          dma16_s(sbase, off, stage + blk * 512);
+        } else {
+          dma16_s(qrow, 0u, stage + blk * 512);
+        }
+      }
+      return;
+    }
     const bf16_t* qb = a.Q + n0 * a.q_tok + (int64_t)h * a.q_head;
-    const bf16_t* ob = w.dO + n0 * ((int64_t)a.H * DV) + (int64_t)h * DV;
+    const bf16_t* ob = w.dO + n0 * o_tok + (int64_t)h * DV;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int blk = wave + 4 * p;
@@ -404,11 +432,10 @@ struct DvStage {
       } else if (blk < NQB + NOB) {
         const int e = ((blk - NQB) * 1024 + 16 * lane) / 2;
         const int r = min(e / LDO, DV_BQ - 1), c0 = e % LDO, c = c0 < DV ? c0 : 0;
-        src = ob + (int64_t)min(q0 + r, last) * ((int64_t)a.H * DV) + c;
+        src = ob + (int64_t)min(q0 + r, last) * o_tok + c;
       } else if (blk == NQB + NOB) {
-        // lanes 0-7: lse2 of queries q0 + 4 l .. + 3; lanes 8-15: delta; the rest repeat
         const int part = (lane >> 3) & 1, c = 4 * (lane & 7);
-        src = (const bf16_t*)(w.statT + (((int64_t)part * a.H + h) * a.B + b) * w.tpad + q0 + c);
+        src = (const bf16_t*)(sbase + (int64_t)part * a.H * a.B * w.tpad + c);
       } else {
         src = qb + (int64_t)min(q0, last) * a.q_tok;
       }

@@ -122,6 +122,24 @@ __device__ __forceinline__ void dma16(const bf16_t* gsrc, bf16_t* lds_dst) {
 // With EXACT, every wavefront issues the same number (PER) of copies: the block count is
 // padded to a multiple of the wavefront count (the extra blocks land in reserved LDS), so
 // that a counter wait can name how many copies of later tiles may still be in flight.
+// Same copy with the global address split into a wave-uniform base (SGPRs) and a per-lane
+// 32-bit byte offset: the per-lane part is usually loop-invariant, so a copy costs no
+// 64-bit address arithmetic.  sbase must be the same in every lane.
+__device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff_bytes, bf16_t* lds_dst) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_dst);
+  // the base is uniform by contract; reading it from the first lane puts it in SGPRs (the
+  // builtin returns a signed int: each half is zero-extended explicitly)
+  const uint64_t a = (uint64_t)(uintptr_t)sbase;
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  const uint64_t su = ((uint64_t)hi << 32) | (uint64_t)lo;
+  // s_nop 4: five wait states between a VALU write of the base SGPRs (the readfirstlane
+  // above) and their read by the memory instruction, which the compiler cannot see inside
+  // the asm; this also covers the m0 write before the LDS copy
+  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff_bytes), "s"(su), "{m0}"(l)
+               : "memory");
+}
+
 template <int ROWS, int D, int LD, int NW, bool EXACT = false>
 struct DmaTile {
   static constexpr int BYTES = ROWS * LD * 2;
@@ -153,6 +171,17 @@ struct DmaTile {
       const int b = wave + p * NW;
       if (NBLK % NW == 0 || b < NBLK)
         dma16(src(row[p], col[p]), lds + b * 512);
+    }
+  }
+  // off(row, col) -> element offset of the chunk from sbase (uniform), below 2^31 bytes
+  template <class F>
+  __device__ __forceinline__ void issue_s(bf16_t* lds, const bf16_t* sbase, F off) const {
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int b = wave + p * NW;
+      if (NBLK % NW == 0 || b < NBLK)
+        dma16_s(sbase, 2u * (uint32_t)off(row[p], col[p]), lds + b * 512);
     }
   }
 };

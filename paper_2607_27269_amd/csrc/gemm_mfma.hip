@@ -101,13 +101,10 @@ struct Loader<true, ROWS, NTHR, BK> {
       *(u32x4*)(lds + (c / (BK / 8)) * KM_LD + (c % (BK / 8)) * 8) = r[i];
     }
   }
-  // full k-slice straight from HBM into LDS (rows past the end repeat the last row;
-  // their outputs are not stored)
+  // full k-slice of a full tile straight from HBM into LDS (uniform base + lane offset)
   __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
-    const bf16_t* base = p + (int64_t)row0 * ld + k0;
-    const int rl = rows_valid - 1;
-    t.issue(lds, [&](int r, int c) { return base + (int64_t)min(r, rl) * ld + c; });
+    t.issue_s(lds, p + (int64_t)row0 * ld + k0, [&](int r, int c) { return r * (int)ld + c; });
   }
   // operand fragment: rows row0 + lane%32, k = 16 kk + 8 half + 0..7
   static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
@@ -148,9 +145,7 @@ struct Loader<false, ROWS, NTHR, BK> {
   }
   __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
-    const bf16_t* base = p + (int64_t)k0 * ld + row0;
-    const int cl = rows_valid - 8;
-    t.issue(lds, [&](int r, int c) { return base + (int64_t)r * ld + min(c, cl); });
+    t.issue_s(lds, p + (int64_t)k0 * ld + row0, [&](int r, int c) { return r * (int)ld + c; });
   }
   static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
     const int klo = 16 * kk + 8 * ((threadIdx.x & 63) >> 5);
@@ -262,8 +257,13 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   const int mvalid = g.M - m0, nvalid = g.N - n0;
   const int nkg = (kend - kbeg + BK - 1) / BK;  // slices per operand group
   const int nk = nkg * (g.causal ? g.kgroups : 1);
-  const int nfull = (kend - kbeg) / BK;  // slices copied straight to LDS; a ragged last
-                                         // slice goes through registers with zero fill
+  // slices copied straight to LDS; a ragged last slice, and every slice of a tile that is
+  // cut by the matrix edge or whose operand rows are too far apart for 32-bit offsets,
+  // goes through registers with zero fill
+  const bool dma_ok = mvalid >= BM && nvalid >= BN &&
+                      (AK ? (int64_t)BM * g.lda : (int64_t)BK * g.lda) < (1ll << 30) &&
+                      (BKM ? (int64_t)BN * g.ldb : (int64_t)BK * g.ldb) < (1ll << 30);
+  const int nfull = dma_ok ? (kend - kbeg) / BK : 0;
   auto stage = [&](int kt, bf16_t* dst) {
     const int grp = kt / nkg, ks = kt - grp * nkg;
     const int k0 = kbeg + ks * BK;
