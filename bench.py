@@ -43,16 +43,24 @@ def parse():
 
 
 # kernel-name fragments of each timing class, as rocprofv3 reports them
+# kernel-name patterns of each timing class: a kernel belongs to the class when every
+# substring of one of the alternatives occurs in its name
 CLASS_PATTERNS = {
-    "gemm_nt": ("gemm_mfma_kernel<", ", true, true,"),
-    "gemm_nn": ("gemm_mfma_kernel<", ", true, false,"),
-    "gemm_tn": ("gemm_mfma_kernel<", ", false, false,"),
-    "attn_fwd": ("attn_fwd_mfma_kernel<",),
-    "attn_bwd_dkdv": ("attn_dkdv_mfma_kernel<",),
-    "attn_bwd_dq": ("attn_ds_gemm_kernel<", ", false, false,"),
-    "attn_bwd_dk": ("attn_ds_gemm_kernel<", ", true, false,"),
-    "loss": ("loss_main_kernel<",),
+    "gemm_nt": [("gemm_mfma_kernel<", ", true, true,")],
+    "gemm_nn": [("gemm_mfma_kernel<", ", true, false,")],
+    "gemm_tn": [("gemm_mfma_kernel<", ", false, false,")],
+    "attn_fwd": [("attn_fwd_mfma_kernel<",)],
+    "attn_bwd_dkdv": [("attn_dv_mfma_kernel<",), ("attn_dkdv_mfma_kernel<",)],
+    "attn_bwd_dq": [("attn_ds_gemm_kernel<", ", false, false,"), ("attn_dq_mfma_kernel<",)],
+    "attn_bwd_dk": [("attn_ds_gemm_kernel<", ", true, false,")],
+    "loss": [("loss_main_kernel<",)],
 }
+
+
+def _in_class(name, alts):
+    return any(all(p in name for p in pats) for pats in alts)
+
+
 # sources whose change invalidates stored counter readings
 TRAFFIC_SOURCES = ["paper_2607_27269_amd/csrc/gemm_mfma.hip", "paper_2607_27269_amd/csrc/attn_fwd.hip",
                    "paper_2607_27269_amd/csrc/attn_bwd.hip", "paper_2607_27269_amd/csrc/attn_common.h",
@@ -90,9 +98,9 @@ def summarize_traffic(fetch_csv, write_csv, copy_mb):
     fc, wc = copy_value(fetch), copy_value(write)
     out = {"copy_mb": copy_mb, "fetch_scale": known / fc if fc else None,
            "write_scale": known / wc if wc else None, "classes": {}}
-    for cls, pats in CLASS_PATTERNS.items():
-        fv = [v for (i, n), v in fetch.items() if all(p in n for p in pats)]
-        wv = [v for (i, n), v in write.items() if all(p in n for p in pats)]
+    for cls, alts in CLASS_PATTERNS.items():
+        fv = [v for (i, n), v in fetch.items() if _in_class(n, alts)]
+        wv = [v for (i, n), v in write.items() if _in_class(n, alts)]
         if not fv or not wv or not fc or not wc:
             continue
         out["classes"][cls] = {"launches": len(fv),

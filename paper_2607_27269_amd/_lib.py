@@ -32,7 +32,7 @@ KCLASS_KERNELS = {"gemm_nt": "gemm_mfma_kernel<..., true, true, ...>",
                   "gemm_nn": "gemm_mfma_kernel<..., true, false, ...>",
                   "gemm_tn": "gemm_mfma_kernel<..., false, false, float> + splitk_reduce_kernel",
                   "attn_fwd": "attn_fwd_mfma_kernel",
-                  "attn_bwd_dkdv": "attn_dkdv_mfma_kernel",
+                  "attn_bwd_dkdv": "attn_dv_mfma_kernel (or attn_dkdv_mfma_kernel)",
                   "attn_bwd_dq": "attn_ds_gemm_kernel<..., false, false, ...> (or attn_dq_mfma_kernel)",
                   "attn_bwd_dk": "attn_ds_gemm_kernel<..., true, false, float>",
                   "loss": "mask_count_kernel + loss_main_kernel + loss_final_kernel",
