@@ -204,13 +204,19 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   const bf16_t* gB = g.B;
   TC* C = (TC*)g.C;
   if (g.causal) {
-    // the longest K ranges (last row tiles) of every batch entry first; batch entry z runs
-    // on XCD z % 8, so its B panel stays in one L2
+    // the longest K ranges first (row tile by row tile); inside one row tile, batch entries
+    // that share their B panel (bdiv consecutive entries) are dispatched to one XCD
+    // (workgroup ids go round-robin over the 8 XCDs) so that they stream it through one L2
     const int pid = blockIdx.x;
     const int per = g.nbatch * ntn;
     tm = g.rev ? pid / per : ntm - 1 - pid / per;
-    const int z = pid % per % g.nbatch;
-    tn = pid % per / g.nbatch;
+    const int r = pid % per;
+    tn = r / g.nbatch;
+    int z = r % g.nbatch;
+    if (g.bdiv > 1 && g.nbatch % (8 * g.bdiv) == 0) {
+      const int x = z % 8, j = z / 8;
+      z = (x + 8 * (j / g.bdiv)) * g.bdiv + j % g.bdiv;
+    }
     const int z1 = z / g.zdiv, z2 = z % g.zdiv;
     gA += z * g.sA;
     gB += z1 * g.sB1 + (z2 / g.bdiv) * g.sB2;
@@ -264,8 +270,11 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
                       (AK ? (int64_t)BM * g.lda : (int64_t)BK * g.lda) < (1ll << 30) &&
                       (BKM ? (int64_t)BN * g.ldb : (int64_t)BK * g.ldb) < (1ll << 30);
   const int nfull = dma_ok ? (kend - kbeg) / BK : 0;
+  // rev: slices are walked from the top of the K range down, so that all row tiles of a
+  // batch entry (whose ranges share their top) stream the same B rows at the same time
   auto stage = [&](int kt, bf16_t* dst) {
-    const int grp = kt / nkg, ks = kt - grp * nkg;
+    const int grp = kt / nkg, ks0 = kt - grp * nkg;
+    const int ks = g.causal && g.rev ? nkg - 1 - ks0 : ks0;
     const int k0 = kbeg + ks * BK;
     const bf16_t* pa = gA + grp * g.sAk;
     const bf16_t* pb = gB + grp * g.sBk;
