@@ -342,10 +342,7 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
 // one counter wait names exactly the copies that must have landed.
 constexpr int DV_BQ = 32;
 constexpr int DS_STORES = DV_BQ / 8;  // 8-byte dS^T stores per lane per step
-#ifndef DV_STAGES
-#define DV_STAGES 2
-#endif
-constexpr int DV_NST = DV_STAGES;  // ring depth: copies are issued DV_NST - 1 steps ahead
+constexpr int DV_NST = 2;  // LDS stages: a step's copies are issued one step ahead
 
 // [2][H][B][Tpad] fp32: log2-scaled lse (+inf past the sequence end) and delta (0 there)
 __global__ void attn_stats_t_kernel(const float* __restrict__ lse, const float* __restrict__ delta,
@@ -385,7 +382,7 @@ struct DvStage {
   // loop-invariant lane offsets; the last, partial block clamps rows to the sequence end.
   __device__ __forceinline__ void issue(const BwdDev& w, int b, int h, int q0, bf16_t* stage) const {
     const AttnDev& a = w.f;
-    const int wave = threadIdx.x >> 6;
+    const int wave = wave_id();
     // opaque copy of the lane id: the lane offsets below are recomputed (32-bit arithmetic)
     // at every issue instead of being kept live across the loop
     int lane = threadIdx.x & 63;
@@ -450,7 +447,7 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
   constexpr int LDQ = Stage::LDQ, LDO = Stage::LDO;
   constexpr int NKK = DQK / 16, NVK = DV / 16, NCV = DV / 32;
   constexpr int D = Stage::PER;
-  static_assert(D + 2 * DS_STORES < 64, "counter range");
+  static_assert(DS_STORES < 64, "counter range");
   __shared__ __attribute__((aligned(1024))) bf16_t smem[DV_NST * Stage::ELEMS];
   const AttnDev& a = w.f;
 
@@ -460,7 +457,7 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
   const int b = bg / w.G, g = bg % w.G;
   const int hpg = a.H / w.G;
   const int k0 = kb * BKB;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5, col = lane & 31;
   const int kw0 = k0 + 32 * wave;
   const int my_key = kw0 + col;
@@ -511,41 +508,36 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
   const int nper = nqb - qb0;
   const int niter = hpg * nper;  // >= 1
   Stage stg;
-  // step it -> (query block, head): query blocks in descending order with the group's heads
+  // steps walk (query block, head): query blocks in descending order with the group's heads
   // innermost, so that all key blocks of a (sequence, group) stream the same Q/dO tile at
-  // the same time and share it through L2; steps past the end re-copy the last block
-  auto q_of = [&](int it) { return (nqb - 1 - min(it, niter - 1) / hpg) * DV_BQ; };
-  auto h_of = [&](int it) { return i0 + min(it, niter - 1) % hpg; };
-  auto stage_of = [&](int it) { return smem + (it % DV_NST) * Stage::ELEMS; };
+  // the same time and share it through L2.  (qc, hc) is this step's pair, (qn, hn) the
+  // next one (the last step's "next" re-copies the last pair into the free stage).
+  int qc = (nqb - 1) * DV_BQ, hc = i0;
+  int qn = qc, hn = hc;
+  auto advance = [&](int& q, int& h) {
+    if (++h == i0 + hpg) { h = i0; q -= DV_BQ; }
+  };
+  if (niter > 1) advance(qn, hn);
+  auto stage_of = [&](int it) { return smem + (it & 1) * Stage::ELEMS; };
   bf16_t* scratch = w.ds_dummy + 64 * lane;
-  static_assert(DV_NST == 2 || DV_NST == 3, "ring depth");
-  stg.issue(w, b, h_of(0), q_of(0), stage_of(0));
-  if constexpr (DV_NST == 3) {
-    stg.issue(w, b, h_of(1), q_of(1), stage_of(1));
-    // stand-ins for the stores of step -1, so that every step's wait counts the same
-#pragma unroll
-    for (int j = 0; j < DS_STORES; ++j) st_global8(scratch + 8 * j, u32x2{0u, 0u});
-    wait_vm<D + DS_STORES>();  // stage 0 has landed
-  } else {
-    wait_vm<0>();
-  }
+  stg.issue(w, b, hc, qc, stage_of(0));
+  wait_vm<0>();
   lds_barrier();
 
   for (int it = 0; it < niter; ++it) {
-    const int q0 = q_of(it);
+    const int q0 = qc;
     const bf16_t* Qs = stage_of(it);
     const bf16_t* dOs = Qs + Stage::OFF_O;
     const float* st_lse = (const float*)(Qs + Stage::OFF_S);
     const float* st_dl = st_lse + DV_BQ;
-    // the stage of step it + DV_NST - 1 (= it - 1) is free: every wave passed the barrier
-    // after reading it
-    stg.issue(w, b, h_of(it + DV_NST - 1), q_of(it + DV_NST - 1), stage_of(it + DV_NST - 1));
+    // the stage of step it - 1 is free: every wave passed the barrier after reading it
+    stg.issue(w, b, hn, qn, stage_of(it + 1));
 
     // this lane's dS^T row segment for the block: queries q0 + 4 half + {0..3, 8..11, ...};
     // lanes past the sequence end write a scratch row instead, so that every wavefront
     // issues exactly DS_STORES stores per step
     bf16_t* dsrow = my_key < a.T
-                        ? w.dsT + ((int64_t)b * a.H + h_of(it)) * a.T * w.ds_ld +
+                        ? w.dsT + ((int64_t)b * a.H + hc) * a.T * w.ds_ld +
                               (int64_t)my_key * w.ds_ld + q0 + 4 * half
                         : scratch + 4 * half;
     if (kw0 <= min(q0 + DV_BQ - 1, a.T - 1)) {  // wave-uniform: some pair is visible
@@ -600,14 +592,13 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
 #pragma unroll
       for (int o = 0; o < DV_BQ; o += 8) st_global8(dsrow + o, u32x2{0u, 0u});
     }
-    // step it + 1's copies have landed; younger are this step's stores and, with three
-    // stages, the stores of step it - 1 and the copies of step it + 2 (counters complete in
-    // issue order)
-    if constexpr (DV_NST == 3)
-      wait_vm<D + 2 * DS_STORES>();
-    else
-      wait_vm<DS_STORES>();
+    // step it + 1's copies have landed; younger are only this step's stores (counters
+    // complete in issue order)
+    wait_vm<DS_STORES>();
     lds_barrier();
+    qc = qn;
+    hc = hn;
+    if (it + 2 < niter) advance(qn, hn);
   }
 
   // epilogue: this lane's key; rows d = 32c + 8(e/4) + 4 half + e%4
@@ -642,7 +633,7 @@ __global__ __launch_bounds__(256) void attn_dq_mfma_kernel(BwdDev w) {
   const int qb = nqb - 1 - pid % nqb;
   const int b = bh / a.H, i = bh % a.H;
   const int q0 = qb * DQ_BQ;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5, col = lane & 31;
   const int qw0 = q0 + 32 * wave;
   const int my_q = qw0 + col;

@@ -50,7 +50,7 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   const int b = bh / a.H, i = bh % a.H;
   const int q0 = qb * FWD_BQ;
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5, col = lane & 31;
   const int qw0 = q0 + wave * 32;
   const int my_q = qw0 + col;

@@ -59,6 +59,13 @@ __device__ __forceinline__ double warp_sum_d(double v) {
 }
 
 // Remap a linear workgroup id so that consecutive logical tiles land on the same XCD.
+// Index of the calling wavefront in its workgroup, in an SGPR: the compiler does not treat
+// threadIdx.x / 64 as uniform by itself, and branches on it would be lowered as divergent
+// (exec-mask) code.
+__device__ __forceinline__ int wave_id() {
+  return __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+}
+
 // Workgroups are dispatched round-robin over the 8 XCDs (id % 8); the remap gives XCD x
 // the contiguous logical range [x*per, (x+1)*per), keeping neighbouring tiles (which
 // share A rows or B columns) in one XCD's L2.
@@ -150,7 +157,7 @@ struct DmaTile {
   short row[PER], col[PER];
 
   __device__ __forceinline__ void init() {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63, wave = wave_id();
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int b = wave + p * NW;
@@ -165,7 +172,7 @@ struct DmaTile {
   // src(row, col) -> global address of the 16-byte chunk at (row, col) of this tile
   template <class F>
   __device__ __forceinline__ void issue(bf16_t* lds, F src) const {
-    const int wave = threadIdx.x >> 6;
+    const int wave = wave_id();
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int b = wave + p * NW;
@@ -176,7 +183,7 @@ struct DmaTile {
   // off(row, col) -> element offset of the chunk from sbase (uniform), below 2^31 bytes
   template <class F>
   __device__ __forceinline__ void issue_s(bf16_t* lds, const bf16_t* sbase, F off) const {
-    const int wave = threadIdx.x >> 6;
+    const int wave = wave_id();
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int b = wave + p * NW;

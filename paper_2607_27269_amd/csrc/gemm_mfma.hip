@@ -242,7 +242,7 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
     kend = min(g.ktotal, kbeg + g.kchunk);
   }
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = wave_id();
   const int wm = wave / WN, wn = wave % WN;
   const int wrow0 = wm * (BM / WM), wcol0 = wn * (BN / WN);
 
@@ -273,7 +273,7 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   // rev: slices are walked from the top of the K range down, so that all row tiles of a
   // batch entry (whose ranges share their top) stream the same B rows at the same time
   auto stage = [&](int kt, bf16_t* dst) {
-    const int grp = kt / nkg, ks0 = kt - grp * nkg;
+    const int grp = g.causal && g.kgroups > 1 ? kt / nkg : 0, ks0 = kt - grp * nkg;
     const int ks = g.causal && g.rev ? nkg - 1 - ks0 : ks0;
     const int k0 = kbeg + ks * BK;
     const bf16_t* pa = gA + grp * g.sAk;
