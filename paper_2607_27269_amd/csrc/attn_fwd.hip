@@ -53,6 +53,9 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5, col = lane & 31;
   const int qw0 = q0 + wave * 32;
+  // this lane's part of a transposing V read (lds_operand_tr's addressing): key row
+  // 4 (lane half) + (lane % 16) / 4, column 16 ((lane / 16) % 2) + 4 (lane % 4)
+  const int vlane = (4 * half + ((lane & 15) >> 2)) * LDV + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   const int my_q = qw0 + col;
   const int64_t nq = (int64_t)b * a.T + min(my_q, a.T - 1);
 
@@ -81,6 +84,11 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   if (nkb > 1) st.issue(BKV, smem + (KS + VS), smem + (KS + VS) + KS);
   wait_all();
   __syncthreads();
+  // the query fragments are in registers from here on: otherwise the compiler keeps
+  // waiting for their loads inside the loop, and its counter waits there would also wait
+  // for the K/V copies in flight
+#pragma unroll
+  for (int kk = 0; kk < NKK; ++kk) asm volatile("" : "+v"(qf[kk]));
 
   // S^T of 32 keys (rows of ks) against this lane's query
   auto logits = [&](const bf16_t* ks, f32x16& s) {
@@ -98,20 +106,24 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   // they come from a stale but finite stage and are not used), then O^T += V^T P^T.
   auto step = [&](int kb, int h, f32x16& sc, f32x16& sn) {
     const int j0 = kb * BKV + 32 * h;
-    const bf16_t* ksn = h == 0 ? smem + (kb % NST) * (KS + VS) + 32 * LDK
-                               : smem + ((kb + 1) % NST) * (KS + VS);
-    const bf16_t* vs = smem + (kb % NST) * (KS + VS) + KS;
+    // stage offsets pass through readfirstlane: opaque to the loop optimiser, which would
+    // otherwise keep one induction variable per LDS read and add the stage in per read
+    const int cur = __builtin_amdgcn_readfirstlane((kb % NST) * (KS + VS));
+    const int nxt = __builtin_amdgcn_readfirstlane(((kb + 1) % NST) * (KS + VS));
+    const bf16_t* ksn = h == 0 ? smem + cur + 32 * LDK : smem + nxt;
+    const bf16_t* vs = smem + cur + KS;
     // causal mask on diagonal halves; max of this lane's query (raw logits)
-    const bool diag = j0 + 31 > qw0;
+    // (the empty asm keeps this a branch: the compiler would otherwise select per element
+    // on every half)
+    if (j0 + 31 > qw0) {
+      asm volatile("");
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (j0 + 8 * (e >> 2) + 4 * half + (e & 3) > my_q) sc[e] = -INFINITY;
+    }
     float mx = -INFINITY;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      if (diag) {
-        const int key = j0 + 8 * (e >> 2) + 4 * half + (e & 3);
-        if (key > my_q) sc[e] = -INFINITY;
-      }
-      mx = fmaxf(mx, sc[e]);
-    }
+    for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[e]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.sl2;
     // lazy rescale: the reference max moves only when a block max exceeds it by more
     // than RESCALE_SLACK (so P <= 2^RESCALE_SLACK); wave-uniform branch
@@ -142,14 +154,18 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
       pf[u] = __builtin_bit_cast(bf16x8, w);
     }
     // O^T += V^T P^T; K-step u covers keys 32 h + 16 u + {4h'..4h'+3, 8+4h'..8+4h'+3}
-    // (h' = the lane half)
+    // (h' = the lane half): transposing reads at the lane's offset plus constants
+    const bf16_t* vp = vs + vlane + 32 * h * LDV;
 #pragma unroll
     for (int u = 0; u < 2; ++u) {
-      const int klo = 32 * h + 16 * u + 4 * half;
 #pragma unroll
-      for (int c = 0; c < NC; ++c)
-        acc_o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(vs, LDV, 32 * c, klo, klo + 8),
-                                                           pf[u], acc_o[c], 0, 0, 0);
+      for (int c = 0; c < NC; ++c) {
+        const u32x2 lo = lds_read_tr4(vp + 16 * u * LDV + 32 * c);
+        const u32x2 hi = lds_read_tr4(vp + (16 * u + 8) * LDV + 32 * c);
+        const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+        acc_o[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, w), pf[u],
+                                                           acc_o[c], 0, 0, 0);
+      }
     }
   };
 
@@ -160,9 +176,9 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
       bf16_t* nxt = smem + ((kb + 2) % NST) * (KS + VS);
       st.issue((kb + 2) * BKV, nxt, nxt + KS);
     }
-    if (kb < nvis) {  // wave-uniform
+    if (kb < nvis) {  // wave-uniform; a second half entirely above the diagonal is skipped
       step(kb, 0, sa, sb);
-      step(kb, 1, sb, sa);
+      if (kb * BKV + 32 <= qw0) step(kb, 1, sb, sa);
     }
     // tile kb + 2 has landed and nobody reads tile kb's stage any more
     wait_all();
