@@ -177,10 +177,7 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, f32x4 v, float alpha, 
     o[0] += beta * bf2f((bf16_t)(c[0] & 0xffff)); o[1] += beta * bf2f((bf16_t)(c[0] >> 16));
     o[2] += beta * bf2f((bf16_t)(c[1] & 0xffff)); o[3] += beta * bf2f((bf16_t)(c[1] >> 16));
   }
-  u32x2 w;
-  w[0] = (uint32_t)f2bf(o[0]) | ((uint32_t)f2bf(o[1]) << 16);
-  w[1] = (uint32_t)f2bf(o[2]) | ((uint32_t)f2bf(o[3]) << 16);
-  *(u32x2*)p = w;
+  *(u32x2*)p = u32x2{pack2bf(o[0], o[1]), pack2bf(o[2], o[3])};
 }
 
 // ---- the kernel --------------------------------------------------------------------------
@@ -419,43 +416,57 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits,
   store_out<TC>(c, v);
 }
 
-// tile shape: 256 x 256 on 8 wavefronts when that still yields enough workgroups
+// Tile shape and split-K factor.  Candidates: 256 x 256 and 256 x 192 tiles on 8
+// wavefronts (one workgroup per CU) and 128 x 128 tiles on 4 (two per CU).  Workgroups run
+// in rounds of one per CU slot, so a grid of 1.5 rounds costs two: the plan minimises
+// rounds x (work of one workgroup) / (relative matrix-core rate of its tile), plus the
+// split-K partials' traffic, over tile shapes and split factors.
 struct Plan {
-  bool big;
+  int kind;  // 0: 256 x 256, 1: 256 x 192, 2: 128 x 128
   int bm, bn, splits, kchunk;
 };
 
+constexpr int NUM_CU = 256;
+
 Plan plan_of(const Gemm& g, bool allow_split) {
-  Plan p;
-  const int t256 = ((g.M + 255) / 256) * ((g.N + 255) / 256);
-  const int t128 = ((g.M + 127) / 128) * ((g.N + 127) / 128);
-  // a 256-tile wastes work on ragged edges; use it when the padded area stays small
-  const double waste = (double)((g.M + 255) / 256 * 256) * ((g.N + 255) / 256 * 256) /
-                       ((double)((g.M + 127) / 128 * 128) * ((g.N + 127) / 128 * 128));
-  const bool splittable = allow_split && g.K >= 8 * BK * 8;
-  p.big = waste < 1.15 && (t256 >= 192 || splittable);
-  p.bm = p.bn = p.big ? 256 : 128;
-  const int tiles = p.big ? t256 : t128;
-  p.splits = 1;
-  if (splittable && tiles < 512) {
-    const int want = (512 + tiles - 1) / tiles;
-    const int maxs = g.K / (BK * 8);  // at least 512 k per split
-    p.splits = std::max(1, std::min(want, maxs));
+  struct Cand { int kind, bm, bn, per_cu; double rate; };
+  // relative per-CU rates (measured on the step's shapes): the narrower tile reads more
+  // LDS bytes per matrix op; two 4-wavefront workgroups share one CU
+  const Cand cands[] = {{0, 256, 256, 1, 1.0}, {1, 256, 192, 1, 0.93}, {2, 128, 128, 2, 0.62}};
+  Plan best{2, 128, 128, 1, 0};
+  double best_t = 1e300;
+  const int kslices = (g.K + BK - 1) / BK;
+  for (const Cand& c : cands) {
+    const int64_t tiles = (int64_t)((g.M + c.bm - 1) / c.bm) * ((g.N + c.bn - 1) / c.bn);
+    const int max_s = allow_split && g.K >= 8 * BK * 8 ? std::max(1, kslices / 8) : 1;
+    for (int sp = 1; sp <= std::min(max_s, 64); ++sp) {
+      const int kc_sl = (kslices + sp - 1) / sp;  // K slices per split
+      const int splits = (kslices + kc_sl - 1) / kc_sl;
+      if (splits != sp) continue;
+      const int64_t wgs = tiles * splits;
+      const int64_t slots = (int64_t)NUM_CU * c.per_cu;
+      const int64_t rounds = (wgs + slots - 1) / slots;
+      // time units: one 64-deep slice of a 256 x 256 tile at full rate on one CU
+      double t = (double)rounds * kc_sl * ((double)c.bm * c.bn / 65536.0) * c.per_cu / c.rate;
+      // partials written and read back (fp32), at ~one 256 x 256 slice per 128 KB per CU
+      if (splits > 1) t += (double)(splits + 1) * g.M * g.N * 4 / (131072.0 * NUM_CU);
+      if (t < best_t * 0.999) {
+        best_t = t;
+        best = Plan{c.kind, c.bm, c.bn, splits, kc_sl * BK};
+      }
+    }
   }
-  int kchunk = (g.K + p.splits - 1) / p.splits;
-  kchunk = (kchunk + BK - 1) / BK * BK;
-  p.kchunk = std::max(kchunk, BK);
-  p.splits = (g.K + p.kchunk - 1) / p.kchunk;
-  if (p.splits < 1) p.splits = 1;
-  return p;
+  return best;
 }
 
 template <bool AK, bool BKM, typename TC>
 void launch(const GemmDev& d, const Plan& p, hipStream_t s) {
   const int tiles = ((d.M + p.bm - 1) / p.bm) * ((d.N + p.bn - 1) / p.bn);
   dim3 grid(tiles, p.splits);
-  if (p.big)
+  if (p.kind == 0)
     gemm_mfma_kernel<256, 256, GWM, GWN, AK, BKM, TC, GBK, GNST><<<grid, 64 * GWM * GWN, 0, s>>>(d);
+  else if (p.kind == 1)
+    gemm_mfma_kernel<256, 192, 4, 2, AK, BKM, TC, GBK, GNST><<<grid, 512, 0, s>>>(d);
   else
     gemm_mfma_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(d);
 }
