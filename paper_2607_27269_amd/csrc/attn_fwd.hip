@@ -124,7 +124,7 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
     float mx = -INFINITY;
 #pragma unroll
     for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64)) * a.sl2;
+    mx = pair_max32(mx) * a.sl2;
     // lazy rescale: the reference max moves only when a block max exceeds it by more
     // than RESCALE_SLACK (so P <= 2^RESCALE_SLACK); wave-uniform branch
     if (__ballot(mx > m_run + RESCALE_SLACK) != 0) {
@@ -186,7 +186,7 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   }
 
   // normalise and store: lane holds query my_q, d = 32c + 8(e/4) + 4 half + e%4
-  const float l = l_run + __shfl_xor(l_run, 32, 64);
+  const float l = pair_sum32(l_run);
   if (my_q >= a.T) return;
   const float inv = 1.f / l;
   bf16_t* op = a.O + ((int64_t)b * a.T + my_q) * a.o_tok + (int64_t)i * DV + 4 * half;
