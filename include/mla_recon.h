@@ -138,6 +138,18 @@ int mla_recon_bwd(const mla_recon_cfg *cfg, const void *h, const mla_student_w *
                   const void *Wo, const void *dA, const mla_student_grads *grads, void *ws,
                   size_t ws_bytes, void *hip_stream);
 
+/* One whole reconstruction step: teacher forward, student forward, Eq. 11 and the
+ * backward, as the four calls above make it, with one difference: A_t and A_s are not
+ * formed.  Both blocks end in the same frozen W_O (Sec. 4.1), so A_s - A_t =
+ * (o_s - o_t) W_O^T, the only quantity Eq. 11 and its gradient depend on; the step
+ * forms o_s - o_t (storage dtype) and applies W_O once.  tw->Wo is that shared W_O.
+ * mask [B, T] uint8 or NULL (all valid).  Writes loss[0] = L (device fp32; loss[1] = NaN:
+ * the relative error needs A_t), dA [B, T, D] (storage dtype, 16-byte aligned) = dL/dA_s,
+ * and the requested gradients (fp32, overwritten).  ws as for the other calls. */
+int mla_recon_step(const mla_recon_cfg *cfg, const void *h, const mla_teacher_w *tw,
+                   const mla_student_w *sw, const uint8_t *mask, float *loss, void *dA,
+                   const mla_student_grads *grads, void *ws, size_t ws_bytes, void *hip_stream);
+
 /* Text of the last error on the calling thread ("" if none). */
 const char *mla_recon_last_error(void);
 

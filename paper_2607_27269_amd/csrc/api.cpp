@@ -131,8 +131,8 @@ struct Layout {
   size_t b_statT;
   size_t b_ds_bytes;
   size_t b_split_elems;
-  // loss scratch
-  size_t l_scr;
+  // loss scratch; A_s - A_t of the fused step (fp32 [N, D])
+  size_t l_scr, l_diff;
   size_t total;
 };
 
@@ -174,6 +174,7 @@ static Layout layout_of(const Dims& d) {
   L.b_split_elems = se;
   L.b_split = take(se * 4);
   L.l_scr = take(loss_scratch_bytes());
+  L.l_diff = take(N * d.D * 4);
   L.total = o;
   return L;
 }
@@ -226,17 +227,11 @@ size_t mla_recon_workspace_size(const mla_recon_cfg* cfg) {
   return layout_of(dims_of(cfg)).total;
 }
 
-int mla_recon_teacher_fwd(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w* w,
-                          float* A_t, void* ws, size_t ws_bytes, void* hip_stream) {
-  g_err[0] = 0;
-  int rc = check_cfg(cfg);
-  if (rc) return rc;
-  if (!h || !w || !A_t || !w->Wq || !w->Wk || !w->Wv || !w->Wo || !w->inv_freq)
-    return fail(MLA_ERR_INVALID_ARG, "teacher_fwd: NULL pointer argument");
-  Layout L;
-  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+// Teacher forward up to the attention output o_t (ws region t_o); with A_t also the frozen
+// output projection.
+static int teacher_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
+                        const mla_teacher_w* w, float* A_t, void* ws, hipStream_t s) {
   const Dims d = dims_of(cfg);
-  hipStream_t s = (hipStream_t)hip_stream;
   const int N = (int)d.N, D = (int)d.D, H = (int)d.H, G = (int)d.G, dk = (int)d.dk;
   const int64_t ld_qkv = (H + 2 * G) * (int64_t)dk;
   float* cs = (float*)at(ws, L.t_cos);
@@ -263,23 +258,35 @@ int mla_recon_teacher_fwd(const mla_recon_cfg* cfg, const void* h, const mla_tea
   a.O = o; a.o_tok = (int64_t)H * dk; a.lse = nullptr; a.scale = cfg->softmax_scale; a.t = d.t;
   HIP_TRY(attn_fwd(a, s));
   // the fixed output projection: A = concat_i o_i W_O^T
-  HIP_TRY(gemm(mk(N, D, H * dk, o, (int64_t)H * dk, true, w->Wo, (int64_t)H * dk, true, A_t, D, d.t, DT_F32), nullptr, 0, s));
+  if (A_t)
+    HIP_TRY(gemm(mk(N, D, H * dk, o, (int64_t)H * dk, true, w->Wo, (int64_t)H * dk, true, A_t, D, d.t, DT_F32), nullptr, 0, s));
   return MLA_OK;
 }
 
-int mla_recon_student_fwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* w,
-                          const void* Wo, float* A_s, void* ws, size_t ws_bytes,
-                          void* hip_stream) {
+int mla_recon_teacher_fwd(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w* w,
+                          float* A_t, void* ws, size_t ws_bytes, void* hip_stream) {
   g_err[0] = 0;
   int rc = check_cfg(cfg);
   if (rc) return rc;
-  if (!h || !w || !Wo || !A_s || !w->Wuq || !w->Wdkv_kr || !w->Wuv || !w->inv_freq ||
-      (cfg->q_rank > 0 && !w->Wdq) || (cfg->nope_dim > 0 && !w->Wuk))
-    return fail(MLA_ERR_INVALID_ARG, "student_fwd: NULL pointer argument");
+  if (!h || !w || !A_t || !w->Wq || !w->Wk || !w->Wv || !w->Wo || !w->inv_freq)
+    return fail(MLA_ERR_INVALID_ARG, "teacher_fwd: NULL pointer argument");
   Layout L;
   if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  return teacher_impl(cfg, L, h, w, A_t, ws, (hipStream_t)hip_stream);
+}
+
+static bool student_w_ok(const mla_recon_cfg* cfg, const mla_student_w* w) {
+  return w && w->Wuq && w->Wdkv_kr && w->Wuv && w->inv_freq && (cfg->q_rank == 0 || w->Wdq) &&
+         (cfg->nope_dim == 0 || w->Wuk);
+}
+
+// Student forward up to the attention output o_s (kept in ws for the backward); then
+// A_s = o_s W_O^T when A_s is given, and o_diff = o_s - o_ref (storage dtype, same layout)
+// when o_diff is given.
+static int student_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
+                        const mla_student_w* w, const void* Wo, float* A_s, const void* o_ref,
+                        void* o_diff, void* ws, hipStream_t s) {
   const Dims d = dims_of(cfg);
-  hipStream_t s = (hipStream_t)hip_stream;
   const int N = (int)d.N, D = (int)d.D, H = (int)d.H, T = (int)d.T;
   const int rq = (int)d.rq, rkv = (int)d.rkv, dn = (int)d.dn, dr = (int)d.dr, dqk = (int)d.dqk;
   const int dv = (int)d.dv, Gkv = (int)d.Gkv, Gr = (int)d.Gr, kv_out = (int)d.kv_out;
@@ -322,8 +329,23 @@ int mla_recon_student_fwd(const mla_recon_cfg* cfg, const void* h, const mla_stu
   a.O = o; a.o_tok = (int64_t)H * dv; a.lse = lse; a.scale = cfg->softmax_scale; a.t = d.t;
   HIP_TRY(attn_fwd(a, s));
   // the teacher's frozen W_O
-  HIP_TRY(gemm(mk(N, D, H * dv, o, (int64_t)H * dv, true, Wo, (int64_t)H * dv, true, A_s, D, d.t, DT_F32), nullptr, 0, s));
+  if (A_s)
+    HIP_TRY(gemm(mk(N, D, H * dv, o, (int64_t)H * dv, true, Wo, (int64_t)H * dv, true, A_s, D, d.t, DT_F32), nullptr, 0, s));
+  if (o_diff) HIP_TRY(sub_elementwise(o, o_ref, o_diff, (int64_t)N * H * dv, d.t, s));
   return MLA_OK;
+}
+
+int mla_recon_student_fwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* w,
+                          const void* Wo, float* A_s, void* ws, size_t ws_bytes,
+                          void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!h || !Wo || !A_s || !student_w_ok(cfg, w))
+    return fail(MLA_ERR_INVALID_ARG, "student_fwd: NULL pointer argument");
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  return student_impl(cfg, L, h, w, Wo, A_s, nullptr, nullptr, ws, (hipStream_t)hip_stream);
 }
 
 int mla_recon_loss(const mla_recon_cfg* cfg, const float* A_s, const float* A_t,
@@ -343,26 +365,21 @@ int mla_recon_loss(const mla_recon_cfg* cfg, const float* A_s, const float* A_t,
   return MLA_OK;
 }
 
-int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* w,
-                  const void* Wo, const void* dA, const mla_student_grads* gr, void* ws,
-                  size_t ws_bytes, void* hip_stream) {
-  g_err[0] = 0;
-  int rc = check_cfg(cfg);
-  if (rc) return rc;
-  if (!h || !w || !Wo || !dA || !gr || !w->Wuq || !w->Wuv || (cfg->q_rank > 0 && !w->Wdq) ||
-      (cfg->nope_dim > 0 && !w->Wuk))
-    return fail(MLA_ERR_INVALID_ARG, "bwd: NULL pointer argument");
+static int check_grads(const mla_recon_cfg* cfg, const mla_student_grads* gr, const char* who) {
   if (cfg->q_rank == 0 && gr->dWdq)
-    return fail(MLA_ERR_INVALID_ARG, "bwd: dWdq given but q_rank == 0 (no W_DQ)");
+    return fail(MLA_ERR_INVALID_ARG, "%s: dWdq given but q_rank == 0 (no W_DQ)", who);
   if (cfg->nope_dim == 0 && gr->dWuk)
-    return fail(MLA_ERR_INVALID_ARG, "bwd: dWuk given but nope_dim == 0 (no W_UK)");
-  Layout L;
-  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+    return fail(MLA_ERR_INVALID_ARG, "%s: dWuk given but nope_dim == 0 (no W_UK)", who);
+  return MLA_OK;
+}
+
+static int bwd_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
+                    const mla_student_w* w, const void* Wo, const void* dA,
+                    const mla_student_grads* gr, void* ws, hipStream_t s) {
   const bool need_q = gr->dWuq || gr->dWdq;
   const bool need_kv = gr->dWuk || gr->dWuv || gr->dWdkv_kr;
   if (!need_q && !need_kv) return MLA_OK;
   const Dims d = dims_of(cfg);
-  hipStream_t s = (hipStream_t)hip_stream;
   const int N = (int)d.N, D = (int)d.D, H = (int)d.H, T = (int)d.T;
   const int rq = (int)d.rq, rkv = (int)d.rkv, dn = (int)d.dn, dr = (int)d.dr, dqk = (int)d.dqk;
   const int dv = (int)d.dv, Gkv = (int)d.Gkv, Gr = (int)d.Gr, kv_out = (int)d.kv_out;
@@ -440,6 +457,49 @@ int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* 
     }
   }
   return MLA_OK;
+}
+
+int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* w,
+                  const void* Wo, const void* dA, const mla_student_grads* gr, void* ws,
+                  size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!h || !Wo || !dA || !gr || !student_w_ok(cfg, w))
+    return fail(MLA_ERR_INVALID_ARG, "bwd: NULL pointer argument");
+  if ((rc = check_grads(cfg, gr, "bwd"))) return rc;
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  return bwd_impl(cfg, L, h, w, Wo, dA, gr, ws, (hipStream_t)hip_stream);
+}
+
+int mla_recon_step(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w* tw,
+                   const mla_student_w* sw, const uint8_t* mask, float* loss, void* dA,
+                   const mla_student_grads* gr, void* ws, size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!h || !tw || !tw->Wq || !tw->Wk || !tw->Wv || !tw->Wo || !tw->inv_freq ||
+      !student_w_ok(cfg, sw) || !loss || !dA || !gr)
+    return fail(MLA_ERR_INVALID_ARG, "step: NULL pointer argument");
+  if ((uintptr_t)dA % 16) return fail(MLA_ERR_INVALID_ARG, "step: dA must be 16-byte aligned");
+  if ((rc = check_grads(cfg, gr, "step"))) return rc;
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  const Dims d = dims_of(cfg);
+  hipStream_t s = (hipStream_t)hip_stream;
+  // o_t -> ws t_o; o_s (kept for the backward) and o_s - o_t, the latter into the teacher's
+  // q/k/v region, which is free once the teacher's attention has run
+  if ((rc = teacher_impl(cfg, L, h, tw, nullptr, ws, s))) return rc;
+  void* odiff = at(ws, L.t_qkv);
+  if ((rc = student_impl(cfg, L, h, sw, tw->Wo, nullptr, at(ws, L.t_o), odiff, ws, s))) return rc;
+  // A_s - A_t = (o_s - o_t) W_O^T: both blocks end in the same frozen W_O
+  float* diff = (float*)at(ws, L.l_diff);
+  const int N = (int)d.N, D = (int)d.D, HV = (int)(d.H * d.dv);
+  HIP_TRY(gemm(mk(N, D, HV, odiff, HV, true, tw->Wo, HV, true, diff, D, d.t, DT_F32), nullptr, 0, s));
+  // Eq. 11 and dL/dA_s from the difference
+  HIP_TRY(recon_loss(diff, nullptr, mask, d.N, D, loss, dA, d.t, at(ws, L.l_scr), s));
+  return bwd_impl(cfg, L, h, sw, tw->Wo, dA, gr, ws, s);
 }
 
 int mla_recon_prof_enable(int k, int on) {

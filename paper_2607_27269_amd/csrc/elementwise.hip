@@ -251,7 +251,8 @@ __global__ __launch_bounds__(LOSS_THREADS) void loss_main_kernel(
     int64_t n = v / dv;
     float m = (mask == nullptr || mask[n]) ? 1.f : 0.f;
     float4 a = ((const float4*)As)[v];
-    float4 b = ((const float4*)At)[v];
+    // (no reference: As already holds the difference A_s - A_t)
+    float4 b = At ? ((const float4*)At)[v] : make_float4(0.f, 0.f, 0.f, 0.f);
     float e0 = m * (a.x - b.x), e1 = m * (a.y - b.y), e2 = m * (a.z - b.z), e3 = m * (a.w - b.w);
     sse += e0 * e0 + e1 * e1 + e2 * e2 + e3 * e3;
     float r0 = m * b.x, r1 = m * b.y, r2 = m * b.z, r3 = m * b.w;
@@ -277,7 +278,7 @@ __global__ __launch_bounds__(LOSS_THREADS) void loss_main_kernel(
 }
 
 __global__ __launch_bounds__(256) void loss_final_kernel(const LossScratch* __restrict__ ws,
-                                                         int nblocks, int D,
+                                                         int nblocks, int D, bool has_ref,
                                                          float* __restrict__ loss) {
   // thread t sums partials t, t+256, ... in order; then a fixed tree over the 256 threads
   __shared__ double red[2][256];
@@ -306,7 +307,7 @@ __global__ __launch_bounds__(256) void loss_final_kernel(const LossScratch* __re
     return;
   }
   loss[0] = (float)(s / den);
-  loss[1] = r > 0.0 ? (float)(s / r) : (s == 0.0 ? 0.f : INFINITY);
+  loss[1] = !has_ref ? NAN : r > 0.0 ? (float)(s / r) : (s == 0.0 ? 0.f : INFINITY);
 }
 
 hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, int64_t N, int D,
@@ -320,9 +321,44 @@ hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, i
     loss_main_kernel<bf16_t><<<blocks, LOSS_THREADS, 0, s>>>(A_s, A_t, mask, N, D, (bf16_t*)dA, ws);
   else
     loss_main_kernel<float><<<blocks, LOSS_THREADS, 0, s>>>(A_s, A_t, mask, N, D, (float*)dA, ws);
-  loss_final_kernel<<<1, 256, 0, s>>>(ws, blocks, D, loss);
-  double bytes = (double)N * D * (8.0 + (dA ? dsize(t) : 0)) + (mask ? N : 0);
+  loss_final_kernel<<<1, 256, 0, s>>>(ws, blocks, D, A_t != nullptr, loss);
+  double bytes = (double)N * D * ((A_t ? 8.0 : 4.0) + (dA ? dsize(t) : 0)) + (mask ? N : 0);
   prof_end(KC_LOSS, s, 0.0, bytes);
+  return hipGetLastError();
+}
+
+// four consecutive elements (8- or 16-byte aligned) as fp32
+__device__ __forceinline__ f32x4 load4(const float* p) { return *(const f32x4*)p; }
+__device__ __forceinline__ f32x4 load4(const bf16_t* p) {
+  const u32x2 w = *(const u32x2*)p;
+  return f32x4{__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
+               __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u)};
+}
+
+// out = a - b elementwise (n elements of the storage dtype), computed in fp32
+template <typename T>
+__global__ void sub_kernel(const T* __restrict__ a, const T* __restrict__ b, T* __restrict__ out,
+                           int64_t n) {
+  const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i0 >= n) return;
+  if (i0 + 4 <= n) {
+    const f32x4 x = load4(a + i0), y = load4(b + i0);
+    store4<T>(out + i0, x[0] - y[0], x[1] - y[1], x[2] - y[2], x[3] - y[3]);
+  } else {
+    for (int64_t i = i0; i < n; ++i) st<T>(out + i, ld(a + i) - ld(b + i));
+  }
+}
+
+hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, DType t,
+                           hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  const unsigned grid = (unsigned)((n + 4 * 256 - 1) / (4 * 256));
+  prof_begin(KC_ELEM, s);
+  if (t == DT_BF16)
+    sub_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)a, (const bf16_t*)b, (bf16_t*)out, n);
+  else
+    sub_kernel<float><<<grid, 256, 0, s>>>((const float*)a, (const float*)b, (float*)out, n);
+  prof_end(KC_ELEM, s, 0.0, 3.0 * n * dsize(t));
   return hipGetLastError();
 }
 

@@ -117,8 +117,13 @@ hipError_t dkpe_finish(const float* part, void* out, DType t, int64_t out_tok, i
                        int Gr, int per, int drope, const float* cos_t, const float* sin_t,
                        hipStream_t s);
 
+// out = a - b elementwise over n elements of dtype t (fp32 arithmetic)
+hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, DType t,
+                           hipStream_t s);
+
 // Loss (Eq. 11) -------------------------------------------------------------------------
-// scratch: at least loss_scratch_bytes(); loss[0] = L, loss[1] = relative error.
+// scratch: at least loss_scratch_bytes(); loss[0] = L, loss[1] = relative error.  With
+// A_t == nullptr, A_s holds the difference A_s - A_t and loss[1] is NaN.
 size_t loss_scratch_bytes();
 hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, int64_t N, int D,
                       float* loss, void* dA, DType t, void* scratch, hipStream_t s);

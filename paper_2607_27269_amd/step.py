@@ -99,6 +99,13 @@ class DeviceStep:
         self.loss()
         self.bwd()
 
+    def fused_step(self):
+        """The same step through mla_recon_step: W_O applied once to o_s - o_t, A_t and A_s
+        not formed (loss, dA and the gradients only)."""
+        L.mla_recon_step(self.ccfg, _ptr(self.h), self.tw, self.sw, _ptr(self.mask),
+                         _ptr(self.loss_buf), _ptr(self.dA), self.sg, _ptr(self.ws),
+                         self.ws_bytes, self.stream)
+
     def upload(self, x: np.ndarray, dtype: str | None = None) -> torch.Tensor:
         return _dev_tensor(x, dtype or self.dtype, self.device)
 

@@ -28,7 +28,8 @@ def header_functions():
 def test_exports_every_declared_function():
     names = header_functions()
     assert {"mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
-            "mla_recon_bwd", "mla_recon_workspace_size", "mla_recon_last_error"} <= set(names)
+            "mla_recon_bwd", "mla_recon_step", "mla_recon_workspace_size",
+            "mla_recon_last_error"} <= set(names)
     lib = ctypes.CDLL(L.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -98,6 +99,26 @@ def test_null_pointers_and_small_workspace_rejected():
     with pytest.raises(L.MlaError) as e:   # dW_DQ requested without a W_DQ
         L.mla_recon_bwd(c0, 1, L.StudentW(None, 1, 1, 1, 1, 1), 1, 1, g, 256, 1 << 40, None)
     assert e.value.code == L.MLA_ERR_INVALID_ARG
+
+
+def test_step_arguments_validated():
+    cfg = configs.shrink(configs.get(1), batch=1, seq=64)
+    c = L.make_cfg(cfg)
+    ws = L.mla_recon_workspace_size(c)
+    tw = L.TeacherW(1, 1, 1, 1, 1)
+    sw = L.StudentW(1, 1, 1, 1, 1, 1)
+    g = L.StudentGrads(1, 1, 1, 1, 1)
+    for args, code in [
+        ((c, 1, tw, sw, None, None, 256, g, 256, ws, None), L.MLA_ERR_INVALID_ARG),   # no loss
+        ((c, 1, tw, sw, None, 256, None, g, 256, ws, None), L.MLA_ERR_INVALID_ARG),   # no dA
+        ((c, 1, tw, sw, None, 256, 264, g, 256, ws, None), L.MLA_ERR_INVALID_ARG),    # dA align
+        ((c, 1, L.TeacherW(1, 1, 1, None, 1), sw, None, 256, 256, g, 256, ws, None),
+         L.MLA_ERR_INVALID_ARG),                                                      # no W_O
+        ((c, 1, tw, sw, None, 256, 256, g, 256, ws - 1, None), L.MLA_ERR_WORKSPACE),
+    ]:
+        with pytest.raises(L.MlaError) as e:
+            L.mla_recon_step(*args)
+        assert e.value.code == code, (args, L.last_error())
 
 
 def test_prof_class_validation():

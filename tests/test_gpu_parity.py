@@ -54,6 +54,33 @@ def test_step_parity(name):
     print(f"[parity] {name} loss={out['loss']:.6e} ref={ref['loss']:.6e} errs={errs}", flush=True)
 
 
+FUSED_CASES = ("cfg0_ragged_fp32", "cfg0_bf16", "cfg1_ragged", "cfg3_short", "cfg4_short")
+
+
+@pytest.mark.parametrize("name", FUSED_CASES)
+def test_fused_step_parity(name):
+    """mla_recon_step (W_O applied once to o_s - o_t) against the oracle's separate
+    post-W_O outputs: the loss, dL/dA_s and the weight gradients."""
+    import math
+    from paper_2607_27269_amd.step import DeviceStep
+    print(f"[parity] fused case={name}", flush=True)
+    cfg, wl = make_case(name)
+    ref = oracle_step(wl)
+    dev = DeviceStep(wl)
+    dev.fused_step()
+    out = dev.results()
+    tol = TOL[cfg.dtype]
+    errs = compare(out, ref, ("dA",) + GRADS, tol, label=f"fused {name}: ")
+    assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
+    assert math.isnan(out["rel"])
+    # the separate path on the same device state gives the same loss
+    dev.step()
+    again = dev.results()
+    assert abs(again["loss"] - out["loss"]) <= LOSS_TOL * abs(ref["loss"])
+    print(f"[parity] fused {name} loss={out['loss']:.6e} ref={ref['loss']:.6e} errs={errs}",
+          flush=True)
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_loss_kernel_parity(dtype):
     """Eq. 11 kernel alone on seeded A_s, A_t with a ragged mask (oracle in fp64)."""
