@@ -327,11 +327,11 @@ static int student_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h
   a.Kb = HeadView{ckv + (size_t)rkv * ts, kv_out, dr, H / Gr};
   a.V = HeadView{v, (int64_t)Gkv * dv, dv, H / Gkv};
   a.O = o; a.o_tok = (int64_t)H * dv; a.lse = lse; a.scale = cfg->softmax_scale; a.t = d.t;
+  a.o_ref = o_ref; a.o_diff = o_diff;
   HIP_TRY(attn_fwd(a, s));
   // the teacher's frozen W_O
   if (A_s)
     HIP_TRY(gemm(mk(N, D, H * dv, o, (int64_t)H * dv, true, Wo, (int64_t)H * dv, true, A_s, D, d.t, DT_F32), nullptr, 0, s));
-  if (o_diff) HIP_TRY(sub_elementwise(o, o_ref, o_diff, (int64_t)N * H * dv, d.t, s));
   return MLA_OK;
 }
 

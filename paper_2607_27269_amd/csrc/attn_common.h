@@ -34,6 +34,7 @@ struct AttnDev {
   const bf16_t* V; int64_t v_tok; int v_head; int v_div;
   bf16_t* O; int64_t o_tok;
   float* lse;
+  const bf16_t* Oref; bf16_t* Odiff;  // optional: Odiff = O - Oref (rounded O), layout of O
   int nqb;
 };
 
@@ -46,6 +47,7 @@ inline AttnDev to_dev(const Attn& a) {
   d.Kb = (const bf16_t*)a.Kb.p; d.kb_tok = a.Kb.tok; d.kb_head = (int)a.Kb.head; d.kb_div = a.Kb.div;
   d.V = (const bf16_t*)a.V.p; d.v_tok = a.V.tok; d.v_head = (int)a.V.head; d.v_div = a.V.div;
   d.O = (bf16_t*)a.O; d.o_tok = a.o_tok; d.lse = a.lse;
+  d.Oref = (const bf16_t*)a.o_ref; d.Odiff = (bf16_t*)a.o_diff;
   d.nqb = 0;
   return d;
 }

@@ -189,7 +189,8 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   const float l = pair_sum32(l_run);
   if (my_q >= a.T) return;
   const float inv = 1.f / l;
-  bf16_t* op = a.O + ((int64_t)b * a.T + my_q) * a.o_tok + (int64_t)i * DV + 4 * half;
+  const int64_t ooff = ((int64_t)b * a.T + my_q) * a.o_tok + (int64_t)i * DV + 4 * half;
+  bf16_t* op = a.O + ooff;
 #pragma unroll
   for (int c = 0; c < NC; ++c)
 #pragma unroll
@@ -197,6 +198,14 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
       u32x2 w = {pack2bf(acc_o[c][4 * g] * inv, acc_o[c][4 * g + 1] * inv),
                  pack2bf(acc_o[c][4 * g + 2] * inv, acc_o[c][4 * g + 3] * inv)};
       *(u32x2*)(op + 32 * c + 8 * g) = w;
+      if (a.Odiff) {  // uniform
+        const u32x2 r = *(const u32x2*)(a.Oref + ooff + 32 * c + 8 * g);
+        auto lo = [](uint32_t x) { return __uint_as_float(x << 16); };
+        auto hi = [](uint32_t x) { return __uint_as_float(x & 0xffff0000u); };
+        *(u32x2*)(a.Odiff + ooff + 32 * c + 8 * g) =
+            u32x2{pack2bf(lo(w[0]) - lo(r[0]), hi(w[0]) - hi(r[0])),
+                  pack2bf(lo(w[1]) - lo(r[1]), hi(w[1]) - hi(r[1]))};
+      }
     }
   if (LSE && half == 0) a.lse[((int64_t)b * a.T + my_q) * a.H + i] = (m_run + __log2f(l)) * LN2;
 }

@@ -31,10 +31,14 @@ hipError_t attn_fwd(const Attn& a, hipStream_t s) {
   double flops = 2.0 * causal_pairs(a) * (a.dqk + a.dv);
   double N = (double)a.B * a.T;
   double bytes = N * a.H * (a.dqk + a.dv) * dsize(a.t) + N * a.H * (a.lse ? 4.0 : 0.0);
+  if (a.o_diff) bytes += 2.0 * N * a.H * a.dv * dsize(a.t);
+  const bool mfma = a.t == DT_BF16 && attn_mfma_supported(a.dqk, a.dv);
   prof_begin(KC_ATTN_FWD, s);
-  hipError_t e = a.t == DT_BF16 && attn_mfma_supported(a.dqk, a.dv) ? attn_fwd_mfma(a, s)
-                                                                    : attn_fwd_simt(a, s);
+  hipError_t e = mfma ? attn_fwd_mfma(a, s) : attn_fwd_simt(a, s);
   prof_end(KC_ATTN_FWD, s, flops, bytes);
+  // the matrix-core kernel writes o_diff itself; the vector-ALU kernels leave it to a pass
+  if (e == hipSuccess && a.o_diff && !mfma)
+    e = sub_elementwise(a.O, a.o_ref, a.o_diff, (int64_t)N * a.H * a.dv, a.t, s);
   return e;
 }
 

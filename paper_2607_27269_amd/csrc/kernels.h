@@ -57,6 +57,10 @@ struct Attn {
   float* lse;               // [N, H] (natural-log units) or null in the forward
   float scale;
   DType t;
+  // forward only, optional: o_diff = O - o_ref (same layout as O, storage dtype), from the
+  // rounded O
+  const void* o_ref = nullptr;
+  void* o_diff = nullptr;
 };
 hipError_t attn_fwd(const Attn& a, hipStream_t s);
 
