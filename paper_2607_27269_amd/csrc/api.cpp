@@ -137,6 +137,9 @@ struct Layout {
 };
 
 static std::vector<Gemm> bwd_gemm_shapes(const Dims& d);
+static Gemm mk(int M, int N, int K, const void* A, int64_t lda, bool ak, const void* B,
+               int64_t ldb, bool bk, void* C, int64_t ldc, DType in_t, DType c_t,
+               float beta = 0.f);
 
 static Layout layout_of(const Dims& d) {
   Layout L;
@@ -174,7 +177,10 @@ static Layout layout_of(const Dims& d) {
   L.b_split_elems = se;
   L.b_split = take(se * 4);
   L.l_scr = take(loss_scratch_bytes());
-  L.l_diff = take(N * d.D * 4);
+  L.l_diff = take(d.t == DT_F32 ? N * d.D * 4
+                                 : gemm_masked_sse_parts(mk((int)N, (int)d.D, (int)(d.H * d.dv),
+                                                            nullptr, 0, true, nullptr, 0, true,
+                                                            nullptr, 0, d.t, d.t)) * 8);
   L.total = o;
   return L;
 }
@@ -192,7 +198,7 @@ static inline char* at(void* ws, size_t off) { return (char*)ws + off; }
 
 static Gemm mk(int M, int N, int K, const void* A, int64_t lda, bool ak, const void* B,
                int64_t ldb, bool bk, void* C, int64_t ldc, DType in_t, DType c_t,
-               float beta = 0.f) {
+               float beta) {
   Gemm g;
   g.M = M; g.N = N; g.K = K; g.A = A; g.lda = lda; g.a_kmajor = ak; g.B = B; g.ldb = ldb;
   g.b_kmajor = bk; g.C = C; g.ldc = ldc; g.in_t = in_t; g.c_t = c_t; g.alpha = 1.f; g.beta = beta;
@@ -494,11 +500,22 @@ int mla_recon_step(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w*
   void* odiff = at(ws, L.t_qkv);
   if ((rc = student_impl(cfg, L, h, sw, tw->Wo, nullptr, at(ws, L.t_o), odiff, ws, s))) return rc;
   // A_s - A_t = (o_s - o_t) W_O^T: both blocks end in the same frozen W_O
-  float* diff = (float*)at(ws, L.l_diff);
   const int N = (int)d.N, D = (int)d.D, HV = (int)(d.H * d.dv);
-  HIP_TRY(gemm(mk(N, D, HV, odiff, HV, true, tw->Wo, HV, true, diff, D, d.t, DT_F32), nullptr, 0, s));
-  // Eq. 11 and dL/dA_s from the difference
-  HIP_TRY(recon_loss(diff, nullptr, mask, d.N, D, loss, dA, d.t, at(ws, L.l_scr), s));
+  if (d.t == DT_BF16) {
+    // Eq. 11 in the product's epilogue: dA = 2 M (A_s - A_t) / (D sum M) written directly,
+    // the squared masked differences summed per output tile
+    void* scr = at(ws, L.l_scr);
+    double* parts = (double*)at(ws, L.l_diff);
+    int nparts = 0;
+    HIP_TRY(loss_prepare(mask, d.N, D, scr, s));
+    HIP_TRY(gemm_masked_sse(mk(N, D, HV, odiff, HV, true, tw->Wo, HV, true, dA, D, d.t, d.t),
+                            loss_scale(scr), mask, parts, &nparts, s));
+    HIP_TRY(loss_from_parts(parts, nparts, D, loss, scr, s));
+  } else {
+    float* diff = (float*)at(ws, L.l_diff);
+    HIP_TRY(gemm(mk(N, D, HV, odiff, HV, true, tw->Wo, HV, true, diff, D, d.t, DT_F32), nullptr, 0, s));
+    HIP_TRY(recon_loss(diff, nullptr, mask, d.N, D, loss, dA, d.t, at(ws, L.l_scr), s));
+  }
   return bwd_impl(cfg, L, h, sw, tw->Wo, dA, gr, ws, s);
 }
 

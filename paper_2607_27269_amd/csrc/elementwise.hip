@@ -198,13 +198,15 @@ static constexpr int LOSS_THREADS = 256;
 
 struct LossScratch {
   double count;
-  double pad[31];
+  float scale;  // 2 / (D count): dL/dA per unit of masked difference (0 if nothing is valid)
+  float pad_f;
+  double pad[30];
   double part[2 * LOSS_BLOCKS];
 };
 
 size_t loss_scratch_bytes() { return sizeof(LossScratch); }
 
-__global__ void mask_count_kernel(const uint8_t* __restrict__ mask, int64_t N,
+__global__ void mask_count_kernel(const uint8_t* __restrict__ mask, int64_t N, int D,
                                   LossScratch* __restrict__ ws) {
   __shared__ double red[16];
   double c = 0.0;
@@ -221,6 +223,7 @@ __global__ void mask_count_kernel(const uint8_t* __restrict__ mask, int64_t N,
     double t = 0.0;
     for (int i = 0; i < (int)(blockDim.x / 64); ++i) t += red[i];
     ws->count = t;
+    ws->scale = t > 0.0 ? (float)(2.0 / ((double)D * t)) : 0.f;
   }
 }
 
@@ -316,7 +319,7 @@ hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, i
   int64_t nvec = N * (int64_t)D / 4;
   int blocks = (int)std::min<int64_t>(LOSS_BLOCKS, std::max<int64_t>(1, (nvec + LOSS_THREADS - 1) / LOSS_THREADS));
   prof_begin(KC_LOSS, s);
-  mask_count_kernel<<<1, 1024, 0, s>>>(mask, N, ws);
+  mask_count_kernel<<<1, 1024, 0, s>>>(mask, N, D, ws);
   if (t == DT_BF16)
     loss_main_kernel<bf16_t><<<blocks, LOSS_THREADS, 0, s>>>(A_s, A_t, mask, N, D, (bf16_t*)dA, ws);
   else
@@ -324,6 +327,44 @@ hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, i
   loss_final_kernel<<<1, 256, 0, s>>>(ws, blocks, D, A_t != nullptr, loss);
   double bytes = (double)N * D * ((A_t ? 8.0 : 4.0) + (dA ? dsize(t) : 0)) + (mask ? N : 0);
   prof_end(KC_LOSS, s, 0.0, bytes);
+  return hipGetLastError();
+}
+
+// Eq. 11 from per-tile sums of squared masked differences ------------------------------
+hipError_t loss_prepare(const uint8_t* mask, int64_t N, int D, void* scratch, hipStream_t s) {
+  prof_begin(KC_LOSS, s);
+  mask_count_kernel<<<1, 1024, 0, s>>>(mask, N, D, (LossScratch*)scratch);
+  prof_end(KC_LOSS, s, 0.0, mask ? (double)N : 0.0);
+  return hipGetLastError();
+}
+
+const float* loss_scale(const void* scratch) { return &((const LossScratch*)scratch)->scale; }
+
+__global__ __launch_bounds__(256) void loss_parts_kernel(const double* __restrict__ part,
+                                                         int nparts, int D,
+                                                         const LossScratch* __restrict__ ws,
+                                                         float* __restrict__ loss) {
+  // thread t sums parts t, t+256, ... in order; then a fixed tree over the 256 threads
+  __shared__ double red[256];
+  double v = 0.0;
+  for (int i = threadIdx.x; i < nparts; i += 256) v += part[i];
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  if (threadIdx.x != 0) return;
+  const double den = (double)D * ws->count;
+  loss[0] = den > 0.0 ? (float)(red[0] / den) : 0.f;
+  loss[1] = NAN;
+}
+
+hipError_t loss_from_parts(const double* part, int nparts, int D, float* loss,
+                           const void* scratch, hipStream_t s) {
+  prof_begin(KC_LOSS, s);
+  loss_parts_kernel<<<1, 256, 0, s>>>(part, nparts, D, (const LossScratch*)scratch, loss);
+  prof_end(KC_LOSS, s, 0.0, 8.0 * nparts);
   return hipGetLastError();
 }
 

@@ -44,6 +44,9 @@ struct GemmDev {
   const bf16_t* B; int64_t ldb;
   void* C; int64_t ldc;
   float* part;        // split-K partials [splits][M][N], or null
+  // masked-loss epilogue (with lpart set): C = lscale[0] mask[m] acc and lpart[tile] = the
+  // sum over the tile of (mask[m] acc)^2
+  const float* lscale; const uint8_t* lmask; double* lpart;
   float alpha, beta;
   int kchunk;         // K elements per split (multiple of BK)
   int ktotal;
@@ -350,6 +353,9 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   static_assert(NTHR / 64 * 32 * SLD * 4 <= (int)sizeof(lds), "epilogue strip too large");
   float* strip = (float*)lds + wave * 32 * SLD;
   const bool vec = (g.ldc % 4) == 0;
+  const bool lmode = g.lpart != nullptr;  // uniform
+  const float lsc = lmode ? *g.lscale : 0.f;
+  float sse = 0.f;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -365,7 +371,13 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
       const int r = c / CPR, col = (c % CPR) * 4;
       const int m = m0 + wrow0 + i * 32 + r, n = n0 + wcol0 + col;
       if (m >= g.mstore || n >= g.N) continue;
-      const f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+      f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+      if (lmode) {
+        if (n + 4 > g.N) v = f32x4{v[0], n + 1 < g.N ? v[1] : 0.f, n + 2 < g.N ? v[2] : 0.f, 0.f};
+        if (g.lmask && !g.lmask[m]) v = f32x4{0.f, 0.f, 0.f, 0.f};
+        sse += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+        v *= lsc;
+      }
       if (g.part) {
         float* p = g.part + ((int64_t)split * g.M + m) * g.N + n;
         if (n + 4 <= g.N && (g.N % 4) == 0) {
@@ -385,6 +397,20 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
           store_out<TC>(p + q, x);
         }
       }
+    }
+  }
+  if (lmode) {
+    // the tile's sum in a fixed order: lanes (fixed tree), then wavefronts in order
+    // (the last bytes of the operand LDS, past every wavefront's strip)
+    static_assert(NTHR / 64 * 32 * SLD * 4 + 8 * (NTHR / 64) <= (int)sizeof(lds), "LDS");
+    double* lred = (double*)((char*)lds + sizeof(lds)) - NTHR / 64;
+    const double ws = warp_sum_d((double)sse);
+    if (lane == 0) lred[wave] = ws;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double t = 0.0;
+      for (int w = 0; w < NTHR / 64; ++w) t += lred[w];
+      g.lpart[blockIdx.x] = t;
     }
   }
 }
@@ -485,6 +511,7 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = g.beta;
   d.mstore = g.M;
+  d.lscale = nullptr; d.lmask = nullptr; d.lpart = nullptr;
   d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
   d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
   Plan p = plan_of(g, true);
@@ -510,6 +537,37 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   else
     splitk_reduce_kernel<bf16_t><<<grid, 256, 0, s>>>(scratch, p.splits, g.M, g.N, (bf16_t*)g.C,
                                                       g.ldc, g.alpha, g.beta);
+  return hipGetLastError();
+}
+
+size_t gemm_mfma_masked_sse_parts(const Gemm& g) {
+  return (size_t)((g.M + 127) / 128) * ((g.N + 127) / 128);
+}
+
+hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
+                                double* part, int* nparts, hipStream_t s) {
+  if (g.beta != 0.f || g.alpha != 1.f || g.in_t != DT_BF16) return hipErrorInvalidValue;
+  GemmDev d;
+  d.M = g.M; d.N = g.N; d.ktotal = g.K;
+  d.A = (const bf16_t*)g.A; d.lda = g.lda;
+  d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
+  d.C = g.C; d.ldc = g.ldc; d.alpha = 1.f; d.beta = 0.f;
+  d.mstore = g.M;
+  d.lscale = scale; d.lmask = mask; d.lpart = part;
+  d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
+  d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
+  const Plan p = plan_of(g, false);
+  d.kchunk = p.kchunk;
+  d.part = nullptr;
+  *nparts = ((g.M + p.bm - 1) / p.bm) * ((g.N + p.bn - 1) / p.bn);
+  const bool f32 = g.c_t == DT_F32;
+#define L_(AK, BK_)                                                                     \
+  if (g.a_kmajor == AK && g.b_kmajor == BK_) {                                          \
+    if (f32) launch<AK, BK_, float>(d, p, s);                                           \
+    else launch<AK, BK_, bf16_t>(d, p, s);                                              \
+  }
+  L_(true, true) else return hipErrorInvalidValue;
+#undef L_
   return hipGetLastError();
 }
 
@@ -547,6 +605,7 @@ hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s) {
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = 0.f;
   d.part = nullptr;
+  d.lscale = nullptr; d.lmask = nullptr; d.lpart = nullptr;
   d.kchunk = (g.K + BK - 1) / BK * BK;
   d.mstore = bt.mstore;
   d.causal = 1; d.rev = bt.rev; d.nbatch = bt.nbatch; d.zdiv = bt.zdiv; d.bdiv = bt.bdiv;

@@ -121,6 +121,21 @@ hipError_t dkpe_finish(const float* part, void* out, DType t, int64_t out_tok, i
                        int Gr, int per, int drope, const float* cos_t, const float* sin_t,
                        hipStream_t s);
 
+// Eq. 11 with the masked squared differences summed per GEMM tile (gemm_masked_sse):
+// loss_prepare counts the valid tokens and stores the gradient scale 2 / (D count), which
+// loss_scale points to (device fp32); loss_from_parts then writes loss[0] = L from the
+// tile sums (fixed order) and loss[1] = NaN.
+hipError_t loss_prepare(const uint8_t* mask, int64_t N, int D, void* scratch, hipStream_t s);
+const float* loss_scale(const void* scratch);
+hipError_t loss_from_parts(const double* part, int nparts, int D, float* loss,
+                           const void* scratch, hipStream_t s);
+// C = scale[0] mask[m] (A B^T)[m, n] in C's dtype and part[t] = the sum over output tile t
+// of (mask[m] (A B^T)[m, n])^2 (bf16 operands, both K-contiguous); *nparts tiles, at most
+// gemm_masked_sse_parts(g).
+size_t gemm_masked_sse_parts(const Gemm& g);
+hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask, double* part,
+                           int* nparts, hipStream_t s);
+
 // out = a - b elementwise over n elements of dtype t (fp32 arithmetic)
 hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, DType t,
                            hipStream_t s);
