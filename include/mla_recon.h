@@ -142,10 +142,15 @@ int mla_recon_bwd(const mla_recon_cfg *cfg, const void *h, const mla_student_w *
  * backward, as the four calls above make it, with one difference: A_t and A_s are not
  * formed.  Both blocks end in the same frozen W_O (Sec. 4.1), so A_s - A_t =
  * (o_s - o_t) W_O^T, the only quantity Eq. 11 and its gradient depend on; the step
- * forms o_s - o_t (storage dtype) and applies W_O once.  tw->Wo is that shared W_O.
+ * forms o_s - o_t (storage dtype) and applies W_O to it.  tw->Wo is that shared W_O.
  * mask [B, T] uint8 or NULL (all valid).  Writes loss[0] = L (device fp32; loss[1] = NaN:
- * the relative error needs A_t), dA [B, T, D] (storage dtype, 16-byte aligned) = dL/dA_s,
- * and the requested gradients (fp32, overwritten).  ws as for the other calls. */
+ * the relative error needs A_t) and the requested gradients (fp32, overwritten).
+ * dA: NULL, or [B, T, D] (storage dtype, 16-byte aligned) that receives dL/dA_s.  Without
+ * dA (bf16), the backward's dL/do_s = dA W_O is taken as 2 M Y / (D sum M) with
+ * Y = (o_s - o_t) W_O^T W_O, and each token's squared error as its row of Y dotted with
+ * its row of o_s - o_t: W_O^T W_O is formed (every call) and one [B T, H d_k] x
+ * [H d_k, H d_k] product replaces the two [B T, D] x [D, H d_k] ones.  ws as for the
+ * other calls. */
 int mla_recon_step(const mla_recon_cfg *cfg, const void *h, const mla_teacher_w *tw,
                    const mla_student_w *sw, const uint8_t *mask, float *loss, void *dA,
                    const mla_student_grads *grads, void *ws, size_t ws_bytes, void *hip_stream);

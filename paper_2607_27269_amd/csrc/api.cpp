@@ -131,8 +131,9 @@ struct Layout {
   size_t b_statT;
   size_t b_ds_bytes;
   size_t b_split_elems;
-  // loss scratch; A_s - A_t of the fused step (fp32 [N, D])
-  size_t l_scr, l_diff;
+  // loss scratch; the single-call step's per-tile sums (bf16) or A_s - A_t (fp32), its
+  // W_O^T W_O (bf16) and, in fp32, its dA when the caller passes none
+  size_t l_scr, l_diff, l_gram, l_da;
   size_t total;
 };
 
@@ -177,10 +178,16 @@ static Layout layout_of(const Dims& d) {
   L.b_split_elems = se;
   L.b_split = take(se * 4);
   L.l_scr = take(loss_scratch_bytes());
+  const int HV = (int)(d.H * d.dv);
   L.l_diff = take(d.t == DT_F32 ? N * d.D * 4
-                                 : gemm_masked_sse_parts(mk((int)N, (int)d.D, (int)(d.H * d.dv),
-                                                            nullptr, 0, true, nullptr, 0, true,
-                                                            nullptr, 0, d.t, d.t)) * 8);
+                                 : std::max(gemm_masked_sse_parts(mk((int)N, (int)d.D, HV, nullptr, 0,
+                                                                     true, nullptr, 0, true, nullptr,
+                                                                     0, d.t, d.t)),
+                                            gemm_masked_sse_parts(mk((int)N, HV, HV, nullptr, 0,
+                                                                     true, nullptr, 0, true, nullptr,
+                                                                     0, d.t, d.t))) * 8);
+  L.l_gram = take(d.t == DT_BF16 ? (size_t)HV * HV * 2 : 0);
+  L.l_da = take(d.t == DT_F32 ? N * d.D * 4 : 0);
   L.total = o;
   return L;
 }
@@ -412,8 +419,9 @@ static int bwd_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
   const size_t se = L.b_split_elems;
   const int64_t ld_dkv = (int64_t)Gkv * (dn + dv);
 
-  // dO = dA W_O  (W_O frozen: no dW_O)
-  HIP_TRY(gemm(mk(N, H * dv, D, dA, D, true, Wo, (int64_t)H * dv, false, dO, (int64_t)H * dv, t, t), nullptr, 0, s));
+  // dO = dA W_O  (W_O frozen: no dW_O); without dA, dO is already in place
+  if (dA)
+    HIP_TRY(gemm(mk(N, H * dv, D, dA, D, true, Wo, (int64_t)H * dv, false, dO, (int64_t)H * dv, t, t), nullptr, 0, s));
   // softmax-attention backward -> dq (rotary block rotated back), dk^nope, dv, dk^PE partials
   AttnBwd ab;
   Attn& a = ab.f;
@@ -486,7 +494,7 @@ int mla_recon_step(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w*
   int rc = check_cfg(cfg);
   if (rc) return rc;
   if (!h || !tw || !tw->Wq || !tw->Wk || !tw->Wv || !tw->Wo || !tw->inv_freq ||
-      !student_w_ok(cfg, sw) || !loss || !dA || !gr)
+      !student_w_ok(cfg, sw) || !loss || !gr)
     return fail(MLA_ERR_INVALID_ARG, "step: NULL pointer argument");
   if ((uintptr_t)dA % 16) return fail(MLA_ERR_INVALID_ARG, "step: dA must be 16-byte aligned");
   if ((rc = check_grads(cfg, gr, "step"))) return rc;
@@ -501,6 +509,23 @@ int mla_recon_step(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w*
   if ((rc = student_impl(cfg, L, h, sw, tw->Wo, nullptr, at(ws, L.t_o), odiff, ws, s))) return rc;
   // A_s - A_t = (o_s - o_t) W_O^T: both blocks end in the same frozen W_O
   const int N = (int)d.N, D = (int)d.D, HV = (int)(d.H * d.dv);
+  if (d.t == DT_BF16 && !dA) {
+    // dA not requested: with Y = (o_s - o_t) W_O^T W_O, the backward's dO = dA W_O is
+    // 2 M Y / (D sum M) and each token's squared error is its row of Y dotted with its row
+    // of o_s - o_t; W_O^T W_O (frozen weights, H d_v square) is formed here every step
+    void* scr = at(ws, L.l_scr);
+    double* parts = (double*)at(ws, L.l_diff);
+    void* gram = at(ws, L.l_gram);
+    void* dO = at(ws, L.b_do);
+    int nparts = 0;
+    HIP_TRY(gemm(mk(HV, HV, D, tw->Wo, HV, false, tw->Wo, HV, false, gram, HV, d.t, d.t), nullptr, 0, s));
+    HIP_TRY(loss_prepare(mask, d.N, D, scr, s));
+    HIP_TRY(gemm_masked_sse(mk(N, HV, HV, odiff, HV, true, gram, HV, true, dO, HV, d.t, d.t),
+                            loss_scale(scr), mask, odiff, HV, parts, &nparts, s));
+    HIP_TRY(loss_from_parts(parts, nparts, D, loss, scr, s));
+    return bwd_impl(cfg, L, h, sw, tw->Wo, nullptr, gr, ws, s);
+  }
+  if (!dA) dA = at(ws, L.l_da);
   if (d.t == DT_BF16) {
     // Eq. 11 in the product's epilogue: dA = 2 M (A_s - A_t) / (D sum M) written directly,
     // the squared masked differences summed per output tile
@@ -509,7 +534,7 @@ int mla_recon_step(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w*
     int nparts = 0;
     HIP_TRY(loss_prepare(mask, d.N, D, scr, s));
     HIP_TRY(gemm_masked_sse(mk(N, D, HV, odiff, HV, true, tw->Wo, HV, true, dA, D, d.t, d.t),
-                            loss_scale(scr), mask, parts, &nparts, s));
+                            loss_scale(scr), mask, nullptr, 0, parts, &nparts, s));
     HIP_TRY(loss_from_parts(parts, nparts, D, loss, scr, s));
   } else {
     float* diff = (float*)at(ws, L.l_diff);

@@ -25,13 +25,14 @@ hipError_t gemm(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t
 
 size_t gemm_masked_sse_parts(const Gemm& g) { return gemm_mfma_masked_sse_parts(g); }
 
-hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask, double* part,
-                           int* nparts, hipStream_t s) {
+hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
+                           const void* ref, int64_t ldref, double* part, int* nparts,
+                           hipStream_t s) {
   double flops = 2.0 * g.M * g.N * (double)g.K;
   double bytes = ((double)g.M * g.K + (double)g.N * g.K) * dsize(g.in_t) +
-                 (double)g.M * g.N * dsize(g.c_t) + (mask ? (double)g.M : 0.0);
+                 (double)g.M * g.N * dsize(g.c_t) * (ref ? 2.0 : 1.0) + (mask ? (double)g.M : 0.0);
   prof_begin(KC_GEMM_NT, s);
-  hipError_t e = gemm_mfma_masked_sse(g, scale, mask, part, nparts, s);
+  hipError_t e = gemm_mfma_masked_sse(g, scale, mask, ref, ldref, part, nparts, s);
   prof_end(KC_GEMM_NT, s, flops, bytes);
   return e;
 }

@@ -45,8 +45,9 @@ struct GemmDev {
   void* C; int64_t ldc;
   float* part;        // split-K partials [splits][M][N], or null
   // masked-loss epilogue (with lpart set): C = lscale[0] mask[m] acc and lpart[tile] = the
-  // sum over the tile of (mask[m] acc)^2
+  // sum over the tile of mask[m] acc^2, or of mask[m] acc lref[m, n] when lref is set
   const float* lscale; const uint8_t* lmask; double* lpart;
+  const bf16_t* lref; int64_t ldref;
   float alpha, beta;
   int kchunk;         // K elements per split (multiple of BK)
   int ktotal;
@@ -375,7 +376,19 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
       if (lmode) {
         if (n + 4 > g.N) v = f32x4{v[0], n + 1 < g.N ? v[1] : 0.f, n + 2 < g.N ? v[2] : 0.f, 0.f};
         if (g.lmask && !g.lmask[m]) v = f32x4{0.f, 0.f, 0.f, 0.f};
-        sse += v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+        f32x4 r = v;
+        if (g.lref) {
+          const bf16_t* rp = g.lref + (int64_t)m * g.ldref + n;
+          if (n + 4 <= g.N && (g.ldref & 3) == 0) {
+            const u32x2 w = *(const u32x2*)rp;
+            r = f32x4{__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
+                      __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u)};
+          } else {
+            r = f32x4{bf2f(rp[0]), n + 1 < g.N ? bf2f(rp[1]) : 0.f,
+                      n + 2 < g.N ? bf2f(rp[2]) : 0.f, n + 3 < g.N ? bf2f(rp[3]) : 0.f};
+          }
+        }
+        sse += v[0] * r[0] + v[1] * r[1] + v[2] * r[2] + v[3] * r[3];
         v *= lsc;
       }
       if (g.part) {
@@ -511,7 +524,7 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = g.beta;
   d.mstore = g.M;
-  d.lscale = nullptr; d.lmask = nullptr; d.lpart = nullptr;
+  d.lscale = nullptr; d.lmask = nullptr; d.lpart = nullptr; d.lref = nullptr; d.ldref = 0;
   d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
   d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
   Plan p = plan_of(g, true);
@@ -545,7 +558,8 @@ size_t gemm_mfma_masked_sse_parts(const Gemm& g) {
 }
 
 hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
-                                double* part, int* nparts, hipStream_t s) {
+                                const void* ref, int64_t ldref, double* part, int* nparts,
+                                hipStream_t s) {
   if (g.beta != 0.f || g.alpha != 1.f || g.in_t != DT_BF16) return hipErrorInvalidValue;
   GemmDev d;
   d.M = g.M; d.N = g.N; d.ktotal = g.K;
@@ -554,6 +568,7 @@ hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t
   d.C = g.C; d.ldc = g.ldc; d.alpha = 1.f; d.beta = 0.f;
   d.mstore = g.M;
   d.lscale = scale; d.lmask = mask; d.lpart = part;
+  d.lref = (const bf16_t*)ref; d.ldref = ldref;
   d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
   d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
   const Plan p = plan_of(g, false);
@@ -605,7 +620,7 @@ hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s) {
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = 0.f;
   d.part = nullptr;
-  d.lscale = nullptr; d.lmask = nullptr; d.lpart = nullptr;
+  d.lscale = nullptr; d.lmask = nullptr; d.lpart = nullptr; d.lref = nullptr; d.ldref = 0;
   d.kchunk = (g.K + BK - 1) / BK * BK;
   d.mstore = bt.mstore;
   d.causal = 1; d.rev = bt.rev; d.nbatch = bt.nbatch; d.zdiv = bt.zdiv; d.bdiv = bt.bdiv;

@@ -129,12 +129,14 @@ hipError_t loss_prepare(const uint8_t* mask, int64_t N, int D, void* scratch, hi
 const float* loss_scale(const void* scratch);
 hipError_t loss_from_parts(const double* part, int nparts, int D, float* loss,
                            const void* scratch, hipStream_t s);
-// C = scale[0] mask[m] (A B^T)[m, n] in C's dtype and part[t] = the sum over output tile t
-// of (mask[m] (A B^T)[m, n])^2 (bf16 operands, both K-contiguous); *nparts tiles, at most
+// C = scale[0] mask[m] X[m, n] in C's dtype, X = A B^T, and part[t] = the sum over output
+// tile t of mask[m] X[m, n]^2, or of mask[m] X[m, n] ref[m, n] with ref (bf16, row stride
+// ldref) given (bf16 operands, both K-contiguous); *nparts tiles, at most
 // gemm_masked_sse_parts(g).
 size_t gemm_masked_sse_parts(const Gemm& g);
-hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask, double* part,
-                           int* nparts, hipStream_t s);
+hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
+                           const void* ref, int64_t ldref, double* part, int* nparts,
+                           hipStream_t s);
 
 // out = a - b elementwise over n elements of dtype t (fp32 arithmetic)
 hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, DType t,

@@ -5,12 +5,14 @@
 namespace mla {
 size_t gemm_mfma_scratch_elems(const Gemm& g);
 hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s);
-// C = scale[0] mask[m] (A B^T)[m, n] (mask null = all rows) and part[t] = the sum over output
-// tile t of (mask[m] (A B^T)[m, n])^2, in a fixed order; *nparts = the number of tiles
-// (at most gemm_mfma_masked_sse_parts).  Both operands K-contiguous, no split-K.
+// C = scale[0] mask[m] X[m, n] with X = A B^T (mask null = all rows) and part[t] = the sum
+// over output tile t of mask[m] X[m, n]^2, or of mask[m] X[m, n] ref[m, n] (bf16, row
+// stride ldref) when ref is given, in a fixed order; *nparts = the number of tiles (at most
+// gemm_mfma_masked_sse_parts).  Both operands K-contiguous, no split-K.
 size_t gemm_mfma_masked_sse_parts(const Gemm& g);
 hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
-                                double* part, int* nparts, hipStream_t s);
+                                const void* ref, int64_t ldref, double* part, int* nparts,
+                                hipStream_t s);
 // Batch entry z of a batched causal GEMM uses A + z sA, B + (z / zdiv) sB1 +
 // ((z % zdiv) / bdiv) sB2 and C + (z / zdiv) sC1 + (z % zdiv) sC2 (elements).  Row m of C
 // sums k < min(K, end of m's 256-row tile) (rev = 0; A M-contiguous, bf16 C) or

@@ -99,12 +99,12 @@ class DeviceStep:
         self.loss()
         self.bwd()
 
-    def fused_step(self):
-        """The same step through mla_recon_step: W_O applied once to o_s - o_t, A_t and A_s
-        not formed (loss, dA and the gradients only)."""
+    def fused_step(self, with_dA: bool = True):
+        """The same step through mla_recon_step: W_O applied to o_s - o_t, A_t and A_s not
+        formed (loss, the gradients and, with_dA, dL/dA_s)."""
         L.mla_recon_step(self.ccfg, _ptr(self.h), self.tw, self.sw, _ptr(self.mask),
-                         _ptr(self.loss_buf), _ptr(self.dA), self.sg, _ptr(self.ws),
-                         self.ws_bytes, self.stream)
+                         _ptr(self.loss_buf), _ptr(self.dA) if with_dA else None, self.sg,
+                         _ptr(self.ws), self.ws_bytes, self.stream)
 
     def upload(self, x: np.ndarray, dtype: str | None = None) -> torch.Tensor:
         return _dev_tensor(x, dtype or self.dtype, self.device)

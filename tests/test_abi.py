@@ -110,7 +110,8 @@ def test_step_arguments_validated():
     g = L.StudentGrads(1, 1, 1, 1, 1)
     for args, code in [
         ((c, 1, tw, sw, None, None, 256, g, 256, ws, None), L.MLA_ERR_INVALID_ARG),   # no loss
-        ((c, 1, tw, sw, None, 256, None, g, 256, ws, None), L.MLA_ERR_INVALID_ARG),   # no dA
+        ((L.make_cfg(cfg.replace(q_rank=0)), 1, tw, L.StudentW(None, 1, 1, 1, 1, 1), None, 256,
+          None, g, 256, ws, None), L.MLA_ERR_INVALID_ARG),                            # dWdq, no W_DQ
         ((c, 1, tw, sw, None, 256, 264, g, 256, ws, None), L.MLA_ERR_INVALID_ARG),    # dA align
         ((c, 1, L.TeacherW(1, 1, 1, None, 1), sw, None, 256, 256, g, 256, ws, None),
          L.MLA_ERR_INVALID_ARG),                                                      # no W_O

@@ -57,20 +57,21 @@ def test_step_parity(name):
 FUSED_CASES = ("cfg0_ragged_fp32", "cfg0_bf16", "cfg1_ragged", "cfg3_short", "cfg4_short")
 
 
+@pytest.mark.parametrize("with_dA", [True, False])
 @pytest.mark.parametrize("name", FUSED_CASES)
-def test_fused_step_parity(name):
-    """mla_recon_step (W_O applied once to o_s - o_t) against the oracle's separate
-    post-W_O outputs: the loss, dL/dA_s and the weight gradients."""
+def test_fused_step_parity(name, with_dA):
+    """mla_recon_step (W_O applied to o_s - o_t; without dA through W_O^T W_O) against the
+    oracle's separate post-W_O outputs: the loss, dL/dA_s and the weight gradients."""
     import math
     from paper_2607_27269_amd.step import DeviceStep
-    print(f"[parity] fused case={name}", flush=True)
+    print(f"[parity] fused case={name} with_dA={with_dA}", flush=True)
     cfg, wl = make_case(name)
     ref = oracle_step(wl)
     dev = DeviceStep(wl)
-    dev.fused_step()
+    dev.fused_step(with_dA)
     out = dev.results()
     tol = TOL[cfg.dtype]
-    errs = compare(out, ref, ("dA",) + GRADS, tol, label=f"fused {name}: ")
+    errs = compare(out, ref, (("dA",) if with_dA else ()) + GRADS, tol, label=f"fused {name}: ")
     assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
     assert math.isnan(out["rel"])
     # the separate path on the same device state gives the same loss
