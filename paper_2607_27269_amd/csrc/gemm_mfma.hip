@@ -469,9 +469,11 @@ constexpr int NUM_CU = 256;
 
 Plan plan_of(const Gemm& g, bool allow_split) {
   struct Cand { int kind, bm, bn, per_cu; double rate; };
-  // relative per-CU rates (measured on the step's shapes): the narrower tile reads more
-  // LDS bytes per matrix op; two 4-wavefront workgroups share one CU
-  const Cand cands[] = {{0, 256, 256, 1, 1.0}, {1, 256, 192, 1, 0.93}, {2, 128, 128, 2, 0.62}};
+  // relative per-CU rates (fitted to timings of the step's shapes): the narrower tile reads
+  // more LDS bytes per matrix op (much more so with an M-contiguous A); two 4-wavefront
+  // workgroups share one CU
+  const Cand cands[] = {{0, 256, 256, 1, 1.0}, {1, 256, 192, 1, g.a_kmajor ? 0.93 : 0.7},
+                        {2, 128, 128, 2, 0.62}};
   Plan best{2, 128, 128, 1, 0};
   double best_t = 1e300;
   const int kslices = (g.K + BK - 1) / BK;
@@ -487,8 +489,9 @@ Plan plan_of(const Gemm& g, bool allow_split) {
       const int64_t rounds = (wgs + slots - 1) / slots;
       // time units: one 64-deep slice of a 256 x 256 tile at full rate on one CU
       double t = (double)rounds * kc_sl * ((double)c.bm * c.bn / 65536.0) * c.per_cu / c.rate;
-      // partials written and read back (fp32), at ~one 256 x 256 slice per 128 KB per CU
-      if (splits > 1) t += (double)(splits + 1) * g.M * g.N * 4 / (131072.0 * NUM_CU);
+      // partials written and read back (fp32): fitted to the same timings, about 3 MB per
+      // unit of time (one 64-deep slice of a 256 x 256 tile)
+      if (splits > 1) t += (double)(splits + 1) * g.M * g.N * 4 / 3.0e6;
       if (t < best_t * 0.999) {
         best_t = t;
         best = Plan{c.kind, c.bm, c.bn, splits, kc_sl * BK};
