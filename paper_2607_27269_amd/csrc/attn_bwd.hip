@@ -379,12 +379,37 @@ struct DvStage {
   // block blk = wave + 4 p: its kind is wave-uniform (blk < NQB: Q, < NQB + NOB: dO, then
   // the statistics block, then padding that re-copies Q row 0 into unused LDS).  A full
   // block (all 32 queries inside the sequence) is copied from wave-uniform row bases with
-  // loop-invariant lane offsets; the last, partial block clamps rows to the sequence end.
+  // loop-invariant lane offsets, computed once (init); the last, partial block clamps rows
+  // to the sequence end.
+  uint32_t voff[PER];  // byte offset of this lane's chunk from its block's row base
+  __device__ __forceinline__ void init(const BwdDev& w) {
+    const AttnDev& a = w.f;
+    const int wave = wave_id(), lane = threadIdx.x & 63;
+    const int64_t o_tok = (int64_t)a.H * DV;
+    const uint32_t s_part = (uint32_t)a.H * a.B * w.tpad * 4;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int blk = wave + 4 * p;
+      uint32_t off = 0u;
+      if (blk < NQB) {
+        const int e = (blk * 1024 + 16 * lane) / 2;
+        const int r = min(e / LDQ, DV_BQ - 1), c0 = e % LDQ, c = c0 < DQK ? c0 : 0;
+        off = 2u * (uint32_t)(r * (int)a.q_tok + c);
+      } else if (blk < NQB + NOB) {
+        const int e = ((blk - NQB) * 1024 + 16 * lane) / 2;
+        const int r = min(e / LDO, DV_BQ - 1), c0 = e % LDO, c = c0 < DV ? c0 : 0;
+        off = 2u * (uint32_t)(r * (int)o_tok + c);
+      } else if (blk == NQB + NOB) {
+        off = ((lane >> 3) & 1) * s_part + 16u * (lane & 7);
+      }
+      voff[p] = off;
+    }
+  }
   __device__ __forceinline__ void issue(const BwdDev& w, int b, int h, int q0, bf16_t* stage) const {
     const AttnDev& a = w.f;
     const int wave = wave_id();
-    // opaque copy of the lane id: the lane offsets below are recomputed (32-bit arithmetic)
-    // at every issue instead of being kept live across the loop
+    // opaque copy of the lane id: the clamped path below recomputes its lane offsets at
+    // every issue instead of keeping them live across the loop
     int lane = threadIdx.x & 63;
     asm volatile("" : "+v"(lane));
     const int last = a.T - 1;
@@ -398,21 +423,12 @@ struct DvStage {
 #pragma unroll
       for (int p = 0; p < PER; ++p) {
         const int blk = wave + 4 * p;
-        if (blk < NQB) {
-          const int e = (blk * 1024 + 16 * lane) / 2;
-          const int r = min(e / LDQ, DV_BQ - 1), c0 = e % LDQ, c = c0 < DQK ? c0 : 0;
-          dma16_s(qrow, 2u * (uint32_t)(r * (int)a.q_tok + c), stage + blk * 512);
-        } else if (blk < NQB + NOB) {
-          const int e = ((blk - NQB) * 1024 + 16 * lane) / 2;
-          const int r = min(e / LDO, DV_BQ - 1), c0 = e % LDO, c = c0 < DV ? c0 : 0;
-          dma16_s(orow, 2u * (uint32_t)(r * (int)o_tok + c), stage + blk * 512);
-        } else if (blk == NQB + NOB) {
-          // lanes 0-7: lse2 of queries q0 + 4 l .. + 3; lanes 8-15: delta; the rest repeat
-          const uint32_t off = ((lane >> 3) & 1) * s_part + 16u * (lane & 7);
-          dma16_s(sbase, off, stage + blk * 512);
-        } else {
-          dma16_s(qrow, 0u, stage + blk * 512);
-        }
+        // statistics block: lanes 0-7 lse2 of queries q0 + 4 l .. + 3, lanes 8-15 delta, the
+        // rest repeat; padding blocks re-copy Q row 0 (offset 0)
+        const void* base = blk < NQB ? (const void*)qrow
+                           : blk < NQB + NOB ? (const void*)orow
+                           : blk == NQB + NOB ? (const void*)sbase : (const void*)qrow;
+        dma16_s(base, voff[p], stage + blk * 512);
       }
       return;
     }
@@ -508,6 +524,7 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
   const int nper = nqb - qb0;
   const int niter = hpg * nper;  // >= 1
   Stage stg;
+  stg.init(w);
   // steps walk (query block, head): query blocks in descending order with the group's heads
   // innermost, so that all key blocks of a (sequence, group) stream the same Q/dO tile at
   // the same time and share it through L2.  (qc, hc) is this step's pair, (qn, hn) the
