@@ -35,6 +35,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-separate", action="store_true",
                    help="skip the reference timing of the four-call step (profiling runs)")
+    p.add_argument("--no-cached", action="store_true",
+                   help="skip the timing of the cached-teacher step (profiling runs)")
     p.add_argument("--cpu-seq", type=int, default=4096, help="oracle sample: tokens of one sequence")
     p.add_argument("--calib-copy-mb", type=int, default=0,
                    help="run one device-to-device copy of this many MiB first (HBM counter calibration)")
@@ -198,6 +200,20 @@ def main():
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
 
+    # also reported: the step with the teacher cached (its output depends only on h and the
+    # frozen weights, so a training loop can compute it once per minibatch)
+    ms_cached = None
+    if not args.no_cached:
+        dev.teacher_cache()
+        dev.student_step(with_dA=False)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            dev.student_step(with_dA=False)
+        stop.record()
+        torch.cuda.synchronize()
+        ms_cached = start.elapsed_time(stop) / args.steps
+
     # for reference: the four separate calls, which also form A_t and A_s (two W_O products)
     ms_sep = None
     if not args.no_separate:
@@ -266,6 +282,9 @@ def main():
         "alg_gflop_per_step": round(flops / 1e9, 1),
         "ms_per_step_instrumented": round(ms_instr, 4),
         "ms_per_step_separate_outputs": ms_sep,
+        "cached_teacher": None if ms_cached is None else
+                          {"ms_per_step": round(ms_cached, 4),
+                           "value": round(tokens / (ms_cached / 1e3), 1), "unit": "tokens/s"},
         "kernel_ms_per_step": kernel_share,
         "roofline": {"kernel": f"{dom}: {L.KCLASS_KERNELS[dom]}", "bound": bound, "achieved": round(achieved, 2),
                      "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),

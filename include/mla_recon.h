@@ -155,6 +155,20 @@ int mla_recon_step(const mla_recon_cfg *cfg, const void *h, const mla_teacher_w 
                    const mla_student_w *sw, const uint8_t *mask, float *loss, void *dA,
                    const mla_student_grads *grads, void *ws, size_t ws_bytes, void *hip_stream);
 
+/* The single-call step with the teacher cached (the frozen block's output depends only on
+ * h and frozen weights, so it can be reused across steps on the same minibatch).
+ * mla_recon_teacher_cache runs the teacher forward up to its attention output o_t (and,
+ * bf16, W_O^T W_O) into ws; mla_recon_student_step then does everything mla_recon_step
+ * does after the teacher, as often as wanted, for the same h, teacher weights and ws
+ * (which keeps the cache until a call other than mla_recon_student_step uses it).  Wo is
+ * the teacher's W_O; other arguments as for mla_recon_step. */
+int mla_recon_teacher_cache(const mla_recon_cfg *cfg, const void *h, const mla_teacher_w *tw,
+                            void *ws, size_t ws_bytes, void *hip_stream);
+int mla_recon_student_step(const mla_recon_cfg *cfg, const void *h, const mla_student_w *sw,
+                           const void *Wo, const uint8_t *mask, float *loss, void *dA,
+                           const mla_student_grads *grads, void *ws, size_t ws_bytes,
+                           void *hip_stream);
+
 /* Text of the last error on the calling thread ("" if none). */
 const char *mla_recon_last_error(void);
 

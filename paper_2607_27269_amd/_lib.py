@@ -92,9 +92,12 @@ def lib() -> ctypes.CDLL:
         L.mla_recon_bwd.argtypes = [P(Cfg), vp, P(StudentW), vp, vp, P(StudentGrads), vp, sz, vp]
         L.mla_recon_step.argtypes = [P(Cfg), vp, P(TeacherW), P(StudentW), vp, vp, vp,
                                      P(StudentGrads), vp, sz, vp]
+        L.mla_recon_teacher_cache.argtypes = [P(Cfg), vp, P(TeacherW), vp, sz, vp]
+        L.mla_recon_student_step.argtypes = [P(Cfg), vp, P(StudentW), vp, vp, vp, vp,
+                                             P(StudentGrads), vp, sz, vp]
         for f in ("mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
-                  "mla_recon_bwd", "mla_recon_step", "mla_recon_prof_enable",
-                  "mla_recon_prof_read"):
+                  "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
+                  "mla_recon_student_step", "mla_recon_prof_enable", "mla_recon_prof_read"):
             getattr(L, f).restype = i32
         L.mla_recon_last_error.argtypes = []
         L.mla_recon_last_error.restype = ctypes.c_char_p
@@ -156,6 +159,19 @@ def mla_recon_step(cfg: Cfg, h: int, tw: TeacherW, sw: StudentW, mask: int | Non
                    dA: int, grads: StudentGrads, ws: int, ws_bytes: int, stream: int) -> None:
     _check(lib().mla_recon_step(ctypes.byref(cfg), h, ctypes.byref(tw), ctypes.byref(sw), mask,
                                 loss, dA, ctypes.byref(grads), ws, ws_bytes, stream))
+
+
+def mla_recon_teacher_cache(cfg: Cfg, h: int, tw: TeacherW, ws: int, ws_bytes: int,
+                            stream: int) -> None:
+    _check(lib().mla_recon_teacher_cache(ctypes.byref(cfg), h, ctypes.byref(tw), ws, ws_bytes,
+                                         stream))
+
+
+def mla_recon_student_step(cfg: Cfg, h: int, sw: StudentW, Wo: int, mask: int | None, loss: int,
+                           dA: int | None, grads: StudentGrads, ws: int, ws_bytes: int,
+                           stream: int) -> None:
+    _check(lib().mla_recon_student_step(ctypes.byref(cfg), h, ctypes.byref(sw), Wo, mask, loss,
+                                        dA, ctypes.byref(grads), ws, ws_bytes, stream))
 
 
 def mla_recon_prof_enable(kclass: int, on: bool) -> None:

@@ -487,43 +487,40 @@ int mla_recon_bwd(const mla_recon_cfg* cfg, const void* h, const mla_student_w* 
   return bwd_impl(cfg, L, h, w, Wo, dA, gr, ws, (hipStream_t)hip_stream);
 }
 
-int mla_recon_step(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w* tw,
-                   const mla_student_w* sw, const uint8_t* mask, float* loss, void* dA,
-                   const mla_student_grads* gr, void* ws, size_t ws_bytes, void* hip_stream) {
-  g_err[0] = 0;
-  int rc = check_cfg(cfg);
-  if (rc) return rc;
-  if (!h || !tw || !tw->Wq || !tw->Wk || !tw->Wv || !tw->Wo || !tw->inv_freq ||
-      !student_w_ok(cfg, sw) || !loss || !gr)
-    return fail(MLA_ERR_INVALID_ARG, "step: NULL pointer argument");
-  if ((uintptr_t)dA % 16) return fail(MLA_ERR_INVALID_ARG, "step: dA must be 16-byte aligned");
-  if ((rc = check_grads(cfg, gr, "step"))) return rc;
-  Layout L;
-  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+// W_O^T W_O (bf16, ws region l_gram) for the step without dA
+static int gram_impl(const Dims& d, const Layout& L, const void* Wo, void* ws, hipStream_t s) {
+  const int D = (int)d.D, HV = (int)(d.H * d.dv);
+  HIP_TRY(gemm(mk(HV, HV, D, Wo, HV, false, Wo, HV, false, at(ws, L.l_gram), HV, d.t, d.t), nullptr, 0, s));
+  return MLA_OK;
+}
+
+// Everything of the single-call step after the teacher: o_t is in ws (t_o) and, for the
+// bf16 step without dA, W_O^T W_O in ws (l_gram).
+static int student_step_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
+                             const mla_student_w* sw, const void* Wo, const uint8_t* mask,
+                             float* loss, void* dA, const mla_student_grads* gr, void* ws,
+                             hipStream_t s) {
   const Dims d = dims_of(cfg);
-  hipStream_t s = (hipStream_t)hip_stream;
-  // o_t -> ws t_o; o_s (kept for the backward) and o_s - o_t, the latter into the teacher's
-  // q/k/v region, which is free once the teacher's attention has run
-  if ((rc = teacher_impl(cfg, L, h, tw, nullptr, ws, s))) return rc;
+  int rc;
+  // o_s (kept for the backward) and o_s - o_t, the latter into the teacher's q/k/v region,
+  // which is free once the teacher's attention has run
   void* odiff = at(ws, L.t_qkv);
-  if ((rc = student_impl(cfg, L, h, sw, tw->Wo, nullptr, at(ws, L.t_o), odiff, ws, s))) return rc;
+  if ((rc = student_impl(cfg, L, h, sw, Wo, nullptr, at(ws, L.t_o), odiff, ws, s))) return rc;
   // A_s - A_t = (o_s - o_t) W_O^T: both blocks end in the same frozen W_O
   const int N = (int)d.N, D = (int)d.D, HV = (int)(d.H * d.dv);
   if (d.t == DT_BF16 && !dA) {
     // dA not requested: with Y = (o_s - o_t) W_O^T W_O, the backward's dO = dA W_O is
     // 2 M Y / (D sum M) and each token's squared error is its row of Y dotted with its row
-    // of o_s - o_t; W_O^T W_O (frozen weights, H d_v square) is formed here every step
+    // of o_s - o_t
     void* scr = at(ws, L.l_scr);
     double* parts = (double*)at(ws, L.l_diff);
-    void* gram = at(ws, L.l_gram);
     void* dO = at(ws, L.b_do);
     int nparts = 0;
-    HIP_TRY(gemm(mk(HV, HV, D, tw->Wo, HV, false, tw->Wo, HV, false, gram, HV, d.t, d.t), nullptr, 0, s));
     HIP_TRY(loss_prepare(mask, d.N, D, scr, s));
-    HIP_TRY(gemm_masked_sse(mk(N, HV, HV, odiff, HV, true, gram, HV, true, dO, HV, d.t, d.t),
+    HIP_TRY(gemm_masked_sse(mk(N, HV, HV, odiff, HV, true, at(ws, L.l_gram), HV, true, dO, HV, d.t, d.t),
                             loss_scale(scr), mask, odiff, HV, parts, &nparts, s));
     HIP_TRY(loss_from_parts(parts, nparts, D, loss, scr, s));
-    return bwd_impl(cfg, L, h, sw, tw->Wo, nullptr, gr, ws, s);
+    return bwd_impl(cfg, L, h, sw, Wo, nullptr, gr, ws, s);
   }
   if (!dA) dA = at(ws, L.l_da);
   if (d.t == DT_BF16) {
@@ -533,15 +530,71 @@ int mla_recon_step(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w*
     double* parts = (double*)at(ws, L.l_diff);
     int nparts = 0;
     HIP_TRY(loss_prepare(mask, d.N, D, scr, s));
-    HIP_TRY(gemm_masked_sse(mk(N, D, HV, odiff, HV, true, tw->Wo, HV, true, dA, D, d.t, d.t),
+    HIP_TRY(gemm_masked_sse(mk(N, D, HV, odiff, HV, true, Wo, HV, true, dA, D, d.t, d.t),
                             loss_scale(scr), mask, nullptr, 0, parts, &nparts, s));
     HIP_TRY(loss_from_parts(parts, nparts, D, loss, scr, s));
   } else {
     float* diff = (float*)at(ws, L.l_diff);
-    HIP_TRY(gemm(mk(N, D, HV, odiff, HV, true, tw->Wo, HV, true, diff, D, d.t, DT_F32), nullptr, 0, s));
+    HIP_TRY(gemm(mk(N, D, HV, odiff, HV, true, Wo, HV, true, diff, D, d.t, DT_F32), nullptr, 0, s));
     HIP_TRY(recon_loss(diff, nullptr, mask, d.N, D, loss, dA, d.t, at(ws, L.l_scr), s));
   }
-  return bwd_impl(cfg, L, h, sw, tw->Wo, dA, gr, ws, s);
+  return bwd_impl(cfg, L, h, sw, Wo, dA, gr, ws, s);
+}
+
+static bool teacher_w_ok(const mla_teacher_w* tw) {
+  return tw && tw->Wq && tw->Wk && tw->Wv && tw->Wo && tw->inv_freq;
+}
+
+static int check_step_args(const mla_recon_cfg* cfg, const void* h, const mla_student_w* sw,
+                           float* loss, void* dA, const mla_student_grads* gr, const char* who) {
+  if (!h || !student_w_ok(cfg, sw) || !loss || !gr)
+    return fail(MLA_ERR_INVALID_ARG, "%s: NULL pointer argument", who);
+  if ((uintptr_t)dA % 16) return fail(MLA_ERR_INVALID_ARG, "%s: dA must be 16-byte aligned", who);
+  return check_grads(cfg, gr, who);
+}
+
+int mla_recon_step(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w* tw,
+                   const mla_student_w* sw, const uint8_t* mask, float* loss, void* dA,
+                   const mla_student_grads* gr, void* ws, size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!teacher_w_ok(tw)) return fail(MLA_ERR_INVALID_ARG, "step: NULL pointer argument");
+  if ((rc = check_step_args(cfg, h, sw, loss, dA, gr, "step"))) return rc;
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  hipStream_t s = (hipStream_t)hip_stream;
+  if ((rc = teacher_impl(cfg, L, h, tw, nullptr, ws, s))) return rc;
+  if (cfg->dtype == MLA_BF16 && !dA && (rc = gram_impl(dims_of(cfg), L, tw->Wo, ws, s))) return rc;
+  return student_step_impl(cfg, L, h, sw, tw->Wo, mask, loss, dA, gr, ws, s);
+}
+
+int mla_recon_teacher_cache(const mla_recon_cfg* cfg, const void* h, const mla_teacher_w* tw,
+                            void* ws, size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!h || !teacher_w_ok(tw)) return fail(MLA_ERR_INVALID_ARG, "teacher_cache: NULL pointer argument");
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  hipStream_t s = (hipStream_t)hip_stream;
+  if ((rc = teacher_impl(cfg, L, h, tw, nullptr, ws, s))) return rc;
+  if (cfg->dtype == MLA_BF16) return gram_impl(dims_of(cfg), L, tw->Wo, ws, s);
+  return MLA_OK;
+}
+
+int mla_recon_student_step(const mla_recon_cfg* cfg, const void* h, const mla_student_w* sw,
+                           const void* Wo, const uint8_t* mask, float* loss, void* dA,
+                           const mla_student_grads* gr, void* ws, size_t ws_bytes,
+                           void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!Wo) return fail(MLA_ERR_INVALID_ARG, "student_step: NULL pointer argument");
+  if ((rc = check_step_args(cfg, h, sw, loss, dA, gr, "student_step"))) return rc;
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  return student_step_impl(cfg, L, h, sw, Wo, mask, loss, dA, gr, ws, (hipStream_t)hip_stream);
 }
 
 int mla_recon_prof_enable(int k, int on) {

@@ -106,6 +106,17 @@ class DeviceStep:
                          _ptr(self.loss_buf), _ptr(self.dA) if with_dA else None, self.sg,
                          _ptr(self.ws), self.ws_bytes, self.stream)
 
+    def teacher_cache(self):
+        """Teacher forward up to its attention output (and W_O^T W_O), kept in the workspace."""
+        L.mla_recon_teacher_cache(self.ccfg, _ptr(self.h), self.tw, _ptr(self.ws), self.ws_bytes,
+                                  self.stream)
+
+    def student_step(self, with_dA: bool = True):
+        """The single-call step after the teacher, on the cached teacher output."""
+        L.mla_recon_student_step(self.ccfg, _ptr(self.h), self.sw, _ptr(self.Wo), _ptr(self.mask),
+                                 _ptr(self.loss_buf), _ptr(self.dA) if with_dA else None, self.sg,
+                                 _ptr(self.ws), self.ws_bytes, self.stream)
+
     def upload(self, x: np.ndarray, dtype: str | None = None) -> torch.Tensor:
         return _dev_tensor(x, dtype or self.dtype, self.device)
 

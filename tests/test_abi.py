@@ -28,7 +28,8 @@ def header_functions():
 def test_exports_every_declared_function():
     names = header_functions()
     assert {"mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
-            "mla_recon_bwd", "mla_recon_step", "mla_recon_workspace_size",
+            "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
+            "mla_recon_student_step", "mla_recon_workspace_size",
             "mla_recon_last_error"} <= set(names)
     lib = ctypes.CDLL(L.LIB_PATH)
     for n in names:
@@ -120,6 +121,25 @@ def test_step_arguments_validated():
         with pytest.raises(L.MlaError) as e:
             L.mla_recon_step(*args)
         assert e.value.code == code, (args, L.last_error())
+
+
+def test_cached_teacher_arguments_validated():
+    cfg = configs.shrink(configs.get(1), batch=1, seq=64)
+    c = L.make_cfg(cfg)
+    ws = L.mla_recon_workspace_size(c)
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_teacher_cache(c, 1, L.TeacherW(1, 1, 1, None, 1), 256, ws, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_teacher_cache(c, 1, L.TeacherW(1, 1, 1, 1, 1), 256, ws - 1, None)
+    assert e.value.code == L.MLA_ERR_WORKSPACE
+    sw, g = L.StudentW(1, 1, 1, 1, 1, 1), L.StudentGrads(1, 1, 1, 1, 1)
+    with pytest.raises(L.MlaError) as e:                                       # no W_O
+        L.mla_recon_student_step(c, 1, sw, None, None, 256, None, g, 256, ws, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
+    with pytest.raises(L.MlaError) as e:                                       # no loss
+        L.mla_recon_student_step(c, 1, sw, 1, None, None, None, g, 256, ws, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
 
 
 def test_prof_class_validation():

@@ -82,6 +82,32 @@ def test_fused_step_parity(name, with_dA):
           flush=True)
 
 
+@pytest.mark.parametrize("name", ("cfg0_ragged_fp32", "cfg1_ragged", "cfg3_short"))
+def test_cached_teacher_parity(name):
+    """mla_recon_teacher_cache once, then mla_recon_student_step twice (without, then with
+    dA): both match the oracle, and the two steps give bitwise equal gradients."""
+    import torch
+    from paper_2607_27269_amd.step import DeviceStep
+    print(f"[parity] cached teacher case={name}", flush=True)
+    cfg, wl = make_case(name)
+    ref = oracle_step(wl)
+    dev = DeviceStep(wl)
+    dev.teacher_cache()
+    dev.student_step(with_dA=False)
+    first = dev.results()
+    dev.student_step(with_dA=True)
+    second = dev.results()
+    tol = TOL[cfg.dtype]
+    for out, names in ((first, GRADS), (second, ("dA",) + GRADS)):
+        compare(out, ref, names, tol, label=f"cached {name}: ")
+        assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
+    if cfg.dtype == "fp32":
+        for n in GRADS:
+            if n in first:
+                assert np.array_equal(first[n], second[n]), n
+    torch.cuda.synchronize()
+
+
 @pytest.mark.parametrize("dtype", ["fp32", "bf16"])
 def test_loss_kernel_parity(dtype):
     """Eq. 11 kernel alone on seeded A_s, A_t with a ragged mask (oracle in fp64)."""
