@@ -4,3 +4,4 @@ from .mla_recon_oracle import (  # noqa: F401
     teacher_forward, teacher_logits, student_logits, student_forward, recon_loss,
     student_backward, reconstruction_step,
 )
+from .adamw_oracle import adamw_step  # noqa: F401
