@@ -169,6 +169,25 @@ int mla_recon_student_step(const mla_recon_cfg *cfg, const void *h, const mla_st
                            const mla_student_grads *grads, void *ws, size_t ws_bytes,
                            void *hip_stream);
 
+/* Optimizer step of the reconstruction loop (Sec. 4.1 trains the converter-introduced
+ * projections but names no optimizer; this is AdamW: bias-corrected Adam moments, weight
+ * decay decoupled from the gradient).  For each of `count` (1-8) tensors of n elements:
+ *   m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2
+ *   master -= lr ((m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps)
+ *                 + weight_decay master)
+ *   w = master rounded to the storage dtype (round to nearest even for bf16).
+ * master, m, v and grad are fp32, w is in `dtype`; all caller-owned device arrays, 16-byte
+ * aligned, updated in place (fp32 arithmetic).  step counts from 1.  One launch. */
+typedef struct {
+  float *master, *m, *v;
+  void *w;
+  const float *grad;
+  int64_t n;
+} mla_adamw_tensor;
+int mla_recon_adamw(const mla_adamw_tensor *tensors, int32_t count, int32_t dtype, int32_t step,
+                    float lr, float beta1, float beta2, float eps, float weight_decay,
+                    void *hip_stream);
+
 /* Text of the last error on the calling thread ("" if none). */
 const char *mla_recon_last_error(void);
 

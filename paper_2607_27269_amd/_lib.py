@@ -72,6 +72,11 @@ class StudentGrads(ctypes.Structure):
                 ("dWuv", ctypes.c_void_p)]
 
 
+class AdamwTensor(ctypes.Structure):
+    _fields_ = [("master", ctypes.c_void_p), ("m", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("w", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("n", ctypes.c_int64)]
+
+
 _lib = None
 
 
@@ -93,11 +98,15 @@ def lib() -> ctypes.CDLL:
         L.mla_recon_step.argtypes = [P(Cfg), vp, P(TeacherW), P(StudentW), vp, vp, vp,
                                      P(StudentGrads), vp, sz, vp]
         L.mla_recon_teacher_cache.argtypes = [P(Cfg), vp, P(TeacherW), vp, sz, vp]
+        L.mla_recon_adamw.argtypes = [P(AdamwTensor), i32, i32, i32, ctypes.c_float,
+                                      ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                      ctypes.c_float, vp]
         L.mla_recon_student_step.argtypes = [P(Cfg), vp, P(StudentW), vp, vp, vp, vp,
                                              P(StudentGrads), vp, sz, vp]
         for f in ("mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
                   "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
-                  "mla_recon_student_step", "mla_recon_prof_enable", "mla_recon_prof_read"):
+                  "mla_recon_student_step", "mla_recon_adamw", "mla_recon_prof_enable",
+                  "mla_recon_prof_read"):
             getattr(L, f).restype = i32
         L.mla_recon_last_error.argtypes = []
         L.mla_recon_last_error.restype = ctypes.c_char_p
@@ -172,6 +181,13 @@ def mla_recon_student_step(cfg: Cfg, h: int, sw: StudentW, Wo: int, mask: int | 
                            stream: int) -> None:
     _check(lib().mla_recon_student_step(ctypes.byref(cfg), h, ctypes.byref(sw), Wo, mask, loss,
                                         dA, ctypes.byref(grads), ws, ws_bytes, stream))
+
+
+def mla_recon_adamw(tensors: list, dtype: int, step: int, lr: float, beta1: float, beta2: float,
+                    eps: float, weight_decay: float, stream: int) -> None:
+    arr = (AdamwTensor * len(tensors))(*tensors)
+    _check(lib().mla_recon_adamw(arr, len(tensors), dtype, step, lr, beta1, beta2, eps,
+                                 weight_decay, stream))
 
 
 def mla_recon_prof_enable(kclass: int, on: bool) -> None:

@@ -597,6 +597,35 @@ int mla_recon_student_step(const mla_recon_cfg* cfg, const void* h, const mla_st
   return student_step_impl(cfg, L, h, sw, Wo, mask, loss, dA, gr, ws, (hipStream_t)hip_stream);
 }
 
+int mla_recon_adamw(const mla_adamw_tensor* tensors, int32_t count, int32_t dtype, int32_t step,
+                    float lr, float beta1, float beta2, float eps, float weight_decay,
+                    void* hip_stream) {
+  g_err[0] = 0;
+  if (!tensors || count < 1 || count > ADAMW_MAX)
+    return fail(MLA_ERR_INVALID_ARG, "adamw: between 1 and %d tensors", ADAMW_MAX);
+  if (dtype != MLA_BF16 && dtype != MLA_FP32)
+    return fail(MLA_ERR_INVALID_ARG, "adamw: unknown dtype %d", dtype);
+  if (step < 1) return fail(MLA_ERR_INVALID_ARG, "adamw: step counts from 1");
+  if (!(lr >= 0.f && lr < 1e30f) || !(beta1 >= 0.f && beta1 < 1.f) ||
+      !(beta2 >= 0.f && beta2 < 1.f) || !(eps > 0.f && eps < 1e30f) ||
+      !(weight_decay >= 0.f && weight_decay < 1e30f))
+    return fail(MLA_ERR_INVALID_ARG, "adamw: hyperparameters out of range");
+  AdamwTensor t[ADAMW_MAX];
+  for (int i = 0; i < count; ++i) {
+    const mla_adamw_tensor& x = tensors[i];
+    if (x.n < 0) return fail(MLA_ERR_INVALID_ARG, "adamw: tensor %d has negative size", i);
+    if (x.n > 0 && (!x.master || !x.m || !x.v || !x.w || !x.grad))
+      return fail(MLA_ERR_INVALID_ARG, "adamw: tensor %d: NULL pointer", i);
+    if (((uintptr_t)x.master | (uintptr_t)x.m | (uintptr_t)x.v | (uintptr_t)x.w |
+         (uintptr_t)x.grad) % 16)
+      return fail(MLA_ERR_INVALID_ARG, "adamw: tensor %d: arrays must be 16-byte aligned", i);
+    t[i] = AdamwTensor{x.master, x.m, x.v, x.w, x.grad, x.n};
+  }
+  HIP_TRY(adamw_step(t, count, dtype == MLA_FP32 ? DT_F32 : DT_BF16, lr, beta1, beta2, eps,
+                     weight_decay, step, (hipStream_t)hip_stream));
+  return MLA_OK;
+}
+
 int mla_recon_prof_enable(int k, int on) {
   if (k < 0 || k >= KC_COUNT) return fail(MLA_ERR_INVALID_ARG, "bad kernel class %d", k);
   std::lock_guard<std::mutex> lk(g_prof_mu);

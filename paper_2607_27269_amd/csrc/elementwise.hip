@@ -403,4 +403,74 @@ hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, D
   return hipGetLastError();
 }
 
+// AdamW over up to ADAMW_MAX tensors in one launch (blockIdx.y = tensor) ----------------
+struct AdamwArgs {
+  AdamwTensor t[ADAMW_MAX];
+  float lr, b1, b2, eps, wd, bc1, bc2;  // bc = 1 / (1 - beta^step)
+};
+
+template <typename T>
+__device__ __forceinline__ void adamw_one(const AdamwArgs& a, float& w, float& m, float& v, float g) {
+  m = a.b1 * m + (1.f - a.b1) * g;
+  v = a.b2 * v + (1.f - a.b2) * g * g;
+  w = w - a.lr * ((m * a.bc1) / (sqrtf(v * a.bc2) + a.eps) + a.wd * w);
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void adamw_kernel(AdamwArgs a) {
+  const AdamwTensor& t = a.t[blockIdx.y];
+  const int64_t i0 = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i0 >= t.n) return;
+  T* w = (T*)t.w;
+  if (i0 + 4 <= t.n) {
+    f32x4 ws = *(const f32x4*)(t.master + i0), ms = *(const f32x4*)(t.m + i0);
+    f32x4 vs = *(const f32x4*)(t.v + i0);
+    const f32x4 gs = *(const f32x4*)(t.g + i0);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      float wk = ws[k], mk = ms[k], vk = vs[k];
+      adamw_one<T>(a, wk, mk, vk, gs[k]);
+      ws[k] = wk;
+      ms[k] = mk;
+      vs[k] = vk;
+    }
+    *(f32x4*)(t.master + i0) = ws;
+    *(f32x4*)(t.m + i0) = ms;
+    *(f32x4*)(t.v + i0) = vs;
+    store4<T>(w + i0, ws[0], ws[1], ws[2], ws[3]);
+  } else {
+    for (int64_t i = i0; i < t.n; ++i) {
+      float wi = t.master[i], mi = t.m[i], vi = t.v[i];
+      adamw_one<T>(a, wi, mi, vi, t.g[i]);
+      t.master[i] = wi;
+      t.m[i] = mi;
+      t.v[i] = vi;
+      st<T>(w + i, wi);
+    }
+  }
+}
+
+hipError_t adamw_step(const AdamwTensor* t, int count, DType wt, float lr, float beta1,
+                      float beta2, float eps, float weight_decay, int step, hipStream_t s) {
+  if (count < 1 || count > ADAMW_MAX) return hipErrorInvalidValue;
+  AdamwArgs a;
+  int64_t nmax = 0;
+  double bytes = 0.0;
+  for (int i = 0; i < ADAMW_MAX; ++i) {
+    a.t[i] = i < count ? t[i] : AdamwTensor{nullptr, nullptr, nullptr, nullptr, nullptr, 0};
+    nmax = std::max(nmax, a.t[i].n);
+    bytes += (double)a.t[i].n * (4.0 * 7 + dsize(wt));
+  }
+  a.lr = lr; a.b1 = beta1; a.b2 = beta2; a.eps = eps; a.wd = weight_decay;
+  a.bc1 = (float)(1.0 / (1.0 - std::pow((double)beta1, step)));
+  a.bc2 = (float)(1.0 / (1.0 - std::pow((double)beta2, step)));
+  if (nmax == 0) return hipSuccess;
+  const dim3 grid((unsigned)((nmax + 1023) / 1024), (unsigned)count);
+  prof_begin(KC_ELEM, s);
+  if (wt == DT_BF16) adamw_kernel<bf16_t><<<grid, 256, 0, s>>>(a);
+  else adamw_kernel<float><<<grid, 256, 0, s>>>(a);
+  prof_end(KC_ELEM, s, 0.0, bytes);
+  return hipGetLastError();
+}
+
 }  // namespace mla

@@ -138,6 +138,15 @@ hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mas
                            const void* ref, int64_t ldref, double* part, int* nparts,
                            hipStream_t s);
 
+// AdamW (decoupled weight decay) on up to ADAMW_MAX tensors: fp32 master weights, moments
+// and gradient; w (dtype wt) receives the rounded master weights.  16-byte aligned arrays.
+constexpr int ADAMW_MAX = 8;
+struct AdamwTensor {
+  float* master; float* m; float* v; void* w; const float* g; int64_t n;
+};
+hipError_t adamw_step(const AdamwTensor* t, int count, DType wt, float lr, float beta1,
+                      float beta2, float eps, float weight_decay, int step, hipStream_t s);
+
 // out = a - b elementwise over n elements of dtype t (fp32 arithmetic)
 hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, DType t,
                            hipStream_t s);

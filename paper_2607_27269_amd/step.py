@@ -117,6 +117,39 @@ class DeviceStep:
                                  _ptr(self.loss_buf), _ptr(self.dA) if with_dA else None, self.sg,
                                  _ptr(self.ws), self.ws_bytes, self.stream)
 
+    # ---- optimizer (AdamW on the trainable projections, mla_recon_adamw) -----------------
+    def init_optimizer(self):
+        """fp32 master copies of the trainable weights and zero moments."""
+        self.opt = []
+        for gname, W in (("dWdq", self.Wdq), ("dWuq", self.Wuq), ("dWdkv_kr", self.Wdkv_kr),
+                         ("dWuk", self.Wuk), ("dWuv", self.Wuv)):
+            if W is None or gname not in self.grads:
+                continue
+            master = W.float().clone()
+            self.opt.append((W, master, torch.zeros_like(master), torch.zeros_like(master),
+                             self.grads[gname]))
+        self.opt_steps = 0
+
+    def optimizer_step(self, lr: float, beta1: float = 0.9, beta2: float = 0.999,
+                       eps: float = 1e-8, weight_decay: float = 0.0):
+        self.opt_steps += 1
+        ts = [L.AdamwTensor(_ptr(master), _ptr(m), _ptr(v), _ptr(W), _ptr(g), master.numel())
+              for (W, master, m, v, g) in self.opt]
+        L.mla_recon_adamw(ts, L.MLA_FP32 if self.dtype == "fp32" else L.MLA_BF16,
+                          self.opt_steps, lr, beta1, beta2, eps, weight_decay, self.stream)
+
+    def train(self, steps: int, lr: float, **adamw) -> torch.Tensor:
+        """`steps` optimizer steps on this minibatch (teacher recomputed each step, as Eq. 11
+        is written); returns the loss before each update (host fp32 [steps])."""
+        if not hasattr(self, "opt"):
+            self.init_optimizer()
+        losses = torch.empty(steps, dtype=torch.float32, device=self.device)
+        for i in range(steps):
+            self.fused_step(with_dA=False)
+            losses[i] = self.loss_buf[0]
+            self.optimizer_step(lr, **adamw)
+        return losses.cpu()
+
     def upload(self, x: np.ndarray, dtype: str | None = None) -> torch.Tensor:
         return _dev_tensor(x, dtype or self.dtype, self.device)
 

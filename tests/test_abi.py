@@ -29,7 +29,7 @@ def test_exports_every_declared_function():
     names = header_functions()
     assert {"mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
             "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
-            "mla_recon_student_step", "mla_recon_workspace_size",
+            "mla_recon_student_step", "mla_recon_adamw", "mla_recon_workspace_size",
             "mla_recon_last_error"} <= set(names)
     lib = ctypes.CDLL(L.LIB_PATH)
     for n in names:
@@ -140,6 +140,28 @@ def test_cached_teacher_arguments_validated():
     with pytest.raises(L.MlaError) as e:                                       # no loss
         L.mla_recon_student_step(c, 1, sw, 1, None, None, None, g, 256, ws, None)
     assert e.value.code == L.MLA_ERR_INVALID_ARG
+
+
+def test_adamw_arguments_validated():
+    ok = L.AdamwTensor(256, 512, 768, 1024, 1280, 100)
+    cases = [
+        (([ok], L.MLA_BF16, 0, 1e-3, 0.9, 0.999, 1e-8, 0.0), "step 0"),
+        (([ok], L.MLA_BF16, 1, 1e-3, 1.0, 0.999, 1e-8, 0.0), "beta1 = 1"),
+        (([ok], L.MLA_BF16, 1, 1e-3, 0.9, 0.999, 0.0, 0.0), "eps = 0"),
+        (([ok], L.MLA_BF16, 1, -1.0, 0.9, 0.999, 1e-8, 0.0), "negative lr"),
+        (([ok], 7, 1, 1e-3, 0.9, 0.999, 1e-8, 0.0), "dtype"),
+        (([ok] * 9, L.MLA_BF16, 1, 1e-3, 0.9, 0.999, 1e-8, 0.0), "too many tensors"),
+        (([L.AdamwTensor(256, 512, 768, 1024, None, 100)], L.MLA_BF16, 1, 1e-3, 0.9, 0.999,
+          1e-8, 0.0), "NULL grad"),
+        (([L.AdamwTensor(256, 512, 776, 1024, 1280, 100)], L.MLA_BF16, 1, 1e-3, 0.9, 0.999,
+          1e-8, 0.0), "misaligned"),
+        (([L.AdamwTensor(256, 512, 768, 1024, 1280, -1)], L.MLA_BF16, 1, 1e-3, 0.9, 0.999,
+          1e-8, 0.0), "negative size"),
+    ]
+    for args, why in cases:
+        with pytest.raises(L.MlaError) as e:
+            L.mla_recon_adamw(*args, None)
+        assert e.value.code == L.MLA_ERR_INVALID_ARG, why
 
 
 def test_prof_class_validation():
