@@ -37,6 +37,8 @@ def parse():
                    help="skip the reference timing of the four-call step (profiling runs)")
     p.add_argument("--no-cached", action="store_true",
                    help="skip the timing of the cached-teacher step (profiling runs)")
+    p.add_argument("--no-train", action="store_true",
+                   help="skip the timing of the step plus the AdamW update (profiling runs)")
     p.add_argument("--cpu-seq", type=int, default=4096, help="oracle sample: tokens of one sequence")
     p.add_argument("--calib-copy-mb", type=int, default=0,
                    help="run one device-to-device copy of this many MiB first (HBM counter calibration)")
@@ -214,6 +216,25 @@ def main():
         torch.cuda.synchronize()
         ms_cached = start.elapsed_time(stop) / args.steps
 
+    # also reported: a training iteration, the step followed by the AdamW update of the five
+    # projections (its own copies of the weights, so the step timings above are unaffected)
+    ms_train = None
+    if not args.no_train:
+        tr = DeviceStep(wl)
+        tr.init_optimizer()
+        for _ in range(2):
+            tr.fused_step(with_dA=False)
+            tr.optimizer_step(1e-4)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            tr.fused_step(with_dA=False)
+            tr.optimizer_step(1e-4)
+        stop.record()
+        torch.cuda.synchronize()
+        ms_train = start.elapsed_time(stop) / args.steps
+        del tr
+
     # for reference: the four separate calls, which also form A_t and A_s (two W_O products)
     ms_sep = None
     if not args.no_separate:
@@ -282,6 +303,9 @@ def main():
         "alg_gflop_per_step": round(flops / 1e9, 1),
         "ms_per_step_instrumented": round(ms_instr, 4),
         "ms_per_step_separate_outputs": ms_sep,
+        "train_step": None if ms_train is None else
+                      {"ms_per_step": round(ms_train, 4), "optimizer": "AdamW",
+                       "value": round(tokens / (ms_train / 1e3), 1), "unit": "tokens/s"},
         "cached_teacher": None if ms_cached is None else
                           {"ms_per_step": round(ms_cached, 4),
                            "value": round(tokens / (ms_cached / 1e3), 1), "unit": "tokens/s"},
