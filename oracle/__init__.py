@@ -5,3 +5,4 @@ from .mla_recon_oracle import (  # noqa: F401
     student_backward, reconstruction_step,
 )
 from .adamw_oracle import adamw_step  # noqa: F401
+from .stack_oracle import rms_norm, capture  # noqa: F401
