@@ -188,6 +188,15 @@ int mla_recon_adamw(const mla_adamw_tensor *tensors, int32_t count, int32_t dtyp
                     float lr, float beta1, float beta2, float eps, float weight_decay,
                     void *hip_stream);
 
+/* Calibration capture over a frozen attention stack (Sec. 4.1 reconstructs each layer on
+ * cached layer inputs of the frozen model; the stand-in model is an attention-only
+ * residual stack: h^l = x^l / rms(x^l), x^{l+1} = x^l + A^l_orig(h^l)).  For each of `rows`
+ * rows of `hidden` fp32 values: x += A (A may be NULL: no residual add), then
+ * h = x / sqrt(mean(x^2) + eps) in `dtype` (the next layer's input, e.g. the h of
+ * mla_recon_teacher_fwd).  x is updated in place; the row reduction has a fixed order. */
+int mla_recon_residual_rmsnorm(float *x, const float *A, void *h, int64_t rows, int32_t hidden,
+                               int32_t dtype, float eps, void *hip_stream);
+
 /* Text of the last error on the calling thread ("" if none). */
 const char *mla_recon_last_error(void);
 

@@ -98,6 +98,8 @@ def lib() -> ctypes.CDLL:
         L.mla_recon_step.argtypes = [P(Cfg), vp, P(TeacherW), P(StudentW), vp, vp, vp,
                                      P(StudentGrads), vp, sz, vp]
         L.mla_recon_teacher_cache.argtypes = [P(Cfg), vp, P(TeacherW), vp, sz, vp]
+        L.mla_recon_residual_rmsnorm.argtypes = [vp, vp, vp, ctypes.c_int64, i32, i32,
+                                                 ctypes.c_float, vp]
         L.mla_recon_adamw.argtypes = [P(AdamwTensor), i32, i32, i32, ctypes.c_float,
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                       ctypes.c_float, vp]
@@ -105,7 +107,8 @@ def lib() -> ctypes.CDLL:
                                              P(StudentGrads), vp, sz, vp]
         for f in ("mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
                   "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
-                  "mla_recon_student_step", "mla_recon_adamw", "mla_recon_prof_enable",
+                  "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
+                  "mla_recon_prof_enable",
                   "mla_recon_prof_read"):
             getattr(L, f).restype = i32
         L.mla_recon_last_error.argtypes = []
@@ -188,6 +191,11 @@ def mla_recon_adamw(tensors: list, dtype: int, step: int, lr: float, beta1: floa
     arr = (AdamwTensor * len(tensors))(*tensors)
     _check(lib().mla_recon_adamw(arr, len(tensors), dtype, step, lr, beta1, beta2, eps,
                                  weight_decay, stream))
+
+
+def mla_recon_residual_rmsnorm(x: int, A: int | None, h: int, rows: int, hidden: int, dtype: int,
+                               eps: float, stream: int) -> None:
+    _check(lib().mla_recon_residual_rmsnorm(x, A, h, rows, hidden, dtype, eps, stream))
 
 
 def mla_recon_prof_enable(kclass: int, on: bool) -> None:

@@ -626,6 +626,20 @@ int mla_recon_adamw(const mla_adamw_tensor* tensors, int32_t count, int32_t dtyp
   return MLA_OK;
 }
 
+int mla_recon_residual_rmsnorm(float* x, const float* A, void* h, int64_t rows, int32_t hidden,
+                               int32_t dtype, float eps, void* hip_stream) {
+  g_err[0] = 0;
+  if (rows < 0 || hidden < 1 || rows > (int64_t)0x7fffffff)
+    return fail(MLA_ERR_INVALID_ARG, "residual_rmsnorm: bad shape");
+  if (dtype != MLA_BF16 && dtype != MLA_FP32)
+    return fail(MLA_ERR_INVALID_ARG, "residual_rmsnorm: unknown dtype %d", dtype);
+  if (!(eps >= 0.f && eps < 1e30f)) return fail(MLA_ERR_INVALID_ARG, "residual_rmsnorm: bad eps");
+  if (rows > 0 && (!x || !h)) return fail(MLA_ERR_INVALID_ARG, "residual_rmsnorm: NULL pointer");
+  HIP_TRY(residual_rmsnorm(x, A, h, rows, hidden, dtype == MLA_FP32 ? DT_F32 : DT_BF16, eps,
+                           (hipStream_t)hip_stream));
+  return MLA_OK;
+}
+
 int mla_recon_prof_enable(int k, int on) {
   if (k < 0 || k >= KC_COUNT) return fail(MLA_ERR_INVALID_ARG, "bad kernel class %d", k);
   std::lock_guard<std::mutex> lk(g_prof_mu);

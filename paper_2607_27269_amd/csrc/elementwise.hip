@@ -473,4 +473,48 @@ hipError_t adamw_step(const AdamwTensor* t, int count, DType wt, float lr, float
   return hipGetLastError();
 }
 
+// Residual add and RMS normalisation of one row per workgroup -------------------------------
+// x[n] += A[n] (A optional); h[n] = x[n] / sqrt(mean(x[n]^2) + eps) in h's dtype.  The row
+// sum runs in a fixed order (per-thread strided partials, then a fixed tree).
+template <typename T>
+__global__ __launch_bounds__(256) void residual_rmsnorm_kernel(float* __restrict__ x,
+                                                               const float* __restrict__ A,
+                                                               T* __restrict__ h, int D,
+                                                               float eps) {
+  __shared__ float red[256];
+  const int64_t row = blockIdx.x;
+  float* xr = x + row * D;
+  const float* ar = A ? A + row * D : nullptr;
+  float ss = 0.f;
+  for (int d = threadIdx.x; d < D; d += 256) {
+    float v = xr[d];
+    if (ar) {
+      v += ar[d];
+      xr[d] = v;
+    }
+    ss += v * v;
+  }
+  red[threadIdx.x] = ss;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  const float inv = 1.f / sqrtf(red[0] / (float)D + eps);
+  T* hr = h + row * D;
+  for (int d = threadIdx.x; d < D; d += 256) st<T>(hr + d, xr[d] * inv);
+}
+
+hipError_t residual_rmsnorm(float* x, const float* A, void* h, int64_t N, int D, DType t, float eps,
+                            hipStream_t s) {
+  if (N <= 0 || D <= 0) return hipSuccess;
+  prof_begin(KC_ELEM, s);
+  if (t == DT_BF16)
+    residual_rmsnorm_kernel<bf16_t><<<(unsigned)N, 256, 0, s>>>(x, A, (bf16_t*)h, D, eps);
+  else
+    residual_rmsnorm_kernel<float><<<(unsigned)N, 256, 0, s>>>(x, A, (float*)h, D, eps);
+  prof_end(KC_ELEM, s, 0.0, (double)N * D * ((A ? 12.0 : 4.0) + dsize(t)));
+  return hipGetLastError();
+}
+
 }  // namespace mla

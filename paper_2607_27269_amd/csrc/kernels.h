@@ -147,6 +147,11 @@ struct AdamwTensor {
 hipError_t adamw_step(const AdamwTensor* t, int count, DType wt, float lr, float beta1,
                       float beta2, float eps, float weight_decay, int step, hipStream_t s);
 
+// Calibration capture: x[n] += A[n] (A may be null), then h[n] = x[n] / sqrt(mean(x[n]^2)
+// + eps) in dtype t; N rows of D fp32 values.
+hipError_t residual_rmsnorm(float* x, const float* A, void* h, int64_t N, int D, DType t, float eps,
+                            hipStream_t s);
+
 // out = a - b elementwise over n elements of dtype t (fp32 arithmetic)
 hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, DType t,
                            hipStream_t s);

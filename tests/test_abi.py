@@ -29,7 +29,8 @@ def test_exports_every_declared_function():
     names = header_functions()
     assert {"mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
             "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
-            "mla_recon_student_step", "mla_recon_adamw", "mla_recon_workspace_size",
+            "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
+            "mla_recon_workspace_size",
             "mla_recon_last_error"} <= set(names)
     lib = ctypes.CDLL(L.LIB_PATH)
     for n in names:
@@ -162,6 +163,17 @@ def test_adamw_arguments_validated():
         with pytest.raises(L.MlaError) as e:
             L.mla_recon_adamw(*args, None)
         assert e.value.code == L.MLA_ERR_INVALID_ARG, why
+
+
+def test_residual_rmsnorm_arguments_validated():
+    for args in [(256, None, 512, -1, 64, L.MLA_BF16, 1e-6),      # negative rows
+                 (256, None, 512, 4, 0, L.MLA_BF16, 1e-6),        # zero width
+                 (256, None, 512, 4, 64, 9, 1e-6),                # dtype
+                 (256, None, 512, 4, 64, L.MLA_FP32, -1.0),       # eps
+                 (None, None, 512, 4, 64, L.MLA_FP32, 1e-6)]:     # NULL x
+        with pytest.raises(L.MlaError) as e:
+            L.mla_recon_residual_rmsnorm(*args, None)
+        assert e.value.code == L.MLA_ERR_INVALID_ARG
 
 
 def test_prof_class_validation():

@@ -1,0 +1,72 @@
+"""GPU parity of calibration capture (the residual RMS-norm kernel and the frozen stack)
+and of layer-by-layer reconstruction, against the float64 oracles."""
+import numpy as np
+import pytest
+
+from paper_2607_27269_amd import configs, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16_round(x):
+    b = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_residual_rmsnorm_parity(dtype):
+    import torch
+    import oracle as O
+    from paper_2607_27269_amd import _lib as L
+    print(f"[stack] rmsnorm dtype={dtype}", flush=True)
+    rng = np.random.default_rng(3)
+    N, D = 37, 1000                      # D not a multiple of the block width
+    x = (rng.standard_normal((N, D)) * 2).astype(np.float32)
+    a = (rng.standard_normal((N, D)) * 0.5).astype(np.float32)
+    dev = torch.device("cuda:0")
+    tx, ta = torch.from_numpy(x).to(dev), torch.from_numpy(a).to(dev)
+    th = torch.empty(N, D, dtype=torch.bfloat16 if dtype == "bf16" else torch.float32, device=dev)
+    L.mla_recon_residual_rmsnorm(tx.data_ptr(), ta.data_ptr(), th.data_ptr(), N, D,
+                                 L.MLA_BF16 if dtype == "bf16" else L.MLA_FP32, 1e-6,
+                                 torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    assert np.array_equal(tx.cpu().numpy(), x + a)          # the fp32 residual add is exact
+    ref = O.rms_norm((x + a).astype(np.float64), 1e-6)
+    got = th.double().cpu().numpy()
+    tol = 4e-3 if dtype == "bf16" else 2e-6
+    assert np.max(np.abs(got - ref) / (np.abs(ref) + 1e-3)) <= tol
+
+
+def test_capture_parity():
+    """Three frozen layers: every captured layer input against the oracle stack."""
+    import oracle as O
+    from paper_2607_27269_amd.stack import ReconStack
+    print("[stack] capture", flush=True)
+    cfg = configs.shrink(configs.get(1), batch=2, seq=80)
+    st = ReconStack(cfg, 3)
+    st.capture()
+    hs = [l.h.double().cpu().numpy().reshape(cfg.batch, cfg.seq, cfg.hidden) for l in st.layers]
+    layers = []
+    for l in range(3):
+        wl = synth.make_workload(cfg, seed=100 + l)
+        layers.append(dict(Wq=wl.Wq, Wk=wl.Wk, Wv=wl.Wv, Wo=wl.Wo, inv_freq=wl.inv_freq_t))
+    x0 = synth.make_workload(cfg, seed=99, dtype="fp32").h
+    ref = O.capture(x0, layers, cfg.n_heads, cfg.n_kv_groups, cfg.softmax_scale,
+                    round_fn=_bf16_round)
+    for l, (g, r) in enumerate(zip(hs, ref)):
+        err = np.linalg.norm(g - r) / np.linalg.norm(r)
+        print(f"[stack] layer {l} input rel err {err:.3e}", flush=True)
+        assert err <= 2e-2
+
+
+def test_layerwise_reconstruction_lowers_every_layer():
+    from paper_2607_27269_amd.stack import ReconStack
+    print("[stack] reconstruct", flush=True)
+    cfg = configs.shrink(configs.get(1), batch=2, seq=128)
+    st = ReconStack(cfg, 2)
+    st.capture()
+    for l, losses in enumerate(st.reconstruct(12, 1e-3)):
+        losses = losses.numpy()
+        print(f"[stack] layer {l} losses {losses}", flush=True)
+        assert np.all(np.isfinite(losses)) and losses[-1] < 0.8 * losses[0]
