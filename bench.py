@@ -39,6 +39,8 @@ def parse():
                    help="skip the timing of the cached-teacher step (profiling runs)")
     p.add_argument("--no-train", action="store_true",
                    help="skip the timing of the step plus the AdamW update (profiling runs)")
+    p.add_argument("--no-capture", action="store_true",
+                   help="skip the timing of calibration capture (profiling runs)")
     p.add_argument("--cpu-seq", type=int, default=4096, help="oracle sample: tokens of one sequence")
     p.add_argument("--calib-copy-mb", type=int, default=0,
                    help="run one device-to-device copy of this many MiB first (HBM counter calibration)")
@@ -235,6 +237,28 @@ def main():
         ms_train = start.elapsed_time(stop) / args.steps
         del tr
 
+    # also reported: calibration capture, one layer of the frozen stack (teacher forward with
+    # W_O, then the residual update and RMS normalisation that give the next layer's input)
+    ms_cap = None
+    if not args.no_capture:
+        x = dev.A_t.clone()
+        h_next = torch.empty_like(dev.h)
+        dt = L.MLA_FP32 if cfg.dtype == "fp32" else L.MLA_BF16
+
+        def capture_layer():
+            dev.teacher_fwd()
+            L.mla_recon_residual_rmsnorm(x.data_ptr(), dev.A_t.data_ptr(), h_next.data_ptr(),
+                                         cfg.tokens, cfg.hidden, dt, 1e-6, dev.stream)
+        capture_layer()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            capture_layer()
+        stop.record()
+        torch.cuda.synchronize()
+        ms_cap = start.elapsed_time(stop) / args.steps
+        del x, h_next
+
     # for reference: the four separate calls, which also form A_t and A_s (two W_O products)
     ms_sep = None
     if not args.no_separate:
@@ -306,6 +330,9 @@ def main():
         "train_step": None if ms_train is None else
                       {"ms_per_step": round(ms_train, 4), "optimizer": "AdamW",
                        "value": round(tokens / (ms_train / 1e3), 1), "unit": "tokens/s"},
+        "capture": None if ms_cap is None else
+                   {"ms_per_layer": round(ms_cap, 4),
+                    "value": round(tokens / (ms_cap / 1e3), 1), "unit": "tokens/s per layer"},
         "cached_teacher": None if ms_cached is None else
                           {"ms_per_step": round(ms_cached, 4),
                            "value": round(tokens / (ms_cached / 1e3), 1), "unit": "tokens/s"},

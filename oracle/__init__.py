@@ -6,3 +6,4 @@ from .mla_recon_oracle import (  # noqa: F401
 )
 from .adamw_oracle import adamw_step  # noqa: F401
 from .stack_oracle import rms_norm, capture  # noqa: F401
+from .decode_oracle import absorbed_decode  # noqa: F401
