@@ -37,6 +37,8 @@ def absorbed_decode(q, cache, lengths, Wuk, Wuv, *, n_heads, s_kv_groups, s_rope
     out = np.zeros((B, H, dv))
     for b in range(B):
         n = int(lengths[b])
+        if n == 0:                     # an empty cache attends to nothing: o = 0 (reading)
+            continue
         c = cache[b, :n, :r_kv]
         for i in range(H):
             g, r = i // (H // Gkv), i // (H // Gr)
