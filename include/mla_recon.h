@@ -197,6 +197,27 @@ int mla_recon_adamw(const mla_adamw_tensor *tensors, int32_t count, int32_t dtyp
 int mla_recon_residual_rmsnorm(float *x, const float *A, void *h, int64_t rows, int32_t hidden,
                                int32_t dtype, float eps, void *hip_stream);
 
+/* Decoding with the reconstructed MLA block in absorbed form (Eq. 5's cache: per token the
+ * latent c^KV and the rotated positional key; W_UK folded into the query, W_UV applied
+ * after the attention-weighted latent).  One query token per sequence; cfg->batch
+ * sequences; cfg gives H, G_kv, d_nope, d_rope, r_kv, d_k (= d_v) and the softmax scale;
+ * cfg->seq is not used.  Requires bf16, a single positional key (s_rope_groups == 1) and
+ * (r_kv + d_rope, r_kv) one of (576, 512), (288, 256), (160, 128); MLA_ERR_UNSUPPORTED
+ * otherwise.
+ *   q       [B, H, d_nope + d_rope] bf16: the query token's [q^nope ; R_t q^rope]
+ *   cache   [B, max_len, r_kv + d_rope] bf16: rows [c^KV_j | R_j k^PE_j], e.g. the
+ *           [c^KV | k^PE] rows of the student forward
+ *   lengths device int32 [B]: sequence b attends to its first lengths[b] rows (clamped to
+ *           [0, max_len]; 0 rows give o = 0)
+ *   Wuk [G_kv d_nope, r_kv], Wuv [G_kv d_k, r_kv] bf16 (the student's W_UK, W_UV)
+ *   o       [B, H, d_k] bf16 out: the per-head attention outputs before W_O
+ * q, cache, Wuv and ws 16-byte aligned; ws of mla_recon_decode_workspace_size bytes
+ * (0 = unsupported or invalid cfg). */
+size_t mla_recon_decode_workspace_size(const mla_recon_cfg *cfg, int32_t max_len);
+int mla_recon_decode(const mla_recon_cfg *cfg, const void *q, const void *cache, int32_t max_len,
+                     const int32_t *lengths, const void *Wuk, const void *Wuv, void *o, void *ws,
+                     size_t ws_bytes, void *hip_stream);
+
 /* Text of the last error on the calling thread ("" if none). */
 const char *mla_recon_last_error(void);
 

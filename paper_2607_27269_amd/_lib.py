@@ -100,6 +100,9 @@ def lib() -> ctypes.CDLL:
         L.mla_recon_teacher_cache.argtypes = [P(Cfg), vp, P(TeacherW), vp, sz, vp]
         L.mla_recon_residual_rmsnorm.argtypes = [vp, vp, vp, ctypes.c_int64, i32, i32,
                                                  ctypes.c_float, vp]
+        L.mla_recon_decode_workspace_size.argtypes = [P(Cfg), i32]
+        L.mla_recon_decode_workspace_size.restype = sz
+        L.mla_recon_decode.argtypes = [P(Cfg), vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]
         L.mla_recon_adamw.argtypes = [P(AdamwTensor), i32, i32, i32, ctypes.c_float,
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                       ctypes.c_float, vp]
@@ -108,6 +111,7 @@ def lib() -> ctypes.CDLL:
         for f in ("mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
                   "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
                   "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
+                  "mla_recon_decode",
                   "mla_recon_prof_enable",
                   "mla_recon_prof_read"):
             getattr(L, f).restype = i32
@@ -196,6 +200,16 @@ def mla_recon_adamw(tensors: list, dtype: int, step: int, lr: float, beta1: floa
 def mla_recon_residual_rmsnorm(x: int, A: int | None, h: int, rows: int, hidden: int, dtype: int,
                                eps: float, stream: int) -> None:
     _check(lib().mla_recon_residual_rmsnorm(x, A, h, rows, hidden, dtype, eps, stream))
+
+
+def mla_recon_decode_workspace_size(cfg: Cfg, max_len: int) -> int:
+    return int(lib().mla_recon_decode_workspace_size(ctypes.byref(cfg), max_len))
+
+
+def mla_recon_decode(cfg: Cfg, q: int, cache: int, max_len: int, lengths: int, Wuk: int,
+                     Wuv: int, o: int, ws: int, ws_bytes: int, stream: int) -> None:
+    _check(lib().mla_recon_decode(ctypes.byref(cfg), q, cache, max_len, lengths, Wuk, Wuv, o, ws,
+                                  ws_bytes, stream))
 
 
 def mla_recon_prof_enable(kclass: int, on: bool) -> None:

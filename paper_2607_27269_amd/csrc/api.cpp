@@ -640,6 +640,49 @@ int mla_recon_residual_rmsnorm(float* x, const float* A, void* h, int64_t rows, 
   return MLA_OK;
 }
 
+static int decode_check(const mla_recon_cfg* cfg, int32_t max_len) {
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (max_len < 1) return fail(MLA_ERR_INVALID_ARG, "decode: max_len must be positive");
+  if (cfg->dtype != MLA_BF16) return fail(MLA_ERR_UNSUPPORTED, "decode: bf16 only");
+  if (cfg->s_rope_groups != 1)
+    return fail(MLA_ERR_UNSUPPORTED, "decode: one shared positional key (s_rope_groups == 1) only");
+  if (!decode_supported(cfg->kv_rank + cfg->rope_dim, cfg->kv_rank))
+    return fail(MLA_ERR_UNSUPPORTED, "decode: kv_rank %d with rope_dim %d not supported",
+                cfg->kv_rank, cfg->rope_dim);
+  return MLA_OK;
+}
+
+size_t mla_recon_decode_workspace_size(const mla_recon_cfg* cfg, int32_t max_len) {
+  g_err[0] = 0;
+  if (decode_check(cfg, max_len)) return 0;
+  return decode_ws_bytes(cfg->batch, cfg->n_heads, cfg->kv_rank + cfg->rope_dim, cfg->kv_rank,
+                         max_len);
+}
+
+int mla_recon_decode(const mla_recon_cfg* cfg, const void* q, const void* cache, int32_t max_len,
+                     const int32_t* lengths, const void* Wuk, const void* Wuv, void* o, void* ws,
+                     size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = decode_check(cfg, max_len);
+  if (rc) return rc;
+  if (!q || !cache || !lengths || !Wuk || !Wuv || !o || !ws)
+    return fail(MLA_ERR_INVALID_ARG, "decode: NULL pointer argument");
+  if (((uintptr_t)q | (uintptr_t)cache | (uintptr_t)Wuv | (uintptr_t)ws) % 16)
+    return fail(MLA_ERR_INVALID_ARG, "decode: q, cache, Wuv and ws must be 16-byte aligned");
+  const size_t need = decode_ws_bytes(cfg->batch, cfg->n_heads, cfg->kv_rank + cfg->rope_dim,
+                                      cfg->kv_rank, max_len);
+  if (ws_bytes < need)
+    return fail(MLA_ERR_WORKSPACE, "decode: workspace too small: %zu < %zu bytes", ws_bytes, need);
+  Decode d;
+  d.B = cfg->batch; d.H = cfg->n_heads; d.dn = cfg->nope_dim; d.dr = cfg->rope_dim;
+  d.rkv = cfg->kv_rank; d.dv = cfg->head_dim; d.hpg = cfg->n_heads / cfg->s_kv_groups;
+  d.q = q; d.cache = cache; d.Lmax = max_len; d.ldc = cfg->kv_rank + cfg->rope_dim;
+  d.len = lengths; d.Wuk = Wuk; d.Wuv = Wuv; d.scale = cfg->softmax_scale; d.o = o; d.ws = ws;
+  HIP_TRY(decode_attention(d, (hipStream_t)hip_stream));
+  return MLA_OK;
+}
+
 int mla_recon_prof_enable(int k, int on) {
   if (k < 0 || k >= KC_COUNT) return fail(MLA_ERR_INVALID_ARG, "bad kernel class %d", k);
   std::lock_guard<std::mutex> lk(g_prof_mu);

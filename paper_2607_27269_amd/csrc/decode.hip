@@ -1,0 +1,317 @@
+// Decoding with the reconstructed MLA block in absorbed form (one query token per sequence).
+//
+// The cache keeps, per token, the latent c^KV_j and the rotated positional key k^PE_j
+// (Eq. 5; the [c^KV | k^PE] rows the student forward produces).  With a single positional
+// key (G_r = 1) every head attends against the same cache row [c_j ; k^PE_j]: head i uses
+// the absorbed query [W_UK[g]^T q^nope_i ; q^rope_i] and its output is W_UV[g] applied to
+// the attention-weighted latent (g = i / (H / G_kv)).  So decoding is multi-query attention
+// with key width r_kv + d_rope, value width r_kv (the latent itself) and all H heads in one
+// MFMA column block, followed by a per-group projection.
+//
+// Kernels:
+// * absorb_query_kernel: the absorbed queries [B][HP][DK] bf16 (heads padded to HP = 32k).
+// * decode_attn_kernel: split-K over the cache (flash-decoding).  A workgroup (4 waves)
+//   owns one (sequence, key chunk, block of 32 heads).  Key tiles of 32 rows are staged in
+//   LDS through registers (the next tile's loads in flight during the current tile).  Each
+//   wave computes S^T = K Q^T for the tile (key in the MFMA row, head in the column, so each
+//   lane owns one head's online-softmax state), then O^T += V^T P^T for its quarter of the
+//   latent width; V^T is the tile's latent columns read with the transposing LDS read.
+//   The 4 waves repeat the same S^T (small next to the latent product, and decoding is
+//   bound by the cache reads).  Partial (max, sum, unnormalised output) per split.
+// * decode_combine_kernel: merges the splits of a (sequence, head) in split order.
+// * uv_proj_kernel: o = W_UV[g] (latent), one thread per output.
+#include "attn_common.h"
+#include "kernels.h"
+#include "mfma.h"
+
+namespace mla {
+
+namespace {
+
+constexpr int DEC_KT = 32;     // keys per tile
+constexpr int DEC_WAVES = 4;
+
+struct DecodeDev {
+  const bf16_t* qabs;   // [B][HP][DK]
+  const bf16_t* cache;  // [B][Lmax][ldc]
+  int64_t seq_stride;   // Lmax * ldc
+  int ldc;              // row stride of the cache (elements)
+  const int32_t* len;   // [B]
+  int Lmax, HP, nsplit, chunk;
+  float sl2;            // softmax scale * log2(e)
+  float* part_o;        // [B][nsplit][HP][DVL]
+  float* part_ml;       // [B][nsplit][HP][2]
+};
+
+// q_abs[b][i][c] = sum_d q[b][i][d] Wuk[(g dn + d)][c] for c < r_kv; the rope part copied.
+__global__ void absorb_query_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ Wuk,
+                                    bf16_t* __restrict__ qabs, int B, int H, int HP, int dn,
+                                    int dr, int rkv, int hpg) {
+  const int DK = rkv + dr;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)B * HP * DK) return;
+  const int c = (int)(idx % DK);
+  const int i = (int)((idx / DK) % HP);
+  const int b = (int)(idx / ((int64_t)DK * HP));
+  float v = 0.f;
+  if (i < H) {
+    const bf16_t* qr = q + ((int64_t)b * H + i) * (dn + dr);
+    if (c < rkv) {
+      const bf16_t* w = Wuk + (int64_t)(i / hpg) * dn * rkv + c;
+      for (int d = 0; d < dn; ++d) v += bf2f(qr[d]) * bf2f(w[(int64_t)d * rkv]);
+    } else {
+      v = bf2f(qr[dn + (c - rkv)]);
+    }
+  }
+  qabs[idx] = f2bf(v);
+}
+
+template <int DK, int DVL>
+__global__ __launch_bounds__(64 * DEC_WAVES) void decode_attn_kernel(DecodeDev a) {
+  constexpr int LDK = attn::ld_of(DK);        // padded rows: conflict-free operand reads
+  constexpr int NKK = DK / 16;
+  constexpr int WV = DVL / DEC_WAVES;         // latent rows per wave
+  constexpr int NCV = WV / 32;
+  constexpr int CHUNKS = DEC_KT * DK / 8;     // 16-byte chunks per tile
+  constexpr int PER = (CHUNKS + 64 * DEC_WAVES - 1) / (64 * DEC_WAVES);
+  static_assert(DK % 16 == 0 && WV % 32 == 0, "decode shape");
+  __shared__ __attribute__((aligned(16))) bf16_t Qs[32 * LDK];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][DEC_KT * LDK];
+
+  const int split = blockIdx.x, b = blockIdx.y, h0 = 32 * blockIdx.z;
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int half = lane >> 5, col = lane & 31;
+  const int len = min(max(a.len[b], 0), a.Lmax);
+  const int kbeg = split * a.chunk;
+  const int kend = min(len, kbeg + a.chunk);
+  const int64_t pbase = ((int64_t)b * a.nsplit + split) * a.HP + h0;
+
+  // the block of 32 absorbed queries
+  const bf16_t* qsrc = a.qabs + ((int64_t)b * a.HP + h0) * DK;
+  for (int c = threadIdx.x; c < 32 * DK / 8; c += 64 * DEC_WAVES) {
+    const int r = c / (DK / 8), k = (c % (DK / 8)) * 8;
+    *(u32x4*)(Qs + r * LDK + k) = *(const u32x4*)(qsrc + (int64_t)r * DK + k);
+  }
+  const bf16_t* cs = a.cache + (int64_t)b * a.seq_stride;
+  u32x4 reg[PER];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = threadIdx.x + p * 64 * DEC_WAVES;
+      const int r = c / (DK / 8), k = (c % (DK / 8)) * 8;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if (c < CHUNKS && k0 + r < kend) v = *(const u32x4*)(cs + (int64_t)(k0 + r) * a.ldc + k);
+      reg[p] = v;
+    }
+  };
+  auto lstore = [&](bf16_t* dst) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int c = threadIdx.x + p * 64 * DEC_WAVES;
+      if (c < CHUNKS) *(u32x4*)(dst + (c / (DK / 8)) * LDK + (c % (DK / 8)) * 8) = reg[p];
+    }
+  };
+
+  f32x16 acc[NCV];
+#pragma unroll
+  for (int c = 0; c < NCV; ++c)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int ntile = kend > kbeg ? (kend - kbeg + DEC_KT - 1) / DEC_KT : 0;
+  if (ntile > 0) {
+    gload(kbeg);
+    lstore(Ks[0]);
+  }
+  __syncthreads();
+  for (int t = 0; t < ntile; ++t) {
+    const bf16_t* kt = Ks[t & 1];
+    const int k0 = kbeg + t * DEC_KT;
+    if (t + 1 < ntile) gload(k0 + DEC_KT);
+    // S^T (32 keys x 32 heads): key = MFMA row, head = column (this lane's head: col)
+    f32x16 s;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s[e] = 0.f;
+#pragma unroll 4
+    for (int kk = 0; kk < NKK; ++kk)
+      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+          *(const bf16x8*)(kt + col * LDK + 16 * kk + 8 * half),
+          *(const bf16x8*)(Qs + col * LDK + 16 * kk + 8 * half), s, 0, 0, 0);
+    // keys past the chunk end: no weight
+    float mx = -INFINITY;
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int key = k0 + 8 * (e >> 2) + 4 * half + (e & 3);
+      if (key >= kend) s[e] = -INFINITY;
+      mx = fmaxf(mx, s[e]);
+    }
+    mx = pair_max32(mx) * a.sl2;
+    const float m_new = fmaxf(m_run, mx);
+    const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= corr;
+#pragma unroll
+    for (int c = 0; c < NCV; ++c)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[c][e] *= corr;
+    // P^T as the B operand of O^T = V^T P^T (K-step u: keys 16u + {4h'..4h'+3, 8+4h'..})
+    bf16x8 pf[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      u32x4 w;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * u + 2 * q], a.sl2, -m_new));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * u + 2 * q + 1], a.sl2, -m_new));
+        l_run += p0 + p1;
+        w[q] = pack2bf(p0, p1);
+      }
+      pf[u] = __builtin_bit_cast(bf16x8, w);
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int klo = 16 * u + 4 * half;
+#pragma unroll
+      for (int c = 0; c < NCV; ++c)
+        acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            lds_operand_tr(kt, LDK, wave * WV + 32 * c, klo, klo + 8), pf[u], acc[c], 0, 0, 0);
+    }
+    // the other stage was last read in tile t - 1, before the barrier that ended it
+    if (t + 1 < ntile) lstore(Ks[(t + 1) & 1]);
+    __syncthreads();
+  }
+
+  // partial state of this split: lane (head col, half) holds rows
+  // wave WV + 32 c + 8 (e / 4) + 4 half + e % 4 of the unnormalised latent output
+  const float l = pair_sum32(l_run);
+  const int64_t hrow = pbase + col;
+  if (wave == 0 && half == 0) {
+    a.part_ml[2 * hrow] = m_run;
+    a.part_ml[2 * hrow + 1] = l;
+  }
+  float* po = a.part_o + hrow * DVL + wave * WV + 4 * half;
+#pragma unroll
+  for (int c = 0; c < NCV; ++c)
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *(f32x4*)(po + 32 * c + 8 * g) =
+          f32x4{acc[c][4 * g], acc[c][4 * g + 1], acc[c][4 * g + 2], acc[c][4 * g + 3]};
+}
+
+// lat[b][i][d] = sum_s o_s[d] 2^(m_s - M) / sum_s l_s 2^(m_s - M), splits in order
+__global__ void decode_combine_kernel(const float* __restrict__ part_o,
+                                      const float* __restrict__ part_ml, float* __restrict__ lat,
+                                      int H, int HP, int nsplit, int DVL) {
+  const int b = blockIdx.y, i = blockIdx.x;
+  float M = -INFINITY;
+  for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, part_ml[2 * (((int64_t)b * nsplit + sp) * HP + i)]);
+  float L = 0.f;
+  for (int sp = 0; sp < nsplit; ++sp) {
+    const int64_t r = ((int64_t)b * nsplit + sp) * HP + i;
+    const float m = part_ml[2 * r];
+    if (m != -INFINITY) L += part_ml[2 * r + 1] * __builtin_amdgcn_exp2f(m - M);
+  }
+  const float inv = L > 0.f ? 1.f / L : 0.f;
+  for (int d = threadIdx.x; d < DVL; d += blockDim.x) {
+    float v = 0.f;
+    for (int sp = 0; sp < nsplit; ++sp) {
+      const int64_t r = ((int64_t)b * nsplit + sp) * HP + i;
+      const float m = part_ml[2 * r];
+      if (m != -INFINITY) v += part_o[r * DVL + d] * __builtin_amdgcn_exp2f(m - M);
+    }
+    lat[((int64_t)b * H + i) * DVL + d] = v * inv;
+  }
+}
+
+// o[b][i][d] = sum_c Wuv[g dv + d][c] lat[b][i][c]
+__global__ void uv_proj_kernel(const float* __restrict__ lat, const bf16_t* __restrict__ Wuv,
+                               bf16_t* __restrict__ o, int H, int dv, int rkv, int hpg) {
+  const int b = blockIdx.y, i = blockIdx.x;
+  const float* lr = lat + ((int64_t)b * H + i) * rkv;
+  for (int d = threadIdx.x; d < dv; d += blockDim.x) {
+    const bf16_t* w = Wuv + ((int64_t)(i / hpg) * dv + d) * rkv;
+    float v = 0.f;
+    for (int c = 0; c < rkv; c += 8) {
+      const u32x4 ww = *(const u32x4*)(w + c);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        v += lr[c + 2 * k] * __uint_as_float(ww[k] << 16) +
+             lr[c + 2 * k + 1] * __uint_as_float(ww[k] & 0xffff0000u);
+    }
+    o[((int64_t)b * H + i) * dv + d] = f2bf(v);
+  }
+}
+
+#define MLA_DECODE_SHAPES(X) X(576, 512) X(288, 256) X(160, 128)
+
+int decode_chunk(int Lmax, int B) {
+  // enough workgroups to spread the cache reads over the CUs, at least 4 tiles each
+  int chunk = DEC_KT * 4;
+  while ((int64_t)B * ((Lmax + chunk - 1) / chunk) > 1024 && chunk < (1 << 20)) chunk *= 2;
+  return chunk;
+}
+
+}  // namespace
+
+bool decode_supported(int DK, int DVL) {
+#define X(a_, b_) if (DK == a_ && DVL == b_) return true;
+  MLA_DECODE_SHAPES(X)
+#undef X
+  return false;
+}
+
+size_t decode_ws_bytes(int B, int H, int DK, int DVL, int Lmax) {
+  const int HP = (H + 31) / 32 * 32;
+  const int nsplit = (Lmax + decode_chunk(Lmax, B) - 1) / decode_chunk(Lmax, B);
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  return al((size_t)B * HP * DK * 2) + al((size_t)B * nsplit * HP * DVL * 4) +
+         al((size_t)B * nsplit * HP * 2 * 4) + al((size_t)B * H * DVL * 4);
+}
+
+hipError_t decode_attention(const Decode& d, hipStream_t s) {
+  const int DK = d.rkv + d.dr, DVL = d.rkv;
+  if (!decode_supported(DK, DVL)) return hipErrorInvalidValue;
+  const int HP = (d.H + 31) / 32 * 32;
+  const int chunk = decode_chunk(d.Lmax, d.B);
+  const int nsplit = (d.Lmax + chunk - 1) / chunk;
+  auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  char* w = (char*)d.ws;
+  bf16_t* qabs = (bf16_t*)w;
+  w += al((size_t)d.B * HP * DK * 2);
+  float* part_o = (float*)w;
+  w += al((size_t)d.B * nsplit * HP * DVL * 4);
+  float* part_ml = (float*)w;
+  w += al((size_t)d.B * nsplit * HP * 2 * 4);
+  float* lat = (float*)w;
+
+  prof_begin(KC_ELEM, s);
+  const int64_t nq = (int64_t)d.B * HP * DK;
+  absorb_query_kernel<<<(unsigned)((nq + 255) / 256), 256, 0, s>>>(
+      (const bf16_t*)d.q, (const bf16_t*)d.Wuk, qabs, d.B, d.H, HP, d.dn, d.dr, d.rkv, d.hpg);
+  prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dn * d.rkv, (double)nq * 2);
+
+  DecodeDev a;
+  a.qabs = qabs; a.cache = (const bf16_t*)d.cache; a.ldc = d.ldc;
+  a.seq_stride = (int64_t)d.Lmax * d.ldc; a.len = d.len; a.Lmax = d.Lmax; a.HP = HP;
+  a.nsplit = nsplit; a.chunk = chunk; a.sl2 = d.scale * attn::LOG2E;
+  a.part_o = part_o; a.part_ml = part_ml;
+  const dim3 grid(nsplit, d.B, HP / 32);
+  // algorithmic work at full cache lengths: the cache rows once, 2 (DK + DVL) flops per
+  // (head, key)
+  prof_begin(KC_ATTN_FWD, s);
+#define X(a_, b_) \
+  if (DK == a_ && DVL == b_) decode_attn_kernel<a_, b_><<<grid, 64 * DEC_WAVES, 0, s>>>(a);
+  MLA_DECODE_SHAPES(X)
+#undef X
+  prof_end(KC_ATTN_FWD, s, 2.0 * d.B * d.H * (double)d.Lmax * (DK + DVL),
+           (double)d.B * d.Lmax * DK * 2);
+  prof_begin(KC_ELEM, s);
+  decode_combine_kernel<<<dim3(d.H, d.B), 256, 0, s>>>(part_o, part_ml, lat, d.H, HP, nsplit, DVL);
+  uv_proj_kernel<<<dim3(d.H, d.B), 128, 0, s>>>(lat, (const bf16_t*)d.Wuv, (bf16_t*)d.o, d.H,
+                                                 d.dv, d.rkv, d.hpg);
+  prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dv * d.rkv, (double)d.B * d.H * (d.dv * 2 + DVL * 4));
+  return hipGetLastError();
+}
+
+}  // namespace mla

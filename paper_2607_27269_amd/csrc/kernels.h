@@ -152,6 +152,24 @@ hipError_t adamw_step(const AdamwTensor* t, int count, DType wt, float lr, float
 hipError_t residual_rmsnorm(float* x, const float* A, void* h, int64_t N, int D, DType t, float eps,
                             hipStream_t s);
 
+// Decoding with the reconstructed block in absorbed form (one query token per sequence,
+// single positional key): see decode.hip.
+struct Decode {
+  int B, H, dn, dr, rkv, dv, hpg;  // hpg = heads per KV group
+  const void* q;                   // [B][H][dn + dr] bf16, rope part rotated
+  const void* cache;               // [B][Lmax][ldc] bf16: [c^KV | k^PE]
+  int Lmax, ldc;
+  const int32_t* len;              // [B] device
+  const void* Wuk;                 // [G_kv dn][rkv]
+  const void* Wuv;                 // [G_kv dv][rkv]
+  float scale;
+  void* o;                         // [B][H][dv] bf16
+  void* ws;                        // decode_ws_bytes
+};
+bool decode_supported(int DK, int DVL);
+size_t decode_ws_bytes(int B, int H, int DK, int DVL, int Lmax);
+hipError_t decode_attention(const Decode& d, hipStream_t s);
+
 // out = a - b elementwise over n elements of dtype t (fp32 arithmetic)
 hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, DType t,
                            hipStream_t s);

@@ -30,6 +30,7 @@ def test_exports_every_declared_function():
     assert {"mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
             "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
             "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
+            "mla_recon_decode", "mla_recon_decode_workspace_size",
             "mla_recon_workspace_size",
             "mla_recon_last_error"} <= set(names)
     lib = ctypes.CDLL(L.LIB_PATH)
@@ -174,6 +175,20 @@ def test_residual_rmsnorm_arguments_validated():
         with pytest.raises(L.MlaError) as e:
             L.mla_recon_residual_rmsnorm(*args, None)
         assert e.value.code == L.MLA_ERR_INVALID_ARG
+
+
+def test_decode_configuration_checked():
+    c3 = L.make_cfg(configs.get(3))
+    assert L.mla_recon_decode_workspace_size(c3, 4096) > 0
+    assert L.mla_recon_decode_workspace_size(c3, 0) == 0                    # no cache
+    assert L.mla_recon_decode_workspace_size(L.make_cfg(configs.get(4)), 64) == 0   # G_r = H
+    assert L.mla_recon_decode_workspace_size(L.make_cfg(configs.get(0)), 64) == 0   # fp32
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_decode(c3, 256, 256, 64, 256, 256, 256, 256, 256, 1, None)  # small ws
+    assert e.value.code == L.MLA_ERR_WORKSPACE
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_decode(c3, None, 256, 64, 256, 256, 256, 256, 256, 1 << 30, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
 
 
 def test_prof_class_validation():

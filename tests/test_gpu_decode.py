@@ -1,0 +1,74 @@
+"""GPU parity of decoding in absorbed form (mla_recon_decode) against the float64 oracles:
+the absorbed-form oracle on the same bf16 inputs, and the naive block's output at the last
+cached token."""
+import numpy as np
+import pytest
+
+from paper_2607_27269_amd import configs, synth
+
+pytestmark = pytest.mark.gpu
+
+
+def _bf16(x):
+    b = np.asarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return (b.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def _upload(x):
+    import torch
+    bits = (np.asarray(x, dtype=np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(torch.bfloat16).cuda()
+
+
+@pytest.mark.parametrize("idx,T,lengths", [(3, 300, [300, 1, 129]), (1, 200, [200, 77]),
+                                           (2, 96, [96, 0, 33])])
+def test_decode_parity(idx, T, lengths):
+    import torch
+    import oracle as O
+    from paper_2607_27269_amd import _lib as L
+    print(f"[decode] cfg{idx} T={T} lengths={lengths}", flush=True)
+    B = len(lengths)
+    cfg = configs.shrink(configs.get(idx), batch=B, seq=T)
+    wl = synth.make_workload(cfg)
+    s = wl.student_weights()
+    _, cache = O.student_forward(wl.h, s["Wdq"], s["Wuq"], s["Wdkv_kr"], s["Wuk"], s["Wuv"], wl.Wo,
+                                 s["inv_freq"], n_heads=cfg.n_heads, s_kv_groups=cfg.s_kv_groups,
+                                 s_rope_groups=cfg.s_rope_groups, nope_dim=cfg.nope_dim,
+                                 rope_dim=cfg.rope_dim, scale=cfg.softmax_scale)
+    H, dn, dr, rkv = cfg.n_heads, cfg.nope_dim, cfg.rope_dim, cfg.kv_rank
+    q = np.zeros((B, H, dn + dr))
+    kv = np.zeros((B, T, rkv + dr))
+    naive = np.zeros((B, H, cfg.head_dim))
+    for b, n in enumerate(lengths):
+        seq = cache["seq"][b]
+        q[b] = seq["qh"][max(n, 1) - 1]
+        kv[b, :, :rkv] = seq["ckv"]
+        kv[b, :, rkv:] = seq["kh"][:, 0, dn:]
+        if n > 0:
+            naive[b] = seq["o"][n - 1]
+    q, kv = _bf16(q), _bf16(kv)
+    ref = O.absorbed_decode(q, kv, lengths, s["Wuk"], s["Wuv"], n_heads=H,
+                            s_kv_groups=cfg.s_kv_groups, s_rope_groups=1, nope_dim=dn,
+                            rope_dim=dr, scale=cfg.softmax_scale)
+    c = L.make_cfg(cfg)
+    wsb = L.mla_recon_decode_workspace_size(c, T)
+    assert wsb > 0, L.last_error()
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    tq, tkv = _upload(q), _upload(kv)
+    tuk, tuv = _upload(s["Wuk"]), _upload(s["Wuv"])
+    tlen = torch.tensor(lengths, dtype=torch.int32, device="cuda")
+    to = torch.full((B, H, cfg.head_dim), float("nan"), dtype=torch.bfloat16, device="cuda")
+    L.mla_recon_decode(c, tq.data_ptr(), tkv.data_ptr(), T, tlen.data_ptr(), tuk.data_ptr(),
+                       tuv.data_ptr(), to.data_ptr(), ws.data_ptr(), wsb,
+                       torch.cuda.current_stream().cuda_stream)
+    got = to.double().cpu().numpy()
+    assert np.all(np.isfinite(got))
+    for b, n in enumerate(lengths):
+        if n == 0:
+            assert not got[b].any()
+            continue
+        e1 = np.linalg.norm(got[b] - ref[b]) / np.linalg.norm(ref[b])
+        e2 = np.linalg.norm(got[b] - naive[b]) / np.linalg.norm(naive[b])
+        print(f"[decode] seq {b} len {n}: vs absorbed {e1:.2e}, vs naive {e2:.2e}", flush=True)
+        assert e1 <= 1e-2 and e2 <= 2e-2
