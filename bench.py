@@ -41,6 +41,10 @@ def parse():
                    help="skip the timing of the step plus the AdamW update (profiling runs)")
     p.add_argument("--no-capture", action="store_true",
                    help="skip the timing of calibration capture (profiling runs)")
+    p.add_argument("--no-decode", action="store_true",
+                   help="skip the timing of absorbed-form decoding (profiling runs)")
+    p.add_argument("--decode-batch", type=int, default=64,
+                   help="sequences per decoding step (each with a full-length cache)")
     p.add_argument("--cpu-seq", type=int, default=4096, help="oracle sample: tokens of one sequence")
     p.add_argument("--calib-copy-mb", type=int, default=0,
                    help="run one device-to-device copy of this many MiB first (HBM counter calibration)")
@@ -160,6 +164,54 @@ def cpu_baseline(cfg, wl, seq):
                       f"teacher fwd + student fwd + Eq. 11 + backward, float64 numpy; {dt:.1f} s"}
 
 
+def decode_bench(cfg, wl, batch, steps):
+    """One decoding step of `batch` sequences, each over a cache of cfg.seq latent rows
+    (random bf16 stand-ins; the same shapes as the cache the student forward produces)."""
+    import torch
+    from paper_2607_27269_amd import _lib as L
+    from paper_2607_27269_amd.step import _dev_tensor
+    dcfg = cfg.replace(batch=batch)
+    c = L.make_cfg(dcfg)
+    T, H, dqk, ldc = cfg.seq, cfg.n_heads, cfg.qk_dim, cfg.kv_rank + cfg.rope_dim
+    wsb = L.mla_recon_decode_workspace_size(c, T)
+    if wsb == 0:
+        return None
+    g = torch.Generator(device="cuda").manual_seed(7)
+    q = (torch.randn(batch, H, dqk, device="cuda", generator=g) * 0.5).to(torch.bfloat16)
+    kv = torch.randn(batch, T, ldc, device="cuda", generator=g).to(torch.bfloat16)
+    lens = torch.full((batch,), T, dtype=torch.int32, device="cuda")
+    wuk, wuv = _dev_tensor(wl.Wuk, "bf16", "cuda"), _dev_tensor(wl.Wuv, "bf16", "cuda")
+    o = torch.empty(batch, H, cfg.head_dim, dtype=torch.bfloat16, device="cuda")
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+
+    def run():
+        L.mla_recon_decode(c, q.data_ptr(), kv.data_ptr(), T, lens.data_ptr(), wuk.data_ptr(),
+                           wuv.data_ptr(), o.data_ptr(), ws.data_ptr(), wsb, stream)
+    for _ in range(3):
+        run()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        run()
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    L.mla_recon_prof_enable(L.KC_ATTN_FWD, True)
+    for _ in range(steps):
+        run()
+    attn = L.mla_recon_prof_read(L.KC_ATTN_FWD)
+    L.mla_recon_prof_enable(L.KC_ATTN_FWD, False)
+    attn_ms = attn["ms"] / steps
+    cache_bytes = batch * T * ldc * 2
+    return {"batch": batch, "cache_tokens": T, "ms_per_step": round(ms, 4),
+            "value": round(batch / (ms / 1e3), 1), "unit": "tokens/s",
+            "attention_kernel_ms": round(attn_ms, 4),
+            "cache_GBps": round(cache_bytes / (attn_ms / 1e3) / 1e9, 1),
+            "cache_frac_of_hbm_peak": round(cache_bytes / (attn_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
+
+
 def main():
     args = parse()
     if args.summarize_traffic:
@@ -259,6 +311,8 @@ def main():
         ms_cap = start.elapsed_time(stop) / args.steps
         del x, h_next
 
+    decode = None if args.no_decode else decode_bench(cfg, wl, args.decode_batch, args.steps)
+
     # for reference: the four separate calls, which also form A_t and A_s (two W_O products)
     ms_sep = None
     if not args.no_separate:
@@ -333,6 +387,7 @@ def main():
         "capture": None if ms_cap is None else
                    {"ms_per_layer": round(ms_cap, 4),
                     "value": round(tokens / (ms_cap / 1e3), 1), "unit": "tokens/s per layer"},
+        "decode_absorbed": decode,
         "cached_teacher": None if ms_cached is None else
                           {"ms_per_step": round(ms_cached, 4),
                            "value": round(tokens / (ms_cached / 1e3), 1), "unit": "tokens/s"},
