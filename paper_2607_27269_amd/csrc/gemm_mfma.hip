@@ -14,8 +14,9 @@
 // in registers as well: the LDS reads of the next 16-wide k step are in flight while the
 // matrix cores work on the current one, and the first step of the next slice is read
 // right after the barrier that publishes it.  The epilogue stages each 32-row strip of a
-// wavefront's tile in LDS and writes it back with 16-byte (fp32) or 8-byte (bf16) stores.  Row strides are padded so that the
-// operand reads of a wavefront hit distinct banks.  Large problems use 256 x 256 tiles on
+// wavefront's tile in LDS and writes it back with 16-byte (fp32) or 8-byte (bf16) stores.
+// The operand reads of a wavefront hit distinct banks: k-major rows are XOR-swizzled in
+// 16-byte chunks, m-major row strides are padded.  Large problems use 256 x 256 tiles on
 // 8 wavefronts (128 x 64 each), which halves the LDS bytes per MFMA compared with
 // 128 x 128 tiles on 4 wavefronts (64 x 64 each), used for small problems.  Workgroup
 // ids are remapped so that neighbouring tiles (sharing A row panels or B column panels)
@@ -75,23 +76,35 @@ constexpr int mm_ld(int rows) {
 template <bool KMAJOR, int ROWS, int NTHR, int BK>
 struct Loader;
 
-// k-major tile: ROWS x BK, chunk c -> row c / (BK/8), k-chunk c % (BK/8); rows padded by 8
-// elements (BK = 64: 144-byte rows, BK = 32: 80-byte rows; conflict-free operand reads)
+// k-major tile: ROWS x BK, chunk c -> row c / (BK/8), k-chunk c % (BK/8).  Rows are not
+// padded: the 16-byte chunk holding k-chunk c of row r sits at position c ^ swz(r) of its
+// row, so that the 16 rows one operand read covers per LDS cycle (one k-chunk each) fall on
+// 16 distinct 16-byte bank groups (a 256-byte bank window holds 128 / BK rows)
 template <int ROWS, int NTHR, int BK>
 struct Loader<true, ROWS, NTHR, BK> {
-  static constexpr int KM_LD = BK + 8;
-  static constexpr int CHUNKS = ROWS * (BK / 8);
+  static constexpr int KM_LD = BK;
+  static constexpr int NCH = BK / 8;    // 16-byte chunks per row
+  static constexpr int RPW = 128 / BK;  // rows per 256-byte bank window
+  static_assert(BK == 32 || BK == 64, "k-major slice depth");
+  static __device__ __forceinline__ int swz(int row) { return (row / RPW) % NCH; }
+  static constexpr int CHUNKS = ROWS * NCH;
   static constexpr int PER = CHUNKS / NTHR;
   using Dma = DmaTile<ROWS, BK, KM_LD, NTHR / 64, true>;
   static constexpr int ELEMS = Dma::ALLOC;  // whole 1 KB blocks, a multiple per wavefront
   static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
+  // the copy that fills LDS position (row, p) fetches k-chunk p ^ swz(row)
+  static __device__ __forceinline__ void swizzle(Dma& t) {
+#pragma unroll
+    for (int p = 0; p < Dma::PER; ++p)
+      t.col[p] = (short)(8 * ((t.col[p] / 8) ^ swz(t.row[p])));
+  }
   u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
                                        int rows_valid, int k0, int kend) {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = threadIdx.x + i * NTHR;
-      const int row = c / (BK / 8), kc = (c % (BK / 8)) * 8;
+      const int row = c / NCH, kc = (c % NCH) * 8;
       u32x4 v = {0u, 0u, 0u, 0u};
       if (row < rows_valid && k0 + kc < kend)
         v = *(const u32x4*)(p + (int64_t)(row0 + row) * ld + k0 + kc);
@@ -102,7 +115,8 @@ struct Loader<true, ROWS, NTHR, BK> {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = threadIdx.x + i * NTHR;
-      *(u32x4*)(lds + (c / (BK / 8)) * KM_LD + (c % (BK / 8)) * 8) = r[i];
+      const int row = c / NCH;
+      *(u32x4*)(lds + row * KM_LD + 8 * ((c % NCH) ^ swz(row))) = r[i];
     }
   }
   // full k-slice of a full tile straight from HBM into LDS (uniform base + lane offset)
@@ -110,10 +124,12 @@ struct Loader<true, ROWS, NTHR, BK> {
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
     t.issue_s(lds, p + (int64_t)row0 * ld + k0, [&](int r, int c) { return r * (int)ld + c; });
   }
-  // operand fragment: rows row0 + lane%32, k = 16 kk + 8 half + 0..7
+  // operand fragment: rows row0 + lane%32, k = 16 kk + 8 half + 0..7 (row0 is a multiple of
+  // 32, so the swizzle depends on the lane only)
   static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
-    const int lane = threadIdx.x & 63;
-    return *(const bf16x8*)(lds + (row0 + (lane & 31)) * KM_LD + 16 * kk + 8 * (lane >> 5));
+    const int lane = threadIdx.x & 63, l = lane & 31;
+    const int c = 2 * kk + (lane >> 5);
+    return *(const bf16x8*)(lds + (row0 + l) * KM_LD + 8 * (c ^ swz(l)));
   }
 };
 
@@ -127,6 +143,7 @@ struct Loader<false, ROWS, NTHR, BK> {
   using Dma = DmaTile<BK, ROWS, LD, NTHR / 64, true>;
   static constexpr int ELEMS = Dma::ALLOC;  // whole 1 KB blocks, a multiple per wavefront
   static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
+  static __device__ __forceinline__ void swizzle(Dma&) {}
   u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
                                        int rows_valid, int k0, int kend) {
@@ -261,6 +278,8 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   typename LB::Dma db;
   da.init();
   db.init();
+  LA::swizzle(da);
+  LB::swizzle(db);
   const int mvalid = g.M - m0, nvalid = g.N - n0;
   const int nkg = (kend - kbeg + BK - 1) / BK;  // slices per operand group
   const int nk = nkg * (g.causal ? g.kgroups : 1);
