@@ -341,7 +341,10 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
 // number of copies per stage (the block count is padded) and of dS^T stores per step, so
 // one counter wait names exactly the copies that must have landed.
 constexpr int DV_BQ = 32;
-constexpr int DS_STORES = DV_BQ / 8;  // 8-byte dS^T stores per lane per step
+// dS^T stores per lane per step: a wavefront's 32 x 32 block is transposed through a
+// private LDS tile so that each 16-byte store continues its neighbours' along a key row
+// (4 lanes write a row's 64 bytes)
+constexpr int DS_STORES = DV_BQ * 32 * 2 / (64 * 16);
 constexpr int DV_NST = 2;  // LDS stages: a step's copies are issued one step ahead
 
 // [2][H][B][Tpad] fp32: log2-scaled lse (+inf past the sequence end) and delta (0 there)
@@ -464,7 +467,8 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
   constexpr int NKK = DQK / 16, NVK = DV / 16, NCV = DV / 32;
   constexpr int D = Stage::PER;
   static_assert(DS_STORES < 64, "counter range");
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[DV_NST * Stage::ELEMS];
+  // the Q / dO ring, then one 32 x 32 dS^T transpose tile per wavefront
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[DV_NST * Stage::ELEMS + 4 * 32 * DV_BQ];
   const AttnDev& a = w.f;
 
   const int nbg = a.B * w.G;
@@ -537,6 +541,13 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
   if (niter > 1) advance(qn, hn);
   auto stage_of = [&](int it) { return smem + (it & 1) * Stage::ELEMS; };
   bf16_t* scratch = w.ds_dummy + 64 * lane;
+  // transpose tile: key row r holds 64 bytes (32 queries) as four 16-byte segments, segment
+  // s stored at position s ^ ((r / 4) % 4) (the packed writes of 32 rows at one segment
+  // spread over the banks; the 16-byte reads of 4 consecutive rows are conflict-free)
+  bf16_t* tr = smem + DV_NST * Stage::ELEMS + wave * 32 * DV_BQ;
+  static_assert(DV_BQ == 32 && DS_STORES == 2, "transpose tile layout");
+  // reader side: lane handles rows rr + 16 j (j < 2), queries 8 sg .. 8 sg + 7
+  const int rr = lane >> 2, sg = lane & 3;
   stg.issue(w, b, hc, qc, stage_of(0));
   wait_vm<0>();
   lds_barrier();
@@ -550,13 +561,16 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
     // the stage of step it - 1 is free: every wave passed the barrier after reading it
     stg.issue(w, b, hn, qn, stage_of(it + 1));
 
-    // this lane's dS^T row segment for the block: queries q0 + 4 half + {0..3, 8..11, ...};
-    // lanes past the sequence end write a scratch row instead, so that every wavefront
-    // issues exactly DS_STORES stores per step
-    bf16_t* dsrow = my_key < a.T
-                        ? w.dsT + ((int64_t)b * a.H + hc) * a.T * w.ds_ld +
-                              (int64_t)my_key * w.ds_ld + q0 + 4 * half
-                        : scratch + 4 * half;
+    // this lane's dS^T store targets for the block: key rows kw0 + rr + 16 j, queries
+    // q0 + 8 sg .. + 7; rows past the sequence end go to a scratch row instead, so that every
+    // wavefront issues exactly DS_STORES stores per step
+    // (computed where the stores are issued: short-lived registers)
+    auto dst = [&](int j) {
+      const int key = kw0 + rr + 16 * j;
+      return key < a.T ? w.dsT + ((int64_t)b * a.H + hc) * a.T * w.ds_ld + (int64_t)key * w.ds_ld +
+                             q0 + 8 * sg
+                       : scratch + 8 * sg;
+    };
     if (kw0 <= min(q0 + DV_BQ - 1, a.T - 1)) {  // wave-uniform: some pair is visible
       f32x16 sp, dp;
 #pragma unroll
@@ -586,11 +600,16 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
           dp[e] = p * (dp[e] - dl[r]);
         }
       }
-      // dS^T in bf16: element e is query 8 (e/4) + 4 half + e%4
+      // dS^T in bf16: element e is query 8 (e/4) + 4 half + e%4 of key row col, i.e. half
+      // h of 16-byte segment e/4; through the transpose tile to row-contiguous stores
+      // (LDS operations of one wavefront complete in order: the reads see the writes, and
+      // the next step's writes follow these reads)
+      asm volatile("" ::: "memory");
 #pragma unroll
       for (int e4 = 0; e4 < 4; ++e4)
-        st_global8(dsrow + 8 * e4,
-                   u32x2{pack2bf(dp[4 * e4], dp[4 * e4 + 1]), pack2bf(dp[4 * e4 + 2], dp[4 * e4 + 3])});
+        *(u32x2*)(tr + col * DV_BQ + 8 * (e4 ^ ((col >> 2) & 3)) + 4 * half) =
+            u32x2{pack2bf(dp[4 * e4], dp[4 * e4 + 1]), pack2bf(dp[4 * e4 + 2], dp[4 * e4 + 3])};
+      asm volatile("" ::: "memory");
       // dV^T += dO^T P   (K-step u: queries 16 u + {4h.., 8+4h..})
 #pragma unroll
       for (int u = 0; u < 2; ++u) {
@@ -604,10 +623,17 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
           dv[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(dOs, LDO, 32 * c, klo, klo + 8),
                                                          pf, dv[c], 0, 0, 0);
       }
+      asm volatile("" ::: "memory");
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int r = rr + 16 * j;
+        st_global16(dst(j), *(const u32x4*)(tr + r * DV_BQ + 8 * (sg ^ ((r >> 2) & 3))));
+      }
+      asm volatile("" ::: "memory");
     } else {
       // every key of this wavefront follows every query of the block: zeros
 #pragma unroll
-      for (int o = 0; o < DV_BQ; o += 8) st_global8(dsrow + o, u32x2{0u, 0u});
+      for (int j = 0; j < 2; ++j) st_global16(dst(j), u32x4{0u, 0u, 0u, 0u});
     }
     // step it + 1's copies have landed; younger are only this step's stores (counters
     // complete in issue order)

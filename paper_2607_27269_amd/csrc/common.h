@@ -210,6 +210,11 @@ __device__ __forceinline__ void st_global8(bf16_t* p, u32x2 v) {
   *(__attribute__((address_space(1))) u32x2*)p = v;
 }
 
+// 16-byte store through an explicitly global pointer
+__device__ __forceinline__ void st_global16(bf16_t* p, u32x4 v) {
+  *(__attribute__((address_space(1))) u32x4*)p = v;
+}
+
 // at most N vector-memory operations of this wavefront (e.g. LDS DMA copies of later
 // tiles) still in flight
 template <int N>
