@@ -14,9 +14,10 @@
 //   the natural [query][dim] LDS tiles through gfx950's transposing LDS read.  The rotary
 //   part of dK is summed over the group's heads and left as an fp32 partial per group
 //   (the positional key may be shared by several groups).
-//   With a dS^T buffer given, the kernel also stores dS^T in bf16 (the 8-byte groups of
-//   4 consecutive queries it already packs for the dK product), zeros included wherever
-//   the dQ product below reads a masked pair.
+// * dV and dS^T, preferred when a dS^T buffer fits: the same walk (256 keys per
+//   workgroup) computes only dV and stores dS^T in bf16, transposed through LDS so that
+//   the stores run along key rows, zeros included wherever the dQ product below reads a
+//   masked pair; dK = scale dS^T Q is then a GEMM as well.
 // * dQ, preferred: dQ = scale dS K as a batched causal GEMM (one batch entry per
 //   (sequence, head)) over the stored dS^T and the keys gathered per group into one
 //   [token][group][dqk] tensor; no recomputation of S or dP.
@@ -333,19 +334,26 @@ __global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
 // ---------------------------------------------------------------------------------------
 // dV and dS^T (the path where dK and dQ are GEMMs over the stored dS^T)
 // ---------------------------------------------------------------------------------------
-// A workgroup owns 128 keys of one (sequence, KV group), 32 per wavefront, and walks the
-// group's heads and 32-query blocks.  K and V of the lane's key are B-operand fragments
-// held in registers; only the 32-query Q / dO tiles and their softmax statistics pass
-// through LDS, in a ring of three stages (about 72 KB), so two workgroups share a CU and
-// each block's copy is issued two steps before its use.  Every wavefront issues the same
-// number of copies per stage (the block count is padded) and of dS^T stores per step, so
-// one counter wait names exactly the copies that must have landed.
+// A workgroup owns 256 keys of one (sequence, KV group), 32 per wavefront (8 wavefronts,
+// one workgroup per CU), and walks the group's heads and 32-query blocks.  K and V of the
+// lane's key are B-operand fragments held in registers; only the 32-query Q / dO tiles
+// and their softmax statistics pass through LDS, in a ring of two stages, each block's
+// copy issued one step before its use; the more keys share a copied tile, the fewer
+// copies per key.  Every wavefront issues the same number of copies per stage (the block
+// count is padded) and of dS^T stores per step, so one counter wait names exactly the
+// copies that must have landed.
 constexpr int DV_BQ = 32;
 // dS^T stores per lane per step: a wavefront's 32 x 32 block is transposed through a
 // private LDS tile so that each 16-byte store continues its neighbours' along a key row
 // (4 lanes write a row's 64 bytes)
 constexpr int DS_STORES = DV_BQ * 32 * 2 / (64 * 16);
 constexpr int DV_NST = 2;  // LDS stages: a step's copies are issued one step ahead
+#ifndef DV_WAVES_OVERRIDE
+constexpr int DV_WAVES = 8;
+#else
+constexpr int DV_WAVES = DV_WAVES_OVERRIDE;
+#endif
+constexpr int DV_BKB = 32 * DV_WAVES;  // keys per workgroup
 
 // [2][H][B][Tpad] fp32: log2-scaled lse (+inf past the sequence end) and delta (0 there)
 __global__ void attn_stats_t_kernel(const float* __restrict__ lse, const float* __restrict__ delta,
@@ -374,12 +382,12 @@ struct DvStage {
   static constexpr int LDO = ld_of(DV);
   static constexpr int NQB = (DV_BQ * LDQ * 2 + 1023) / 1024;  // 1 KB blocks of the Q tile
   static constexpr int NOB = (DV_BQ * LDO * 2 + 1023) / 1024;  // ... of the dO tile
-  static constexpr int NB = (NQB + NOB + 1 + 3) / 4 * 4;      // + statistics, padded
-  static constexpr int PER = NB / 4;                          // copies per wavefront
+  static constexpr int NB = (NQB + NOB + 1 + DV_WAVES - 1) / DV_WAVES * DV_WAVES;  // + stats, padded
+  static constexpr int PER = NB / DV_WAVES;                   // copies per wavefront
   static constexpr int OFF_O = NQB * 512, OFF_S = (NQB + NOB) * 512;  // bf16 elements
   static constexpr int ELEMS = NB * 512;
 
-  // block blk = wave + 4 p: its kind is wave-uniform (blk < NQB: Q, < NQB + NOB: dO, then
+  // block blk = wave + DV_WAVES p: its kind is wave-uniform (blk < NQB: Q, < NQB + NOB: dO, then
   // the statistics block, then padding that re-copies Q row 0 into unused LDS).  A full
   // block (all 32 queries inside the sequence) is copied from wave-uniform row bases with
   // loop-invariant lane offsets, computed once (init); the last, partial block clamps rows
@@ -392,7 +400,7 @@ struct DvStage {
     const uint32_t s_part = (uint32_t)a.H * a.B * w.tpad * 4;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
-      const int blk = wave + 4 * p;
+      const int blk = wave + DV_WAVES * p;
       uint32_t off = 0u;
       if (blk < NQB) {
         const int e = (blk * 1024 + 16 * lane) / 2;
@@ -425,7 +433,7 @@ struct DvStage {
       const bf16_t* orow = w.dO + (n0 + q0) * o_tok + (int64_t)h * DV;
 #pragma unroll
       for (int p = 0; p < PER; ++p) {
-        const int blk = wave + 4 * p;
+        const int blk = wave + DV_WAVES * p;
         // statistics block: lanes 0-7 lse2 of queries q0 + 4 l .. + 3, lanes 8-15 delta, the
         // rest repeat; padding blocks re-copy Q row 0 (offset 0)
         const void* base = blk < NQB ? (const void*)qrow
@@ -439,7 +447,7 @@ struct DvStage {
     const bf16_t* ob = w.dO + n0 * o_tok + (int64_t)h * DV;
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
-      const int blk = wave + 4 * p;
+      const int blk = wave + DV_WAVES * p;
       const bf16_t* src;
       if (blk < NQB) {
         const int e = (blk * 1024 + 16 * lane) / 2;
@@ -461,14 +469,14 @@ struct DvStage {
 };
 
 template <int DQK, int DV>
-__global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
+__global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kernel(BwdDev w) {
   using Stage = DvStage<DQK, DV>;
   constexpr int LDQ = Stage::LDQ, LDO = Stage::LDO;
   constexpr int NKK = DQK / 16, NVK = DV / 16, NCV = DV / 32;
   constexpr int D = Stage::PER;
   static_assert(DS_STORES < 64, "counter range");
   // the Q / dO ring, then one 32 x 32 dS^T transpose tile per wavefront
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[DV_NST * Stage::ELEMS + 4 * 32 * DV_BQ];
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[DV_NST * Stage::ELEMS + DV_WAVES * 32 * DV_BQ];
   const AttnDev& a = w.f;
 
   const int nbg = a.B * w.G;
@@ -476,7 +484,7 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
   const int bg = blockIdx.x % nbg;
   const int b = bg / w.G, g = bg % w.G;
   const int hpg = a.H / w.G;
-  const int k0 = kb * BKB;
+  const int k0 = kb * DV_BKB;
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5, col = lane & 31;
   const int kw0 = k0 + 32 * wave;
@@ -487,12 +495,12 @@ __global__ __launch_bounds__(256, 2) void attn_dv_mfma_kernel(BwdDev w) {
   // here, so their entries are zeros that no step below writes
   const int zq0 = k0 / DQ_TILE * DQ_TILE;
   if (zq0 < k0) {
-    const int nz = k0 - zq0;                       // multiple of 128
+    const int nz = k0 - zq0;                       // multiple of the key block
     const int cpr = nz / 8;                        // 16-byte chunks per key row
-    const int kr = min(BKB, a.T - k0);
+    const int kr = min(DV_BKB, a.T - k0);
     for (int h = 0; h < hpg; ++h) {
       bf16_t* plane = w.dsT + ((int64_t)b * a.H + i0 + h) * a.T * w.ds_ld;
-      for (int c = threadIdx.x; c < kr * cpr; c += 256) {
+      for (int c = threadIdx.x; c < kr * cpr; c += 64 * DV_WAVES) {
         const int r = c / cpr, q = zq0 + (c % cpr) * 8;
         *(u32x4*)(plane + (int64_t)(k0 + r) * w.ds_ld + q) = u32x4{0u, 0u, 0u, 0u};
       }
@@ -858,7 +866,8 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     prof_begin(KC_ATTN_DKDV, s);
-    attn_dv_mfma_kernel<DQK, DV><<<nkb * at.B * w.G, 256, 0, s>>>(w);
+    const int nkb_dv = (at.T + DV_BKB - 1) / DV_BKB;
+    attn_dv_mfma_kernel<DQK, DV><<<nkb_dv * at.B * w.G, 64 * DV_WAVES, 0, s>>>(w);
     prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV),
              N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0 +
                  pairs * 2.0);
