@@ -27,6 +27,9 @@ CASES = {
     "cfg2_short": (2, 1, 192, None),
     "cfg3_short": (3, 1, 136, [100]),
     "cfg4_short": (4, 1, 130, None),
+    # more than one 256-key block of the dV / dS^T kernel, ragged last block
+    "cfg1_long": (1, 2, 300, [300, 263]),
+    "cfg3_long": (3, 1, 520, [517]),
 }
 
 
@@ -54,7 +57,8 @@ def test_step_parity(name):
     print(f"[parity] {name} loss={out['loss']:.6e} ref={ref['loss']:.6e} errs={errs}", flush=True)
 
 
-FUSED_CASES = ("cfg0_ragged_fp32", "cfg0_bf16", "cfg1_ragged", "cfg3_short", "cfg4_short")
+FUSED_CASES = ("cfg0_ragged_fp32", "cfg0_bf16", "cfg1_ragged", "cfg3_short", "cfg4_short",
+               "cfg1_long", "cfg3_long")
 
 
 @pytest.mark.parametrize("with_dA", [True, False])
