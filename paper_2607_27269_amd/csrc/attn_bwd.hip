@@ -56,6 +56,7 @@ struct BwdDev {
   bf16_t* ds_dummy;      // scratch rows for stores of lanes past the sequence end
   const float* statT;    // [2][H][B][tpad]: log2-scaled lse, delta (dV kernel)
   int tpad;
+  int off32;             // one sequence's Q / dO rows and the statistics span < 2^31 bytes
 };
 
 // dS^T tile rows a dQ GEMM row tile reads: queries from the start of the 256-query tile
@@ -393,9 +394,23 @@ struct DvStage {
   // loop-invariant lane offsets, computed once (init); the last, partial block clamps rows
   // to the sequence end.
   uint32_t voff[PER];  // byte offset of this lane's chunk from its block's row base
-  __device__ __forceinline__ void init(const BwdDev& w) {
+  // with 32-bit row offsets (off32): each copy's base is fixed for the kernel (Q or dO of
+  // the sequence, or the statistics of the sequence) and a step adds a uniform 32-bit row
+  // offset, instead of 64-bit row addresses per step
+  const void* pbase[PER];
+  int pkind[PER];  // 0: Q (and padding), 1: dO, 2: statistics
+  __device__ __forceinline__ void init(const BwdDev& w, int b) {
     const AttnDev& a = w.f;
     const int wave = wave_id(), lane = threadIdx.x & 63;
+    const int64_t n0 = (int64_t)b * a.T;
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int blk = wave + DV_WAVES * p;
+      pkind[p] = blk < NQB ? 0 : blk < NQB + NOB ? 1 : blk == NQB + NOB ? 2 : 0;
+      pbase[p] = pkind[p] == 0   ? (const void*)(a.Q + n0 * a.q_tok)
+                 : pkind[p] == 1 ? (const void*)(w.dO + n0 * (int64_t)a.H * DV)
+                                 : (const void*)(w.statT + (int64_t)b * w.tpad);
+    }
     const int64_t o_tok = (int64_t)a.H * DV;
     const uint32_t s_part = (uint32_t)a.H * a.B * w.tpad * 4;
 #pragma unroll
@@ -428,6 +443,18 @@ struct DvStage {
     const int64_t o_tok = (int64_t)a.H * DV;
     const float* sbase = w.statT + ((int64_t)h * a.B + b) * w.tpad + q0;  // lse2 row
     const uint32_t s_part = (uint32_t)a.H * a.B * w.tpad * 4;          // lse2 -> delta bytes
+    if (w.off32 && q0 + DV_BQ - 1 <= last) {
+      const uint32_t qo = 2u * ((uint32_t)q0 * (uint32_t)a.q_tok + (uint32_t)(h * a.q_head));
+      const uint32_t oo = 2u * ((uint32_t)q0 * (uint32_t)(a.H * DV) + (uint32_t)(h * DV));
+      const uint32_t so = 4u * ((uint32_t)(h * a.B) * (uint32_t)w.tpad + (uint32_t)q0);
+#pragma unroll
+      for (int p = 0; p < PER; ++p) {
+        const int blk = wave + DV_WAVES * p;
+        const uint32_t ro = pkind[p] == 0 ? qo : pkind[p] == 1 ? oo : so;
+        dma16_s(pbase[p], voff[p] + ro, stage + blk * 512);
+      }
+      return;
+    }
     if (q0 + DV_BQ - 1 <= last) {
       const bf16_t* qrow = a.Q + (n0 + q0) * a.q_tok + (int64_t)h * a.q_head;
       const bf16_t* orow = w.dO + (n0 + q0) * o_tok + (int64_t)h * DV;
@@ -536,7 +563,7 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
   const int nper = nqb - qb0;
   const int niter = hpg * nper;  // >= 1
   Stage stg;
-  stg.init(w);
+  stg.init(w, b);
   // steps walk (query block, head): query blocks in descending order with the group's heads
   // innermost, so that all key blocks of a (sequence, group) stream the same Q/dO tile at
   // the same time and share it through L2.  (qc, hc) is this step's pair, (qn, hn) the
@@ -845,6 +872,9 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   w.ds_dummy = w.dsT + (ds_path ? (int64_t)at.B * at.H * at.T * w.ds_ld : 0);
   w.statT = wb.statT;
   w.tpad = attn_stats_tpad(at.T);
+  w.off32 = (int64_t)at.T * at.Q.tok * 2 < (1ll << 31) &&
+            (int64_t)at.T * at.H * at.dv * 2 < (1ll << 31) &&
+            (int64_t)at.H * at.B * w.tpad * 4 * 2 < (1ll << 31);
   const double pairs = attn_causal_pairs(at);
   const double N = (double)at.B * at.T;
   // delta = rowsum(dO . O), then the dK/dV kernel: algorithmic dV = P^T dO, dP = dO V^T,
