@@ -11,13 +11,16 @@
 // Kernels:
 // * absorb_query_kernel: the absorbed queries [B][HP][DK] bf16 (heads padded to HP = 32k).
 // * decode_attn_kernel: split-K over the cache (flash-decoding).  A workgroup (4 waves)
-//   owns one (sequence, key chunk, block of 32 heads).  Key tiles of 32 rows are staged in
-//   LDS through registers (the next tile's loads in flight during the current tile).  Each
-//   wave computes S^T = K Q^T for the tile (key in the MFMA row, head in the column, so each
-//   lane owns one head's online-softmax state), then O^T += V^T P^T for its quarter of the
-//   latent width; V^T is the tile's latent columns read with the transposing LDS read.
-//   The 4 waves repeat the same S^T (small next to the latent product, and decoding is
-//   bound by the cache reads).  Partial (max, sum, unnormalised output) per split.
+//   owns one (sequence, key chunk, block of 32 heads).  Key tiles of 32 rows are copied
+//   straight into LDS in a ring of three stages (two tiles in flight).  The
+//   tile's S^T = K Q^T (key in the MFMA row, head in the column, so each lane owns one
+//   head's online-softmax state) is split over the 4 waves along the key width: each wave
+//   multiplies a quarter of the 16-wide K steps (its absorbed-query fragments held in
+//   registers) and the partial products are summed through
+//   LDS in wave order, so every wave holds the same S^T (the same values in every wave).
+//   Each wave then updates O^T += V^T P^T for its quarter of the latent width; V^T is the
+//   tile's latent columns read with the transposing LDS read.  Partial (max, sum,
+//   unnormalised output) per split.
 // * decode_combine_kernel: merges the splits of a (sequence, head) in split order.
 // * uv_proj_kernel: o = W_UV[g] (latent), one thread per output.
 #include "attn_common.h"
@@ -30,6 +33,7 @@ namespace {
 
 constexpr int DEC_KT = 32;     // keys per tile
 constexpr int DEC_WAVES = 4;
+constexpr float DEC_SLACK = 8.f;  // log2 units the running reference max may lag
 
 struct DecodeDev {
   const bf16_t* qabs;   // [B][HP][DK]
@@ -70,13 +74,16 @@ template <int DK, int DVL>
 __global__ __launch_bounds__(64 * DEC_WAVES) void decode_attn_kernel(DecodeDev a) {
   constexpr int LDK = attn::ld_of(DK);        // padded rows: conflict-free operand reads
   constexpr int NKK = DK / 16;
+  constexpr int QMAX = (NKK + DEC_WAVES - 1) / DEC_WAVES;  // K steps per wave, at most
   constexpr int WV = DVL / DEC_WAVES;         // latent rows per wave
   constexpr int NCV = WV / 32;
-  constexpr int CHUNKS = DEC_KT * DK / 8;     // 16-byte chunks per tile
-  constexpr int PER = (CHUNKS + 64 * DEC_WAVES - 1) / (64 * DEC_WAVES);
+  constexpr int NST = 3;                      // key-tile ring: two tiles in flight
   static_assert(DK % 16 == 0 && WV % 32 == 0, "decode shape");
-  __shared__ __attribute__((aligned(16))) bf16_t Qs[32 * LDK];
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][DEC_KT * LDK];
+  using KT = DmaTile<DEC_KT, DK, LDK, DEC_WAVES, true>;
+  constexpr int D = KT::PER;                  // copies per wave per tile
+  __shared__ __attribute__((aligned(1024))) bf16_t Ks[NST][KT::ALLOC];
+  // partial S^T of each wave: [wave][e / 4][lane][4] (16-byte accesses, conflict-free)
+  __shared__ __attribute__((aligned(16))) float Sp[DEC_WAVES][4][64][4];
 
   const int split = blockIdx.x, b = blockIdx.y, h0 = 32 * blockIdx.z;
   const int lane = threadIdx.x & 63, wave = wave_id();
@@ -85,32 +92,41 @@ __global__ __launch_bounds__(64 * DEC_WAVES) void decode_attn_kernel(DecodeDev a
   const int kbeg = split * a.chunk;
   const int kend = min(len, kbeg + a.chunk);
   const int64_t pbase = ((int64_t)b * a.nsplit + split) * a.HP + h0;
+  // this wave's share of the K steps
+  const int kk0 = wave * NKK / DEC_WAVES, kk1 = (wave + 1) * NKK / DEC_WAVES;
 
-  // the block of 32 absorbed queries
-  const bf16_t* qsrc = a.qabs + ((int64_t)b * a.HP + h0) * DK;
-  for (int c = threadIdx.x; c < 32 * DK / 8; c += 64 * DEC_WAVES) {
-    const int r = c / (DK / 8), k = (c % (DK / 8)) * 8;
-    *(u32x4*)(Qs + r * LDK + k) = *(const u32x4*)(qsrc + (int64_t)r * DK + k);
-  }
   const bf16_t* cs = a.cache + (int64_t)b * a.seq_stride;
-  u32x4 reg[PER];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int c = threadIdx.x + p * 64 * DEC_WAVES;
-      const int r = c / (DK / 8), k = (c % (DK / 8)) * 8;
-      u32x4 v = {0u, 0u, 0u, 0u};
-      if (c < CHUNKS && k0 + r < kend) v = *(const u32x4*)(cs + (int64_t)(k0 + r) * a.ldc + k);
-      reg[p] = v;
+  KT kt_copy;
+  kt_copy.init();
+  // key tile t into stage t % NST; rows past the chunk end repeat its last row (finite,
+  // and given no weight below)
+  auto issue = [&](int t) {
+    const int k0 = kbeg + t * DEC_KT;
+    if (k0 + DEC_KT <= kend) {  // full tile: uniform row base plus 32-bit lane offsets
+      kt_copy.issue_s(Ks[t % NST], cs + (int64_t)k0 * a.ldc,
+                      [&](int r, int c) { return r * a.ldc + c; });
+    } else {
+      kt_copy.issue(Ks[t % NST], [&](int r, int c) {
+        return cs + (int64_t)min(k0 + r, kend - 1) * a.ldc + c;
+      });
     }
   };
-  auto lstore = [&](bf16_t* dst) {
+  const int ntile = kend > kbeg ? (kend - kbeg + DEC_KT - 1) / DEC_KT : 0;
+  if (ntile > 0) issue(0);
+  if (ntile > 1) issue(1);
+  // this lane's head as B-operand fragments for the wave's K steps (head h0 + col,
+  // k = 16 kk + 8 half + 0..7)
+  bf16x8 qf[QMAX];
+  {
+    const bf16_t* qsrc = a.qabs + ((int64_t)b * a.HP + h0 + col) * DK + 8 * half;
 #pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int c = threadIdx.x + p * 64 * DEC_WAVES;
-      if (c < CHUNKS) *(u32x4*)(dst + (c / (DK / 8)) * LDK + (c % (DK / 8)) * 8) = reg[p];
-    }
-  };
+    for (int j = 0; j < QMAX; ++j)
+      qf[j] = kk0 + j < kk1 ? *(const bf16x8*)(qsrc + 16 * (kk0 + j)) : bf16x8{};
+  }
+  wait_vm<0>();
+#pragma unroll
+  for (int j = 0; j < QMAX; ++j) asm volatile("" : "+v"(qf[j]));
+  __syncthreads();
 
   f32x16 acc[NCV];
 #pragma unroll
@@ -119,42 +135,57 @@ __global__ __launch_bounds__(64 * DEC_WAVES) void decode_attn_kernel(DecodeDev a
     for (int e = 0; e < 16; ++e) acc[c][e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int ntile = kend > kbeg ? (kend - kbeg + DEC_KT - 1) / DEC_KT : 0;
-  if (ntile > 0) {
-    gload(kbeg);
-    lstore(Ks[0]);
-  }
-  __syncthreads();
   for (int t = 0; t < ntile; ++t) {
-    const bf16_t* kt = Ks[t & 1];
+    const bf16_t* kt = Ks[t % NST];
     const int k0 = kbeg + t * DEC_KT;
-    if (t + 1 < ntile) gload(k0 + DEC_KT);
-    // S^T (32 keys x 32 heads): key = MFMA row, head = column (this lane's head: col)
+    // the stage of tile t - 1 is free: every wave passed the barrier that ended it
+    if (t + 2 < ntile) issue(t + 2);
+    // S^T (32 keys x 32 heads): key = MFMA row, head = column (this lane's head: col);
+    // this wave's K steps, then the four partial products summed in wave order
     f32x16 s;
 #pragma unroll
     for (int e = 0; e < 16; ++e) s[e] = 0.f;
-#pragma unroll 4
-    for (int kk = 0; kk < NKK; ++kk)
-      s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-          *(const bf16x8*)(kt + col * LDK + 16 * kk + 8 * half),
-          *(const bf16x8*)(Qs + col * LDK + 16 * kk + 8 * half), s, 0, 0, 0);
-    // keys past the chunk end: no weight
+#pragma unroll
+    for (int j = 0; j < QMAX; ++j)
+      if (kk0 + j < kk1)
+        s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+            *(const bf16x8*)(kt + col * LDK + 16 * (kk0 + j) + 8 * half), qf[j], s, 0, 0, 0);
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4)
+      *(f32x4*)Sp[wave][e4][lane] = f32x4{s[4 * e4], s[4 * e4 + 1], s[4 * e4 + 2], s[4 * e4 + 3]};
+    lds_barrier();
+#pragma unroll
+    for (int e4 = 0; e4 < 4; ++e4) {
+      f32x4 u = *(const f32x4*)Sp[0][e4][lane];
+#pragma unroll
+      for (int w2 = 1; w2 < DEC_WAVES; ++w2) u += *(const f32x4*)Sp[w2][e4][lane];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) s[4 * e4 + r] = u[r];
+    }
+    // keys past the chunk end (last tile only; a real branch): no weight
+    if (k0 + DEC_KT > kend) {
+      asm volatile("");
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        if (k0 + 8 * (e >> 2) + 4 * half + (e & 3) >= kend) s[e] = -INFINITY;
+    }
     float mx = -INFINITY;
 #pragma unroll
-    for (int e = 0; e < 16; ++e) {
-      const int key = k0 + 8 * (e >> 2) + 4 * half + (e & 3);
-      if (key >= kend) s[e] = -INFINITY;
-      mx = fmaxf(mx, s[e]);
-    }
+    for (int e = 0; e < 16; ++e) mx = fmaxf(mx, s[e]);
     mx = pair_max32(mx) * a.sl2;
-    const float m_new = fmaxf(m_run, mx);
-    const float corr = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    l_run *= corr;
+    // lazy rescale: the reference max moves only when a block max exceeds it by more than
+    // DEC_SLACK (so P <= 2^DEC_SLACK); wave-uniform, and the same in every wave (same S^T)
+    if (__ballot(mx > m_run + DEC_SLACK) != 0) {
+      const float m_new = fmaxf(m_run, mx);
+      const float corr = __builtin_amdgcn_exp2f(m_run - (m_new == -INFINITY ? 0.f : m_new));
+      m_run = m_new;
+      l_run *= corr;
 #pragma unroll
-    for (int c = 0; c < NCV; ++c)
+      for (int c = 0; c < NCV; ++c)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) acc[c][e] *= corr;
+        for (int e = 0; e < 16; ++e) acc[c][e] *= corr;
+    }
+    const float m_use = m_run == -INFINITY ? 0.f : m_run;
     // P^T as the B operand of O^T = V^T P^T (K-step u: keys 16u + {4h'..4h'+3, 8+4h'..})
     bf16x8 pf[2];
 #pragma unroll
@@ -162,8 +193,8 @@ __global__ __launch_bounds__(64 * DEC_WAVES) void decode_attn_kernel(DecodeDev a
       u32x4 w;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * u + 2 * q], a.sl2, -m_new));
-        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * u + 2 * q + 1], a.sl2, -m_new));
+        const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * u + 2 * q], a.sl2, -m_use));
+        const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(s[8 * u + 2 * q + 1], a.sl2, -m_use));
         l_run += p0 + p1;
         w[q] = pack2bf(p0, p1);
       }
@@ -177,9 +208,11 @@ __global__ __launch_bounds__(64 * DEC_WAVES) void decode_attn_kernel(DecodeDev a
         acc[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             lds_operand_tr(kt, LDK, wave * WV + 32 * c, klo, klo + 8), pf[u], acc[c], 0, 0, 0);
     }
-    // the other stage was last read in tile t - 1, before the barrier that ended it
-    if (t + 1 < ntile) lstore(Ks[(t + 1) & 1]);
-    __syncthreads();
+    // tile t + 1 has landed (tile t + 2's copies may still fly) and every wave is done with
+    // tile t and the partial sums
+    if (t + 2 < ntile) wait_vm<D>();
+    else wait_vm<0>();
+    lds_barrier();
   }
 
   // partial state of this split: lane (head col, half) holds rows
@@ -246,9 +279,10 @@ __global__ void uv_proj_kernel(const float* __restrict__ lat, const bf16_t* __re
 #define MLA_DECODE_SHAPES(X) X(576, 512) X(288, 256) X(160, 128)
 
 int decode_chunk(int Lmax, int B) {
-  // enough workgroups to spread the cache reads over the CUs, at least 4 tiles each
+  // at least 4 tiles per workgroup, and no more workgroups than one round on the CUs (one
+  // workgroup per CU): long streams per workgroup keep its copy ring full
   int chunk = DEC_KT * 4;
-  while ((int64_t)B * ((Lmax + chunk - 1) / chunk) > 1024 && chunk < (1 << 20)) chunk *= 2;
+  while ((int64_t)B * ((Lmax + chunk - 1) / chunk) > 256 && chunk < (1 << 20)) chunk *= 2;
   return chunk;
 }
 
