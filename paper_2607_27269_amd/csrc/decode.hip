@@ -9,7 +9,8 @@
 // MFMA column block, followed by a per-group projection.
 //
 // Kernels:
-// * absorb_query_kernel: the absorbed queries [B][HP][DK] bf16 (heads padded to HP = 32k).
+// * group_gemm_kernel (+ absorb_rest_kernel): the absorbed queries [B][HP][DK] bf16 (heads
+//   padded to HP = 32k), the latent part as one product per KV group.
 // * decode_attn_kernel: split-K over the cache (flash-decoding).  A workgroup (4 waves)
 //   owns one (sequence, key chunk, block of 32 heads).  Key tiles of 32 rows are copied
 //   straight into LDS in a ring of three stages (two tiles in flight).  The
@@ -22,7 +23,7 @@
 //   tile's latent columns read with the transposing LDS read.  Partial (max, sum,
 //   unnormalised output) per split.
 // * decode_combine_kernel: merges the splits of a (sequence, head) in split order.
-// * uv_proj_kernel: o = W_UV[g] (latent), one thread per output.
+// * group_gemm_kernel: o = W_UV[g] (latent), one product per KV group.
 #include "attn_common.h"
 #include "kernels.h"
 #include "mfma.h"
@@ -47,27 +48,92 @@ struct DecodeDev {
   float* part_ml;       // [B][nsplit][HP][2]
 };
 
-// q_abs[b][i][c] = sum_d q[b][i][d] Wuk[(g dn + d)][c] for c < r_kv; the rope part copied.
-__global__ void absorb_query_kernel(const bf16_t* __restrict__ q, const bf16_t* __restrict__ Wuk,
-                                    bf16_t* __restrict__ qabs, int B, int H, int HP, int dn,
-                                    int dr, int rkv, int hpg) {
-  const int DK = rkv + dr;
-  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= (int64_t)B * HP * DK) return;
-  const int c = (int)(idx % DK);
-  const int i = (int)((idx / DK) % HP);
-  const int b = (int)(idx / ((int64_t)DK * HP));
-  float v = 0.f;
-  if (i < H) {
-    const bf16_t* qr = q + ((int64_t)b * H + i) * (dn + dr);
-    if (c < rkv) {
-      const bf16_t* w = Wuk + (int64_t)(i / hpg) * dn * rkv + c;
-      for (int d = 0; d < dn; ++d) v += bf2f(qr[d]) * bf2f(w[(int64_t)d * rkv]);
-    } else {
-      v = bf2f(qr[dn + (c - rkv)]);
+// The per-group products of decoding, C[r][n] = sum_k A[r][k] W(k, n) for the H / G_kv
+// heads of group g = blockIdx.z and sequences b: row r = (b, j) is head i = g hpg + j of
+// sequence b (A row at A + (b H + i) lda, C row at C + (b HC + i) ldc).  W(k, n) is
+// Wg[k][n] (WT = false: W_UK[g] = Wuk[g K + k][n]) or Wg[n][k] (WT = true: W_UV[g] =
+// Wuv[g N + n][k]).  32 x 32 output tiles (enough workgroups for these small products), K
+// in chunks of 32 staged in LDS as fp32; each of the 256 threads owns 2 x 2 outputs.  fp32
+// accumulation in k order, bf16 output.
+template <typename TA, bool WT>
+__global__ __launch_bounds__(256) void group_gemm_kernel(const TA* __restrict__ A, int64_t lda,
+                                                         const bf16_t* __restrict__ W,
+                                                         bf16_t* __restrict__ C, int64_t ldc,
+                                                         int HC, int B, int H, int hpg, int K,
+                                                         int N) {
+  constexpr int TR = 32, TN = 32, TK = 32;
+  __shared__ float As[TK][TR + 1];
+  __shared__ float Ws[TK][TN + 1];
+  const int g = blockIdx.z, n0 = blockIdx.x * TN, r0 = blockIdx.y * TR;
+  const int rows = B * hpg;
+  const int tid = threadIdx.x, tr = tid / 16, tn = tid % 16;
+  const bf16_t* Wg = W + (int64_t)g * K * N;
+  float acc[2][2] = {};
+  for (int k0 = 0; k0 < K; k0 += TK) {
+    // A tile: 64 rows x 32 k, transposed into As[k][r]
+    for (int e = tid; e < TR * TK; e += 256) {
+      const int r = e / TK, k = e % TK, rr = r0 + r, kk = k0 + k;
+      float v = 0.f;
+      if (rr < rows && kk < K) {
+        const int b = rr / hpg, i = g * hpg + rr % hpg;
+        v = ld(A + ((int64_t)b * H + i) * lda + kk);
+      }
+      As[k][r] = v;
+    }
+    // W tile: 32 k x 64 n
+    for (int e = tid; e < TK * TN; e += 256) {
+      int k, n;
+      if (WT) { n = e / TK; k = e % TK; } else { k = e / TN; n = e % TN; }
+      const int kk = k0 + k, nn = n0 + n;
+      float v = 0.f;
+      if (kk < K && nn < N) v = bf2f(WT ? Wg[(int64_t)nn * K + kk] : Wg[(int64_t)kk * N + nn]);
+      Ws[k][n] = v;
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int k = 0; k < TK; ++k) {
+      const float a0 = As[k][tr], a1 = As[k][tr + 16], w0 = Ws[k][tn], w1 = Ws[k][tn + 16];
+      acc[0][0] += a0 * w0;
+      acc[0][1] += a0 * w1;
+      acc[1][0] += a1 * w0;
+      acc[1][1] += a1 * w1;
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    const int rr = r0 + tr + 16 * u;
+    if (rr >= rows) continue;
+    const int b = rr / hpg, i = g * hpg + rr % hpg;
+#pragma unroll
+    for (int v = 0; v < 2; ++v) {
+      const int nn = n0 + tn + 16 * v;
+      if (nn < N) C[((int64_t)b * HC + i) * ldc + nn] = f2bf(acc[u][v]);
     }
   }
-  qabs[idx] = f2bf(v);
+}
+
+// The rest of the absorbed queries [B][HP][DK]: the rotary part copied from q, and zero
+// rows for the padding heads i >= H (the latent part of heads < H comes from the group
+// product).
+__global__ void absorb_rest_kernel(const bf16_t* __restrict__ q, bf16_t* __restrict__ qabs, int B,
+                                   int H, int HP, int dn, int dr, int rkv) {
+  const int DK = rkv + dr;
+  const int64_t n_rope = (int64_t)B * H * dr;
+  const int64_t n_pad = (int64_t)B * (HP - H) * DK;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < n_rope) {
+    const int c = (int)(idx % dr);
+    const int64_t bi = idx / dr;  // b * H + i
+    const int b = (int)(bi / H), i = (int)(bi % H);
+    qabs[((int64_t)b * HP + i) * DK + rkv + c] = q[bi * (dn + dr) + dn + c];
+  } else if (idx < n_rope + n_pad) {
+    const int64_t e = idx - n_rope;
+    const int c = (int)(e % DK);
+    const int64_t bp = e / DK;
+    const int b = (int)(bp / (HP - H)), i = H + (int)(bp % (HP - H));
+    qabs[((int64_t)b * HP + i) * DK + c] = (bf16_t)0;
+  }
 }
 
 template <int DK, int DVL>
@@ -257,25 +323,6 @@ __global__ void decode_combine_kernel(const float* __restrict__ part_o,
   }
 }
 
-// o[b][i][d] = sum_c Wuv[g dv + d][c] lat[b][i][c]
-__global__ void uv_proj_kernel(const float* __restrict__ lat, const bf16_t* __restrict__ Wuv,
-                               bf16_t* __restrict__ o, int H, int dv, int rkv, int hpg) {
-  const int b = blockIdx.y, i = blockIdx.x;
-  const float* lr = lat + ((int64_t)b * H + i) * rkv;
-  for (int d = threadIdx.x; d < dv; d += blockDim.x) {
-    const bf16_t* w = Wuv + ((int64_t)(i / hpg) * dv + d) * rkv;
-    float v = 0.f;
-    for (int c = 0; c < rkv; c += 8) {
-      const u32x4 ww = *(const u32x4*)(w + c);
-#pragma unroll
-      for (int k = 0; k < 4; ++k)
-        v += lr[c + 2 * k] * __uint_as_float(ww[k] << 16) +
-             lr[c + 2 * k + 1] * __uint_as_float(ww[k] & 0xffff0000u);
-    }
-    o[((int64_t)b * H + i) * dv + d] = f2bf(v);
-  }
-}
-
 #define MLA_DECODE_SHAPES(X) X(576, 512) X(288, 256) X(160, 128)
 
 int decode_chunk(int Lmax, int B) {
@@ -321,8 +368,17 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
 
   prof_begin(KC_ELEM, s);
   const int64_t nq = (int64_t)d.B * HP * DK;
-  absorb_query_kernel<<<(unsigned)((nq + 255) / 256), 256, 0, s>>>(
-      (const bf16_t*)d.q, (const bf16_t*)d.Wuk, qabs, d.B, d.H, HP, d.dn, d.dr, d.rkv, d.hpg);
+  const int G = d.H / d.hpg;
+  const int grow = (d.B * d.hpg + 31) / 32;
+  // latent part: q_abs[b][i][:rkv] = q^nope[b][i] W_UK[g]
+  group_gemm_kernel<bf16_t, false><<<dim3((d.rkv + 31) / 32, grow, G), 256, 0, s>>>(
+      (const bf16_t*)d.q, d.dn + d.dr, (const bf16_t*)d.Wuk, qabs, DK, HP, d.B, d.H, d.hpg, d.dn,
+      d.rkv);
+  {
+    const int64_t nrest = (int64_t)d.B * d.H * d.dr + (int64_t)d.B * (HP - d.H) * DK;
+    absorb_rest_kernel<<<(unsigned)((nrest + 255) / 256), 256, 0, s>>>(
+        (const bf16_t*)d.q, qabs, d.B, d.H, HP, d.dn, d.dr, d.rkv);
+  }
   prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dn * d.rkv, (double)nq * 2);
 
   DecodeDev a;
@@ -342,8 +398,9 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
            (double)d.B * d.Lmax * DK * 2);
   prof_begin(KC_ELEM, s);
   decode_combine_kernel<<<dim3(d.H, d.B), 256, 0, s>>>(part_o, part_ml, lat, d.H, HP, nsplit, DVL);
-  uv_proj_kernel<<<dim3(d.H, d.B), 128, 0, s>>>(lat, (const bf16_t*)d.Wuv, (bf16_t*)d.o, d.H,
-                                                 d.dv, d.rkv, d.hpg);
+  // o[b][i] = W_UV[g] lat[b][i]
+  group_gemm_kernel<float, true><<<dim3((d.dv + 31) / 32, grow, G), 256, 0, s>>>(
+      lat, d.rkv, (const bf16_t*)d.Wuv, (bf16_t*)d.o, d.dv, d.H, d.B, d.H, d.hpg, d.rkv, d.dv);
   prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dv * d.rkv, (double)d.B * d.H * (d.dv * 2 + DVL * 4));
   return hipGetLastError();
 }
