@@ -23,7 +23,7 @@
 //   tile's latent columns read with the transposing LDS read.  Partial (max, sum,
 //   unnormalised output) per split.
 // * decode_combine_kernel: merges the splits of a (sequence, head) in split order.
-// * group_gemm_kernel: o = W_UV[g] (latent), one product per KV group.
+// * uv_proj_kernel: o = W_UV[g] (latent), one thread per output.
 #include "attn_common.h"
 #include "kernels.h"
 #include "mfma.h"
@@ -48,14 +48,13 @@ struct DecodeDev {
   float* part_ml;       // [B][nsplit][HP][2]
 };
 
-// The per-group products of decoding, C[r][n] = sum_k A[r][k] W(k, n) for the H / G_kv
-// heads of group g = blockIdx.z and sequences b: row r = (b, j) is head i = g hpg + j of
-// sequence b (A row at A + (b H + i) lda, C row at C + (b HC + i) ldc).  W(k, n) is
-// Wg[k][n] (WT = false: W_UK[g] = Wuk[g K + k][n]) or Wg[n][k] (WT = true: W_UV[g] =
-// Wuv[g N + n][k]).  32 x 32 output tiles (enough workgroups for these small products), K
+// The query absorption as one product per KV group, C[r][n] = sum_k A[r][k] W_g[k][n] for
+// the H / G_kv heads of group g = blockIdx.z and sequences b: row r = (b, j) is head
+// i = g hpg + j of sequence b (A row at A + (b H + i) lda, C row at C + (b HC + i) ldc),
+// W_g = W + g K N (W_UK[g] = Wuk[g K + k][n]).  32 x 32 output tiles (enough workgroups for these small products), K
 // in chunks of 32 staged in LDS as fp32; each of the 256 threads owns 2 x 2 outputs.  fp32
 // accumulation in k order, bf16 output.
-template <typename TA, bool WT>
+template <typename TA>
 __global__ __launch_bounds__(256) void group_gemm_kernel(const TA* __restrict__ A, int64_t lda,
                                                          const bf16_t* __restrict__ W,
                                                          bf16_t* __restrict__ C, int64_t ldc,
@@ -70,7 +69,7 @@ __global__ __launch_bounds__(256) void group_gemm_kernel(const TA* __restrict__ 
   const bf16_t* Wg = W + (int64_t)g * K * N;
   float acc[2][2] = {};
   for (int k0 = 0; k0 < K; k0 += TK) {
-    // A tile: 64 rows x 32 k, transposed into As[k][r]
+    // A tile: 32 rows x 32 k, transposed into As[k][r]
     for (int e = tid; e < TR * TK; e += 256) {
       const int r = e / TK, k = e % TK, rr = r0 + r, kk = k0 + k;
       float v = 0.f;
@@ -80,14 +79,10 @@ __global__ __launch_bounds__(256) void group_gemm_kernel(const TA* __restrict__ 
       }
       As[k][r] = v;
     }
-    // W tile: 32 k x 64 n
+    // W tile: 32 k x 32 n
     for (int e = tid; e < TK * TN; e += 256) {
-      int k, n;
-      if (WT) { n = e / TK; k = e % TK; } else { k = e / TN; n = e % TN; }
-      const int kk = k0 + k, nn = n0 + n;
-      float v = 0.f;
-      if (kk < K && nn < N) v = bf2f(WT ? Wg[(int64_t)nn * K + kk] : Wg[(int64_t)kk * N + nn]);
-      Ws[k][n] = v;
+      const int k = e / TN, n = e % TN, kk = k0 + k, nn = n0 + n;
+      Ws[k][n] = kk < K && nn < N ? bf2f(Wg[(int64_t)kk * N + nn]) : 0.f;
     }
     __syncthreads();
 #pragma unroll 8
@@ -323,6 +318,26 @@ __global__ void decode_combine_kernel(const float* __restrict__ part_o,
   }
 }
 
+// o[b][i][d] = sum_c Wuv[g dv + d][c] lat[b][i][c]: one workgroup per (head, sequence), one
+// thread per output (a W_UV row each, read in 16-byte pieces; the latent row is shared)
+__global__ void uv_proj_kernel(const float* __restrict__ lat, const bf16_t* __restrict__ Wuv,
+                               bf16_t* __restrict__ o, int H, int dv, int rkv, int hpg) {
+  const int b = blockIdx.y, i = blockIdx.x;
+  const float* lr = lat + ((int64_t)b * H + i) * rkv;
+  for (int d = threadIdx.x; d < dv; d += blockDim.x) {
+    const bf16_t* w = Wuv + ((int64_t)(i / hpg) * dv + d) * rkv;
+    float v = 0.f;
+    for (int c = 0; c < rkv; c += 8) {
+      const u32x4 ww = *(const u32x4*)(w + c);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        v += lr[c + 2 * k] * __uint_as_float(ww[k] << 16) +
+             lr[c + 2 * k + 1] * __uint_as_float(ww[k] & 0xffff0000u);
+    }
+    o[((int64_t)b * H + i) * dv + d] = f2bf(v);
+  }
+}
+
 #define MLA_DECODE_SHAPES(X) X(576, 512) X(288, 256) X(160, 128)
 
 int decode_chunk(int Lmax, int B) {
@@ -371,7 +386,7 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
   const int G = d.H / d.hpg;
   const int grow = (d.B * d.hpg + 31) / 32;
   // latent part: q_abs[b][i][:rkv] = q^nope[b][i] W_UK[g]
-  group_gemm_kernel<bf16_t, false><<<dim3((d.rkv + 31) / 32, grow, G), 256, 0, s>>>(
+  group_gemm_kernel<bf16_t><<<dim3((d.rkv + 31) / 32, grow, G), 256, 0, s>>>(
       (const bf16_t*)d.q, d.dn + d.dr, (const bf16_t*)d.Wuk, qabs, DK, HP, d.B, d.H, d.hpg, d.dn,
       d.rkv);
   {
@@ -398,9 +413,8 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
            (double)d.B * d.Lmax * DK * 2);
   prof_begin(KC_ELEM, s);
   decode_combine_kernel<<<dim3(d.H, d.B), 256, 0, s>>>(part_o, part_ml, lat, d.H, HP, nsplit, DVL);
-  // o[b][i] = W_UV[g] lat[b][i]
-  group_gemm_kernel<float, true><<<dim3((d.dv + 31) / 32, grow, G), 256, 0, s>>>(
-      lat, d.rkv, (const bf16_t*)d.Wuv, (bf16_t*)d.o, d.dv, d.H, d.B, d.H, d.hpg, d.rkv, d.dv);
+  uv_proj_kernel<<<dim3(d.H, d.B), 128, 0, s>>>(lat, (const bf16_t*)d.Wuv, (bf16_t*)d.o, d.H,
+                                                 d.dv, d.rkv, d.hpg);
   prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dv * d.rkv, (double)d.B * d.H * (d.dv * 2 + DVL * 4));
   return hipGetLastError();
 }
