@@ -258,8 +258,11 @@ static int teacher_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h
   HIP_TRY(gemm(mk(N, H * dk, D, h, D, true, w->Wq, D, true, qkv, ld_qkv, d.t, d.t), nullptr, 0, s));
   HIP_TRY(gemm(mk(N, G * dk, D, h, D, true, w->Wk, D, true, qkv + (size_t)H * dk * ts, ld_qkv, d.t, d.t), nullptr, 0, s));
   HIP_TRY(gemm(mk(N, G * dk, D, h, D, true, w->Wv, D, true, qkv + (size_t)(H + G) * dk * ts, ld_qkv, d.t, d.t), nullptr, 0, s));
-  // R_t on queries and keys (Sec. 3.1)
-  HIP_TRY(rope_apply(qkv, d.t, N, (int)d.T, H, ld_qkv, dk, 0, dk / 2, H, cs, sn, s));
+  // R_t on queries and keys (Sec. 3.1); on the matrix-core path the attention kernel rotates
+  // the queries as it loads them (the teacher's rotated queries are not needed elsewhere)
+  const bool q_on_load = d.t == DT_BF16 && attn_mfma_supported(dk, dk) && dk % 32 == 0;
+  if (!q_on_load)
+    HIP_TRY(rope_apply(qkv, d.t, N, (int)d.T, H, ld_qkv, dk, 0, dk / 2, H, cs, sn, s));
   HIP_TRY(rope_apply(qkv + (size_t)H * dk * ts, d.t, N, (int)d.T, G, ld_qkv, dk, 0, dk / 2, G, cs, sn, s));
   // Eq. 2-4: causal softmax attention, head i reads KV group i / (H/G)
   Attn a;
@@ -269,6 +272,9 @@ static int teacher_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h
   a.Kb = HeadView{nullptr, 0, 0, 1};
   a.V = HeadView{qkv + (size_t)(H + G) * dk * ts, ld_qkv, dk, H / G};
   a.O = o; a.o_tok = (int64_t)H * dk; a.lse = nullptr; a.scale = cfg->softmax_scale; a.t = d.t;
+  if (q_on_load) {
+    a.q_cos = cs; a.q_sin = sn; a.q_roff = 0; a.q_np = dk / 2;
+  }
   HIP_TRY(attn_fwd(a, s));
   // the fixed output projection: A = concat_i o_i W_O^T
   if (A_t)

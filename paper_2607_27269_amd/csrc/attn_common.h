@@ -35,6 +35,7 @@ struct AttnDev {
   bf16_t* O; int64_t o_tok;
   float* lse;
   const bf16_t* Oref; bf16_t* Odiff;  // optional: Odiff = O - Oref (rounded O), layout of O
+  const float* qcos; const float* qsin; int qroff, qnp;  // optional: Q rotated on load
   int nqb;
 };
 
@@ -48,6 +49,7 @@ inline AttnDev to_dev(const Attn& a) {
   d.V = (const bf16_t*)a.V.p; d.v_tok = a.V.tok; d.v_head = (int)a.V.head; d.v_div = a.V.div;
   d.O = (bf16_t*)a.O; d.o_tok = a.o_tok; d.lse = a.lse;
   d.Oref = (const bf16_t*)a.o_ref; d.Odiff = (bf16_t*)a.o_diff;
+  d.qcos = a.q_cos; d.qsin = a.q_sin; d.qroff = a.q_roff; d.qnp = a.q_np;
   d.nqb = 0;
   return d;
 }

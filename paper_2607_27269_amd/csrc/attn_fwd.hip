@@ -65,6 +65,37 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
     const bf16_t* qp = a.Q + nq * a.q_tok + (int64_t)i * a.q_head + 8 * half;
 #pragma unroll
     for (int kk = 0; kk < NKK; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
+    // optional R_t on the whole query (rotate-half pairs (p, p + DQK / 2)): the lane holds
+    // both dims of each pair (fragments kk and kk + NKK / 2; compile-time indices keep the
+    // fragments in registers)
+    if (a.qcos) {  // uniform
+      const int t = min(my_q, a.T - 1);
+      constexpr int kn = NKK / 2;
+#pragma unroll
+      for (int kk = 0; kk < kn; ++kk) {
+        const int p = 16 * kk + 8 * half;
+        const float* cp = a.qcos + (int64_t)t * a.qnp + p;
+        const float* sp = a.qsin + (int64_t)t * a.qnp + p;
+        const f32x4 c0 = *(const f32x4*)cp, c1 = *(const f32x4*)(cp + 4);
+        const f32x4 s0 = *(const f32x4*)sp, s1 = *(const f32x4*)(sp + 4);
+        const u32x4 w1 = __builtin_bit_cast(u32x4, qf[kk]);
+        const u32x4 w2 = __builtin_bit_cast(u32x4, qf[kk + kn]);
+        u32x4 o1, o2;
+#pragma unroll
+        for (int e2 = 0; e2 < 4; ++e2) {
+          const float ca = e2 < 2 ? c0[2 * e2] : c1[2 * e2 - 4];
+          const float cb = e2 < 2 ? c0[2 * e2 + 1] : c1[2 * e2 - 3];
+          const float sa = e2 < 2 ? s0[2 * e2] : s1[2 * e2 - 4];
+          const float sb = e2 < 2 ? s0[2 * e2 + 1] : s1[2 * e2 - 3];
+          const float x1a = __uint_as_float(w1[e2] << 16), x1b = __uint_as_float(w1[e2] & 0xffff0000u);
+          const float x2a = __uint_as_float(w2[e2] << 16), x2b = __uint_as_float(w2[e2] & 0xffff0000u);
+          o1[e2] = pack2bf(x1a * ca - x2a * sa, x1b * cb - x2b * sb);
+          o2[e2] = pack2bf(x1a * sa + x2a * ca, x1b * sb + x2b * cb);
+        }
+        qf[kk] = __builtin_bit_cast(bf16x8, o1);
+        qf[kk + kn] = __builtin_bit_cast(bf16x8, o2);
+      }
+    }
   }
 
   f32x16 acc_o[NC];

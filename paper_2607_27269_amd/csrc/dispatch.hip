@@ -47,6 +47,9 @@ hipError_t attn_fwd(const Attn& a, hipStream_t s) {
   double bytes = N * a.H * (a.dqk + a.dv) * dsize(a.t) + N * a.H * (a.lse ? 4.0 : 0.0);
   if (a.o_diff) bytes += 2.0 * N * a.H * a.dv * dsize(a.t);
   const bool mfma = a.t == DT_BF16 && attn_mfma_supported(a.dqk, a.dv);
+  // the query rotation on load exists on the matrix-core path only
+  if (a.q_cos && (!mfma || a.q_roff != 0 || 2 * a.q_np != a.dqk || a.dqk % 32))
+    return hipErrorInvalidValue;
   prof_begin(KC_ATTN_FWD, s);
   hipError_t e = mfma ? attn_fwd_mfma(a, s) : attn_fwd_simt(a, s);
   prof_end(KC_ATTN_FWD, s, flops, bytes);

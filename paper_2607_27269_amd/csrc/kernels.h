@@ -61,6 +61,12 @@ struct Attn {
   // rounded O
   const void* o_ref = nullptr;
   void* o_diff = nullptr;
+  // forward only, optional (bf16 matrix-core path): Q is rotated on load as a whole, pairs
+  // (p, p + q_np) with q_np = dqk / 2 and fp32 tables [T][q_np] (R_t of the rotate-half
+  // convention); q_roff must be 0
+  const float* q_cos = nullptr;
+  const float* q_sin = nullptr;
+  int q_roff = 0, q_np = 0;
 };
 hipError_t attn_fwd(const Attn& a, hipStream_t s);
 
