@@ -307,10 +307,42 @@ __global__ __launch_bounds__(64) void attn_dkv_simt_kernel(AttnBwd w) {
   }
 }
 
+// bf16 rows of 8-element multiples: each of a row's 16 lanes loads 16-byte pieces (eight
+// consecutive elements) of dO and O, so a row of 128 takes one load per tensor per lane
+__global__ void attn_delta_bf16x8_kernel(const bf16_t* __restrict__ dO, const bf16_t* __restrict__ O,
+                                         int64_t o_tok, int64_t N, int H, int dv,
+                                         float* __restrict__ delta) {
+  const int64_t row = (int64_t)blockIdx.x * (blockDim.x / 16) + threadIdx.x / 16;
+  const int sub = threadIdx.x % 16;
+  const bool ok = row < N * H;
+  const int64_t n = ok ? row / H : 0;
+  const int i = ok ? (int)(row % H) : 0;
+  const bf16_t* g = dO + n * (int64_t)H * dv + (int64_t)i * dv;
+  const bf16_t* o = O + n * o_tok + (int64_t)i * dv;
+  float s = 0.f;
+  if (ok)
+    for (int d = 8 * sub; d < dv; d += 128) {
+      const u32x4 a = *(const u32x4*)(g + d), b = *(const u32x4*)(o + d);
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        s += __uint_as_float(a[k] << 16) * __uint_as_float(b[k] << 16) +
+             __uint_as_float(a[k] & 0xffff0000u) * __uint_as_float(b[k] & 0xffff0000u);
+    }
+#pragma unroll
+  for (int off = 8; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+  if (ok && sub == 0) delta[row] = s;
+}
+
 template <typename T>
 hipError_t delta_launch(const AttnBwd& w, hipStream_t s) {
   const Attn& a = w.f;
   int64_t rows = (int64_t)a.B * a.T * a.H;
+  if (a.t == DT_BF16 && a.dv % 8 == 0 && a.o_tok % 8 == 0 && (uintptr_t)w.dO % 16 == 0 &&
+      (uintptr_t)a.O % 16 == 0) {
+    attn_delta_bf16x8_kernel<<<(unsigned)((rows + 15) / 16), 256, 0, s>>>(
+        (const bf16_t*)w.dO, (const bf16_t*)a.O, a.o_tok, (int64_t)a.B * a.T, a.H, a.dv, w.delta);
+    return hipGetLastError();
+  }
   attn_delta_kernel<T><<<(unsigned)((rows + 15) / 16), 256, 0, s>>>(w.dO, a.O, a.o_tok,
                                                                   (int64_t)a.B * a.T, a.H, a.dv,
                                                                   w.delta);
