@@ -474,6 +474,19 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits,
   store_out<TC>(c, v);
 }
 
+// the same, four consecutive outputs per thread (N and ldc multiples of 4)
+template <typename TC>
+__global__ void splitk_reduce4_kernel(const float* __restrict__ part, int splits, int M, int N,
+                                      TC* __restrict__ C, int64_t ldc, float alpha, float beta) {
+  const int64_t idx = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
+  const int64_t total = (int64_t)M * N;
+  if (idx >= total) return;
+  const int m = (int)(idx / N), n = (int)(idx % N);
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+  for (int z = 0; z < splits; ++z) acc += *(const f32x4*)(part + (int64_t)z * total + idx);
+  store4<TC>(C + (int64_t)m * ldc + n, acc, alpha, beta);
+}
+
 // Tile shape and split-K factor.  Candidates: 256 x 256 and 256 x 192 tiles on 8
 // wavefronts (one workgroup per CU) and 128 x 128 tiles on 4 (two per CU).  Workgroups run
 // in rounds of one per CU slot, so a grid of 1.5 rounds costs two: the plan minimises
@@ -566,6 +579,16 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   if (e != hipSuccess || p.splits == 1) return e;
   int64_t total = (int64_t)g.M * g.N;
   unsigned grid = (unsigned)((total + 255) / 256);
+  if (g.N % 4 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.C % (f32 ? 16 : 8) == 0) {
+    const unsigned grid4 = (unsigned)((total / 4 + 255) / 256);
+    if (f32)
+      splitk_reduce4_kernel<float><<<grid4, 256, 0, s>>>(scratch, p.splits, g.M, g.N,
+                                                         (float*)g.C, g.ldc, g.alpha, g.beta);
+    else
+      splitk_reduce4_kernel<bf16_t><<<grid4, 256, 0, s>>>(scratch, p.splits, g.M, g.N,
+                                                          (bf16_t*)g.C, g.ldc, g.alpha, g.beta);
+    return hipGetLastError();
+  }
   if (f32)
     splitk_reduce_kernel<float><<<grid, 256, 0, s>>>(scratch, p.splits, g.M, g.N, (float*)g.C,
                                                      g.ldc, g.alpha, g.beta);
