@@ -72,3 +72,46 @@ def test_decode_parity(idx, T, lengths):
         e2 = np.linalg.norm(got[b] - naive[b]) / np.linalg.norm(naive[b])
         print(f"[decode] seq {b} len {n}: vs absorbed {e1:.2e}, vs naive {e2:.2e}", flush=True)
         assert e1 <= 1e-2 and e2 <= 2e-2
+
+
+def test_decode_fullsize_sampled():
+    """The benchmark's decoding shape (64 sequences over caches of 4096 latent rows, the
+    llama-3-8b-layer student widths): the split-K chunks span 1024 rows (32 key tiles per
+    workgroup), some lengths end inside a tile or leave whole chunks empty.  Every output
+    is finite; eight sequences are checked against the absorbed-form oracle."""
+    import torch
+    import oracle as O
+    from paper_2607_27269_amd import _lib as L
+    B, T = 64, 4096
+    cfg = configs.get(3).replace(batch=B, seq=T)
+    H, dn, dr, rkv, dv = cfg.n_heads, cfg.nope_dim, cfg.rope_dim, cfg.kv_rank, cfg.head_dim
+    G = cfg.s_kv_groups
+    rng = np.random.default_rng(20261202)
+    lengths = [T] * B
+    lengths[3], lengths[17], lengths[40], lengths[63] = T - 1, 1000, 1, 2049
+    print(f"[decode] full size B={B} T={T} lengths[3,17,40,63]={[lengths[i] for i in (3, 17, 40, 63)]}",
+          flush=True)
+    q = _bf16(rng.standard_normal((B, H, dn + dr)) * 0.5)
+    kv = _bf16(rng.standard_normal((B, T, rkv + dr)))
+    wuk = _bf16(rng.standard_normal((G * dn, rkv)) / np.sqrt(dn))
+    wuv = _bf16(rng.standard_normal((G * dv, rkv)) / np.sqrt(rkv))
+    c = L.make_cfg(cfg)
+    wsb = L.mla_recon_decode_workspace_size(c, T)
+    assert wsb > 0, L.last_error()
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    tq, tkv, tuk, tuv = _upload(q), _upload(kv), _upload(wuk), _upload(wuv)
+    tlen = torch.tensor(lengths, dtype=torch.int32, device="cuda")
+    to = torch.full((B, H, dv), float("nan"), dtype=torch.bfloat16, device="cuda")
+    L.mla_recon_decode(c, tq.data_ptr(), tkv.data_ptr(), T, tlen.data_ptr(), tuk.data_ptr(),
+                       tuv.data_ptr(), to.data_ptr(), ws.data_ptr(), wsb,
+                       torch.cuda.current_stream().cuda_stream)
+    got = to.double().cpu().numpy()
+    assert np.all(np.isfinite(got))
+    sample = [0, 3, 17, 30, 40, 51, 62, 63]
+    ref = O.absorbed_decode(q[sample], kv[sample], [lengths[b] for b in sample], wuk, wuv,
+                            n_heads=H, s_kv_groups=G, s_rope_groups=1, nope_dim=dn, rope_dim=dr,
+                            scale=cfg.softmax_scale)
+    for j, b in enumerate(sample):
+        e = np.linalg.norm(got[b] - ref[j]) / np.linalg.norm(ref[j])
+        print(f"[decode] full size seq {b} len {lengths[b]}: vs absorbed {e:.2e}", flush=True)
+        assert e <= 1e-2
