@@ -133,17 +133,29 @@ struct Loader<true, ROWS, NTHR, BK> {
   }
 };
 
-// m-major tile (global [k][row]): BK x ROWS, chunk c -> k-row c / (ROWS/8), row-chunk c % (ROWS/8)
+// m-major tile (global [k][row]): BK x ROWS, chunk c -> k-row c / (ROWS/8), row-chunk c % (ROWS/8).
+// Rows of a multiple of 128 elements are unpadded and XOR-swizzled: 16-byte chunk c of
+// k-row k sits at position c ^ (4 (k mod 4)), i.e. the aligned groups of four chunks (64
+// bytes) trade places, so that the 4 k-rows x 64 bytes one transposing read covers per
+// half-wavefront fall on 4 distinct 16-bank groups.  Other widths keep padded rows.
 template <int ROWS, int NTHR, int BK>
 struct Loader<false, ROWS, NTHR, BK> {
-  static constexpr int LD = mm_ld(ROWS);
+  static constexpr bool SWZ = ROWS % 128 == 0;
+  static constexpr int LD = SWZ ? ROWS : mm_ld(ROWS);
   static constexpr int CPR = ROWS / 8;
   static constexpr int CHUNKS = BK * CPR;
   static constexpr int PER = CHUNKS / NTHR;
   using Dma = DmaTile<BK, ROWS, LD, NTHR / 64, true>;
   static constexpr int ELEMS = Dma::ALLOC;  // whole 1 KB blocks, a multiple per wavefront
   static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
-  static __device__ __forceinline__ void swizzle(Dma&) {}
+  static __device__ __forceinline__ int pos(int k, int c) { return SWZ ? c ^ (4 * (k & 3)) : c; }
+  // the copy that fills LDS position (k, p) fetches chunk pos(k, p) (an involution)
+  static __device__ __forceinline__ void swizzle(Dma& t) {
+    if constexpr (SWZ) {
+#pragma unroll
+      for (int p = 0; p < Dma::PER; ++p) t.col[p] = (short)(8 * pos(t.row[p], t.col[p] / 8));
+    }
+  }
   u32x4 r[PER];
   __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
                                        int rows_valid, int k0, int kend) {
@@ -161,16 +173,26 @@ struct Loader<false, ROWS, NTHR, BK> {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       const int c = threadIdx.x + i * NTHR;
-      *(u32x4*)(lds + (c / CPR) * LD + (c % CPR) * 8) = r[i];
+      const int kr = c / CPR;
+      *(u32x4*)(lds + kr * LD + pos(kr, c % CPR) * 8) = r[i];
     }
   }
   __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
     t.issue_s(lds, p + (int64_t)k0 * ld + row0, [&](int r, int c) { return r * (int)ld + c; });
   }
+  // operand fragment through the transposing read (lds_operand_tr's lane pattern: k-rows
+  // klo + lane%16/4 and klo + 4 + lane%16/4, columns row0 + 16 ((lane/16) % 2) + 4 (lane % 4));
+  // klo is a multiple of 4, so the swizzle's k mod 4 is the lane's lane%16/4
   static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
-    const int klo = 16 * kk + 8 * ((threadIdx.x & 63) >> 5);
-    return lds_operand_tr(lds, LD, row0, klo, klo + 4);
+    const int lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
+    const int klo = 16 * kk + 8 * (lane >> 5), kq = r >> 2;
+    const int m = row0 + 16 * (g & 1) + 4 * (r & 3);
+    const int mc = SWZ ? pos(kq, m >> 3) * 8 + (m & 7) : m;
+    const u32x2 lo = lds_read_tr4(lds + (klo + kq) * LD + mc);
+    const u32x2 hi = lds_read_tr4(lds + (klo + 4 + kq) * LD + mc);
+    const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+    return __builtin_bit_cast(bf16x8, w);
   }
 };
 
