@@ -134,13 +134,16 @@ struct Loader<true, ROWS, NTHR, BK> {
 };
 
 // m-major tile (global [k][row]): BK x ROWS, chunk c -> k-row c / (ROWS/8), row-chunk c % (ROWS/8).
-// Rows of a multiple of 128 elements are unpadded and XOR-swizzled: 16-byte chunk c of
-// k-row k sits at position c ^ (4 (k mod 4)), i.e. the aligned groups of four chunks (64
-// bytes) trade places, so that the 4 k-rows x 64 bytes one transposing read covers per
-// half-wavefront fall on 4 distinct 16-bank groups.  Other widths keep padded rows.
+// Rows of a multiple of 64 elements are unpadded and XOR-swizzled in aligned groups of four
+// 16-byte chunks (64 bytes, 16 banks), so that the 4 k-rows x 64 bytes one transposing read
+// covers per half-wavefront fall on 4 distinct 16-bank groups: with rows a multiple of
+// 256 bytes long every row starts on the same bank, and group G of k-row k sits at
+// G ^ (k mod 4); with rows an odd multiple of 128 bytes, odd rows start half a bank
+// window (two groups) later, and group G sits at G ^ ((k / 2) mod 2).  Other widths keep padded rows.
 template <int ROWS, int NTHR, int BK>
 struct Loader<false, ROWS, NTHR, BK> {
-  static constexpr bool SWZ = ROWS % 128 == 0;
+  static constexpr bool SWZ = ROWS % 64 == 0;
+  static constexpr bool SWZ4 = ROWS % 128 == 0;  // else rows are an odd multiple of 128 B
   static constexpr int LD = SWZ ? ROWS : mm_ld(ROWS);
   static constexpr int CPR = ROWS / 8;
   static constexpr int CHUNKS = BK * CPR;
@@ -148,7 +151,9 @@ struct Loader<false, ROWS, NTHR, BK> {
   using Dma = DmaTile<BK, ROWS, LD, NTHR / 64, true>;
   static constexpr int ELEMS = Dma::ALLOC;  // whole 1 KB blocks, a multiple per wavefront
   static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
-  static __device__ __forceinline__ int pos(int k, int c) { return SWZ ? c ^ (4 * (k & 3)) : c; }
+  static __device__ __forceinline__ int pos(int k, int c) {
+    return !SWZ ? c : SWZ4 ? c ^ (4 * (k & 3)) : c ^ (4 * ((k >> 1) & 1));
+  }
   // the copy that fills LDS position (k, p) fetches chunk pos(k, p) (an involution)
   static __device__ __forceinline__ void swizzle(Dma& t) {
     if constexpr (SWZ) {
