@@ -75,6 +75,40 @@ __global__ void rope_apply_kernel(T* __restrict__ x, int N, int Tseq, int nheads
   Vec4<T>::store(base + p + np, x1 * sn + x2 * c);
 }
 
+// the same for bf16 with 8 consecutive pairs per thread (16-byte loads and stores)
+__global__ void rope_apply8_kernel(bf16_t* __restrict__ x, int N, int Tseq, int nheads, int64_t tok,
+                                   int64_t head, int off, int np, int div,
+                                   const float* __restrict__ cos_t,
+                                   const float* __restrict__ sin_t, float sgn) {
+  const int nq = np / 8;
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= (int64_t)N * nheads * nq) return;
+  const int p = (int)(idx % nq) * 8;
+  const int h = (int)((idx / nq) % nheads);
+  const int64_t n = idx / ((int64_t)nq * nheads);
+  const int t = (int)(n % Tseq), g = h / div;
+  const float* cp = cos_t + ((int64_t)g * Tseq + t) * np + p;
+  const float* sp = sin_t + ((int64_t)g * Tseq + t) * np + p;
+  bf16_t* base = x + n * tok + (int64_t)h * head + off;
+  const u32x4 a = *(const u32x4*)(base + p), b = *(const u32x4*)(base + p + np);
+  u32x4 oa, ob;
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const f32x4 c = *(const f32x4*)(cp + 4 * q), sn = *(const f32x4*)(sp + 4 * q) * sgn;
+    const f32x4 x1 = {__uint_as_float(a[2 * q] << 16), __uint_as_float(a[2 * q] & 0xffff0000u),
+                      __uint_as_float(a[2 * q + 1] << 16), __uint_as_float(a[2 * q + 1] & 0xffff0000u)};
+    const f32x4 x2 = {__uint_as_float(b[2 * q] << 16), __uint_as_float(b[2 * q] & 0xffff0000u),
+                      __uint_as_float(b[2 * q + 1] << 16), __uint_as_float(b[2 * q + 1] & 0xffff0000u)};
+    const f32x4 r1 = x1 * c - x2 * sn, r2 = x1 * sn + x2 * c;
+    oa[2 * q] = pack2bf(r1[0], r1[1]);
+    oa[2 * q + 1] = pack2bf(r1[2], r1[3]);
+    ob[2 * q] = pack2bf(r2[0], r2[1]);
+    ob[2 * q + 1] = pack2bf(r2[2], r2[3]);
+  }
+  *(u32x4*)(base + p) = oa;
+  *(u32x4*)(base + p + np) = ob;
+}
+
 hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, int64_t head,
                       int off, int npairs, int div, const float* cos_t, const float* sin_t,
                       hipStream_t s, bool inverse) {
@@ -83,7 +117,12 @@ hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, i
   if (total == 0) return hipSuccess;
   unsigned grid = (unsigned)((total + 255) / 256);
   prof_begin(KC_ELEM, s);
-  if (t == DT_BF16)
+  if (t == DT_BF16 && npairs % 8 == 0 && tok % 8 == 0 && head % 8 == 0 && off % 8 == 0 &&
+      (uintptr_t)x % 16 == 0) {
+    const int64_t total8 = (int64_t)N * nheads * (npairs / 8);
+    rope_apply8_kernel<<<(unsigned)((total8 + 255) / 256), 256, 0, s>>>(
+        (bf16_t*)x, N, T, nheads, tok, head, off, npairs, div, cos_t, sin_t, sgn);
+  } else if (t == DT_BF16)
     rope_apply_kernel<bf16_t><<<grid, 256, 0, s>>>((bf16_t*)x, N, T, nheads, tok, head, off,
                                                    npairs, div, cos_t, sin_t, sgn);
   else
