@@ -58,9 +58,9 @@ def parse():
 # kernel-name patterns of each timing class: a kernel belongs to the class when every
 # substring of one of the alternatives occurs in its name
 CLASS_PATTERNS = {
-    "gemm_nt": [("gemm_mfma_kernel<", ", true, true,")],
-    "gemm_nn": [("gemm_mfma_kernel<", ", true, false,")],
-    "gemm_tn": [("gemm_mfma_kernel<", ", false, false,")],
+    "gemm_nt": [("gemm_mfma_kernel<", ", true, true,"), ("gemm_mfma_persist_kernel<", ", true, true,")],
+    "gemm_nn": [("gemm_mfma_kernel<", ", true, false,"), ("gemm_mfma_persist_kernel<", ", true, false,")],
+    "gemm_tn": [("gemm_mfma_kernel<", ", false, false,"), ("gemm_mfma_persist_kernel<", ", false, false,")],
     "attn_fwd": [("attn_fwd_mfma_kernel<",)],
     "attn_bwd_dkdv": [("attn_dv_mfma_kernel<",), ("attn_dkdv_mfma_kernel<",)],
     "attn_bwd_dq": [("attn_ds_gemm_kernel<", ", false, false,"), ("attn_dq_mfma_kernel<",)],

@@ -15,6 +15,8 @@
 // matrix cores work on the current one, and the first step of the next slice is read
 // right after the barrier that publishes it.  The epilogue stages each 32-row strip of a
 // wavefront's tile in LDS and writes it back with 16-byte (fp32) or 8-byte (bf16) stores.
+// Plain products run persistent: one workgroup per CU slot walks the tiles, and the next
+// tile's first slice is copied while the current one finishes and writes its epilogue.
 // The operand reads of a wavefront hit distinct banks: k-major rows are XOR-swizzled in
 // 16-byte chunks, m-major row strides are padded.  Large problems use 256 x 256 tiles on
 // 8 wavefronts (128 x 64 each), which halves the LDS bytes per MFMA compared with
@@ -51,6 +53,7 @@ struct GemmDev {
   const bf16_t* lref; int64_t ldref;
   float alpha, beta;
   int kchunk;         // K elements per split (multiple of BK)
+  int nsplit;         // split-K chunks (persistent launch)
   int ktotal;
   int mstore;         // rows of C written (M is the row count operand A may be read at)
   // batched causal mode (causal != 0): workgroup z of nbatch works on A + z sA,
@@ -474,6 +477,223 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   }
 }
 
+
+// Persistent variant (plain products: no causal batches, no loss epilogue): a grid of one
+// workgroup per CU slot walks the output tiles (x split-K chunks) in steps of the grid size,
+// in the same tile order as the one-tile-per-workgroup launch.  The ring of two LDS stages
+// runs on across tiles: the next tile's first slice is copied into the free stage while
+// the last slice of this tile feeds the matrix cores, and while the epilogue stages its
+// 16-row half strips in the stage the last slice occupied.
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST>
+__device__ __forceinline__ void gemm_persist(const GemmDev& g) {
+  static_assert(NST == 2, "the cross-tile copy assumes a two-stage ring");
+  constexpr int NTHR = 64 * WM * WN;
+  constexpr int TM = BM / WM / 32;
+  constexpr int TN = BN / WN / 32;
+  constexpr int KK = BK / 16;
+  using LA = Loader<AK, BM, NTHR, BK>;
+  using LB = Loader<BKM, BN, NTHR, BK>;
+  constexpr int STAGE = LA::ELEMS + LB::ELEMS;
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
+
+  const int ntm = (g.M + BM - 1) / BM, ntn = (g.N + BN - 1) / BN;
+  const int ntiles = ntm * ntn;
+  const int nitems = ntiles * g.nsplit;
+  int w = blockIdx.x;
+  if (w >= nitems) return;
+
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int wm = wave / WN, wn = wave % WN;
+  const int wrow0 = wm * (BM / WM), wcol0 = wn * (BN / WN);
+
+  LA la;
+  LB lb;
+  typename LA::Dma da;
+  typename LB::Dma db;
+  da.init();
+  db.init();
+  LA::swizzle(da);
+  LB::swizzle(db);
+
+  struct Item { int m0, n0, split, kbeg, kend, nk, nfull; };
+  auto item = [&](int it) {
+    Item t;
+    const int x = it % ntiles;
+    t.split = it / ntiles;
+    const int pid = xcd_remap(x, ntiles);
+    const int GROUP = 8;
+    const int group = pid / (GROUP * ntn);
+    const int first = group * GROUP;
+    const int gsz = min(ntm - first, GROUP);
+    const int tm = first + (pid % (GROUP * ntn)) % gsz;
+    const int tn = (pid % (GROUP * ntn)) / gsz;
+    t.m0 = tm * BM;
+    t.n0 = tn * BN;
+    t.kbeg = t.split * g.kchunk;
+    t.kend = min(g.ktotal, t.kbeg + g.kchunk);
+    t.nk = (t.kend - t.kbeg + BK - 1) / BK;
+    const bool dma_ok = g.M - t.m0 >= BM && g.N - t.n0 >= BN &&
+                        (AK ? (int64_t)BM * g.lda : (int64_t)BK * g.lda) < (1ll << 30) &&
+                        (BKM ? (int64_t)BN * g.ldb : (int64_t)BK * g.ldb) < (1ll << 30);
+    t.nfull = dma_ok ? (t.kend - t.kbeg) / BK : 0;
+    // uniform by construction: keep every field in scalar registers
+    t.m0 = __builtin_amdgcn_readfirstlane(t.m0);
+    t.n0 = __builtin_amdgcn_readfirstlane(t.n0);
+    t.split = __builtin_amdgcn_readfirstlane(t.split);
+    t.kbeg = __builtin_amdgcn_readfirstlane(t.kbeg);
+    t.kend = __builtin_amdgcn_readfirstlane(t.kend);
+    t.nk = __builtin_amdgcn_readfirstlane(t.nk);
+    t.nfull = __builtin_amdgcn_readfirstlane(t.nfull);
+    return t;
+  };
+  auto stage = [&](const Item& t, int ks, bf16_t* dst) {
+    const int k0 = t.kbeg + ks * BK;
+    if (ks < t.nfull) {
+      la.dma(da, g.A, g.lda, t.m0, g.M - t.m0, k0, dst);
+      lb.dma(db, g.B, g.ldb, t.n0, g.N - t.n0, k0, dst + LA::ELEMS);
+    } else {
+      la.load(g.A, g.lda, t.m0, g.M - t.m0, k0, t.kend);
+      lb.load(g.B, g.ldb, t.n0, g.N - t.n0, k0, t.kend);
+      la.store(dst);
+      lb.store(dst + LA::ELEMS);
+    }
+  };
+  bf16x8 af[2][TM], bfr[2][TN];
+  auto load_frags = [&](const bf16_t* As, int kk, bf16x8* a, bf16x8* b) {
+    const bf16_t* Bs = As + LA::ELEMS;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) a[i] = LA::frag(As, wrow0 + i * 32, kk);
+#pragma unroll
+    for (int j = 0; j < TN; ++j) b[j] = LB::frag(Bs, wcol0 + j * 32, kk);
+  };
+  f32x16 acc[TM][TN];
+  auto mma = [&](const bf16x8* a, const bf16x8* b) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  };
+
+  constexpr int WTN = BN / WN;
+  constexpr int SLD = WTN + 8;
+  static_assert(NTHR / 64 * 16 * SLD * 4 <= STAGE * 2, "epilogue half strip too large");
+  const bool vec = (g.ldc % 4) == 0;
+  TC* C = (TC*)g.C;
+
+  Item cur = item(w);
+  int rb = 0;          // stage of the current tile's first slice
+  bool issued = false; // the current tile's first slice is already in flight
+  for (;;) {
+    const int wnext = w + (int)gridDim.x;
+    const bool has_next = wnext < nitems;
+    Item nxt{};
+    if (has_next) nxt = item(wnext);
+    if (!issued) {
+      lds_barrier();  // every wavefront is past its previous epilogue
+      if (cur.nk > 0) stage(cur, 0, lds + rb * STAGE);
+    }
+    bool pre = false;  // the next tile's first slice was issued during this tile
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    // the first slice (and the previous epilogue's stores) complete; every wavefront is done
+    // with the previous epilogue's strips before the other stage is refilled
+    wait_vm<0>();
+    lds_barrier();
+    if (cur.nk > 0) load_frags(lds + rb * STAGE, 0, af[0], bfr[0]);
+    for (int kt = 0; kt < cur.nk; ++kt) {
+      const bf16_t* As = lds + ((rb + kt) & 1) * STAGE;
+      bf16_t* other = lds + ((rb + kt + 1) & 1) * STAGE;
+      const bool last = kt + 1 == cur.nk;
+      // the other stage is free: every wave passed the barrier after its last read
+      if (!last) {
+        stage(cur, kt + 1, other);
+      } else if (has_next && nxt.nk > 0) {
+        stage(nxt, 0, other);
+        pre = true;
+      }
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        if (kk + 1 < KK) {
+          load_frags(As, kk + 1, af[(kk + 1) & 1], bfr[(kk + 1) & 1]);
+        } else if (!last) {
+          wait_vm<0>();
+          lds_barrier();
+          load_frags(other, 0, af[0], bfr[0]);
+        } else {
+          // every wave is done reading this stage (the epilogue reuses it); the next
+          // tile's copies stay in flight
+          lds_barrier();
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mma(af[kk & 1], bfr[kk & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // epilogue in the stage of the last slice, 16 rows of a wavefront's strip at a time
+    const int es = cur.nk > 0 ? (rb + cur.nk - 1) & 1 : rb;
+    // the lane index made opaque here, so that the epilogue's per-lane addresses are formed
+    // per tile instead of being hoisted out of the tile loop (and held through the main loop)
+    int el = lane;
+    asm volatile("" : "+v"(el));
+    float* strip = (float*)(lds + es * STAGE) + wave * 16 * SLD;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int e = 8 * h; e < 8 * h + 8; ++e)
+            strip[(((e >> 2) & 1) * 8 + (el >> 5) * 4 + (e & 3)) * SLD + j * 32 + (el & 31)] =
+                acc[i][j][e];
+        constexpr int CPR = WTN / 4;
+#pragma unroll
+        for (int it = 0; it < 16 * CPR / 64; ++it) {
+          const int c = it * 64 + el;
+          const int r = c / CPR, col = (c % CPR) * 4;
+          const int m = cur.m0 + wrow0 + i * 32 + 16 * h + r, n = cur.n0 + wcol0 + col;
+          if (m >= g.mstore || n >= g.N) continue;
+          const f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+          if (g.part) {
+            float* p = g.part + ((int64_t)cur.split * g.M + m) * g.N + n;
+            if (n + 4 <= g.N && (g.N % 4) == 0) {
+              *(f32x4*)p = v;
+            } else {
+              for (int q = 0; q < 4 && n + q < g.N; ++q) p[q] = v[q];
+            }
+            continue;
+          }
+          TC* p = C + (int64_t)m * g.ldc + n;
+          if (vec && n + 4 <= g.N) {
+            store4<TC>(p, v, g.alpha, g.beta);
+          } else {
+            for (int q = 0; q < 4 && n + q < g.N; ++q) {
+              float x = g.alpha * v[q];
+              if (g.beta != 0.f) x += g.beta * ld(p + q);
+              store_out<TC>(p + q, x);
+            }
+          }
+        }
+      }
+    }
+    if (!has_next) break;
+    rb = (rb + cur.nk) & 1;
+    issued = pre;
+    cur = nxt;
+    w = wnext;
+  }
+}
+
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST>
+__global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_persist_kernel(GemmDev g) {
+  gemm_persist<BM, BN, WM, WN, AK, BKM, TC, BK, NST>(g);
+}
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST>
 __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
   gemm_tile<BM, BN, WM, WN, AK, BKM, TC, BK, NST>(g);
@@ -563,6 +783,20 @@ Plan plan_of(const Gemm& g, bool allow_split) {
 template <bool AK, bool BKM, typename TC>
 void launch(const GemmDev& d, const Plan& p, hipStream_t s) {
   const int tiles = ((d.M + p.bm - 1) / p.bm) * ((d.N + p.bn - 1) / p.bn);
+  const bool persist = d.lpart == nullptr;
+  if (persist) {
+    GemmDev e = d;
+    e.nsplit = p.splits;
+    const int per_cu = p.kind == 2 ? 2 : 1;
+    const int grid = std::min(tiles * p.splits, NUM_CU * per_cu);
+    if (p.kind == 0)
+      gemm_mfma_persist_kernel<256, 256, GWM, GWN, AK, BKM, TC, GBK, GNST><<<grid, 64 * GWM * GWN, 0, s>>>(e);
+    else if (p.kind == 1)
+      gemm_mfma_persist_kernel<256, 192, 4, 2, AK, BKM, TC, GBK, GNST><<<grid, 512, 0, s>>>(e);
+    else
+      gemm_mfma_persist_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(e);
+    return;
+  }
   dim3 grid(tiles, p.splits);
   if (p.kind == 0)
     gemm_mfma_kernel<256, 256, GWM, GWN, AK, BKM, TC, GBK, GNST><<<grid, 64 * GWM * GWN, 0, s>>>(d);
@@ -571,6 +805,7 @@ void launch(const GemmDev& d, const Plan& p, hipStream_t s) {
   else
     gemm_mfma_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(d);
 }
+
 
 }  // namespace
 
@@ -581,7 +816,7 @@ size_t gemm_mfma_scratch_elems(const Gemm& g) {
 
 hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s) {
   GemmDev d;
-  d.M = g.M; d.N = g.N; d.ktotal = g.K;
+  d.M = g.M; d.N = g.N; d.ktotal = g.K; d.nsplit = 1;
   d.A = (const bf16_t*)g.A; d.lda = g.lda;
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = g.beta;
@@ -634,7 +869,7 @@ hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t
                                 hipStream_t s) {
   if (g.beta != 0.f || g.alpha != 1.f || g.in_t != DT_BF16) return hipErrorInvalidValue;
   GemmDev d;
-  d.M = g.M; d.N = g.N; d.ktotal = g.K;
+  d.M = g.M; d.N = g.N; d.ktotal = g.K; d.nsplit = 1;
   d.A = (const bf16_t*)g.A; d.lda = g.lda;
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = 1.f; d.beta = 0.f;
@@ -687,7 +922,7 @@ hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s) {
                                                  : (!bt.rev && g.c_t == DT_BF16));
   if (!ok) return hipErrorInvalidValue;
   GemmDev d;
-  d.M = g.M; d.N = g.N; d.ktotal = g.K;
+  d.M = g.M; d.N = g.N; d.ktotal = g.K; d.nsplit = 1;
   d.A = (const bf16_t*)g.A; d.lda = g.lda;
   d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
   d.C = g.C; d.ldc = g.ldc; d.alpha = g.alpha; d.beta = 0.f;
