@@ -34,7 +34,7 @@ KCLASS_KERNELS = {"gemm_nt": "gemm_mfma_persist_kernel<..., true, true, ...> (an
                   "attn_fwd": "attn_fwd_mfma_kernel",
                   "attn_bwd_dkdv": "attn_dv_mfma_kernel (or attn_dkdv_mfma_kernel)",
                   "attn_bwd_dq": "attn_ds_gemm_kernel<..., false, false, ...> (or attn_dq_mfma_kernel)",
-                  "attn_bwd_dk": "attn_ds_gemm_kernel<..., true, false, float>",
+                  "attn_bwd_dk": "attn_ds_gemm_persist_kernel<..., true, false, float>",
                   "loss": "mask_count_kernel + loss_main_kernel + loss_final_kernel",
                   "elementwise": "rope_table_kernel, rope_apply_kernel, attn_delta_kernel, dkpe_finish_kernel, "
                                  "kcat_kernel, dk_split_kernel"}
