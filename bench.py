@@ -61,7 +61,7 @@ CLASS_PATTERNS = {
     "gemm_nt": [("gemm_mfma_kernel<", ", true, true,"), ("gemm_mfma_persist_kernel<", ", true, true,")],
     "gemm_nn": [("gemm_mfma_kernel<", ", true, false,"), ("gemm_mfma_persist_kernel<", ", true, false,")],
     "gemm_tn": [("gemm_mfma_kernel<", ", false, false,"), ("gemm_mfma_persist_kernel<", ", false, false,")],
-    "attn_fwd": [("attn_fwd_mfma_kernel<",)],
+    "attn_fwd": [("attn_fwd_mfma_kernel<",), ("attn_fwd_persist_kernel<",)],
     "attn_bwd_dkdv": [("attn_dv_mfma_kernel<",), ("attn_dkdv_mfma_kernel<",)],
     "attn_bwd_dq": [("attn_ds_gemm_kernel<", ", false, false,"), ("attn_ds_gemm_persist_kernel<", ", false, false,"),
                     ("attn_dq_mfma_kernel<",)],

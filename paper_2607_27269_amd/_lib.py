@@ -31,7 +31,7 @@ KCLASS_NAMES = {KC_GEMM_NT: "gemm_nt", KC_GEMM_NN: "gemm_nn", KC_GEMM_TN: "gemm_
 KCLASS_KERNELS = {"gemm_nt": "gemm_mfma_persist_kernel<..., true, true, ...> (and the loss-epilogue gemm_mfma_kernel)",
                   "gemm_nn": "gemm_mfma_persist_kernel<..., true, false, ...>",
                   "gemm_tn": "gemm_mfma_persist_kernel<..., false, false, float> + splitk_reduce_kernel",
-                  "attn_fwd": "attn_fwd_mfma_kernel",
+                  "attn_fwd": "attn_fwd_persist_kernel (or attn_fwd_mfma_kernel)",
                   "attn_bwd_dkdv": "attn_dv_mfma_kernel (or attn_dkdv_mfma_kernel)",
                   "attn_bwd_dq": "attn_ds_gemm_kernel<..., false, false, ...> (or attn_dq_mfma_kernel)",
                   "attn_bwd_dk": "attn_ds_gemm_persist_kernel<..., true, false, float>",

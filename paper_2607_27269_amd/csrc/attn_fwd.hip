@@ -32,19 +32,16 @@ constexpr int FWD_BQ = 32 * FWD_WAVES;   // queries per workgroup
 constexpr float RESCALE_SLACK = 8.f;     // log2 units the running reference max may lag
 
 template <int DQK, int DV, bool LSE>
-__global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a) {
+__device__ __forceinline__ void fwd_tile(const AttnDev& a, int pid, bf16_t* smem) {
   using Stage = KVStage<DQK, DV, FWD_WAVES>;
   constexpr int LDK = Stage::LDK, LDV = Stage::LDV;
   constexpr int KS = Stage::KS, VS = Stage::VS;
   constexpr int NST = 3;  // K/V ring: tile kb (V in use), kb + 1 (K in use), kb + 2 (landing)
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[NST * (KS + VS)];
   constexpr int NKK = DQK / 16;  // MFMA K-steps of the logits
   constexpr int NC = DV / 32;    // 32-row tiles of O^T
 
-  // work item: XCD-aware remap so that the query blocks of neighbouring heads (which share
-  // K/V) run on one XCD; heavy (late) query blocks first inside each head
-  const int nwork = a.B * a.H * a.nqb;
-  const int pid = xcd_remap(blockIdx.x, nwork);
+  // work item pid (XCD-aware order: the query blocks of neighbouring heads, which share
+  // K/V, run on one XCD); heavy (late) query blocks first inside each head
   const int bh = pid / a.nqb;
   const int qb = a.nqb - 1 - pid % a.nqb;
   const int b = bh / a.H, i = bh % a.H;
@@ -241,11 +238,46 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a
   if (LSE && half == 0) a.lse[((int64_t)b * a.T + my_q) * a.H + i] = (m_run + __log2f(l)) * LN2;
 }
 
+// one work item per workgroup
+template <int DQK, int DV, bool LSE>
+__global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a) {
+  using Stage = KVStage<DQK, DV, FWD_WAVES>;
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[3 * (Stage::KS + Stage::VS)];
+  const int nwork = a.B * a.H * a.nqb;
+  fwd_tile<DQK, DV, LSE>(a, xcd_remap(blockIdx.x, nwork), smem);
+}
+
+// persistent: FWD_PCU workgroups per XCD (one per CU) walk that XCD's share of the work
+// items in the same order (rounds of FWD_PCU items), in snake order (forward in even rounds,
+// backward in odd ones), so that heavy and light query blocks of a head pair up on a CU
+constexpr int FWD_PCU = 32;
+template <int DQK, int DV, bool LSE>
+__global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_persist_kernel(AttnDev a) {
+  using Stage = KVStage<DQK, DV, FWD_WAVES>;
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[3 * (Stage::KS + Stage::VS)];
+  const int per = a.B * a.H * a.nqb / 8;  // items of one XCD
+  const int x = blockIdx.x % 8, j = blockIdx.x / 8;
+  for (int r = 0;; ++r) {
+    const int local = r * FWD_PCU + ((r & 1) ? FWD_PCU - 1 - j : j);
+    if (local >= per) break;
+    if (r > 0) __syncthreads();  // every wavefront is done with the previous item's LDS
+    fwd_tile<DQK, DV, LSE>(a, x * per + local, smem);
+  }
+}
+
 template <int DQK, int DV>
 hipError_t fwd_launch(const Attn& at, hipStream_t s) {
   AttnDev d = to_dev(at);
   d.nqb = (at.T + FWD_BQ - 1) / FWD_BQ;
   const int nwork = d.B * d.H * d.nqb;
+  // the persistent walk needs whole XCD shares of several rounds
+  if (nwork % 8 == 0 && nwork / 8 >= 2 * FWD_PCU) {
+    if (at.lse)
+      attn_fwd_persist_kernel<DQK, DV, true><<<8 * FWD_PCU, 64 * FWD_WAVES, 0, s>>>(d);
+    else
+      attn_fwd_persist_kernel<DQK, DV, false><<<8 * FWD_PCU, 64 * FWD_WAVES, 0, s>>>(d);
+    return hipGetLastError();
+  }
   if (at.lse)
     attn_fwd_mfma_kernel<DQK, DV, true><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
   else
