@@ -43,6 +43,8 @@ def parse():
                    help="skip the timing of calibration capture (profiling runs)")
     p.add_argument("--no-decode", action="store_true",
                    help="skip the timing of absorbed-form decoding (profiling runs)")
+    p.add_argument("--no-other-configs", action="store_true",
+                   help="skip the timing of the other layer shapes (profiling runs)")
     p.add_argument("--decode-batch", type=int, default=64,
                    help="sequences per decoding step (each with a full-length cache)")
     p.add_argument("--cpu-seq", type=int, default=4096, help="oracle sample: tokens of one sequence")
@@ -50,28 +52,38 @@ def parse():
                    help="run one device-to-device copy of this many MiB first (HBM counter calibration)")
     p.add_argument("--summarize-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="turn two rocprofv3 --pmc counter_collection.csv files (FETCH_SIZE, WRITE_SIZE) "
-                        "of a --calib-copy-mb run into per-class HBM bytes per launch; print JSON")
+                        "of a --calib-copy-mb run into per-kernel HBM bytes per launch; print JSON")
+    p.add_argument("--summarize-counters", nargs="+", metavar="CSV",
+                   help="turn rocprofv3 --pmc counter_collection.csv files (and the kernel_trace.csv of "
+                        "a --kernel-trace run given as --trace) into a per-kernel markdown table; print it")
+    p.add_argument("--trace", help="kernel_trace.csv for --summarize-counters (durations)")
     return p.parse_args()
 
 
-# kernel-name fragments of each timing class, as rocprofv3 reports them
-# kernel-name patterns of each timing class: a kernel belongs to the class when every
-# substring of one of the alternatives occurs in its name
-CLASS_PATTERNS = {
-    "gemm_nt": [("gemm_mfma_kernel<", ", true, true,"), ("gemm_mfma_persist_kernel<", ", true, true,")],
-    "gemm_nn": [("gemm_mfma_kernel<", ", true, false,"), ("gemm_mfma_persist_kernel<", ", true, false,")],
-    "gemm_tn": [("gemm_mfma_kernel<", ", false, false,"), ("gemm_mfma_persist_kernel<", ", false, false,")],
-    "attn_fwd": [("attn_fwd_mfma_kernel<",), ("attn_fwd_persist_kernel<",)],
-    "attn_bwd_dkdv": [("attn_dv_mfma_kernel<",), ("attn_dkdv_mfma_kernel<",)],
-    "attn_bwd_dq": [("attn_ds_gemm_kernel<", ", false, false,"), ("attn_ds_gemm_persist_kernel<", ", false, false,"),
-                    ("attn_dq_mfma_kernel<",)],
-    "attn_bwd_dk": [("attn_ds_gemm_kernel<", ", true, false,"), ("attn_ds_gemm_persist_kernel<", ", true, false,")],
-    "loss": [("loss_main_kernel<",)],
-}
-
-
-def _in_class(name, alts):
-    return any(all(p in name for p in pats) for pats in alts)
+# Kernel names as the library's instrumentation reports them, derived from the names
+# rocprofv3 reports (so that counter readings and live timings refer to the same kernel)
+def rocprof_label(name):
+    """The instrumentation's name for a kernel rocprofv3 reports as `name`."""
+    import re
+    base = name.split("(")[0] if not name.startswith("void ") else name[5:].split("(")[0]
+    base = base.replace("mla::", "").replace("attn::", "").replace("(anonymous namespace)::", "")
+    m = re.match(r"(\w+)<(.*)>$", base.strip())
+    if not m:
+        return base.strip()
+    fn, args = m.group(1), [x.strip() for x in m.group(2).split(",")]
+    ty = lambda t: "fp32" if t == "float" else "bf16"
+    if fn in ("gemm_mfma_persist_kernel", "gemm_mfma_kernel") and len(args) >= 7:
+        lay = {("true", "true"): "NT", ("true", "false"): "NN", ("false", "false"): "TN",
+               ("false", "true"): "TT"}[(args[4], args[5])]
+        tag = fn if fn == "gemm_mfma_persist_kernel" else "gemm_mfma_kernel(masked loss)"
+        return f"{tag}<{args[0]},{args[1]},{lay},{ty(args[6])}>"
+    if fn in ("attn_ds_gemm_persist_kernel", "attn_ds_gemm_kernel") and len(args) >= 7:
+        return f"{fn}<{args[0]},{args[1]},{'dK' if args[4] == 'true' else 'dQ'},{ty(args[6])}>"
+    if fn in ("attn_fwd_persist_kernel", "attn_fwd_mfma_kernel") and len(args) >= 3:
+        return f"{fn}<{args[0]},{args[1]}{',lse' if args[2] == 'true' else ''}>"
+    if fn == "attn_dv_mfma_kernel":
+        return f"{fn}<{args[0]},{args[1]}>"
+    return fn
 
 
 # sources whose change invalidates stored counter readings
@@ -92,8 +104,8 @@ def sources_digest():
 
 
 def summarize_traffic(fetch_csv, write_csv, copy_mb):
-    """HBM bytes per launch of each timing class from FETCH_SIZE / WRITE_SIZE (KiB per
-    dispatch), each scaled so that the calibration copy reads and writes copy_mb MiB."""
+    """HBM bytes per launch of each kernel from FETCH_SIZE / WRITE_SIZE (KiB per dispatch),
+    each scaled so that the calibration copy reads and writes copy_mb MiB."""
     import csv
     def read(path, counter):
         rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
@@ -105,27 +117,76 @@ def summarize_traffic(fetch_csv, write_csv, copy_mb):
     fetch, write = read(fetch_csv, "FETCH_SIZE"), read(write_csv, "WRITE_SIZE")
     known = copy_mb * 1024.0 * 1024.0
     def copy_value(d):
-        # the calibration copy is the largest non-library dispatch named like a copy
-        cands = [v for (i, n), v in d.items() if "copy" in n.lower() or "Copy" in n]
+        # the calibration copy is the largest dispatch named like a copy
+        cands = [v for (i, n), v in d.items() if "copy" in n.lower()]
         return max(cands) if cands else None
     fc, wc = copy_value(fetch), copy_value(write)
     out = {"copy_mb": copy_mb, "fetch_scale": known / fc if fc else None,
-           "write_scale": known / wc if wc else None, "classes": {}}
-    for cls, alts in CLASS_PATTERNS.items():
-        fv = [v for (i, n), v in fetch.items() if _in_class(n, alts)]
-        wv = [v for (i, n), v in write.items() if _in_class(n, alts)]
-        if not fv or not wv or not fc or not wc:
+           "write_scale": known / wc if wc else None, "kernels": {}}
+    if not fc or not wc:
+        return out
+    labels = sorted({rocprof_label(n) for (i, n) in fetch if "copy" not in n.lower()})
+    for lab in labels:
+        fv = [v for (i, n), v in fetch.items() if rocprof_label(n) == lab]
+        wv = [v for (i, n), v in write.items() if rocprof_label(n) == lab]
+        if not fv or not wv:
             continue
-        out["classes"][cls] = {"launches": len(fv),
-                               "bytes_per_launch": (sum(fv) * out["fetch_scale"] + sum(wv) * out["write_scale"]) / len(fv),
+        out["kernels"][lab] = {"launches": len(fv),
+                               "bytes_per_launch": sum(fv) * out["fetch_scale"] / len(fv) +
+                                                   sum(wv) * out["write_scale"] / len(wv),
                                "read_bytes_per_launch": sum(fv) * out["fetch_scale"] / len(fv),
                                "write_bytes_per_launch": sum(wv) * out["write_scale"] / len(wv)}
     out["sources_sha1"] = sources_digest()
     return out
 
 
-def stored_traffic(cls):
-    """Counter-derived HBM bytes per launch for `cls`, if taken on the current sources."""
+def summarize_counters(csvs, trace):
+    """Per-kernel averages of rocprofv3 --pmc readings (one or more passes), with the MFMA
+    and vector-ALU busy fractions and, from a kernel trace, the average duration."""
+    import collections
+    import csv
+    vals = collections.defaultdict(lambda: collections.defaultdict(list))
+    for path in csvs:
+        per = collections.defaultdict(float)
+        for r in csv.DictReader(open(path)):
+            per[(r["Dispatch_Id"], r["Kernel_Name"], r["Counter_Name"])] += float(r["Counter_Value"])
+        for (i, n, c), v in per.items():
+            vals[rocprof_label(n)][c].append(v)
+    dur = collections.defaultdict(list)
+    if trace:
+        for r in csv.DictReader(open(trace)):
+            dur[rocprof_label(r["Kernel_Name"])].append(int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    mean = lambda xs: sum(xs) / len(xs) if xs else float("nan")
+    rows = []
+    for lab, cs in vals.items():
+        m = {c: mean(v) for c, v in cs.items()}
+        busy = m.get("SQ_BUSY_CYCLES")
+        row = {"kernel": lab, "us": mean(dur.get(lab, [])) / 1e3}
+        # SQ_BUSY_CYCLES counts per SE (32 per chip: 8 XCDs x 4), SQ_VALU_MFMA_BUSY_CYCLES per
+        # SIMD (1024): the two ratios are the busy fraction of the matrix / vector units
+        if busy:
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in m:
+                row["mfma_busy"] = m["SQ_VALU_MFMA_BUSY_CYCLES"] / 1024 / (busy / 32)
+            if "SQ_ACTIVE_INST_VALU" in m:
+                row["valu_active_per_cu"] = m["SQ_ACTIVE_INST_VALU"] / 256 / (busy / 32)
+        for c in ("SQ_INSTS_MFMA", "SQ_INSTS_VALU", "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT",
+                  "SQ_WAIT_INST_LDS", "SQ_INSTS_SALU"):
+            if c in m:
+                row[c] = m[c]
+        rows.append(row)
+    rows.sort(key=lambda r: -(r["us"] if r["us"] == r["us"] else 0))
+    cols = ["kernel", "us", "mfma_busy", "valu_active_per_cu", "SQ_INSTS_MFMA", "SQ_INSTS_VALU",
+            "SQ_INSTS_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS", "SQ_INSTS_SALU"]
+    cols = [c for c in cols if any(c in r for r in rows)]
+    fmt = lambda v: f"{v:.3g}" if isinstance(v, float) else str(v)
+    lines = ["| " + " | ".join(cols) + " |", "|" + "---|" * len(cols)]
+    for r in rows:
+        lines.append("| " + " | ".join(fmt(r.get(c, "")) for c in cols) + " |")
+    return "\n".join(lines)
+
+
+def stored_traffic(kernel):
+    """Counter-derived HBM bytes per launch of `kernel`, if taken on the current sources."""
     try:
         with open(TRAFFIC_FILE) as fh:
             t = json.load(fh)
@@ -133,7 +194,7 @@ def stored_traffic(cls):
         return None
     if t.get("sources_sha1") != sources_digest():
         return None
-    c = t.get("classes", {}).get(cls)
+    c = t.get("kernels", {}).get(kernel)
     return None if c is None else c["bytes_per_launch"]
 
 
@@ -163,6 +224,43 @@ def cpu_baseline(cfg, wl, seq):
     return {"value": seq / dt, "unit": "tokens/s", "cores": min(cores, threads), "kind": "oracle",
             "sample": f"1 sequence x {seq} tokens of the {cfg.name} layer (full widths), "
                       f"teacher fwd + student fwd + Eq. 11 + backward, float64 numpy; {dt:.1f} s"}
+
+
+def step_flops(cfg):
+    """Algorithmic FLOPs of the single-call step as run: the paper's step with the two W_O
+    products and dA W_O replaced by W_O^T W_O and one product with it."""
+    HV = cfg.n_heads * cfg.head_dim
+    return (cfg.total_flops() - 3 * cfg.flops()["T4_wo"] + 2.0 * HV * HV * cfg.hidden
+            + 2.0 * cfg.tokens * HV * HV)
+
+
+def time_config(idx, steps, warmup):
+    """The timed step (mla_recon_step without dA) on another layer shape."""
+    import torch
+    from paper_2607_27269_amd import configs, synth
+    from paper_2607_27269_amd.step import DeviceStep
+    cfg = configs.get(idx)
+    dev = DeviceStep(synth.make_workload(cfg))
+    for _ in range(warmup):
+        dev.fused_step(with_dA=False)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(steps):
+        dev.fused_step(with_dA=False)
+    stop.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(stop) / steps
+    out = {"workload": f"{cfg.name}: B={cfg.batch} T={cfg.seq} D={cfg.hidden} H={cfg.n_heads} "
+                       f"G={cfg.n_kv_groups} d_k={cfg.head_dim}; student r_q={cfg.q_rank} "
+                       f"r_kv={cfg.kv_rank} d_nope={cfg.nope_dim} d_rope={cfg.rope_dim} "
+                       f"G_kv={cfg.s_kv_groups} G_r={cfg.s_rope_groups}",
+           "ms_per_step": round(ms, 4), "value": round(cfg.tokens / (ms / 1e3), 1),
+           "unit": "tokens/s", "mfma_peak_frac": round(step_flops(cfg) / (ms / 1e3) / (PEAK_BF16_TFLOPS * 1e12), 4),
+           "loss": float(dev.loss_buf[0])}
+    del dev
+    torch.cuda.empty_cache()
+    return out
 
 
 def decode_bench(cfg, wl, batch, steps):
@@ -217,6 +315,9 @@ def main():
     args = parse()
     if args.summarize_traffic:
         print(json.dumps(summarize_traffic(*args.summarize_traffic, args.calib_copy_mb or 1024), indent=1))
+        return
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters, args.trace))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: the reconstruction step is not sharded across "
@@ -338,28 +439,37 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     ms_instr = start.elapsed_time(stop) / args.steps
+    kern = [dict(k, cls=L.KCLASS_NAMES[c]) for c in classes for k in L.mla_recon_prof_kernels(c)]
     prof = {L.KCLASS_NAMES[k]: L.mla_recon_prof_read(k) for k in classes}
     for k in classes:
         L.mla_recon_prof_enable(k, False)
 
     loss = float(dev.loss_buf[0])
     tokens = cfg.tokens
-    # algorithmic work of the step as run: the two W_O products and dA W_O replaced by
-    # W_O^T W_O and one product with it
-    HV = cfg.n_heads * cfg.head_dim
-    flops = (cfg.total_flops() - 3 * cfg.flops()["T4_wo"] + 2.0 * HV * HV * cfg.hidden
-             + 2.0 * cfg.tokens * HV * HV)
+    flops = step_flops(cfg)
     tok_s = tokens / (ms / 1e3)
+
+    def rate(p):
+        """(bound, achieved, peak, unit) of a kernel's algorithmic work over its time"""
+        if p["flops"] > 0:
+            return "mfma", p["flops"] / (p["ms"] / 1e3) / 1e12, PEAK_BF16_TFLOPS, "TFLOP/s"
+        return "hbm", p["bytes"] / (p["ms"] / 1e3) / 1e9, PEAK_HBM_GBS, "GB/s"
+    # the dominant single kernel (one kernel function and template instance)
+    top = max(kern, key=lambda k: k["ms"])
+    bound, achieved, peak, unit = rate(top)
+    kernels = []
+    for k in sorted(kern, key=lambda k: -k["ms"]):
+        kb, ka, kp, ku = rate(k)
+        kernels.append({"kernel": k["kernel"], "ms_per_step": round(k["ms"] / args.steps, 4),
+                        "launches_per_step": k["launches"] / args.steps, "bound": kb,
+                        "achieved": round(ka, 1), "unit": ku, "frac": round(ka / kp, 4)})
     dom = max(prof, key=lambda k: prof[k]["ms"])
-    p = prof[dom]
-    bound = "mfma" if p["flops"] > 0 else "hbm"
-    if bound == "mfma":
-        achieved = p["flops"] / (p["ms"] / 1e3) / 1e12
-        peak, unit = PEAK_BF16_TFLOPS, "TFLOP/s"
-    else:
-        achieved = p["bytes"] / (p["ms"] / 1e3) / 1e9
-        peak, unit = PEAK_HBM_GBS, "GB/s"
+    cb, ca, cp, cu = rate(prof[dom])
     kernel_share = {k: round(v["ms"] / args.steps, 4) for k, v in prof.items()}
+    # the other layer shapes (the tiny fp32 one is a parity case only)
+    others = None
+    if not args.no_other_configs:
+        others = {str(i): time_config(i, args.steps, args.warmup) for i in (1, 2, 4) if i != args.config}
     out = {
         "metric": "calibration tokens/sec per layer (fwd+bwd recon)",
         "value": round(tok_s, 1),
@@ -393,10 +503,18 @@ def main():
                           {"ms_per_step": round(ms_cached, 4),
                            "value": round(tokens / (ms_cached / 1e3), 1), "unit": "tokens/s"},
         "kernel_ms_per_step": kernel_share,
-        "roofline": {"kernel": f"{dom}: {L.KCLASS_KERNELS[dom]}", "bound": bound, "achieved": round(achieved, 2),
+        "roofline": {"kernel": top["kernel"], "bound": bound, "achieved": round(achieved, 2),
                      "peak": peak, "unit": unit, "frac": round(achieved / peak, 4),
-                     "traffic": stored_traffic(dom),
-                     "launches_per_step": p["launches"] / args.steps},
+                     "traffic": stored_traffic(top["kernel"]),
+                     "launches_per_step": top["launches"] / args.steps,
+                     "ms_per_launch": round(top["ms"] / top["launches"], 4),
+                     "alg_per_launch": top["flops"] / top["launches"] if bound == "mfma"
+                     else top["bytes"] / top["launches"]},
+        "kernels": kernels,
+        "class_roofline": {"class": f"{dom}: {L.KCLASS_KERNELS[dom]}", "bound": cb,
+                           "achieved": round(ca, 2), "peak": cp, "unit": cu,
+                           "frac": round(ca / cp, 4)},
+        "other_configs": others,
         "loss": loss,
     }
     if not args.no_cpu_baseline:

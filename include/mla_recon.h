@@ -1,11 +1,12 @@
 /*
  * mla_recon.h -- C ABI of the MI355X (gfx950) end-to-end functional-reconstruction step.
  *
- * One converted multi-head-latent-attention (MLA) layer is trained to reproduce the
- * post-output-projection response of the frozen original GQA/MHA layer on calibration
- * hidden states ("Beyond KV Reconstruction: Functional Reconstruction for MLA Draft
- * Models in Speculative Decoding", Sec. 4.1, Eq. 11).  One step is four calls, all
- * enqueued on the caller's HIP stream:
+ * The objective of Sec. 4.1 (Eq. 11) of "Beyond KV Reconstruction: Functional
+ * Reconstruction for MLA Draft Models in Speculative Decoding": the layer's output after
+ * the shared, frozen W_O is computed twice on the same hidden states, once by the
+ * original GQA/MHA attention and once by its MLA conversion, and the masked squared
+ * difference is minimised over the MLA side's new projections.  One step is four calls,
+ * all enqueued on the caller's HIP stream:
  *
  *   mla_recon_teacher_fwd  A_orig = W_O . GQA(h)                       (Eq. 1-4, Sec. 4.1)
  *   mla_recon_student_fwd  A_MLA  = W_O . MLA(h)                       (Eq. 5, Sec. 4)
@@ -33,10 +34,14 @@
  *  - Every call validates all arguments before enqueueing anything; on error it returns a
  *    negative mla_status, enqueues nothing and sets mla_recon_last_error().  On success it
  *    returns MLA_OK after only enqueueing work (no host synchronisation).
- *  - Workspace: ws must be at least mla_recon_workspace_size(cfg) bytes, 256-byte aligned.
- *    mla_recon_student_fwd stores the activations mla_recon_bwd needs in ws, so the same
- *    ws, unmodified, must be passed from student_fwd to bwd.  teacher_fwd and loss only
- *    use scratch parts of ws that student_fwd/bwd do not keep.
+ *  - Workspace: ws is 256-byte aligned and holds at least mla_recon_workspace_size_min(cfg)
+ *    bytes; mla_recon_workspace_size(cfg) is the preferred size.  A smaller workspace only
+ *    makes the bf16 backward run its attention in more chunks of sequences (the dS^T
+ *    buffer at the end of ws holds as many whole sequences as fit, at most 16 GiB of
+ *    them); results are the same.  mla_recon_student_fwd stores the activations
+ *    mla_recon_bwd needs in ws, so the same ws and ws_bytes, unmodified, must be passed
+ *    from student_fwd to bwd.  teacher_fwd and loss only use scratch parts of ws that
+ *    student_fwd/bwd do not keep.
  *  - Calls that share one ws (or overlapping outputs) must not run concurrently.
  */
 #ifndef MLA_RECON_H
@@ -69,7 +74,10 @@ typedef enum { MLA_BF16 = 0, MLA_FP32 = 1 } mla_dtype;
  * multiples of 8; G_kv a multiple of G_r.  Attention widths: the teacher's (d_k, d_k) and
  * the student's (d_nope + d_rope, d_k) must be one of (64,64), (96,64), (128,64),
  * (128,128), (192,128) (matrix-core kernels) or, through the vector-ALU kernels, (64,32),
- * (32,32), (16,16), (12,8), (8,8); MLA_ERR_UNSUPPORTED otherwise.  Any seq >= 1. */
+ * (32,32), (16,16), (12,8), (8,8); MLA_ERR_UNSUPPORTED otherwise.  Any seq >= 1.  In
+ * bf16 the backward stores dS^T (2 bytes per (head, key, query) of a sequence) for as
+ * many whole sequences as fit in 16 GiB at a time (the workspace holds one such chunk);
+ * a single sequence with n_heads * seq^2 * 2 bytes above 16 GiB is MLA_ERR_UNSUPPORTED. */
 typedef struct {
   int32_t batch, seq, hidden;               /* B, T, D                                    */
   int32_t n_heads, n_kv_groups, head_dim;   /* H, G, d_k                                  */
@@ -103,8 +111,10 @@ typedef struct {
   float *dWdq, *dWuq, *dWdkv_kr, *dWuk, *dWuv;
 } mla_student_grads;
 
-/* Bytes of workspace the four calls need for `cfg` (0 if cfg is invalid). */
+/* Preferred bytes of workspace for `cfg` (the backward's attention in one pass when its
+ * dS^T fits 16 GiB), and the minimum (one sequence per pass); 0 if cfg is invalid. */
 size_t mla_recon_workspace_size(const mla_recon_cfg *cfg);
+size_t mla_recon_workspace_size_min(const mla_recon_cfg *cfg);
 
 /* Teacher forward (Eq. 1-4 and the frozen W_O, Sec. 4.1).
  * h [B, T, D] (storage dtype); writes A_t [B, T, D] fp32 = the post-W_O attention
@@ -227,11 +237,23 @@ const char *mla_recon_last_error(void);
  * waits for those events, returns the summed kernel time (ms), the launch count and the
  * algorithmic FLOPs and HBM bytes those launches account for, and clears the record.
  * Classes: 0 GEMM C = A B^T, 1 GEMM with B N-contiguous, 2 GEMM with both operands
- * M/N-contiguous (weight gradients), 3 attention forward, 4 attention backward dK/dV
- * (dV only, plus the stored dS^T, when class 8 runs), 5 attention backward dQ, 6 loss,
- * 7 elementwise (RoPE, reductions, conversions), 8 attention backward dK as a GEMM over
- * the stored dS^T.  Up to 4096 launches are recorded per class. */
+ * M/N-contiguous (weight gradients), 3 attention forward, 4 attention backward dV and
+ * the stored dS^T, 5 attention backward dQ (a GEMM over dS^T), 6 loss, 7 elementwise
+ * (RoPE, reductions, conversions, split-K sums), 8 attention backward dK (a GEMM over
+ * dS^T).  Up to 4096 launches are recorded per class.
+ * mla_recon_prof_kernels splits the same record by kernel (one entry per kernel function
+ * and template instance, e.g. "gemm_mfma_persist_kernel<256,256,NT,bf16>"): it writes up
+ * to cap entries, returns how many kernels the class ran (or a negative mla_status) and
+ * leaves the record in place for mla_recon_prof_read.  The names are static strings. */
+typedef struct {
+  const char *kernel;
+  double ms;            /* summed duration of its launches                                 */
+  int64_t launches;
+  double alg_flops;     /* algorithmic FLOPs of those launches                              */
+  double alg_bytes;     /* algorithmic HBM bytes of those launches                          */
+} mla_prof_kernel;
 int mla_recon_prof_enable(int kernel_class, int on);
+int mla_recon_prof_kernels(int kernel_class, mla_prof_kernel *out, int cap);
 int mla_recon_prof_read(int kernel_class, double *total_ms, int64_t *launches,
                         double *alg_flops, double *alg_bytes);
 

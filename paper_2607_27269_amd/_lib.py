@@ -72,6 +72,11 @@ class StudentGrads(ctypes.Structure):
                 ("dWuv", ctypes.c_void_p)]
 
 
+class ProfKernel(ctypes.Structure):
+    _fields_ = [("kernel", ctypes.c_char_p), ("ms", ctypes.c_double), ("launches", ctypes.c_int64),
+                ("alg_flops", ctypes.c_double), ("alg_bytes", ctypes.c_double)]
+
+
 class AdamwTensor(ctypes.Structure):
     _fields_ = [("master", ctypes.c_void_p), ("m", ctypes.c_void_p), ("v", ctypes.c_void_p),
                 ("w", ctypes.c_void_p), ("grad", ctypes.c_void_p), ("n", ctypes.c_int64)]
@@ -91,6 +96,8 @@ def lib() -> ctypes.CDLL:
         P = ctypes.POINTER
         L.mla_recon_workspace_size.argtypes = [P(Cfg)]
         L.mla_recon_workspace_size.restype = sz
+        L.mla_recon_workspace_size_min.argtypes = [P(Cfg)]
+        L.mla_recon_workspace_size_min.restype = sz
         L.mla_recon_teacher_fwd.argtypes = [P(Cfg), vp, P(TeacherW), vp, vp, sz, vp]
         L.mla_recon_student_fwd.argtypes = [P(Cfg), vp, P(StudentW), vp, vp, vp, sz, vp]
         L.mla_recon_loss.argtypes = [P(Cfg), vp, vp, vp, vp, vp, vp, sz, vp]
@@ -120,6 +127,8 @@ def lib() -> ctypes.CDLL:
         L.mla_recon_prof_enable.argtypes = [i32, i32]
         L.mla_recon_prof_read.argtypes = [i32, P(ctypes.c_double), P(ctypes.c_int64),
                                           P(ctypes.c_double), P(ctypes.c_double)]
+        L.mla_recon_prof_kernels.argtypes = [i32, P(ProfKernel), i32]
+        L.mla_recon_prof_kernels.restype = i32
         _lib = L
     return _lib
 
@@ -145,6 +154,10 @@ def make_cfg(c) -> Cfg:
 
 def mla_recon_workspace_size(cfg: Cfg) -> int:
     return int(lib().mla_recon_workspace_size(ctypes.byref(cfg)))
+
+
+def mla_recon_workspace_size_min(cfg: Cfg) -> int:
+    return int(lib().mla_recon_workspace_size_min(ctypes.byref(cfg)))
 
 
 def mla_recon_teacher_fwd(cfg: Cfg, h: int, w: TeacherW, A_t: int, ws: int, ws_bytes: int,
@@ -214,6 +227,17 @@ def mla_recon_decode(cfg: Cfg, q: int, cache: int, max_len: int, lengths: int, W
 
 def mla_recon_prof_enable(kclass: int, on: bool) -> None:
     _check(lib().mla_recon_prof_enable(kclass, 1 if on else 0))
+
+
+def mla_recon_prof_kernels(kclass: int) -> list:
+    """Per-kernel split of class `kclass`'s record (not cleared): a list of dicts."""
+    cap = 64
+    arr = (ProfKernel * cap)()
+    n = lib().mla_recon_prof_kernels(kclass, arr, cap)
+    if n < 0:
+        _check(n)
+    return [dict(kernel=arr[i].kernel.decode(), ms=arr[i].ms, launches=arr[i].launches,
+                 flops=arr[i].alg_flops, bytes=arr[i].alg_bytes) for i in range(min(n, cap))]
 
 
 def mla_recon_prof_read(kclass: int):

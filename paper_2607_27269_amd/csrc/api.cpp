@@ -43,6 +43,8 @@ static int fail(int code, const char* fmt, ...) {
 struct ProfClass {
   bool on = false;
   std::vector<hipEvent_t> ev;  // 2 per launch
+  std::vector<const char*> kernel;  // per launch: its kernel's name
+  std::vector<double> kflops, kbytes;  // per launch: its algorithmic FLOPs and bytes
   int used = 0;
   double flops = 0.0, bytes = 0.0;
 };
@@ -56,10 +58,13 @@ void prof_begin(int k, hipStream_t s) {
   (void)hipEventRecord(p.ev[2 * p.used], s);
 }
 
-void prof_end(int k, hipStream_t s, double flops, double bytes) {
+void prof_end(int k, hipStream_t s, double flops, double bytes, const char* kernel) {
   ProfClass& p = g_prof[k];
   if (!p.on || p.used >= PROF_MAX) return;
   (void)hipEventRecord(p.ev[2 * p.used + 1], s);
+  p.kernel[p.used] = kernel ? kernel : "unnamed";
+  p.kflops[p.used] = flops;
+  p.kbytes[p.used] = bytes;
   p.used++;
   p.flops += flops;
   p.bytes += bytes;
@@ -116,6 +121,9 @@ static int check_cfg(const mla_recon_cfg* c) {
     return fail(MLA_ERR_UNSUPPORTED, "teacher head_dim %d not supported by the attention kernels", c->head_dim);
   if (!attn_supported(d, (int)d.dqk, (int)d.dv))
     return fail(MLA_ERR_UNSUPPORTED, "student logit width %d with value width %d not supported", (int)d.dqk, (int)d.dv);
+  if (attn_bwd_chunk_seqs((int)d.B, (int)d.H, (int)d.T, (int)d.dqk, (int)d.dv, d.t) < 0)
+    return fail(MLA_ERR_UNSUPPORTED, "attention backward: one sequence's dS^T (%d heads x %d^2 tokens) exceeds 16 GiB",
+                c->n_heads, c->seq);
   return MLA_OK;
 }
 
@@ -134,6 +142,7 @@ struct Layout {
   // loss scratch; the single-call step's per-tile sums (bf16) or A_s - A_t (fp32), its
   // W_O^T W_O (bf16) and, in fp32, its dA when the caller passes none
   size_t l_scr, l_diff, l_gram, l_da;
+  int chunk;  // sequences per chunk of the backward's dS^T
   size_t total;
 };
 
@@ -142,7 +151,11 @@ static Gemm mk(int M, int N, int K, const void* A, int64_t lda, bool ak, const v
                int64_t ldb, bool bk, void* C, int64_t ldc, DType in_t, DType c_t,
                float beta = 0.f);
 
-static Layout layout_of(const Dims& d) {
+// Workspace layout.  The matrix-core backward's dS^T and per-token scratch come last and
+// are sized for `chunk` sequences at a time (<= the 16 GiB cap): every other offset is
+// independent of the chunk, so any workspace between the minimum (one sequence) and the
+// preferred size (the largest chunk) serves, and the backward runs ceil(B / chunk) chunks.
+static Layout layout_of(const Dims& d, int chunk) {
   Layout L;
   size_t o = 0;
   auto take = [&](size_t bytes) { size_t r = o; o += al(bytes); return r; };
@@ -168,11 +181,6 @@ static Layout layout_of(const Dims& d) {
   L.b_dkpe = take(d.Gkv * N * d.dr * 4);
   L.b_dckv = take(N * d.kv_out * ts);
   L.b_dcq = take(N * d.rq * ts);
-  L.b_ds_bytes = attn_bwd_ds_bytes((int)d.B, (int)d.H, (int)d.T, (int)d.dqk, (int)d.dv, d.t);
-  L.b_ds = take(L.b_ds_bytes);
-  L.b_kcat = take(L.b_ds_bytes ? N * d.Gkv * d.dqk * ts : 0);
-  L.b_dktmp = take(L.b_ds_bytes ? N * d.Gkv * d.dqk * 4 : 0);
-  L.b_statT = take(L.b_ds_bytes ? attn_stats_bytes((int)d.B, (int)d.H, (int)d.T) : 0);
   size_t se = 0;
   for (const Gemm& g : bwd_gemm_shapes(d)) se = std::max(se, gemm_scratch_elems(g));
   L.b_split_elems = se;
@@ -188,16 +196,43 @@ static Layout layout_of(const Dims& d) {
                                                                      0, d.t, d.t))) * 8);
   L.l_gram = take(d.t == DT_BF16 ? (size_t)HV * HV * 2 : 0);
   L.l_da = take(d.t == DT_F32 ? N * d.D * 4 : 0);
+  // the backward's dS^T chunk and its per-token scratch
+  L.chunk = chunk;
+  const size_t ctok = (size_t)chunk * d.T;
+  L.b_ds_bytes = chunk ? attn_ds_bytes(chunk, (int)d.H, (int)d.T) : 0;
+  L.b_ds = take(L.b_ds_bytes);
+  L.b_kcat = take(ctok * d.Gkv * d.dqk * ts);
+  L.b_dktmp = take(ctok * d.Gkv * d.dqk * 4);
+  L.b_statT = take(chunk ? attn_stats_bytes(chunk, (int)d.H, (int)d.T) : 0);
   L.total = o;
   return L;
 }
 
+// largest chunk of sequences the backward may use (0: no dS^T on this path)
+static int max_chunk(const Dims& d) {
+  return std::max(0, attn_bwd_chunk_seqs((int)d.B, (int)d.H, (int)d.T, (int)d.dqk, (int)d.dv, d.t));
+}
+
+// the layout for a workspace of ws_bytes: the largest chunk that fits (at least one
+// sequence when the path has a chunk at all)
+static Layout layout_for(const Dims& d, size_t ws_bytes) {
+  int hi = max_chunk(d);
+  if (hi <= 1) return layout_of(d, hi);
+  int lo = 1;
+  while (lo < hi) {  // largest c in [1, hi] with total(c) <= ws_bytes
+    const int mid = lo + (hi - lo + 1) / 2;
+    if (layout_of(d, mid).total <= ws_bytes) lo = mid; else hi = mid - 1;
+  }
+  return layout_of(d, lo);
+}
+
 static int check_ws(const mla_recon_cfg* cfg, void* ws, size_t ws_bytes, Layout* L) {
-  *L = layout_of(dims_of(cfg));
+  const Dims d = dims_of(cfg);
+  *L = layout_for(d, ws_bytes);
   if (!ws) return fail(MLA_ERR_INVALID_ARG, "workspace is NULL");
   if ((uintptr_t)ws % 256) return fail(MLA_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   if (ws_bytes < L->total)
-    return fail(MLA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes", ws_bytes, L->total);
+    return fail(MLA_ERR_WORKSPACE, "workspace too small: %zu < %zu bytes (minimum)", ws_bytes, L->total);
   return MLA_OK;
 }
 
@@ -237,7 +272,14 @@ const char* mla_recon_last_error(void) { return g_err; }
 
 size_t mla_recon_workspace_size(const mla_recon_cfg* cfg) {
   if (check_cfg(cfg) != MLA_OK) return 0;
-  return layout_of(dims_of(cfg)).total;
+  const Dims d = dims_of(cfg);
+  return layout_of(d, max_chunk(d)).total;
+}
+
+size_t mla_recon_workspace_size_min(const mla_recon_cfg* cfg) {
+  if (check_cfg(cfg) != MLA_OK) return 0;
+  const Dims d = dims_of(cfg);
+  return layout_of(d, std::min(1, max_chunk(d))).total;
 }
 
 // Teacher forward up to the attention output o_t (ws region t_o); with A_t also the frozen
@@ -446,6 +488,7 @@ static int bwd_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
   ab.kcat = L.b_ds_bytes ? at(ws, L.b_kcat) : nullptr;
   ab.dk_tmp = L.b_ds_bytes ? (float*)at(ws, L.b_dktmp) : nullptr;
   ab.statT = L.b_ds_bytes ? (float*)at(ws, L.b_statT) : nullptr;
+  ab.chunk_seqs = L.chunk;
   HIP_TRY(attn_bwd(ab, s));
 
   if (need_q) {
@@ -696,11 +739,36 @@ int mla_recon_prof_enable(int k, int on) {
   if (on && p.ev.empty()) {
     p.ev.resize(2 * PROF_MAX);
     for (auto& e : p.ev) HIP_TRY(hipEventCreate(&e));
+    p.kernel.assign(PROF_MAX, nullptr);
+    p.kflops.assign(PROF_MAX, 0.0);
+    p.kbytes.assign(PROF_MAX, 0.0);
   }
   p.on = on != 0;
   p.used = 0;
   p.flops = p.bytes = 0.0;
   return MLA_OK;
+}
+
+int mla_recon_prof_kernels(int k, mla_prof_kernel* out, int cap) {
+  if (k < 0 || k >= KC_COUNT) return fail(MLA_ERR_INVALID_ARG, "bad kernel class %d", k);
+  if (cap < 0 || (cap > 0 && !out)) return fail(MLA_ERR_INVALID_ARG, "prof_kernels: bad output array");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  ProfClass& p = g_prof[k];
+  std::vector<mla_prof_kernel> acc;
+  for (int i = 0; i < p.used; ++i) {
+    HIP_TRY(hipEventSynchronize(p.ev[2 * i + 1]));
+    float e = 0.f;
+    HIP_TRY(hipEventElapsedTime(&e, p.ev[2 * i], p.ev[2 * i + 1]));
+    size_t j = 0;
+    while (j < acc.size() && strcmp(acc[j].kernel, p.kernel[i]) != 0) ++j;
+    if (j == acc.size()) acc.push_back(mla_prof_kernel{p.kernel[i], 0.0, 0, 0.0, 0.0});
+    acc[j].ms += e;
+    acc[j].launches += 1;
+    acc[j].alg_flops += p.kflops[i];
+    acc[j].alg_bytes += p.kbytes[i];
+  }
+  for (size_t j = 0; j < acc.size() && (int)j < cap; ++j) out[j] = acc[j];
+  return (int)acc.size();
 }
 
 int mla_recon_prof_read(int k, double* total_ms, int64_t* launches, double* alg_flops,

@@ -4,27 +4,19 @@
 //   dP = dO V^T, dS = P (dP - delta) with delta = rowsum(dO . O),
 //   dQ = scale dS K, dK = scale dS^T Q.
 //
-// Two kernels, each sized so that its accumulators stay in registers:
-//
-// * dK/dV: a workgroup owns 128 keys of one (sequence, KV group); each of its 4
-//   wavefronts owns 32 keys (K staged once in LDS, V held as MFMA B-operand fragments) and walks
-//   every 64-query block at or after its keys (last block first) and every head of the group.  S = Q K^T and
-//   dP = dO V^T put the key in the MFMA column, so the accumulators of P and dS are
-//   directly the B operands of dV^T += dO^T P and dK^T += Q^T dS; dO^T and Q^T come from
-//   the natural [query][dim] LDS tiles through gfx950's transposing LDS read.  The rotary
-//   part of dK is summed over the group's heads and left as an fp32 partial per group
-//   (the positional key may be shared by several groups).
-// * dV and dS^T, preferred when a dS^T buffer fits: the same walk (256 keys per
-//   workgroup) computes only dV and stores dS^T in bf16, transposed through LDS so that
-//   the stores run along key rows, zeros included wherever the dQ product below reads a
-//   masked pair; dK = scale dS^T Q is then a GEMM as well.
-// * dQ, preferred: dQ = scale dS K as a batched causal GEMM (one batch entry per
-//   (sequence, head)) over the stored dS^T and the keys gathered per group into one
-//   [token][group][dqk] tensor; no recomputation of S or dP.
-// * dQ, when no dS^T buffer fits: a kernel laid out like the forward (a lane owns one
-//   query; 4 wavefronts x 32 queries): S^T = K Q^T, dP^T = V dO^T, and dQ^T += K^T dS^T
-//   with K^T read transposed from the [key][dim] tile, written once in bf16.
-// Either way the rotary block of dQ is then rotated back with R^T.
+// * dV and dS^T: a workgroup owns 256 keys of one (sequence, KV group) and walks the
+//   group's heads and 32-query blocks; it accumulates dV in registers and stores dS^T in
+//   bf16, transposed through LDS so that the stores run along key rows, zeros included
+//   wherever the products below read a masked pair.
+// * dK = scale dS^T Q: a batched causal GEMM per (sequence, group), the group's heads
+//   stacked along K.
+// * dQ = scale dS K: a batched causal GEMM per (sequence, head) over the stored dS^T and
+//   the keys gathered per group into one [token][group][dqk] tensor; no recomputation of
+//   S or dP.
+// The dS^T buffer holds at most 16 GiB: larger batches run in chunks of whole sequences.
+// The rotary block of dQ is then rotated back with R^T.
+#include <algorithm>
+
 #include "attn_common.h"
 #include "mfma.h"
 #include "simt.h"
@@ -33,28 +25,15 @@ namespace mla {
 namespace attn {
 namespace {
 
-constexpr int BKB = 128;  // keys per dK/dV workgroup
-constexpr int BQB = 64;   // queries per dK/dV step
-constexpr int DQ_BQ = 128;  // queries per dQ workgroup
-
 struct BwdDev {
   AttnDev f;
   const bf16_t* dO;      // [N][H*dv]
-  const float* delta;    // [N][H]
-  bf16_t* dq;            // [N][H*dqk]
-  int rdiv;
-  const float* cos_t;
-  const float* sin_t;
-  bf16_t* dKa; int64_t dka_tok;
   bf16_t* dV; int64_t dv_tok;
-  float* dkb_part;       // [G][N][dqk - dnope]
   int G;                 // Ka groups
-  float scale;
-  bf16_t* dsT;           // [B*H][T][ds_ld] when ds_on
+  bf16_t* dsT;           // [B*H][T][ds_ld]
   int64_t ds_ld;
-  int ds_on;
   bf16_t* ds_dummy;      // scratch rows for stores of lanes past the sequence end
-  const float* statT;    // [2][H][B][tpad]: log2-scaled lse, delta (dV kernel)
+  const float* statT;    // [2][H][B][tpad]: log2-scaled lse, delta
   int tpad;
   int off32;             // one sequence's Q / dO rows and the statistics span < 2^31 bytes
 };
@@ -62,275 +41,6 @@ struct BwdDev {
 // dS^T tile rows a dQ GEMM row tile reads: queries from the start of the 256-query tile
 // that holds the key (the GEMM's row tile) to the end
 constexpr int DQ_TILE = 256;
-
-// ---------------------------------------------------------------------------------------
-// dK / dV
-// ---------------------------------------------------------------------------------------
-template <int DQK, int DV, int BQ = BQB>
-struct QStage {
-  static constexpr int LDQ = ld_of(DQK);
-  static constexpr int LDO = ld_of(DV);
-  using QT = DmaTile<BQ, DQK, LDQ, 4>;
-  using OT = DmaTile<BQ, DV, LDO, 4>;
-  static constexpr int QS = QT::ALLOC, OS = OT::ALLOC;
-  static constexpr int BUF = QS + OS + 2 * BQ * 2;  // bf16 elements incl. lse2, delta
-  QT qt;
-  OT ot;
-  float stat;
-
-  __device__ __forceinline__ void init() {
-    qt.init();
-    ot.init();
-  }
-
-  // queries q0 .. q0+BQ-1 of head i into buf (rows past the end load the last valid row;
-  // their lse is +inf so they carry zero probability)
-  __device__ __forceinline__ void issue(const BwdDev& w, int b, int i, int q0, bf16_t* buf) {
-    const AttnDev& a = w.f;
-    const int last = a.T - 1;
-    const int64_t n0 = (int64_t)b * a.T;
-    const bf16_t* qb = a.Q + n0 * a.q_tok + (int64_t)i * a.q_head;
-    const bf16_t* ob = w.dO + n0 * ((int64_t)a.H * DV) + (int64_t)i * DV;
-    qt.issue(buf, [&](int r, int c) { return qb + (int64_t)min(q0 + r, last) * a.q_tok + c; });
-    ot.issue(buf + QS, [&](int r, int c) {
-      return ob + (int64_t)min(q0 + r, last) * ((int64_t)a.H * DV) + c;
-    });
-    const int q = q0 + (int)(threadIdx.x % BQ);
-    if (threadIdx.x < BQ)
-      stat = q < a.T ? a.lse[(n0 + q) * a.H + i] * LOG2E : INFINITY;
-    else if (threadIdx.x < 2 * BQ)
-      stat = q < a.T ? w.delta[(n0 + q) * a.H + i] : 0.f;
-  }
-
-  __device__ __forceinline__ void store_stats(bf16_t* buf) const {
-    float* st = (float*)(buf + QS + OS);
-    if (threadIdx.x < 2 * BQ) st[threadIdx.x] = stat;
-  }
-};
-
-// WITH_DK = false: dK is left to the GEMM over the stored dS^T (no dK accumulators here)
-template <int DQK, int DV, bool WITH_DK>
-__global__ __launch_bounds__(256) void attn_dkdv_mfma_kernel(BwdDev w) {
-  using Stage = QStage<DQK, DV>;
-  constexpr int LDQ = Stage::LDQ, LDO = Stage::LDO;
-  constexpr int NKK = DQK / 16, NVK = DV / 16;
-  constexpr int NCK = DQK / 32, NCV = DV / 32;
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * Stage::BUF + BKB * ld_of(DQK)];
-  const AttnDev& a = w.f;
-
-  const int nbg = a.B * w.G;
-  const int kb = blockIdx.x / nbg;  // early key blocks (the most query blocks) first
-  const int bg = blockIdx.x % nbg;
-  const int b = bg / w.G, g = bg % w.G;
-  const int hpg = a.H / w.G;
-  const int k0 = kb * BKB;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int half = lane >> 5, col = lane & 31;
-  const int kw0 = k0 + 32 * wave;
-  const int my_key = kw0 + col;
-  const int i0 = g * hpg;
-
-  // keys of this workgroup in LDS ([key][d], read as B operand fragments each step); this
-  // lane's value as B operand fragments in registers (col = key, k = 16 kk + 8 half + 0..7)
-  bf16_t* Ks = smem + 2 * Stage::BUF;
-  {
-    constexpr int KCH = BKB * (DQK / 8);
-    const int ga = i0 / a.ka_div, gb = i0 / a.kb_div;
-    for (int c = threadIdx.x; c < KCH; c += 256) {
-      const int key = c / (DQK / 8), dc = (c % (DQK / 8)) * 8;
-      const int j = k0 + key;
-      u32x4 val = {0u, 0u, 0u, 0u};
-      if (j < a.T) {
-        const int64_t n = (int64_t)b * a.T + j;
-        const bf16_t* src = dc < a.dnope ? a.Ka + n * a.ka_tok + (int64_t)ga * a.ka_head + dc
-                                         : a.Kb + n * a.kb_tok + (int64_t)gb * a.kb_head + (dc - a.dnope);
-        val = *(const u32x4*)src;
-      }
-      *(u32x4*)(Ks + key * LDQ + dc) = val;
-    }
-  }
-  // dS^T rows of this workgroup's keys: the queries in [tile start, k0) precede every key
-  // here, so their entries are zeros that no step below writes
-  const int zq0 = k0 / DQ_TILE * DQ_TILE;
-  if (w.ds_on && zq0 < k0) {
-    const int nz = k0 - zq0;                       // multiple of 128
-    const int cpr = nz / 8;                        // 16-byte chunks per key row
-    const int kr = min(BKB, a.T - k0);
-    for (int h = 0; h < hpg; ++h) {
-      bf16_t* plane = w.dsT + ((int64_t)b * a.H + i0 + h) * a.T * w.ds_ld;
-      for (int c = threadIdx.x; c < kr * cpr; c += 256) {
-        const int r = c / cpr, q = zq0 + (c % cpr) * 8;
-        *(u32x4*)(plane + (int64_t)(k0 + r) * w.ds_ld + q) = u32x4{0u, 0u, 0u, 0u};
-      }
-    }
-  }
-  const bf16_t* krow = Ks + (32 * wave + col) * LDQ + 8 * half;
-  bf16x8 vf[NVK];
-  {
-    const int jj = min(my_key, a.T - 1);
-    const int64_t n = (int64_t)b * a.T + jj;
-    const int gv = i0 / a.v_div;
-    const bf16_t* vp = a.V + n * a.v_tok + (int64_t)gv * a.v_head + 8 * half;
-#pragma unroll
-    for (int kk = 0; kk < NVK; ++kk) {
-      u32x4 v = *(const u32x4*)(vp + 16 * kk);
-      if (my_key >= a.T) v = u32x4{0u, 0u, 0u, 0u};
-      vf[kk] = __builtin_bit_cast(bf16x8, v);
-    }
-  }
-
-  constexpr int NCKA = WITH_DK ? NCK : 1;
-  f32x16 dk[NCKA], dv[NCV];
-#pragma unroll
-  for (int c = 0; c < NCKA; ++c)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) dk[c][e] = 0.f;
-#pragma unroll
-  for (int c = 0; c < NCV; ++c)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) dv[c][e] = 0.f;
-
-  const int qb0 = k0 / BQB;
-  const int nqb = (a.T + BQB - 1) / BQB;
-  const int nper = nqb - qb0;
-  const int niter = hpg * nper;
-  Stage stg;
-  stg.init();
-  // step it -> (query block, head): query blocks in descending order with the group's heads
-  // innermost, so that all key blocks of a (sequence, group) stream the same Q/dO tile at
-  // the same time and share it through L2
-  auto q_of = [&](int it) { return (nqb - 1 - it / hpg) * BQB; };
-  auto h_of = [&](int it) { return i0 + it % hpg; };
-  if (niter > 0) {
-    stg.issue(w, b, h_of(0), q_of(0), smem);
-    stg.store_stats(smem);
-  }
-  wait_all();
-  __syncthreads();
-
-  for (int it = 0; it < niter; ++it) {
-    const int q0 = q_of(it);
-    const bf16_t* Qs = smem + (it & 1) * Stage::BUF;
-    const bf16_t* dOs = Qs + Stage::QS;
-    const float* st_lse = (const float*)(dOs + Stage::OS);
-    const float* st_dl = st_lse + BQB;
-    if (it + 1 < niter)
-      stg.issue(w, b, h_of(it + 1), q_of(it + 1), smem + ((it + 1) & 1) * Stage::BUF);
-
-    // this lane's dS^T row segment for the block: queries q0 + 4 half + {0..3, 8..11, ...}
-    // (a wave-uniform plane base and a 32-bit lane offset)
-    bf16_t* dsplane = w.ds_on ? w.dsT + ((int64_t)b * a.H + h_of(it)) * a.T * w.ds_ld : nullptr;
-    const uint32_t dsoff = (uint32_t)my_key * (uint32_t)w.ds_ld + (uint32_t)(q0 + 4 * half);
-    const bool dsrow = dsplane != nullptr && my_key < a.T;
-    if (kw0 <= min(q0 + BQB - 1, a.T - 1)) {  // wave-uniform: some pair is visible
-      f32x16 sp[2], dp[2];
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) { sp[qt][e] = 0.f; dp[qt][e] = 0.f; }
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk) {
-        const bf16x8 kf = *(const bf16x8*)(krow + 16 * kk);
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-          sp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              *(const bf16x8*)(Qs + (32 * qt + col) * LDQ + 16 * kk + 8 * half), kf, sp[qt], 0, 0, 0);
-      }
-#pragma unroll
-      for (int kk = 0; kk < NVK; ++kk)
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-          dp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              *(const bf16x8*)(dOs + (32 * qt + col) * LDO + 16 * kk + 8 * half), vf[kk], dp[qt], 0, 0, 0);
-      // P = 2^(S sl2 - lse2), dS = P (dP - delta); rows q = q0 + 32 qt + 8(e/4) + 4 half + e%4
-      const bool diag = kw0 + 31 > q0;
-#pragma unroll
-      for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const int qr = 32 * qt + 8 * e4 + 4 * half;
-          const f32x4 l2 = *(const f32x4*)(st_lse + qr);
-          const f32x4 dl = *(const f32x4*)(st_dl + qr);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int e = 4 * e4 + r;
-            float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sp[qt][e], a.sl2, -l2[r]));
-            if (diag && my_key > q0 + qr + r) p = 0.f;
-            sp[qt][e] = p;
-            dp[qt][e] = p * (dp[qt][e] - dl[r]);
-          }
-        }
-      // dS^T in bf16: element e of tile qt is query 32 qt + 8 (e/4) + 4 half + e%4
-      if (dsrow) {
-#pragma unroll
-        for (int qt = 0; qt < 2; ++qt)
-#pragma unroll
-          for (int e4 = 0; e4 < 4; ++e4)
-            st_global8(dsplane + dsoff + (32 * qt + 8 * e4),
-                       u32x2{pack2bf(dp[qt][4 * e4], dp[qt][4 * e4 + 1]),
-                             pack2bf(dp[qt][4 * e4 + 2], dp[qt][4 * e4 + 3])});
-      }
-      // dV^T += dO^T P,  dK^T += Q^T dS   (K-step u: queries 32(u/2) + 16(u%2) + {4h.., 8+4h..})
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        u32x4 wp, wd;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          wp[q] = pack2bf(sp[u >> 1][8 * (u & 1) + 2 * q], sp[u >> 1][8 * (u & 1) + 2 * q + 1]);
-          wd[q] = pack2bf(dp[u >> 1][8 * (u & 1) + 2 * q], dp[u >> 1][8 * (u & 1) + 2 * q + 1]);
-        }
-        const bf16x8 pf = __builtin_bit_cast(bf16x8, wp), sf = __builtin_bit_cast(bf16x8, wd);
-        const int klo = 32 * (u >> 1) + 16 * (u & 1) + 4 * half;
-#pragma unroll
-        for (int c = 0; c < NCV; ++c)
-          dv[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(dOs, LDO, 32 * c, klo, klo + 8),
-                                                         pf, dv[c], 0, 0, 0);
-        if constexpr (WITH_DK) {
-#pragma unroll
-          for (int c = 0; c < NCK; ++c)
-            dk[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                lds_operand_tr(Qs, LDQ, 32 * c, klo, klo + 8), sf, dk[c], 0, 0, 0);
-        }
-      }
-    } else if (dsrow) {
-      // every key of this wavefront follows every query of the block: zeros
-#pragma unroll
-      for (int o = 0; o < BQB; o += 8) st_global8(dsplane + dsoff + o, u32x2{0u, 0u});
-    }
-    if (it + 1 < niter) stg.store_stats(smem + ((it + 1) & 1) * Stage::BUF);
-    wait_all();
-    __syncthreads();
-  }
-
-  // epilogue: this lane's key; rows d = 32c + 8(e/4) + 4 half + e%4
-  if (my_key >= a.T) return;
-  const int64_t n = (int64_t)b * a.T + my_key;
-  const int dr = DQK - a.dnope;
-#pragma unroll
-  for (int c = 0; c < NCV; ++c)
-#pragma unroll
-    for (int e4 = 0; e4 < 4; ++e4) {
-      const int d = 32 * c + 8 * e4 + 4 * half;
-      u32x2 wv = {pack2bf(dv[c][4 * e4], dv[c][4 * e4 + 1]), pack2bf(dv[c][4 * e4 + 2], dv[c][4 * e4 + 3])};
-      *(u32x2*)(w.dV + n * w.dv_tok + (int64_t)g * DV + d) = wv;
-    }
-  if constexpr (!WITH_DK) return;
-  const float sc = w.scale;
-#pragma unroll
-  for (int c = 0; c < NCKA; ++c)
-#pragma unroll
-    for (int e4 = 0; e4 < 4; ++e4) {
-      const int d = 32 * c + 8 * e4 + 4 * half;
-      if (d < a.dnope) {
-        u32x2 wv = {pack2bf(sc * dk[c][4 * e4], sc * dk[c][4 * e4 + 1]),
-                    pack2bf(sc * dk[c][4 * e4 + 2], sc * dk[c][4 * e4 + 3])};
-        *(u32x2*)(w.dKa + n * w.dka_tok + (int64_t)g * a.dnope + d) = wv;
-      } else {
-        f32x4 v = {sc * dk[c][4 * e4], sc * dk[c][4 * e4 + 1], sc * dk[c][4 * e4 + 2], sc * dk[c][4 * e4 + 3]};
-        *(f32x4*)(w.dkb_part + ((int64_t)g * ((int64_t)a.B * a.T) + n) * dr + (d - a.dnope)) = v;
-      }
-    }
-}
 
 // ---------------------------------------------------------------------------------------
 // dV and dS^T (the path where dK and dQ are GEMMs over the stored dS^T)
@@ -349,11 +59,7 @@ constexpr int DV_BQ = 32;
 // (4 lanes write a row's 64 bytes)
 constexpr int DS_STORES = DV_BQ * 32 * 2 / (64 * 16);
 constexpr int DV_NST = 2;  // LDS stages: a step's copies are issued one step ahead
-#ifndef DV_WAVES_OVERRIDE
 constexpr int DV_WAVES = 8;
-#else
-constexpr int DV_WAVES = DV_WAVES_OVERRIDE;
-#endif
 constexpr int DV_BKB = 32 * DV_WAVES;  // keys per workgroup
 
 // [2][H][B][Tpad] fp32: log2-scaled lse (+inf past the sequence end) and delta (0 there)
@@ -692,129 +398,6 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
     }
 }
 
-// ---------------------------------------------------------------------------------------
-// dQ
-// ---------------------------------------------------------------------------------------
-template <int DQK, int DV>
-__global__ __launch_bounds__(256) void attn_dq_mfma_kernel(BwdDev w) {
-  using Stage = KVStage<DQK, DV, 4>;
-  constexpr int LDK = Stage::LDK, LDV = Stage::LDV;
-  constexpr int KS = Stage::KS, VS = Stage::VS;
-  constexpr int NKK = DQK / 16, NVK = DV / 16, NCK = DQK / 32;
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[2 * (KS + VS)];
-  const AttnDev& a = w.f;
-
-  const int nqb = (a.T + DQ_BQ - 1) / DQ_BQ;
-  const int nwork = a.B * a.H * nqb;
-  const int pid = xcd_remap(blockIdx.x, nwork);
-  const int bh = pid / nqb;
-  const int qb = nqb - 1 - pid % nqb;
-  const int b = bh / a.H, i = bh % a.H;
-  const int q0 = qb * DQ_BQ;
-  const int lane = threadIdx.x & 63, wave = wave_id();
-  const int half = lane >> 5, col = lane & 31;
-  const int qw0 = q0 + 32 * wave;
-  const int my_q = qw0 + col;
-  const bool qvalid = my_q < a.T;
-  const int64_t nq = (int64_t)b * a.T + min(my_q, a.T - 1);
-
-  // this lane's query and output gradient as B operand fragments (col = query)
-  bf16x8 qf[NKK], of[NVK];
-  {
-    const bf16_t* qp = a.Q + nq * a.q_tok + (int64_t)i * a.q_head + 8 * half;
-#pragma unroll
-    for (int kk = 0; kk < NKK; ++kk) qf[kk] = *(const bf16x8*)(qp + 16 * kk);
-    const bf16_t* op = w.dO + nq * ((int64_t)a.H * DV) + (int64_t)i * DV + 8 * half;
-#pragma unroll
-    for (int kk = 0; kk < NVK; ++kk) of[kk] = *(const bf16x8*)(op + 16 * kk);
-  }
-  const float lse2 = qvalid ? a.lse[nq * a.H + i] * LOG2E : INFINITY;
-  const float dlt = qvalid ? w.delta[nq * a.H + i] : 0.f;
-
-  f32x16 dq[NCK];
-#pragma unroll
-  for (int c = 0; c < NCK; ++c)
-#pragma unroll
-    for (int e = 0; e < 16; ++e) dq[c][e] = 0.f;
-
-  const int kend = min(a.T, q0 + DQ_BQ);
-  const int nkb = (kend + BKV - 1) / BKV;
-  Stage st;
-  st.init(a, b, i);
-  st.issue(0, smem, smem + KS);
-  wait_all();
-  __syncthreads();
-
-  for (int kb = 0; kb < nkb; ++kb) {
-    const int cur = kb & 1;
-    const int j0 = kb * BKV;
-    if (kb + 1 < nkb) {
-      bf16_t* nxt = smem + (cur ^ 1) * (KS + VS);
-      st.issue(j0 + BKV, nxt, nxt + KS);
-    }
-    const bf16_t* ks = smem + cur * (KS + VS);
-    const bf16_t* vs = ks + KS;
-    if (j0 <= qw0 + 31) {
-      f32x16 s[2], dp[2];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) { s[t][e] = 0.f; dp[t][e] = 0.f; }
-#pragma unroll
-      for (int kk = 0; kk < NKK; ++kk)
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-          s[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              *(const bf16x8*)(ks + (32 * t + col) * LDK + 16 * kk + 8 * half), qf[kk], s[t], 0, 0, 0);
-#pragma unroll
-      for (int kk = 0; kk < NVK; ++kk)
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-          dp[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-              *(const bf16x8*)(vs + (32 * t + col) * LDV + 16 * kk + 8 * half), of[kk], dp[t], 0, 0, 0);
-      const bool diag = j0 + BKV - 1 > qw0;
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(s[t][e], a.sl2, -lse2));
-          if (diag && j0 + 32 * t + 8 * (e >> 2) + 4 * half + (e & 3) > my_q) p = 0.f;
-          dp[t][e] = p * (dp[t][e] - dlt);
-        }
-      // dQ^T += K^T dS^T; K-step u covers keys 32(u/2) + 16(u%2) + {4h.., 8+4h..}
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        u32x4 wd;
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-          wd[q] = pack2bf(dp[u >> 1][8 * (u & 1) + 2 * q], dp[u >> 1][8 * (u & 1) + 2 * q + 1]);
-        const bf16x8 sf = __builtin_bit_cast(bf16x8, wd);
-        const int klo = 32 * (u >> 1) + 16 * (u & 1) + 4 * half;
-#pragma unroll
-        for (int c = 0; c < NCK; ++c)
-          dq[c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(lds_operand_tr(ks, LDK, 32 * c, klo, klo + 8),
-                                                         sf, dq[c], 0, 0, 0);
-      }
-    }
-    wait_all();
-    __syncthreads();
-  }
-
-  // epilogue: rows d = 32c + 8(e/4) + 4 half + e%4 of this lane's query (the rotary block is
-  // rotated back by the caller's R^T pass)
-  if (!qvalid) return;
-  const float sc = w.scale;
-  bf16_t* dst = w.dq + nq * ((int64_t)a.H * DQK) + (int64_t)i * DQK + 4 * half;
-#pragma unroll
-  for (int c = 0; c < NCK; ++c)
-#pragma unroll
-    for (int e4 = 0; e4 < 4; ++e4) {
-      u32x2 wv = {pack2bf(sc * dq[c][4 * e4], sc * dq[c][4 * e4 + 1]),
-                  pack2bf(sc * dq[c][4 * e4 + 2], sc * dq[c][4 * e4 + 3])};
-      *(u32x2*)(dst + 32 * c + 8 * e4) = wv;
-    }
-}
-
 // kcat[n][g][d] = the logit key of Ka group g at token n: d < dnope from Ka, the rest from
 // Kb (rope group of the group's first head); 8 elements per thread
 __global__ void kcat_kernel(AttnDev a, int G, int DQK, bf16_t* __restrict__ out) {
@@ -835,10 +418,10 @@ __global__ void kcat_kernel(AttnDev a, int G, int DQK, bf16_t* __restrict__ out)
 
 // dK of the GEMM ([N][G][DQK] fp32) split into the layouts the caller expects: the first
 // dnope dims in bf16 at dKa[n*dka_tok + g*dnope + d], the rest as the per-group fp32
-// partials dkb_part[g][n][d - dnope]; 4 elements per thread
+// partials dkb_part[g*gstride + n*(DQK - dnope) + d - dnope]; 4 elements per thread
 __global__ void dk_split_kernel(const float* __restrict__ dk, int64_t N, int G, int DQK,
                                 int dnope, bf16_t* __restrict__ dKa, int64_t dka_tok,
-                                float* __restrict__ dkb_part) {
+                                float* __restrict__ dkb_part, int64_t gstride) {
   const int cpr = DQK / 4;
   const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (c >= N * G * cpr) return;
@@ -850,26 +433,45 @@ __global__ void dk_split_kernel(const float* __restrict__ dk, int64_t N, int G, 
   if (d < dnope) {
     *(u32x2*)(dKa + n * dka_tok + (int64_t)g * dnope + d) = u32x2{pack2bf(v[0], v[1]), pack2bf(v[2], v[3])};
   } else {
-    *(f32x4*)(dkb_part + ((int64_t)g * N + n) * (DQK - dnope) + (d - dnope)) = v;
+    *(f32x4*)(dkb_part + (int64_t)g * gstride + n * (DQK - dnope) + (d - dnope)) = v;
   }
 }
 
+// The attention of sequences b0 .. b0 + nb - 1 as a problem of its own (token-major views
+// shifted by b0 T tokens)
+static Attn seq_slice(const Attn& a, int b0, int nb) {
+  Attn c = a;
+  const int64_t n0 = (int64_t)b0 * a.T;
+  auto shift = [&](HeadView& v) {
+    if (v.p) v.p = (const bf16_t*)v.p + n0 * v.tok;
+  };
+  shift(c.Q); shift(c.Ka); shift(c.Kb); shift(c.V);
+  c.O = (bf16_t*)a.O + n0 * a.o_tok;
+  c.lse = a.lse + n0 * a.H;
+  c.B = nb;
+  return c;
+}
+
+// dV, dK and dQ of sequences b0 .. b0 + nb - 1 (their dS^T fits the buffer)
 template <int DQK, int DV>
-hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
-  const Attn& at = wb.f;
+hipError_t bwd_chunk(const AttnBwd& wb, int b0, int nb, hipStream_t s) {
+  const Attn at = seq_slice(wb.f, b0, nb);
+  const int64_t n0 = (int64_t)b0 * at.T;
+  const int64_t Ntot = (int64_t)wb.f.B * at.T;
+  const int dr = DQK - at.dnope;
+  const bf16_t* dO = (const bf16_t*)wb.dO + n0 * at.H * DV;
+  const float* delta = wb.delta + n0 * at.H;
+  bf16_t* dq = (bf16_t*)wb.dq + n0 * at.H * DQK;
+  bf16_t* dKa = (bf16_t*)wb.dKa + n0 * wb.dka_tok;
+  float* dkb = wb.dkb_part + n0 * dr;
   BwdDev w;
   w.f = to_dev(at);
-  w.dO = (const bf16_t*)wb.dO; w.delta = wb.delta;
-  w.dq = (bf16_t*)wb.dq; w.rdiv = wb.rdiv; w.cos_t = wb.cos_t; w.sin_t = wb.sin_t;
-  w.dKa = (bf16_t*)wb.dKa; w.dka_tok = wb.dka_tok;
-  w.dV = (bf16_t*)wb.dV; w.dv_tok = wb.dv_tok;
-  w.dkb_part = wb.dkb_part; w.G = wb.n_ka_groups; w.scale = at.scale;
-  const bool ds_path = wb.dsT != nullptr && wb.kcat != nullptr && wb.dk_tmp != nullptr &&
-                       wb.statT != nullptr;
+  w.dO = dO;
+  w.dV = (bf16_t*)wb.dV + n0 * wb.dv_tok; w.dv_tok = wb.dv_tok;
+  w.G = wb.n_ka_groups;
   w.dsT = (bf16_t*)wb.dsT;
-  w.ds_on = ds_path ? 1 : 0;
   w.ds_ld = attn_ds_ld(at.T);
-  w.ds_dummy = w.dsT + (ds_path ? (int64_t)at.B * at.H * at.T * w.ds_ld : 0);
+  w.ds_dummy = w.dsT + (int64_t)at.B * at.H * at.T * w.ds_ld;
   w.statT = wb.statT;
   w.tpad = attn_stats_tpad(at.T);
   w.off32 = (int64_t)at.T * at.Q.tok * 2 < (1ll << 31) &&
@@ -877,99 +479,95 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
             (int64_t)at.H * at.B * w.tpad * 4 * 2 < (1ll << 31);
   const double pairs = attn_causal_pairs(at);
   const double N = (double)at.B * at.T;
-  // delta = rowsum(dO . O), then the dK/dV kernel: algorithmic dV = P^T dO, dP = dO V^T,
-  // dK = dS^T Q; reads Q, dO, K, V, lse, delta once, writes dK, dV
+  const int hpg = at.H / w.G;
+  // statistics per (head, sequence) in query order, then dV and dS^T: algorithmic
+  // dV = P^T dO, dP = dO V^T
+  prof_begin(KC_ELEM, s);
+  const int64_t nst = 2LL * at.H * at.B * w.tpad;
+  attn_stats_t_kernel<<<(unsigned)((nst + 255) / 256), 256, 0, s>>>(at.lse, delta, at.B, at.T, at.H,
+                                                                    w.tpad, wb.statT);
+  prof_end(KC_ELEM, s, 0.0, nst * 4.0 * 2.0, KLABEL("attn_stats_t_kernel"));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  prof_begin(KC_ATTN_DKDV, s);
+  const int nkb_dv = (at.T + DV_BKB - 1) / DV_BKB;
+  attn_dv_mfma_kernel<DQK, DV><<<nkb_dv * at.B * w.G, 64 * DV_WAVES, 0, s>>>(w);
+  prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV),
+           N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0 +
+               pairs * 2.0,
+           KLABEL("attn_dv_mfma_kernel<%d,%d>", DQK, DV));
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  // dK = scale dS^T Q per (sequence, group), the group's heads stacked along K:
+  // algorithmic dS read once, Q read once, dK written once (fp32)
+  {
+    Gemm g;
+    g.M = at.T; g.N = DQK; g.K = at.T;
+    g.A = wb.dsT; g.lda = w.ds_ld; g.a_kmajor = true;
+    g.B = at.Q.p; g.ldb = at.Q.tok; g.b_kmajor = false;
+    g.C = wb.dk_tmp; g.ldc = (int64_t)w.G * DQK;
+    g.in_t = DT_BF16; g.c_t = DT_F32; g.alpha = at.scale; g.beta = 0.f;
+    GemmBatch bt;
+    bt.nbatch = at.B * w.G; bt.zdiv = w.G; bt.bdiv = 1; bt.mstore = at.T;
+    bt.rev = 1; bt.kgroups = hpg;
+    bt.sA = (int64_t)hpg * at.T * w.ds_ld; bt.sAk = (int64_t)at.T * w.ds_ld;
+    bt.sB1 = (int64_t)at.T * at.Q.tok; bt.sB2 = (int64_t)hpg * at.Q.head; bt.sBk = at.Q.head;
+    bt.sC1 = (int64_t)at.T * w.G * DQK; bt.sC2 = DQK;
+    prof_begin(KC_ATTN_DK, s);
+    e = gemm_mfma_causal(g, bt, s);
+    prof_end(KC_ATTN_DK, s, 2.0 * pairs * DQK, pairs * 2.0 + N * at.H * DQK * 2.0 + N * w.G * DQK * 4.0,
+             KLABEL("attn_ds_gemm_persist_kernel<256,%d,dK,fp32>", DQK));
+    if (e != hipSuccess) return e;
+    prof_begin(KC_ELEM, s);
+    const int64_t chunks = (int64_t)at.B * at.T * w.G * (DQK / 4);
+    dk_split_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(
+        wb.dk_tmp, (int64_t)at.B * at.T, w.G, DQK, at.dnope, dKa, wb.dka_tok, dkb, Ntot * dr);
+    prof_end(KC_ELEM, s, 0.0, N * w.G * DQK * 4.0 * 2.0, KLABEL("dk_split_kernel"));
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  // keys of each group gathered into one operand, then dQ = scale dS K per (sequence,
+  // head): algorithmic dS read once, K read once per head, dQ written once
+  prof_begin(KC_ELEM, s);
+  const int64_t chunks = (int64_t)at.B * at.T * w.G * (DQK / 8);
+  kcat_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(w.f, w.G, DQK, (bf16_t*)wb.kcat);
+  prof_end(KC_ELEM, s, 0.0, N * w.G * DQK * 2.0 * 2.0, KLABEL("kcat_kernel"));
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  Gemm g;
+  g.M = (int)w.ds_ld; g.N = DQK; g.K = at.T;
+  g.A = wb.dsT; g.lda = w.ds_ld; g.a_kmajor = false;
+  g.B = wb.kcat; g.ldb = (int64_t)w.G * DQK; g.b_kmajor = false;
+  g.C = dq; g.ldc = (int64_t)at.H * DQK;
+  g.in_t = DT_BF16; g.c_t = DT_BF16; g.alpha = at.scale; g.beta = 0.f;
+  GemmBatch bt;
+  bt.nbatch = at.B * at.H; bt.zdiv = at.H; bt.bdiv = at.H / w.G; bt.mstore = at.T;
+  bt.sA = (int64_t)at.T * w.ds_ld;
+  bt.sB1 = (int64_t)at.T * w.G * DQK; bt.sB2 = DQK;
+  bt.sC1 = (int64_t)at.T * at.H * DQK; bt.sC2 = DQK;
+  bt.rev = 0; bt.kgroups = 1; bt.sAk = bt.sBk = 0;
+  prof_begin(KC_ATTN_DQ, s);
+  e = gemm_mfma_causal(g, bt, s);
+  prof_end(KC_ATTN_DQ, s, 2.0 * pairs * DQK, pairs * 2.0 + N * at.H * DQK * 2.0 * 2.0,
+           KLABEL("attn_ds_gemm_kernel<256,%d,dQ,bf16>", DQK));
+  return e;
+}
+
+template <int DQK, int DV>
+hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
+  const Attn& at = wb.f;
+  const int chunk = wb.chunk_seqs;
+  if (chunk < 1 || chunk > attn_bwd_chunk_seqs(at.B, at.H, at.T, at.dqk, at.dv, at.t) || !wb.dsT || !wb.kcat || !wb.dk_tmp || !wb.statT) return hipErrorInvalidValue;
+  // delta = rowsum(dO . O) of every token
   prof_begin(KC_ELEM, s);
   hipError_t e = attn_delta(wb, s);
-  prof_end(KC_ELEM, s, 0.0, N * at.H * (2.0 * DV * 2.0 + 4.0));
+  prof_end(KC_ELEM, s, 0.0, (double)at.B * at.T * at.H * (2.0 * DV * 2.0 + 4.0),
+           KLABEL("attn_delta_bf16x8_kernel"));
   if (e != hipSuccess) return e;
-  const int nkb = (at.T + BKB - 1) / BKB;
-  const int hpg = at.H / w.G;
-  if (ds_path) {
-    // statistics per (head, sequence) in query order, then dV (and dS^T) from the fused
-    // kernel: algorithmic dV = P^T dO, dP = dO V^T
-    prof_begin(KC_ELEM, s);
-    const int64_t nst = 2LL * at.H * at.B * w.tpad;
-    attn_stats_t_kernel<<<(unsigned)((nst + 255) / 256), 256, 0, s>>>(at.lse, wb.delta, at.B, at.T, at.H,
-                                                                      w.tpad, wb.statT);
-    prof_end(KC_ELEM, s, 0.0, nst * 4.0 * 2.0);
-    e = hipGetLastError();
+  for (int b0 = 0; b0 < at.B; b0 += chunk) {
+    e = bwd_chunk<DQK, DV>(wb, b0, std::min(chunk, at.B - b0), s);
     if (e != hipSuccess) return e;
-    prof_begin(KC_ATTN_DKDV, s);
-    const int nkb_dv = (at.T + DV_BKB - 1) / DV_BKB;
-    attn_dv_mfma_kernel<DQK, DV><<<nkb_dv * at.B * w.G, 64 * DV_WAVES, 0, s>>>(w);
-    prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV),
-             N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0 +
-                 pairs * 2.0);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    // dK = scale dS^T Q per (sequence, group), the group's heads stacked along K:
-    // algorithmic dS read once, Q read once, dK written once (fp32)
-    {
-      Gemm g;
-      g.M = at.T; g.N = DQK; g.K = at.T;
-      g.A = wb.dsT; g.lda = w.ds_ld; g.a_kmajor = true;
-      g.B = at.Q.p; g.ldb = at.Q.tok; g.b_kmajor = false;
-      g.C = wb.dk_tmp; g.ldc = (int64_t)w.G * DQK;
-      g.in_t = DT_BF16; g.c_t = DT_F32; g.alpha = at.scale; g.beta = 0.f;
-      GemmBatch bt;
-      bt.nbatch = at.B * w.G; bt.zdiv = w.G; bt.bdiv = 1; bt.mstore = at.T;
-      bt.rev = 1; bt.kgroups = hpg;
-      bt.sA = (int64_t)hpg * at.T * w.ds_ld; bt.sAk = (int64_t)at.T * w.ds_ld;
-      bt.sB1 = (int64_t)at.T * at.Q.tok; bt.sB2 = (int64_t)hpg * at.Q.head; bt.sBk = at.Q.head;
-      bt.sC1 = (int64_t)at.T * w.G * DQK; bt.sC2 = DQK;
-      prof_begin(KC_ATTN_DK, s);
-      e = gemm_mfma_causal(g, bt, s);
-      prof_end(KC_ATTN_DK, s, 2.0 * pairs * DQK, pairs * 2.0 + N * at.H * DQK * 2.0 + N * w.G * DQK * 4.0);
-      if (e != hipSuccess) return e;
-      prof_begin(KC_ELEM, s);
-      const int64_t chunks = (int64_t)at.B * at.T * w.G * (DQK / 4);
-      dk_split_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(
-          wb.dk_tmp, (int64_t)at.B * at.T, w.G, DQK, at.dnope, w.dKa, w.dka_tok, w.dkb_part);
-      prof_end(KC_ELEM, s, 0.0, N * w.G * DQK * 4.0 * 2.0);
-      e = hipGetLastError();
-      if (e != hipSuccess) return e;
-    }
-    // keys of each group gathered into one operand, then dQ = scale dS K per (sequence,
-    // head): algorithmic dS read once, K read once per head, dQ written once
-    prof_begin(KC_ELEM, s);
-    const int64_t chunks = (int64_t)at.B * at.T * w.G * (DQK / 8);
-    kcat_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(w.f, w.G, DQK, (bf16_t*)wb.kcat);
-    prof_end(KC_ELEM, s, 0.0, N * w.G * DQK * 2.0 * 2.0);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    Gemm g;
-    g.M = (int)w.ds_ld; g.N = DQK; g.K = at.T;
-    g.A = wb.dsT; g.lda = w.ds_ld; g.a_kmajor = false;
-    g.B = wb.kcat; g.ldb = (int64_t)w.G * DQK; g.b_kmajor = false;
-    g.C = wb.dq; g.ldc = (int64_t)at.H * DQK;
-    g.in_t = DT_BF16; g.c_t = DT_BF16; g.alpha = at.scale; g.beta = 0.f;
-    GemmBatch bt;
-    bt.nbatch = at.B * at.H; bt.zdiv = at.H; bt.bdiv = at.H / w.G; bt.mstore = at.T;
-    bt.sA = (int64_t)at.T * w.ds_ld;
-    bt.sB1 = (int64_t)at.T * w.G * DQK; bt.sB2 = DQK;
-    bt.sC1 = (int64_t)at.T * at.H * DQK; bt.sC2 = DQK;
-    bt.rev = 0; bt.kgroups = 1; bt.sAk = bt.sBk = 0;
-    prof_begin(KC_ATTN_DQ, s);
-    e = gemm_mfma_causal(g, bt, s);
-    prof_end(KC_ATTN_DQ, s, 2.0 * pairs * DQK,
-             pairs * 2.0 + N * at.H * DQK * 2.0 * 2.0);
-  } else {
-    prof_begin(KC_ATTN_DKDV, s);
-    attn_dkdv_mfma_kernel<DQK, DV, true><<<nkb * at.B * w.G, 256, 0, s>>>(w);
-    prof_end(KC_ATTN_DKDV, s, 2.0 * pairs * (2.0 * DV + DQK),
-             N * at.H * (DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 4.0 + N * at.H * 8.0);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    // dQ kernel: algorithmic dQ = dS K
-    prof_begin(KC_ATTN_DQ, s);
-    const int nqb = (at.T + DQ_BQ - 1) / DQ_BQ;
-    attn_dq_mfma_kernel<DQK, DV><<<nqb * at.B * at.H, 256, 0, s>>>(w);
-    prof_end(KC_ATTN_DQ, s, 2.0 * pairs * DQK,
-             N * at.H * (2.0 * DQK + DV) * 2.0 + N * w.G * (DQK + DV) * 2.0 + N * at.H * 8.0);
-    e = hipGetLastError();
   }
-  if (e != hipSuccess) return e;
   // rotary block of dQ back to the pre-rotation basis: R^T
   const int np = (DQK - at.dnope) / 2;
   return rope_apply(wb.dq, DT_BF16, at.B * at.T, at.T, at.H, (int64_t)at.H * DQK, DQK, at.dnope,

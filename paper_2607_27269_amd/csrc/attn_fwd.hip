@@ -266,22 +266,28 @@ __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_persist_kernel(AttnDe
 }
 
 template <int DQK, int DV>
-hipError_t fwd_launch(const Attn& at, hipStream_t s) {
+hipError_t fwd_launch(const Attn& at, hipStream_t s, const char** kernel) {
   AttnDev d = to_dev(at);
   d.nqb = (at.T + FWD_BQ - 1) / FWD_BQ;
   const int nwork = d.B * d.H * d.nqb;
   // the persistent walk needs whole XCD shares of several rounds
   if (nwork % 8 == 0 && nwork / 8 >= 2 * FWD_PCU) {
-    if (at.lse)
+    if (at.lse) {
       attn_fwd_persist_kernel<DQK, DV, true><<<8 * FWD_PCU, 64 * FWD_WAVES, 0, s>>>(d);
-    else
+      *kernel = KLABEL("attn_fwd_persist_kernel<%d,%d,lse>", DQK, DV);
+    } else {
       attn_fwd_persist_kernel<DQK, DV, false><<<8 * FWD_PCU, 64 * FWD_WAVES, 0, s>>>(d);
+      *kernel = KLABEL("attn_fwd_persist_kernel<%d,%d>", DQK, DV);
+    }
     return hipGetLastError();
   }
-  if (at.lse)
+  if (at.lse) {
     attn_fwd_mfma_kernel<DQK, DV, true><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
-  else
+    *kernel = KLABEL("attn_fwd_mfma_kernel<%d,%d,lse>", DQK, DV);
+  } else {
     attn_fwd_mfma_kernel<DQK, DV, false><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
+    *kernel = KLABEL("attn_fwd_mfma_kernel<%d,%d>", DQK, DV);
+  }
   return hipGetLastError();
 }
 
@@ -299,8 +305,8 @@ bool supported(int dqk, int dv) {
 
 bool attn_mfma_supported(int dqk, int dv) { return attn::supported(dqk, dv); }
 
-hipError_t attn_fwd_mfma(const Attn& a, hipStream_t s) {
-#define X(a_, b_) if (a.dqk == a_ && a.dv == b_) return attn::fwd_launch<a_, b_>(a, s);
+hipError_t attn_fwd_mfma(const Attn& a, hipStream_t s, const char** kernel) {
+#define X(a_, b_) if (a.dqk == a_ && a.dv == b_) return attn::fwd_launch<a_, b_>(a, s, kernel);
   MLA_MFMA_SHAPES(X)
 #undef X
   return hipErrorInvalidValue;

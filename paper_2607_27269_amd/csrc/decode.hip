@@ -394,7 +394,7 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
     absorb_rest_kernel<<<(unsigned)((nrest + 255) / 256), 256, 0, s>>>(
         (const bf16_t*)d.q, qabs, d.B, d.H, HP, d.dn, d.dr, d.rkv);
   }
-  prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dn * d.rkv, (double)nq * 2);
+  prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dn * d.rkv, (double)nq * 2, KLABEL("group_gemm_kernel + absorb_rest_kernel"));
 
   DecodeDev a;
   a.qabs = qabs; a.cache = (const bf16_t*)d.cache; a.ldc = d.ldc;
@@ -410,12 +410,12 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
   MLA_DECODE_SHAPES(X)
 #undef X
   prof_end(KC_ATTN_FWD, s, 2.0 * d.B * d.H * (double)d.Lmax * (DK + DVL),
-           (double)d.B * d.Lmax * DK * 2);
+           (double)d.B * d.Lmax * DK * 2, KLABEL("decode_attn_kernel"));
   prof_begin(KC_ELEM, s);
   decode_combine_kernel<<<dim3(d.H, d.B), 256, 0, s>>>(part_o, part_ml, lat, d.H, HP, nsplit, DVL);
   uv_proj_kernel<<<dim3(d.H, d.B), 128, 0, s>>>(lat, (const bf16_t*)d.Wuv, (bf16_t*)d.o, d.H,
                                                  d.dv, d.rkv, d.hpg);
-  prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dv * d.rkv, (double)d.B * d.H * (d.dv * 2 + DVL * 4));
+  prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dv * d.rkv, (double)d.B * d.H * (d.dv * 2 + DVL * 4), KLABEL("decode_combine_kernel + uv_proj_kernel"));
   return hipGetLastError();
 }
 

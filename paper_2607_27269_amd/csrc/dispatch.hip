@@ -1,5 +1,7 @@
 // Kernel selection: bf16 storage runs the MFMA kernels, fp32 (check mode) the vector-ALU
 // kernels.  Also owns the per-launch FLOP/byte accounting of the instrumentation.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 #include "mfma.h"
@@ -17,9 +19,11 @@ hipError_t gemm(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t
   double bytes = ((double)g.M * g.K + (double)g.N * g.K) * dsize(g.in_t) +
                  (double)g.M * g.N * dsize(g.c_t) * (g.beta != 0.f ? 2.0 : 1.0);
   const int kc = g.a_kmajor ? (g.b_kmajor ? KC_GEMM_NT : KC_GEMM_NN) : KC_GEMM_TN;
+  // the matrix-core path brackets its product and its split-K sum separately
+  if (g.in_t == DT_BF16) return gemm_mfma(g, scratch, scratch_elems, s, kc, flops, bytes);
   prof_begin(kc, s);
-  hipError_t e = g.in_t == DT_BF16 ? gemm_mfma(g, scratch, scratch_elems, s) : gemm_simt(g, s);
-  prof_end(kc, s, flops, bytes);
+  hipError_t e = gemm_simt(g, s);
+  prof_end(kc, s, flops, bytes, KLABEL("gemm_simt_kernel"));
   return e;
 }
 
@@ -32,8 +36,9 @@ hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mas
   double bytes = ((double)g.M * g.K + (double)g.N * g.K) * dsize(g.in_t) +
                  (double)g.M * g.N * dsize(g.c_t) * (ref ? 2.0 : 1.0) + (mask ? (double)g.M : 0.0);
   prof_begin(KC_GEMM_NT, s);
-  hipError_t e = gemm_mfma_masked_sse(g, scale, mask, ref, ldref, part, nparts, s);
-  prof_end(KC_GEMM_NT, s, flops, bytes);
+  const char* kname = nullptr;
+  hipError_t e = gemm_mfma_masked_sse(g, scale, mask, ref, ldref, part, nparts, s, &kname);
+  prof_end(KC_GEMM_NT, s, flops, bytes, kname);
   return e;
 }
 
@@ -51,8 +56,9 @@ hipError_t attn_fwd(const Attn& a, hipStream_t s) {
   if (a.q_cos && (!mfma || a.q_roff != 0 || 2 * a.q_np != a.dqk || a.dqk % 32))
     return hipErrorInvalidValue;
   prof_begin(KC_ATTN_FWD, s);
-  hipError_t e = mfma ? attn_fwd_mfma(a, s) : attn_fwd_simt(a, s);
-  prof_end(KC_ATTN_FWD, s, flops, bytes);
+  const char* kname = nullptr;
+  hipError_t e = mfma ? attn_fwd_mfma(a, s, &kname) : attn_fwd_simt(a, s);
+  prof_end(KC_ATTN_FWD, s, flops, bytes, mfma ? kname : KLABEL("attn_fwd_simt_kernel"));
   // the matrix-core kernel writes o_diff itself; the vector-ALU kernels leave it to a pass
   if (e == hipSuccess && a.o_diff && !mfma)
     e = sub_elementwise(a.O, a.o_ref, a.o_diff, (int64_t)N * a.H * a.dv, a.t, s);
@@ -68,16 +74,20 @@ hipError_t attn_bwd(const AttnBwd& w, hipStream_t s) {
   double bytes = N * a.H * (a.dqk + 2.0 * a.dv) * dsize(a.t) + N * a.H * (8.0 + 4.0 * a.dqk);
   prof_begin(KC_ATTN_DKDV, s);
   hipError_t e = attn_bwd_simt(w, s);
-  prof_end(KC_ATTN_DKDV, s, flops, bytes);
+  prof_end(KC_ATTN_DKDV, s, flops, bytes, KLABEL("attn_dq_simt_kernel + attn_dkv_simt_kernel"));
   return e;
 }
 
 double attn_causal_pairs(const Attn& a) { return causal_pairs(a); }
 
-size_t attn_bwd_ds_bytes(int B, int H, int T, int dqk, int dv, DType t) {
+int attn_bwd_chunk_seqs(int B, int H, int T, int dqk, int dv, DType t) {
   if (t != DT_BF16 || !attn_mfma_supported(dqk, dv)) return 0;
-  const size_t b = attn_ds_bytes(B, H, T);
-  return b <= ((size_t)16 << 30) ? b : 0;
+  const size_t limit = (size_t)16 << 30;
+  const size_t one = attn_ds_bytes(1, H, T);
+  if (one > limit) return -1;
+  const size_t per = one - attn_ds_bytes(0, H, T);  // without the scratch rows
+  const size_t fit = (limit - attn_ds_bytes(0, H, T)) / per;
+  return (int)std::min<size_t>((size_t)B, fit);
 }
 
 }  // namespace mla

@@ -32,7 +32,7 @@ hipError_t rope_tables(const float* inv_freq, int G, int T, int npairs, float* c
   prof_begin(KC_ELEM, s);
   rope_table_kernel<<<(unsigned)((total + 255) / 256), 256, 0, s>>>(inv_freq, G, T, npairs,
                                                                     cos_t, sin_t);
-  prof_end(KC_ELEM, s, 0.0, (double)total * 8.0 + G * npairs * 4.0);
+  prof_end(KC_ELEM, s, 0.0, (double)total * 8.0 + G * npairs * 4.0, KLABEL("rope_table_kernel"));
   return hipGetLastError();
 }
 
@@ -117,8 +117,9 @@ hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, i
   if (total == 0) return hipSuccess;
   unsigned grid = (unsigned)((total + 255) / 256);
   prof_begin(KC_ELEM, s);
-  if (t == DT_BF16 && npairs % 8 == 0 && tok % 8 == 0 && head % 8 == 0 && off % 8 == 0 &&
-      (uintptr_t)x % 16 == 0) {
+  const bool v8 = t == DT_BF16 && npairs % 8 == 0 && tok % 8 == 0 && head % 8 == 0 &&
+                  off % 8 == 0 && (uintptr_t)x % 16 == 0;
+  if (v8) {
     const int64_t total8 = (int64_t)N * nheads * (npairs / 8);
     rope_apply8_kernel<<<(unsigned)((total8 + 255) / 256), 256, 0, s>>>(
         (bf16_t*)x, N, T, nheads, tok, head, off, npairs, div, cos_t, sin_t, sgn);
@@ -128,7 +129,8 @@ hipError_t rope_apply(void* x, DType t, int N, int T, int nheads, int64_t tok, i
   else
     rope_apply_kernel<float><<<grid, 256, 0, s>>>((float*)x, N, T, nheads, tok, head, off,
                                                   npairs, div, cos_t, sin_t, sgn);
-  prof_end(KC_ELEM, s, 0.0, (double)N * nheads * npairs * 4.0 * dsize(t));
+  prof_end(KC_ELEM, s, 0.0, (double)N * nheads * npairs * 4.0 * dsize(t), 
+           v8 ? KLABEL("rope_apply8_kernel") : KLABEL("rope_apply_kernel"));
   return hipGetLastError();
 }
 
@@ -179,7 +181,7 @@ hipError_t dq_finish(const float* dq_acc, void* dq, DType t, int N, int T, int H
   else
     dq_finish_kernel<float><<<grid, 256, 0, s>>>(dq_acc, (float*)dq, N, T, H, dqk, dnope, rdiv,
                                                  cos_t, sin_t);
-  prof_end(KC_ELEM, s, 0.0, (double)N * H * dqk * (4.0 + dsize(t)));
+  prof_end(KC_ELEM, s, 0.0, (double)N * H * dqk * (4.0 + dsize(t)), KLABEL("dq_finish_kernel"));
   return hipGetLastError();
 }
 
@@ -222,7 +224,7 @@ hipError_t dkpe_finish(const float* part, void* out, DType t, int64_t out_tok, i
   else
     dkpe_finish_kernel<float><<<grid, 256, 0, s>>>(part, (float*)out, out_tok, N, T, Gr, per,
                                                    drope, cos_t, sin_t);
-  prof_end(KC_ELEM, s, 0.0, (double)N * Gr * drope * (4.0 * per + dsize(t)));
+  prof_end(KC_ELEM, s, 0.0, (double)N * Gr * drope * (4.0 * per + dsize(t)), KLABEL("dkpe_finish_kernel"));
   return hipGetLastError();
 }
 
@@ -365,7 +367,7 @@ hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, i
     loss_main_kernel<float><<<blocks, LOSS_THREADS, 0, s>>>(A_s, A_t, mask, N, D, (float*)dA, ws);
   loss_final_kernel<<<1, 256, 0, s>>>(ws, blocks, D, A_t != nullptr, loss);
   double bytes = (double)N * D * ((A_t ? 8.0 : 4.0) + (dA ? dsize(t) : 0)) + (mask ? N : 0);
-  prof_end(KC_LOSS, s, 0.0, bytes);
+  prof_end(KC_LOSS, s, 0.0, bytes, KLABEL("mask_count_kernel + loss_main_kernel + loss_final_kernel"));
   return hipGetLastError();
 }
 
@@ -373,7 +375,7 @@ hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, i
 hipError_t loss_prepare(const uint8_t* mask, int64_t N, int D, void* scratch, hipStream_t s) {
   prof_begin(KC_LOSS, s);
   mask_count_kernel<<<1, 1024, 0, s>>>(mask, N, D, (LossScratch*)scratch);
-  prof_end(KC_LOSS, s, 0.0, mask ? (double)N : 0.0);
+  prof_end(KC_LOSS, s, 0.0, mask ? (double)N : 0.0, KLABEL("mask_count_kernel"));
   return hipGetLastError();
 }
 
@@ -403,7 +405,7 @@ hipError_t loss_from_parts(const double* part, int nparts, int D, float* loss,
                            const void* scratch, hipStream_t s) {
   prof_begin(KC_LOSS, s);
   loss_parts_kernel<<<1, 256, 0, s>>>(part, nparts, D, (const LossScratch*)scratch, loss);
-  prof_end(KC_LOSS, s, 0.0, 8.0 * nparts);
+  prof_end(KC_LOSS, s, 0.0, 8.0 * nparts, KLABEL("loss_parts_kernel"));
   return hipGetLastError();
 }
 
@@ -438,7 +440,7 @@ hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, D
     sub_kernel<bf16_t><<<grid, 256, 0, s>>>((const bf16_t*)a, (const bf16_t*)b, (bf16_t*)out, n);
   else
     sub_kernel<float><<<grid, 256, 0, s>>>((const float*)a, (const float*)b, (float*)out, n);
-  prof_end(KC_ELEM, s, 0.0, 3.0 * n * dsize(t));
+  prof_end(KC_ELEM, s, 0.0, 3.0 * n * dsize(t), KLABEL("sub_kernel"));
   return hipGetLastError();
 }
 
@@ -508,7 +510,7 @@ hipError_t adamw_step(const AdamwTensor* t, int count, DType wt, float lr, float
   prof_begin(KC_ELEM, s);
   if (wt == DT_BF16) adamw_kernel<bf16_t><<<grid, 256, 0, s>>>(a);
   else adamw_kernel<float><<<grid, 256, 0, s>>>(a);
-  prof_end(KC_ELEM, s, 0.0, bytes);
+  prof_end(KC_ELEM, s, 0.0, bytes, KLABEL("adamw_kernel"));
   return hipGetLastError();
 }
 
@@ -552,7 +554,7 @@ hipError_t residual_rmsnorm(float* x, const float* A, void* h, int64_t N, int D,
     residual_rmsnorm_kernel<bf16_t><<<(unsigned)N, 256, 0, s>>>(x, A, (bf16_t*)h, D, eps);
   else
     residual_rmsnorm_kernel<float><<<(unsigned)N, 256, 0, s>>>(x, A, (float*)h, D, eps);
-  prof_end(KC_ELEM, s, 0.0, (double)N * D * ((A ? 12.0 : 4.0) + dsize(t)));
+  prof_end(KC_ELEM, s, 0.0, (double)N * D * ((A ? 12.0 : 4.0) + dsize(t)), KLABEL("residual_rmsnorm_kernel"));
   return hipGetLastError();
 }
 

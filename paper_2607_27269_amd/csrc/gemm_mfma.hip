@@ -25,6 +25,8 @@
 // run on one XCD and hit its L2.  Weight gradients reduce over all tokens (K up to 1e5)
 // and have few output tiles: they are split along K into fp32 partials that a second
 // kernel sums in a fixed order (deterministic).
+#include <atomic>
+
 #include "common.h"
 #include "kernels.h"
 #include "mfma.h"
@@ -833,29 +835,38 @@ Plan plan_of(const Gemm& g, bool allow_split) {
 }
 
 template <bool AK, bool BKM, typename TC>
-void launch(const GemmDev& d, const Plan& p, hipStream_t s) {
+const char* launch(const GemmDev& d, const Plan& p, hipStream_t s) {
   const int tiles = ((d.M + p.bm - 1) / p.bm) * ((d.N + p.bn - 1) / p.bn);
   const bool persist = d.lpart == nullptr;
+#define GL_(name, bm, bn) KLABEL(name "<%d,%d,%s,%s>", bm, bn, AK ? (BKM ? "NT" : "NN") : (BKM ? "TT" : "TN"), \
+                                 sizeof(TC) == 4 ? "fp32" : "bf16")
   if (persist) {
     GemmDev e = d;
     e.nsplit = p.splits;
     const int per_cu = p.kind == 2 ? 2 : 1;
     const int grid = std::min(tiles * p.splits, NUM_CU * per_cu);
-    if (p.kind == 0)
+    if (p.kind == 0) {
       gemm_mfma_persist_kernel<256, 256, GWM, GWN, AK, BKM, TC, GBK, GNST><<<grid, 64 * GWM * GWN, 0, s>>>(e);
-    else if (p.kind == 1)
+      return GL_("gemm_mfma_persist_kernel", 256, 256);
+    } else if (p.kind == 1) {
       gemm_mfma_persist_kernel<256, 192, 4, 2, AK, BKM, TC, GBK, GNST><<<grid, 512, 0, s>>>(e);
-    else
-      gemm_mfma_persist_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(e);
-    return;
+      return GL_("gemm_mfma_persist_kernel", 256, 192);
+    }
+    gemm_mfma_persist_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(e);
+    return GL_("gemm_mfma_persist_kernel", 128, 128);
   }
+  // the masked-loss epilogue
   dim3 grid(tiles, p.splits);
-  if (p.kind == 0)
+  if (p.kind == 0) {
     gemm_mfma_kernel<256, 256, GWM, GWN, AK, BKM, TC, GBK, GNST><<<grid, 64 * GWM * GWN, 0, s>>>(d);
-  else if (p.kind == 1)
+    return GL_("gemm_mfma_kernel(masked loss)", 256, 256);
+  } else if (p.kind == 1) {
     gemm_mfma_kernel<256, 192, 4, 2, AK, BKM, TC, GBK, GNST><<<grid, 512, 0, s>>>(d);
-  else
-    gemm_mfma_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(d);
+    return GL_("gemm_mfma_kernel(masked loss)", 256, 192);
+  }
+  gemm_mfma_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(d);
+  return GL_("gemm_mfma_kernel(masked loss)", 128, 128);
+#undef GL_
 }
 
 
@@ -866,7 +877,8 @@ size_t gemm_mfma_scratch_elems(const Gemm& g) {
   return p.splits > 1 ? (size_t)p.splits * g.M * g.N : 0;
 }
 
-hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s) {
+hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s, int kc,
+                     double flops, double bytes) {
   GemmDev d;
   d.M = g.M; d.N = g.N; d.ktotal = g.K; d.nsplit = 1;
   d.A = (const bf16_t*)g.A; d.lda = g.lda;
@@ -882,17 +894,23 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   d.kchunk = p.kchunk;
   d.part = p.splits > 1 ? scratch : nullptr;
   const bool f32 = g.c_t == DT_F32;
+  const char* kname = nullptr;
+  prof_begin(kc, s);
 #define L_(AK, BK_)                                                                     \
   if (g.a_kmajor == AK && g.b_kmajor == BK_) {                                          \
-    if (f32) launch<AK, BK_, float>(d, p, s);                                           \
-    else launch<AK, BK_, bf16_t>(d, p, s);                                              \
+    if (f32) kname = launch<AK, BK_, float>(d, p, s);                                   \
+    else kname = launch<AK, BK_, bf16_t>(d, p, s);                                      \
   }
   L_(true, true) else L_(true, false) else L_(false, false) else L_(false, true)
 #undef L_
+  prof_end(kc, s, flops, bytes, kname);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || p.splits == 1) return e;
+  // the split-K partials summed in a fixed order (an elementwise launch of its own)
   int64_t total = (int64_t)g.M * g.N;
   unsigned grid = (unsigned)((total + 255) / 256);
+  const double rbytes = (double)total * (4.0 * p.splits + (f32 ? 4.0 : 2.0) * (g.beta != 0.f ? 2.0 : 1.0));
+  prof_begin(KC_ELEM, s);
   if (g.N % 4 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.C % (f32 ? 16 : 8) == 0) {
     const unsigned grid4 = (unsigned)((total / 4 + 255) / 256);
     if (f32)
@@ -901,6 +919,7 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
     else
       splitk_reduce4_kernel<bf16_t><<<grid4, 256, 0, s>>>(scratch, p.splits, g.M, g.N,
                                                           (bf16_t*)g.C, g.ldc, g.alpha, g.beta);
+    prof_end(KC_ELEM, s, 0.0, rbytes, KLABEL("splitk_reduce4_kernel"));
     return hipGetLastError();
   }
   if (f32)
@@ -909,6 +928,7 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   else
     splitk_reduce_kernel<bf16_t><<<grid, 256, 0, s>>>(scratch, p.splits, g.M, g.N, (bf16_t*)g.C,
                                                       g.ldc, g.alpha, g.beta);
+  prof_end(KC_ELEM, s, 0.0, rbytes, KLABEL("splitk_reduce_kernel"));
   return hipGetLastError();
 }
 
@@ -918,7 +938,7 @@ size_t gemm_mfma_masked_sse_parts(const Gemm& g) {
 
 hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
                                 const void* ref, int64_t ldref, double* part, int* nparts,
-                                hipStream_t s) {
+                                hipStream_t s, const char** kernel) {
   if (g.beta != 0.f || g.alpha != 1.f || g.in_t != DT_BF16) return hipErrorInvalidValue;
   GemmDev d;
   d.M = g.M; d.N = g.N; d.ktotal = g.K; d.nsplit = 1;
@@ -935,13 +955,8 @@ hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t
   d.part = nullptr;
   *nparts = ((g.M + p.bm - 1) / p.bm) * ((g.N + p.bn - 1) / p.bn);
   const bool f32 = g.c_t == DT_F32;
-#define L_(AK, BK_)                                                                     \
-  if (g.a_kmajor == AK && g.b_kmajor == BK_) {                                          \
-    if (f32) launch<AK, BK_, float>(d, p, s);                                           \
-    else launch<AK, BK_, bf16_t>(d, p, s);                                              \
-  }
-  L_(true, true) else return hipErrorInvalidValue;
-#undef L_
+  if (!g.a_kmajor || !g.b_kmajor) return hipErrorInvalidValue;
+  *kernel = f32 ? launch<true, true, float>(d, p, s) : launch<true, true, bf16_t>(d, p, s);
   return hipGetLastError();
 }
 
@@ -960,7 +975,12 @@ static void launch_causal(const GemmDev& d, int nbatch, hipStream_t s) {
   } else {
     // dK (K ranges start at the diagonal): persistent, 2.6% faster; as many workgroups as
     // fit on the CUs at once (the narrow tiles leave room for two per CU)
-    static int per_cu = 0;
+    // resident workgroups per CU, queried once per device
+    constexpr int MAXDEV = 64;
+    static std::atomic<int> occ[MAXDEV];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= MAXDEV) dev = 0;
+    int per_cu = occ[dev].load(std::memory_order_relaxed);
     if (per_cu == 0) {
       int n = 0;
       if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
@@ -968,6 +988,7 @@ static void launch_causal(const GemmDev& d, int nbatch, hipStream_t s) {
               64 * WM * WN, 0) != hipSuccess || n < 1)
         n = 1;
       per_cu = n;
+      occ[dev].store(n, std::memory_order_relaxed);
     }
     attn_ds_gemm_persist_kernel<256, BN, WM, WN, AK, false, TC, 64, 2>
         <<<dim3(std::min(items, NUM_CU * per_cu), 1), 64 * WM * WN, 0, s>>>(d);

@@ -2,6 +2,9 @@
 #pragma once
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+#include <stdio.h>
+
+#include <mutex>
 
 namespace mla {
 
@@ -23,9 +26,20 @@ enum KClass {
 };
 
 // Timing instrumentation hooks (implemented in api.cpp).  prof_end also records the
-// algorithmic FLOPs / bytes of the bracketed launch(es).
+// algorithmic FLOPs / bytes of the bracketed launch and the name of its kernel (a string
+// that lives as long as the process, e.g. from KLABEL).
 void prof_begin(int kclass, hipStream_t s);
-void prof_end(int kclass, hipStream_t s, double flops, double bytes);
+void prof_end(int kclass, hipStream_t s, double flops, double bytes, const char* kernel = nullptr);
+
+// A stable name for the kernel of one launch site, formatted once per site (and per
+// template instance of the enclosing function).
+#define KLABEL(...)                                                                      \
+  ([&]() -> const char* {                                                                \
+    static char kl_buf_[112];                                                            \
+    static std::once_flag kl_once_;                                                      \
+    std::call_once(kl_once_, [&] { snprintf(kl_buf_, sizeof(kl_buf_), __VA_ARGS__); });  \
+    return kl_buf_;                                                                      \
+  }())
 
 // C[m, n] = alpha * sum_k A(m, k) B(n, k) + beta * C[m, n]
 //   A(m, k) = A[m*lda + k] if a_kmajor else A[k*lda + m]
@@ -83,24 +97,26 @@ struct AttnBwd {
   void* dV;  int64_t dv_tok;   // group g's value grads at dV[n*dv_tok + g*dv]
   float* dkb_part;           // [Gka, N, dqk - dnope] fp32 partial grads of the Kb part per Ka group
   int n_ka_groups;           // number of Ka groups (heads i / f.Ka.div)
-  // Optional (matrix-core path): with both set, dS^T is stored in bf16 by the dK/dV kernel
-  // as [B*H][T keys][ds_ld queries] (ds_ld = T rounded up to 64) and dQ = scale dS K is a
-  // batched causal GEMM against the keys gathered as kcat [N][n_ka_groups][dqk].
-  // dK = scale dS^T Q is then a GEMM as well, into dk_tmp before the split into dKa and
-  // dkb_part.
-  void* dsT;                 // attn_ds_bytes(f.B, f.H, f.T) bytes, or null
-  void* kcat;                // N * n_ka_groups * dqk bf16, or null
-  float* dk_tmp;             // N * n_ka_groups * dqk fp32, or null
-  float* statT;              // attn_stats_bytes(f.B, f.H, f.T), or null
+  // Matrix-core path: dS^T is stored in bf16 by the dV kernel as [B'*H][T keys][ds_ld
+  // queries] (ds_ld = T rounded up to 64) for B' = attn_bwd_chunk_seqs sequences at a time;
+  // dQ = scale dS K is a batched causal GEMM against the keys gathered as kcat
+  // [B' T][n_ka_groups][dqk], and dK = scale dS^T Q a GEMM into dk_tmp before the split into
+  // dKa and dkb_part.
+  void* dsT;                 // attn_ds_bytes(B', f.H, f.T) bytes
+  void* kcat;                // B' T * n_ka_groups * dqk bf16
+  float* dk_tmp;             // B' T * n_ka_groups * dqk fp32
+  float* statT;              // attn_stats_bytes(B', f.H, f.T)
+  int chunk_seqs;            // B' (>= 1, at most attn_bwd_chunk_seqs)
 };
 // Row stride and size of the stored dS^T of the matrix-core backward.
 int64_t attn_ds_ld(int T);
 size_t attn_ds_bytes(int B, int H, int T);
 int attn_stats_tpad(int T);
 size_t attn_stats_bytes(int B, int H, int T);
-// Bytes of dS^T buffer the backward of this attention shape uses (0: dQ is recomputed by
-// its own kernel; the case for the vector-ALU path and when dS^T would exceed 16 GiB).
-size_t attn_bwd_ds_bytes(int B, int H, int T, int dqk, int dv, DType t);
+// Sequences per chunk of the matrix-core backward (whose dS^T buffer holds at most
+// 16 GiB): 0 when the backward stores no dS^T (vector-ALU path), -1 when one sequence's
+// dS^T alone exceeds the limit (unsupported).
+int attn_bwd_chunk_seqs(int B, int H, int T, int dqk, int dv, DType t);
 hipError_t attn_bwd(const AttnBwd& a, hipStream_t s);
 // (sequence, head, query, key) pairs with key <= query: B H T (T+1) / 2
 double attn_causal_pairs(const Attn& a);

@@ -4,7 +4,10 @@
 
 namespace mla {
 size_t gemm_mfma_scratch_elems(const Gemm& g);
-hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s);
+// Timed as class kc with the given algorithmic FLOPs / bytes (the split-K sum, if any, as
+// an elementwise launch of its own).
+hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s, int kc,
+                     double flops, double bytes);
 // C = scale[0] mask[m] X[m, n] with X = A B^T (mask null = all rows) and part[t] = the sum
 // over output tile t of mask[m] X[m, n]^2, or of mask[m] X[m, n] ref[m, n] (bf16, row
 // stride ldref) when ref is given, in a fixed order; *nparts = the number of tiles (at most
@@ -12,7 +15,7 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
 size_t gemm_mfma_masked_sse_parts(const Gemm& g);
 hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
                                 const void* ref, int64_t ldref, double* part, int* nparts,
-                                hipStream_t s);
+                                hipStream_t s, const char** kernel);
 // Batch entry z of a batched causal GEMM uses A + z sA, B + (z / zdiv) sB1 +
 // ((z % zdiv) / bdiv) sB2 and C + (z / zdiv) sC1 + (z % zdiv) sC2 (elements).  Row m of C
 // sums k < min(K, end of m's 256-row tile) (rev = 0; A M-contiguous, bf16 C) or
@@ -25,6 +28,6 @@ struct GemmBatch {
 };
 hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s);
 bool attn_mfma_supported(int dqk, int dv);
-hipError_t attn_fwd_mfma(const Attn& a, hipStream_t s);
+hipError_t attn_fwd_mfma(const Attn& a, hipStream_t s, const char** kernel);
 hipError_t attn_bwd_mfma(const AttnBwd& w, hipStream_t s);
 }  // namespace mla

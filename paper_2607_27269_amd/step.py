@@ -26,7 +26,8 @@ def _ptr(t):
 
 
 class DeviceStep:
-    def __init__(self, wl: "synth.Workload", device: str = "cuda:0", grads: tuple = None):
+    def __init__(self, wl: "synth.Workload", device: str = "cuda:0", grads: tuple = None,
+                 ws_bytes: int | None = None):
         if not torch.cuda.is_available():
             raise RuntimeError("DeviceStep needs a ROCm GPU")
         L.lib()  # fail loudly if the HIP library is not built
@@ -57,7 +58,9 @@ class DeviceStep:
             if W is not None and name in want:
                 self.grads[name] = torch.full(tuple(W.shape), float("nan"), dtype=torch.float32,
                                               device=dev)
-        self.ws_bytes = L.mla_recon_workspace_size(self.ccfg)
+        # the preferred workspace unless the caller asks for another size (a smaller one
+        # runs the backward's attention in more chunks of sequences)
+        self.ws_bytes = ws_bytes or L.mla_recon_workspace_size(self.ccfg)
         if self.ws_bytes == 0:
             raise L.MlaError(L.MLA_ERR_INVALID_ARG, L.last_error())
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=dev)

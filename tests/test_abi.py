@@ -31,7 +31,7 @@ def test_exports_every_declared_function():
             "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
             "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
             "mla_recon_decode", "mla_recon_decode_workspace_size",
-            "mla_recon_workspace_size",
+            "mla_recon_workspace_size", "mla_recon_workspace_size_min",
             "mla_recon_last_error"} <= set(names)
     lib = ctypes.CDLL(L.LIB_PATH)
     for n in names:
@@ -51,6 +51,32 @@ def test_workspace_size_positive(idx):
     # monotone in the number of tokens
     c2 = L.make_cfg(configs.shrink(configs.get(idx), batch=1, seq=64))
     assert L.mla_recon_workspace_size(c2) < ws
+
+
+@pytest.mark.parametrize("idx", [1, 3, 4])
+def test_workspace_chunks(idx):
+    """The backward's dS^T buffer holds one chunk of sequences: the minimum workspace has
+    room for one sequence's, the preferred one for the whole batch's when that fits 16 GiB,
+    else for as many sequences as fit; one sequence beyond 16 GiB is unsupported."""
+    cfg = configs.get(idx)
+    H, T = cfg.n_heads, cfg.seq
+    ds_seq = H * T * ((T + 63) // 64 * 64) * 2
+    pref = L.mla_recon_workspace_size(L.make_cfg(cfg))
+    lo = L.mla_recon_workspace_size_min(L.make_cfg(cfg))
+    assert 0 < lo < pref
+    assert pref - lo >= (cfg.batch - 1) * ds_seq
+    # a batch whose dS^T exceeds 16 GiB: the preferred workspace stops at the cap
+    nb = 2 * (16 << 30) // ds_seq + 1
+    big = cfg.replace(batch=nb)
+    assert nb * ds_seq > (16 << 30)
+    wbig = L.mla_recon_workspace_size(L.make_cfg(big))
+    assert 0 < wbig < L.mla_recon_workspace_size_min(L.make_cfg(big)) + (16 << 30) + (1 << 30)
+    # fp32 check mode stores no dS^T: one size
+    f32 = L.make_cfg(configs.shrink(cfg, batch=2, seq=64).replace(dtype="fp32"))
+    assert L.mla_recon_workspace_size(f32) == L.mla_recon_workspace_size_min(f32) > 0
+    # one sequence whose dS^T alone exceeds 16 GiB
+    long = L.make_cfg(cfg.replace(batch=1, seq=32768))
+    assert L.mla_recon_workspace_size(long) == 0 and L.mla_recon_workspace_size_min(long) == 0
 
 
 def bad(**kw):

@@ -16,20 +16,20 @@ import pytest
 
 import oracle as O
 from paper_2607_27269_amd import configs, synth
-from parity_util import TOL, compare, rel_err
+from parity_util import LOSS_TOL, TOL, compare, oracle_step, rel_err
 
 pytestmark = pytest.mark.gpu
 
 GRADS = ("dWdq", "dWuq", "dWdkv_kr", "dWuk", "dWuv")
 
 
-def prefix_workload(wl, b, tc):
-    """The same layer restricted to sequence b, tokens 0..tc-1."""
+def prefix_workload(wl, b, tc, nb=1):
+    """The same layer restricted to sequences b .. b+nb-1, tokens 0..tc-1 (all valid)."""
     import copy
     w = copy.copy(wl)
-    w.cfg = wl.cfg.replace(batch=1, seq=tc)
-    w.h = wl.h[b:b + 1, :tc]
-    w.mask = np.ones((1, tc), dtype=np.uint8)
+    w.cfg = wl.cfg.replace(batch=nb, seq=tc)
+    w.h = wl.h[b:b + nb, :tc]
+    w.mask = np.ones((nb, tc), dtype=np.uint8)
     return w
 
 
@@ -78,9 +78,9 @@ def test_fullsize_step(idx):
     pw = prefix_workload(wl, 0, tc)
     A_t, A_s, cache = oracle_fwd(pw)
     compare(dict(A_t=out["A_t"][0, :tc], A_s=out["A_s"][0, :tc]), dict(A_t=A_t[0], A_s=A_s[0]),
-            ("A_t", "A_s"), tol, label=f"cfg{idx} prefix: ")
+            ("A_t", "A_s"), tol, label=f"cfg{idx} prefix: ", cfg=cfg)
     g = O.student_backward(cache, dA[0:1, :tc])
-    errs = compare(out, g, GRADS, tol, label=f"cfg{idx} grads: ")
+    errs = compare(out, g, GRADS, tol, label=f"cfg{idx} grads: ", cfg=cfg)
     print(f"[fullsize] cfg{idx} grad errs {errs}", flush=True)
 
     # the whole last sequence: sampled rows including the final tokens
@@ -111,5 +111,82 @@ def test_fullsize_loss(idx):
     assert abs(got[1] - rel) <= 1e-5 * rel, (got[1], rel)
     gdA = dev.dA.double().cpu().numpy().reshape(dA.shape)
     assert rel_err(gdA, dA) <= 4e-3
+    del dev
+    torch.cuda.empty_cache()
+
+
+# the sequence whose tokens alone are valid in the one-sequence mask (last / an inner one)
+WHOLE_SEQ = {3: 3, 4: 1}
+
+
+@pytest.mark.parametrize("idx", [3, 4])
+def test_fullsize_timed_step_one_sequence(idx):
+    """The call the benchmark times, at full size and in its launch configuration:
+    mla_recon_step without dA (o_s - o_t, the W_O^T W_O product with the masked-loss
+    epilogue summed over its tile partials, dO = 2 M Y / (D sum M), the whole backward).
+    The mask keeps one whole sequence, so Eq. 11 and every gradient equal those of that
+    sequence alone, which the oracle evaluates: every dS^T entry of that sequence, the
+    long-range dV / dK / dQ sums and the split-K reductions over all 16384 rows carry real
+    data.  The four-call step on the same device state (A_t, A_s, Eq. 11, dA non-zero over
+    the whole sequence, backward) must agree as well."""
+    import torch
+    from paper_2607_27269_amd.step import DeviceStep
+    cfg = configs.get(idx)
+    B, T = cfg.batch, cfg.seq
+    bs = WHOLE_SEQ[idx]
+    print(f"[fullsize] timed step, config {idx}, mask = sequence {bs} of {B} x {T}", flush=True)
+    wl = synth.make_workload(cfg, lengths=[T if b == bs else 0 for b in range(B)])
+    ref = oracle_step(prefix_workload(wl, bs, T))
+    print(f"[fullsize] oracle loss {ref['loss']:.6e} rel {ref['rel']:.6e}", flush=True)
+    tol = TOL[cfg.dtype]
+    dev = DeviceStep(wl)
+
+    dev.fused_step(with_dA=False)
+    out = dev.results()
+    assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
+    errs = compare(out, ref, GRADS, tol, label=f"cfg{idx} timed step: ", cfg=cfg)
+    print(f"[fullsize] timed step loss {out['loss']:.6e} grad errs {errs}", flush=True)
+    fused_loss = out["loss"]
+
+    dev.step()
+    out = dev.results()
+    assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
+    assert abs(out["rel"] - ref["rel"]) <= LOSS_TOL * abs(ref["rel"]), (out["rel"], ref["rel"])
+    assert abs(out["loss"] - fused_loss) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], fused_loss)
+    sel = dict(A_t=out["A_t"][bs], A_s=out["A_s"][bs], dA=out["dA"][bs],
+               **{n: out[n] for n in GRADS if n in out})
+    errs = compare(sel, dict(A_t=ref["A_t"][0], A_s=ref["A_s"][0], dA=ref["dA"][0],
+                             **{n: ref[n] for n in GRADS}),
+                   ("A_t", "A_s", "dA") + GRADS, tol, label=f"cfg{idx} four-call: ", cfg=cfg)
+    others = [b for b in range(B) if b != bs]
+    assert not out["dA"][others].any(), "dA must vanish on masked sequences"
+    print(f"[fullsize] four-call errs {errs}", flush=True)
+    del dev
+    torch.cuda.empty_cache()
+
+
+def test_chunked_backward_fullsize():
+    """The timed call with the smallest workspace: the backward's attention then runs one
+    sequence per pass (4 chunks at the Llama-3-8B-shaped layer) with the dS^T buffer,
+    gathered keys, statistics and dK scratch reused by every chunk and the per-token
+    results written at each chunk's offset.  The mask keeps sequences 1 and 2 (two
+    chunks): the gradients sum both and equal the oracle's on those two sequences alone."""
+    import torch
+    from paper_2607_27269_amd import _lib as L
+    from paper_2607_27269_amd.step import DeviceStep
+    cfg = configs.get(3)
+    B, T = cfg.batch, cfg.seq
+    ws_min = L.mla_recon_workspace_size_min(L.make_cfg(cfg))
+    ws_pref = L.mla_recon_workspace_size(L.make_cfg(cfg))
+    print(f"[fullsize] chunked backward, workspace {ws_min} of {ws_pref} bytes", flush=True)
+    assert 0 < ws_min < ws_pref
+    wl = synth.make_workload(cfg, lengths=[0, T, T, 0])
+    ref = oracle_step(prefix_workload(wl, 1, T, nb=2))
+    dev = DeviceStep(wl, ws_bytes=ws_min)
+    dev.fused_step(with_dA=False)
+    out = dev.results()
+    assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
+    errs = compare(out, ref, GRADS, TOL[cfg.dtype], label="chunked: ", cfg=cfg)
+    print(f"[fullsize] chunked backward grad errs {errs}", flush=True)
     del dev
     torch.cuda.empty_cache()

@@ -51,7 +51,7 @@ def test_step_parity(name):
     dev.step()
     out = dev.results()
     tol = TOL[cfg.dtype]
-    errs = compare(out, ref, ("A_t", "A_s") + GRADS, tol, label=f"{name}: ")
+    errs = compare(out, ref, ("A_t", "A_s") + GRADS, tol, label=f"{name}: ", cfg=cfg)
     assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
     assert abs(out["rel"] - ref["rel"]) <= LOSS_TOL * abs(ref["rel"]), (out["rel"], ref["rel"])
     print(f"[parity] {name} loss={out['loss']:.6e} ref={ref['loss']:.6e} errs={errs}", flush=True)
@@ -75,7 +75,7 @@ def test_fused_step_parity(name, with_dA):
     dev.fused_step(with_dA)
     out = dev.results()
     tol = TOL[cfg.dtype]
-    errs = compare(out, ref, (("dA",) if with_dA else ()) + GRADS, tol, label=f"fused {name}: ")
+    errs = compare(out, ref, (("dA",) if with_dA else ()) + GRADS, tol, label=f"fused {name}: ", cfg=cfg)
     assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
     assert math.isnan(out["rel"])
     # the separate path on the same device state gives the same loss
@@ -103,7 +103,7 @@ def test_cached_teacher_parity(name):
     second = dev.results()
     tol = TOL[cfg.dtype]
     for out, names in ((first, GRADS), (second, ("dA",) + GRADS)):
-        compare(out, ref, names, tol, label=f"cached {name}: ")
+        compare(out, ref, names, tol, label=f"cached {name}: ", cfg=cfg)
         assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
     if cfg.dtype == "fp32":
         for n in GRADS:
@@ -142,3 +142,30 @@ def test_loss_kernel_parity(dtype):
     dev.loss(tA_s, tA_t)
     torch.cuda.synchronize()
     assert float(dev.loss_buf[0]) == 0.0 and not dev.dA.any()
+
+
+@pytest.mark.parametrize("name", ("cfg1_ragged", "cfg3_long"))
+def test_chunked_backward_parity(name):
+    """The smallest workspace (one sequence per pass of the backward's attention) gives the
+    oracle's gradients, and the same as the preferred workspace up to rounding order."""
+    from paper_2607_27269_amd import _lib as L
+    from paper_2607_27269_amd.step import DeviceStep
+    cfg, wl = make_case(name)
+    if cfg.batch < 2:
+        cfg = cfg.replace(batch=3)
+        wl = synth.make_workload(cfg, lengths=[cfg.seq, cfg.seq - 3, 100])
+    print(f"[parity] chunked backward case={name} B={cfg.batch}", flush=True)
+    ref = oracle_step(wl)
+    ws_min = L.mla_recon_workspace_size_min(L.make_cfg(cfg))
+    assert ws_min < L.mla_recon_workspace_size(L.make_cfg(cfg))
+    dev = DeviceStep(wl, ws_bytes=ws_min)
+    for with_dA in (False, True):
+        dev.fused_step(with_dA)
+        out = dev.results()
+        assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
+        compare(out, ref, (("dA",) if with_dA else ()) + GRADS, TOL[cfg.dtype],
+                label=f"chunked {name}: ", cfg=cfg)
+    dev.step()
+    out = dev.results()
+    compare(out, ref, ("A_t", "A_s") + GRADS, TOL[cfg.dtype], label=f"chunked four-call {name}: ",
+            cfg=cfg)
