@@ -228,6 +228,21 @@ int mla_recon_decode(const mla_recon_cfg *cfg, const void *q, const void *cache,
                      const int32_t *lengths, const void *Wuk, const void *Wuv, void *o, void *ws,
                      size_t ws_bytes, void *hip_stream);
 
+/* mla_recon_decode without a workspace, for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops that decode one token per call, harnesses
+ * that forbid allocation).  Same arguments and result as mla_recon_decode minus ws; the
+ * scratch lives in a static buffer of MLA_DECODE_NOALLOC_SCRATCH_BYTES (32 MiB) that the
+ * library holds on each GPU it runs on until the process ends, and this call allocates
+ * nothing.  Returns MLA_ERR_UNSUPPORTED when mla_recon_decode_workspace_size(cfg, max_len)
+ * exceeds that buffer (e.g. H = 32, r_kv = 512: up to about 100 sequences).  Every call on
+ * one GPU uses the same buffer and overwrites what the previous call left there: calls that
+ * may overlap on one GPU (concurrent streams, threads) race and must be serialised by the
+ * caller. */
+#define MLA_DECODE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int mla_recon_decode_noalloc(const mla_recon_cfg *cfg, const void *q, const void *cache,
+                             int32_t max_len, const int32_t *lengths, const void *Wuk,
+                             const void *Wuv, void *o, void *hip_stream);
+
 /* Text of the last error on the calling thread ("" if none). */
 const char *mla_recon_last_error(void);
 

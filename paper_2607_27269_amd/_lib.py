@@ -21,6 +21,8 @@ MLA_ERR_WORKSPACE = -3
 MLA_ERR_HIP = -4
 MLA_BF16 = 0
 MLA_FP32 = 1
+# static scratch of mla_recon_decode_noalloc (include/mla_recon.h)
+MLA_DECODE_NOALLOC_SCRATCH_BYTES = 32 << 20
 
 (KC_GEMM_NT, KC_GEMM_NN, KC_GEMM_TN, KC_ATTN_FWD, KC_ATTN_DKDV, KC_ATTN_DQ, KC_LOSS, KC_ELEM,
  KC_ATTN_DK) = range(9)
@@ -110,6 +112,7 @@ def lib() -> ctypes.CDLL:
         L.mla_recon_decode_workspace_size.argtypes = [P(Cfg), i32]
         L.mla_recon_decode_workspace_size.restype = sz
         L.mla_recon_decode.argtypes = [P(Cfg), vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.mla_recon_decode_noalloc.argtypes = [P(Cfg), vp, vp, i32, vp, vp, vp, vp, vp]
         L.mla_recon_adamw.argtypes = [P(AdamwTensor), i32, i32, i32, ctypes.c_float,
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                       ctypes.c_float, vp]
@@ -118,7 +121,7 @@ def lib() -> ctypes.CDLL:
         for f in ("mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
                   "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
                   "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
-                  "mla_recon_decode",
+                  "mla_recon_decode", "mla_recon_decode_noalloc",
                   "mla_recon_prof_enable",
                   "mla_recon_prof_read"):
             getattr(L, f).restype = i32
@@ -223,6 +226,12 @@ def mla_recon_decode(cfg: Cfg, q: int, cache: int, max_len: int, lengths: int, W
                      Wuv: int, o: int, ws: int, ws_bytes: int, stream: int) -> None:
     _check(lib().mla_recon_decode(ctypes.byref(cfg), q, cache, max_len, lengths, Wuk, Wuv, o, ws,
                                   ws_bytes, stream))
+
+
+def mla_recon_decode_noalloc(cfg: Cfg, q: int, cache: int, max_len: int, lengths: int, Wuk: int,
+                             Wuv: int, o: int, stream: int) -> None:
+    _check(lib().mla_recon_decode_noalloc(ctypes.byref(cfg), q, cache, max_len, lengths, Wuk,
+                                          Wuv, o, stream))
 
 
 def mla_recon_prof_enable(kclass: int, on: bool) -> None:

@@ -709,26 +709,62 @@ size_t mla_recon_decode_workspace_size(const mla_recon_cfg* cfg, int32_t max_len
                          max_len);
 }
 
+static int decode_args(const mla_recon_cfg* cfg, const void* q, const void* cache,
+                       const int32_t* lengths, const void* Wuk, const void* Wuv, void* o,
+                       const char* who) {
+  if (!q || !cache || !lengths || !Wuk || !Wuv || !o)
+    return fail(MLA_ERR_INVALID_ARG, "%s: NULL pointer argument", who);
+  if (((uintptr_t)q | (uintptr_t)cache | (uintptr_t)Wuv) % 16)
+    return fail(MLA_ERR_INVALID_ARG, "%s: q, cache and Wuv must be 16-byte aligned", who);
+  return MLA_OK;
+}
+
+static Decode decode_of(const mla_recon_cfg* cfg, const void* q, const void* cache, int32_t max_len,
+                        const int32_t* lengths, const void* Wuk, const void* Wuv, void* o, void* ws) {
+  Decode d;
+  d.B = cfg->batch; d.H = cfg->n_heads; d.dn = cfg->nope_dim; d.dr = cfg->rope_dim;
+  d.rkv = cfg->kv_rank; d.dv = cfg->head_dim; d.hpg = cfg->n_heads / cfg->s_kv_groups;
+  d.q = q; d.cache = cache; d.Lmax = max_len; d.ldc = cfg->kv_rank + cfg->rope_dim;
+  d.len = lengths; d.Wuk = Wuk; d.Wuv = Wuv; d.scale = cfg->softmax_scale; d.o = o; d.ws = ws;
+  return d;
+}
+
 int mla_recon_decode(const mla_recon_cfg* cfg, const void* q, const void* cache, int32_t max_len,
                      const int32_t* lengths, const void* Wuk, const void* Wuv, void* o, void* ws,
                      size_t ws_bytes, void* hip_stream) {
   g_err[0] = 0;
   int rc = decode_check(cfg, max_len);
   if (rc) return rc;
-  if (!q || !cache || !lengths || !Wuk || !Wuv || !o || !ws)
-    return fail(MLA_ERR_INVALID_ARG, "decode: NULL pointer argument");
-  if (((uintptr_t)q | (uintptr_t)cache | (uintptr_t)Wuv | (uintptr_t)ws) % 16)
-    return fail(MLA_ERR_INVALID_ARG, "decode: q, cache, Wuv and ws must be 16-byte aligned");
+  if ((rc = decode_args(cfg, q, cache, lengths, Wuk, Wuv, o, "decode"))) return rc;
+  if (!ws) return fail(MLA_ERR_INVALID_ARG, "decode: NULL workspace");
+  if ((uintptr_t)ws % 16) return fail(MLA_ERR_INVALID_ARG, "decode: ws must be 16-byte aligned");
   const size_t need = decode_ws_bytes(cfg->batch, cfg->n_heads, cfg->kv_rank + cfg->rope_dim,
                                       cfg->kv_rank, max_len);
   if (ws_bytes < need)
     return fail(MLA_ERR_WORKSPACE, "decode: workspace too small: %zu < %zu bytes", ws_bytes, need);
-  Decode d;
-  d.B = cfg->batch; d.H = cfg->n_heads; d.dn = cfg->nope_dim; d.dr = cfg->rope_dim;
-  d.rkv = cfg->kv_rank; d.dv = cfg->head_dim; d.hpg = cfg->n_heads / cfg->s_kv_groups;
-  d.q = q; d.cache = cache; d.Lmax = max_len; d.ldc = cfg->kv_rank + cfg->rope_dim;
-  d.len = lengths; d.Wuk = Wuk; d.Wuv = Wuv; d.scale = cfg->softmax_scale; d.o = o; d.ws = ws;
-  HIP_TRY(decode_attention(d, (hipStream_t)hip_stream));
+  HIP_TRY(decode_attention(decode_of(cfg, q, cache, max_len, lengths, Wuk, Wuv, o, ws),
+                           (hipStream_t)hip_stream));
+  return MLA_OK;
+}
+
+int mla_recon_decode_noalloc(const mla_recon_cfg* cfg, const void* q, const void* cache,
+                             int32_t max_len, const int32_t* lengths, const void* Wuk,
+                             const void* Wuv, void* o, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = decode_check(cfg, max_len);
+  if (rc) return rc;
+  if ((rc = decode_args(cfg, q, cache, lengths, Wuk, Wuv, o, "decode_noalloc"))) return rc;
+  const size_t need = decode_ws_bytes(cfg->batch, cfg->n_heads, cfg->kv_rank + cfg->rope_dim,
+                                      cfg->kv_rank, max_len);
+  if (need > decode_scratch_bytes())
+    return fail(MLA_ERR_UNSUPPORTED,
+                "decode_noalloc: %d sequences over %d rows need %zu bytes of scratch, above the "
+                "%zu-byte static buffer (use mla_recon_decode with a workspace)",
+                cfg->batch, max_len, need, decode_scratch_bytes());
+  void* ws = nullptr;
+  HIP_TRY(decode_scratch(&ws));
+  HIP_TRY(decode_attention(decode_of(cfg, q, cache, max_len, lengths, Wuk, Wuv, o, ws),
+                           (hipStream_t)hip_stream));
   return MLA_OK;
 }
 

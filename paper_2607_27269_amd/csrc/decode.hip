@@ -24,11 +24,45 @@
 //   unnormalised output) per split.
 // * decode_combine_kernel: merges the splits of a (sequence, head) in split order.
 // * uv_proj_kernel: o = W_UV[g] (latent), one thread per output.
+#include <mutex>
+
 #include "attn_common.h"
 #include "kernels.h"
 #include "mfma.h"
+#include "mla_recon.h"
 
 namespace mla {
+
+// Scratch of the allocation-free decoding entry point (mla_recon_decode_noalloc): a
+// file-scope device array, one copy per GPU, held until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in symbol): it uses
+// the per-device address hipGetSymbolAddress returns, obtained once per device with that
+// device current.
+constexpr size_t DECODE_SCRATCH_BYTES = MLA_DECODE_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) char scratch[DECODE_SCRATCH_BYTES];
+
+constexpr int SCRATCH_MAX_DEVICES = 64;
+static std::mutex g_scratch_mu;
+static void* g_scratch_ptr[SCRATCH_MAX_DEVICES];
+
+size_t decode_scratch_bytes() { return DECODE_SCRATCH_BYTES; }
+
+hipError_t decode_scratch(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= SCRATCH_MAX_DEVICES) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (p == nullptr) return hipErrorInvalidSymbol;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 namespace {
 

@@ -190,6 +190,10 @@ struct Decode {
 };
 bool decode_supported(int DK, int DVL);
 size_t decode_ws_bytes(int B, int H, int DK, int DVL, int Lmax);
+// The static scratch of the allocation-free entry point: its size, and its address on the
+// current device (looked up once per device).
+size_t decode_scratch_bytes();
+hipError_t decode_scratch(void** out);
 hipError_t decode_attention(const Decode& d, hipStream_t s);
 
 // out = a - b elementwise over n elements of dtype t (fp32 arithmetic)

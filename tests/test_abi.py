@@ -220,3 +220,22 @@ def test_decode_configuration_checked():
 def test_prof_class_validation():
     with pytest.raises(L.MlaError):
         L.mla_recon_prof_read(99)
+
+
+def test_decode_noalloc_rejects_before_any_launch():
+    """Validation of the allocation-free decode happens on the host before any HIP call:
+    an invalid or oversized call returns its error here, without a GPU."""
+    cfg = configs.get(3)
+    big = L.make_cfg(cfg.replace(batch=512, seq=4096))
+    assert L.mla_recon_decode_workspace_size(big, 4096) > L.MLA_DECODE_NOALLOC_SCRATCH_BYTES
+    with pytest.raises(L.MlaError) as e:
+        L.mla_recon_decode_noalloc(big, 256, 256, 4096, 256, 256, 256, 256, None)
+    assert e.value.code == L.MLA_ERR_UNSUPPORTED and "static buffer" in L.last_error()
+    small = L.make_cfg(cfg.replace(batch=4, seq=64))
+    with pytest.raises(L.MlaError) as e:  # NULL output
+        L.mla_recon_decode_noalloc(small, 256, 256, 64, 256, 256, 256, 0, None)
+    assert e.value.code == L.MLA_ERR_INVALID_ARG
+    with pytest.raises(L.MlaError) as e:  # two positional keys: not an MQA problem
+        L.mla_recon_decode_noalloc(L.make_cfg(configs.get(4).replace(batch=4)), 256, 256, 64, 256,
+                                   256, 256, 256, None)
+    assert e.value.code == L.MLA_ERR_UNSUPPORTED
