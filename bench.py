@@ -65,8 +65,9 @@ def parse():
 def rocprof_label(name):
     """The instrumentation's name for a kernel rocprofv3 reports as `name`."""
     import re
-    base = name.split("(")[0] if not name.startswith("void ") else name[5:].split("(")[0]
-    base = base.replace("mla::", "").replace("attn::", "").replace("(anonymous namespace)::", "")
+    base = name[5:] if name.startswith("void ") else name
+    base = base.replace("(anonymous namespace)::", "").replace("mla::", "").replace("attn::", "")
+    base = base.split("(")[0]
     m = re.match(r"(\w+)<(.*)>$", base.strip())
     if not m:
         return base.strip()
@@ -81,7 +82,7 @@ def rocprof_label(name):
         return f"{fn}<{args[0]},{args[1]},{'dK' if args[4] == 'true' else 'dQ'},{ty(args[6])}>"
     if fn in ("attn_fwd_persist_kernel", "attn_fwd_mfma_kernel") and len(args) >= 3:
         return f"{fn}<{args[0]},{args[1]}{',lse' if args[2] == 'true' else ''}>"
-    if fn == "attn_dv_mfma_kernel":
+    if fn.startswith("attn_dv_"):
         return f"{fn}<{args[0]},{args[1]}>"
     return fn
 
