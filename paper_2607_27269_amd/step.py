@@ -153,7 +153,56 @@ class DeviceStep:
             self.optimizer_step(lr, **adamw)
         return losses.cpu()
 
+    # ---- training over calibration minibatches (E_b of Eq. 11) ------------------------
+    def set_minibatch(self, h: torch.Tensor, mask: torch.Tensor | None = None):
+        """Run the following calls on another calibration minibatch already in HBM: h
+        [B*T, D] in the storage dtype (referenced, not copied), mask [B*T] uint8 (copied;
+        default all tokens valid)."""
+        if h.shape != self.h.shape or h.dtype != self.h.dtype or h.device != self.h.device:
+            raise ValueError("minibatch must match the layer's [B*T, D] shape, dtype and device")
+        self.h = h
+        if mask is None:
+            self.mask.fill_(1)
+        else:
+            self.mask.copy_(mask.reshape(-1))
+
+    def train_minibatches(self, minibatches, epochs: int, lr: float,
+                          steps_per_minibatch: int = 1, masks=None, **adamw) -> torch.Tensor:
+        """E_b of Eq. 11 by stochastic optimisation: `epochs` passes over the calibration
+        minibatches in order; on each one the frozen teacher's output is computed once
+        (mla_recon_teacher_cache), then `steps_per_minibatch` student steps
+        (mla_recon_student_step), each followed by AdamW.  Returns the loss before each
+        update (host fp32 [epochs * len(minibatches) * steps_per_minibatch])."""
+        if not hasattr(self, "opt"):
+            self.init_optimizer()
+        n = epochs * len(minibatches) * steps_per_minibatch
+        losses = torch.empty(n, dtype=torch.float32, device=self.device)
+        i = 0
+        for _ in range(epochs):
+            for k, h in enumerate(minibatches):
+                self.set_minibatch(h, None if masks is None else masks[k])
+                self.teacher_cache()
+                for _ in range(steps_per_minibatch):
+                    self.student_step(with_dA=False)
+                    losses[i] = self.loss_buf[0]
+                    self.optimizer_step(lr, **adamw)
+                    i += 1
+        return losses.cpu()
+
+    def eval_loss(self, h: torch.Tensor | None = None, mask: torch.Tensor | None = None) -> float:
+        """Eq. 11 on a minibatch (e.g. a held-out one) without computing gradients."""
+        if h is not None:
+            self.set_minibatch(h, mask)
+        none = L.StudentGrads(None, None, None, None, None)
+        L.mla_recon_step(self.ccfg, _ptr(self.h), self.tw, self.sw, _ptr(self.mask),
+                         _ptr(self.loss_buf), None, none, _ptr(self.ws), self.ws_bytes, self.stream)
+        return float(self.loss_buf[0].cpu())
+
     def upload(self, x: np.ndarray, dtype: str | None = None) -> torch.Tensor:
+        """A host array on this device in `dtype` (default the storage dtype); 3-d token
+        arrays [B, T, D] become [B*T, D]."""
+        if x.ndim == 3:
+            x = x.reshape(-1, x.shape[-1])
         return _dev_tensor(x, dtype or self.dtype, self.device)
 
     def results(self) -> dict:

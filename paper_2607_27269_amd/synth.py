@@ -107,10 +107,12 @@ def make_rng(seed: int) -> np.random.Generator:
 # ----------------------------------------------------------------------------
 
 
-def hidden_states(cfg: LayerConfig, rng: np.random.Generator) -> np.ndarray:
-    """RMS-normalised Gaussian tokens with optional outlier channels."""
+def hidden_states(cfg: LayerConfig, rng: np.random.Generator, perm=None) -> np.ndarray:
+    """RMS-normalised Gaussian tokens with optional outlier channels (the first
+    cfg.outlier_channels entries of `perm`, drawn here when not given)."""
     h = rng.standard_normal((cfg.batch, cfg.seq, cfg.hidden))
-    perm = rng.permutation(cfg.hidden)
+    if perm is None:
+        perm = rng.permutation(cfg.hidden)
     if cfg.outlier_channels:
         h[..., perm[: cfg.outlier_channels]] *= cfg.outlier_scale
     h /= np.sqrt(np.mean(h * h, axis=-1, keepdims=True) + 1e-6)
@@ -306,6 +308,25 @@ def make_workload(cfg: LayerConfig, lengths=None, dtype: str | None = None,
                     inv_freq_t=to_f32(inv_freq_t).astype(np.float64),
                     Wdq=r(Wdq), Wuq=r(Wuq), Wdkv_kr=r(Wdkv_kr), Wuk=r(Wuk), Wuv=r(Wuv),
                     inv_freq_s=to_f32(inv_freq_s).astype(np.float64), kept_pairs=kept)
+
+
+def outlier_permutation(cfg: LayerConfig, seed: int | None = None) -> np.ndarray:
+    """The channel permutation make_workload(cfg, seed=seed) draws (its first
+    cfg.outlier_channels entries are the outlier channels of that layer's inputs)."""
+    rng = make_rng(cfg.seed if seed is None else seed)
+    rng.standard_normal((cfg.batch, cfg.seq, cfg.hidden))
+    return rng.permutation(cfg.hidden)
+
+
+def calibration_minibatches(cfg: LayerConfig, n: int, seed: int, dtype: str | None = None,
+                            base_seed: int | None = None) -> list:
+    """`n` more calibration minibatches [B, T, D] for the layer of make_workload(cfg,
+    seed=base_seed): fresh tokens (minibatch k from seed + k) with the same outlier
+    channels, rounded to the storage dtype.  They stand in for further batches of cached
+    layer inputs of the same model."""
+    perm = outlier_permutation(cfg, base_seed)
+    return [round_to(hidden_states(cfg, make_rng(seed + k), perm), dtype or cfg.dtype)
+            for k in range(n)]
 
 
 def random_outputs(cfg: LayerConfig, seed: int, dtype: str = "fp32", scale: float = 1.0):

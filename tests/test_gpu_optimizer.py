@@ -65,9 +65,10 @@ def test_adamw_kernel_parity(dtype):
             assert np.array_equal(t["w"].double().cpu().numpy(), want)
 
 
-def _oracle_train(wl, steps, lr, adamw):
+def _oracle_train(wl, steps, lr, adamw, schedule=None):
     """The oracle loop: Eq. 11 step, then AdamW on fp64 masters; the forward uses the
-    weights in storage precision (bf16-rounded masters), as the device loop does."""
+    weights in storage precision (bf16-rounded masters), as the device loop does.  With a
+    schedule, step t runs on the hidden states schedule[t] (all tokens valid)."""
     import oracle as O
     names = ("Wdq", "Wuq", "Wdkv_kr", "Wuk", "Wuv")
     gnames = {"Wdq": "dWdq", "Wuq": "dWuq", "Wdkv_kr": "dWdkv_kr", "Wuk": "dWuk", "Wuv": "dWuv"}
@@ -78,6 +79,9 @@ def _oracle_train(wl, steps, lr, adamw):
     for t in range(1, steps + 1):
         for n, w in master.items():
             setattr(wl, n, _bf16_round(w) if wl.cfg.dtype == "bf16" else w)
+        if schedule is not None:
+            wl.h = schedule[t - 1]
+            wl.mask = np.ones(wl.h.shape[:2], dtype=np.uint8)
         ref = oracle_step(wl)
         losses.append(ref["loss"])
         for n in master:
@@ -116,3 +120,46 @@ def test_training_reduces_loss():
     print(f"[optimizer] losses {losses}", flush=True)
     assert np.all(np.isfinite(losses))
     assert losses[-1] < 0.7 * losses[0]
+
+
+@pytest.mark.parametrize("dtype,per", [("fp32", 1), ("bf16", 2)])
+def test_minibatch_loop_parity(dtype, per):
+    """E_b of Eq. 11 over four calibration minibatches: the teacher output cached once per
+    minibatch, `per` student steps on it, AdamW after each; the device losses follow the
+    oracle loop on the same schedule (two epochs)."""
+    from paper_2607_27269_amd.step import DeviceStep
+    print(f"[optimizer] minibatch loop dtype={dtype} steps per minibatch={per}", flush=True)
+    cfg = configs.shrink(configs.get(1), batch=2, seq=64).replace(dtype=dtype)
+    f32 = lambda x: float(np.float32(x))
+    lr, adamw = f32(1e-3), dict(beta1=f32(0.9), beta2=f32(0.999), eps=f32(1e-8), weight_decay=0.0)
+    wl = synth.make_workload(cfg)
+    hs = [wl.h] + synth.calibration_minibatches(cfg, 3, seed=500)
+    dev = DeviceStep(wl)
+    tb = [dev.upload(h) for h in hs]
+    got = dev.train_minibatches(tb, 2, lr, steps_per_minibatch=per, **adamw).numpy().astype(np.float64)
+    schedule = [h for _ in range(2) for h in hs for _ in range(per)]
+    want = _oracle_train(synth.make_workload(cfg), len(schedule), lr, adamw, schedule=schedule)
+    print(f"[optimizer] losses device {got} oracle {want}", flush=True)
+    tol = 1e-3 if dtype == "bf16" else 1e-5
+    assert abs(got[0] - want[0]) <= tol * want[0]
+    assert np.all(np.abs(got - want) <= 10 * tol * want)
+    # the minibatches differ: so do their losses at the first pass
+    assert len({round(float(x), 7) for x in got[: 4 * per: per]}) == 4
+
+
+def test_minibatch_training_lowers_heldout_loss():
+    """Training over four calibration minibatches lowers Eq. 11 on a fifth, held-out one."""
+    from paper_2607_27269_amd.step import DeviceStep
+    print("[optimizer] held-out loss", flush=True)
+    cfg = configs.shrink(configs.get(1), batch=2, seq=256)
+    wl = synth.make_workload(cfg)
+    dev = DeviceStep(wl)
+    train = [dev.upload(h) for h in [wl.h] + synth.calibration_minibatches(cfg, 3, seed=600)]
+    held = dev.upload(synth.calibration_minibatches(cfg, 1, seed=700)[0])
+    before = dev.eval_loss(held)
+    losses = dev.train_minibatches(train, 5, 1e-3).numpy()
+    after = dev.eval_loss(held)
+    print(f"[optimizer] held-out loss {before:.4e} -> {after:.4e}; train {losses[0]:.4e} -> {losses[-1]:.4e}",
+          flush=True)
+    assert np.all(np.isfinite(losses)) and np.isfinite(after)
+    assert after < 0.8 * before

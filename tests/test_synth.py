@@ -57,3 +57,19 @@ def test_right_padding_mask():
 def test_flop_model_matches_llama_8b_total():
     f = configs.get(3).total_flops()
     assert f == pytest.approx(6683.6e9, rel=2e-4)
+
+
+def test_calibration_minibatches_share_outlier_channels():
+    """Further calibration minibatches: new tokens, the base layer's outlier channels."""
+    cfg = configs.shrink(configs.get(1), batch=2, seq=32)
+    wl = synth.make_workload(cfg, dtype="fp32")
+    more = synth.calibration_minibatches(cfg, 2, seed=10, dtype="fp32")
+    perm = synth.outlier_permutation(cfg)
+    k = cfg.outlier_channels
+    assert k > 0
+    for h in [wl.h] + more:
+        rms = np.sqrt(np.mean(h.reshape(-1, cfg.hidden) ** 2, axis=0))
+        assert set(np.argsort(rms)[-k:]) == set(perm[:k])
+    assert not np.allclose(more[0], wl.h) and not np.allclose(more[0], more[1])
+    again = synth.calibration_minibatches(cfg, 2, seed=10, dtype="fp32")
+    assert all(np.array_equal(a, b) for a, b in zip(more, again))
