@@ -212,8 +212,9 @@ int mla_recon_residual_rmsnorm(float *x, const float *A, void *h, int64_t rows, 
  * after the attention-weighted latent).  One query token per sequence; cfg->batch
  * sequences; cfg gives H, G_kv, d_nope, d_rope, r_kv, d_k (= d_v) and the softmax scale;
  * cfg->seq is not used.  Requires bf16, a single positional key (s_rope_groups == 1) and
- * (r_kv + d_rope, r_kv) one of (576, 512), (288, 256), (160, 128); MLA_ERR_UNSUPPORTED
- * otherwise.
+ * (r_kv + d_rope, r_kv) one of (576, 512), (288, 256), (160, 128), d_k 64 or 128 and at most
+ * 65535 sequences; MLA_ERR_UNSUPPORTED otherwise.  W_UV is applied to the weighted latent
+ * of each head on the matrix cores (the latent rounded to bf16).
  *   q       [B, H, d_nope + d_rope] bf16: the query token's [q^nope ; R_t q^rope]
  *   cache   [B, max_len, r_kv + d_rope] bf16: rows [c^KV_j | R_j k^PE_j], e.g. the
  *           [c^KV | k^PE] rows of the student forward
@@ -242,6 +243,33 @@ int mla_recon_decode(const mla_recon_cfg *cfg, const void *q, const void *cache,
 int mla_recon_decode_noalloc(const mla_recon_cfg *cfg, const void *q, const void *cache,
                              int32_t max_len, const int32_t *lengths, const void *Wuk,
                              const void *Wuv, void *o, void *hip_stream);
+
+/* Prefill in absorbed form: every token of cfg->batch sequences of cfg->seq tokens attends,
+ * causally, to the latent cache of its own sequence (Eq. 5's rows [c^KV_j | R_j k^PE_j],
+ * j <= t) with the absorbed query [W_UK^T q^nope ; q^rope]; the output is the block's
+ * per-head attention output o = W_UV[g] (weighted latent) and/or its post-W_O output A
+ * (the student side of Eq. 11), computed either as o W_O^T or, given the folded weights of
+ * mla_recon_fold_uv_into_o, as (weighted latent) W_O'^T.  Same shape requirements as
+ * mla_recon_decode, and at most 65535 tokens (batch * seq) per call.
+ *   q     [B, T, H, d_nope + d_rope] bf16 (q^rope rotated by R_t)
+ *   cache [B, T, r_kv + d_rope] bf16
+ *   Wuk [G_kv d_nope, r_kv], Wuv [G_kv d_k, r_kv], Wo [D, H d_k] bf16; Wo_folded
+ *   [D, H r_kv] bf16 or NULL
+ *   o     [B, T, H, d_k] bf16 out, or NULL; A [B, T, D] fp32 out, or NULL (not both NULL;
+ *   A needs Wo_folded, or Wo and Wuv; o needs Wuv)
+ * q, cache, Wuv and ws 16-byte aligned; ws of mla_recon_prefill_workspace_size bytes. */
+size_t mla_recon_prefill_workspace_size(const mla_recon_cfg *cfg);
+int mla_recon_prefill(const mla_recon_cfg *cfg, const void *q, const void *cache, const void *Wuk,
+                      const void *Wuv, const void *Wo, const void *Wo_folded, void *o, float *A,
+                      void *ws, size_t ws_bytes, void *hip_stream);
+
+/* W_UV folded into the frozen W_O (Eq. 5's value up-projection absorbed into the output
+ * projection): Wo_folded[:, i r_kv + c] = sum_e Wo[:, i d_k + e] Wuv[g(i) d_k + e][c] for
+ * every head i, bf16 [D, H r_kv].  With it the block's output is the attention-weighted
+ * latent times Wo_folded^T.  (At r_kv > d_k the folded matrix is r_kv / d_k times larger
+ * than W_O, so the unfolded products are cheaper per token; both are offered.) */
+int mla_recon_fold_uv_into_o(const mla_recon_cfg *cfg, const void *Wo, const void *Wuv,
+                             void *Wo_folded, void *hip_stream);
 
 /* Text of the last error on the calling thread ("" if none). */
 const char *mla_recon_last_error(void);

@@ -113,6 +113,10 @@ def lib() -> ctypes.CDLL:
         L.mla_recon_decode_workspace_size.restype = sz
         L.mla_recon_decode.argtypes = [P(Cfg), vp, vp, i32, vp, vp, vp, vp, vp, sz, vp]
         L.mla_recon_decode_noalloc.argtypes = [P(Cfg), vp, vp, i32, vp, vp, vp, vp, vp]
+        L.mla_recon_prefill_workspace_size.argtypes = [P(Cfg)]
+        L.mla_recon_prefill_workspace_size.restype = sz
+        L.mla_recon_prefill.argtypes = [P(Cfg), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.mla_recon_fold_uv_into_o.argtypes = [P(Cfg), vp, vp, vp, vp]
         L.mla_recon_adamw.argtypes = [P(AdamwTensor), i32, i32, i32, ctypes.c_float,
                                       ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                       ctypes.c_float, vp]
@@ -121,7 +125,8 @@ def lib() -> ctypes.CDLL:
         for f in ("mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
                   "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
                   "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
-                  "mla_recon_decode", "mla_recon_decode_noalloc",
+                  "mla_recon_decode", "mla_recon_decode_noalloc", "mla_recon_prefill",
+                  "mla_recon_fold_uv_into_o",
                   "mla_recon_prof_enable",
                   "mla_recon_prof_read"):
             getattr(L, f).restype = i32
@@ -232,6 +237,20 @@ def mla_recon_decode_noalloc(cfg: Cfg, q: int, cache: int, max_len: int, lengths
                              Wuv: int, o: int, stream: int) -> None:
     _check(lib().mla_recon_decode_noalloc(ctypes.byref(cfg), q, cache, max_len, lengths, Wuk,
                                           Wuv, o, stream))
+
+
+def mla_recon_prefill_workspace_size(cfg: Cfg) -> int:
+    return int(lib().mla_recon_prefill_workspace_size(ctypes.byref(cfg)))
+
+
+def mla_recon_prefill(cfg: Cfg, q: int, cache: int, Wuk: int, Wuv: int, Wo: int, Wo_folded: int,
+                      o: int, A: int, ws: int, ws_bytes: int, stream: int) -> None:
+    _check(lib().mla_recon_prefill(ctypes.byref(cfg), q, cache, Wuk, Wuv, Wo, Wo_folded, o, A, ws,
+                                   ws_bytes, stream))
+
+
+def mla_recon_fold_uv_into_o(cfg: Cfg, Wo: int, Wuv: int, Wo_folded: int, stream: int) -> None:
+    _check(lib().mla_recon_fold_uv_into_o(ctypes.byref(cfg), Wo, Wuv, Wo_folded, stream))
 
 
 def mla_recon_prof_enable(kclass: int, on: bool) -> None:

@@ -699,6 +699,9 @@ static int decode_check(const mla_recon_cfg* cfg, int32_t max_len) {
   if (!decode_supported(cfg->kv_rank + cfg->rope_dim, cfg->kv_rank))
     return fail(MLA_ERR_UNSUPPORTED, "decode: kv_rank %d with rope_dim %d not supported",
                 cfg->kv_rank, cfg->rope_dim);
+  if (cfg->head_dim != 128 && cfg->head_dim != 64)
+    return fail(MLA_ERR_UNSUPPORTED, "decode: d_k must be 64 or 128");
+  if (cfg->batch > 65535) return fail(MLA_ERR_UNSUPPORTED, "decode: at most 65535 sequences per call");
   return MLA_OK;
 }
 
@@ -765,6 +768,90 @@ int mla_recon_decode_noalloc(const mla_recon_cfg* cfg, const void* q, const void
   HIP_TRY(decode_scratch(&ws));
   HIP_TRY(decode_attention(decode_of(cfg, q, cache, max_len, lengths, Wuk, Wuv, o, ws),
                            (hipStream_t)hip_stream));
+  return MLA_OK;
+}
+
+// ---- absorbed-form prefill and the W_UV fold -------------------------------------------
+static size_t prefill_layout(const mla_recon_cfg* cfg, size_t* off_o, size_t* off_lat) {
+  const int64_t rows = (int64_t)cfg->batch * cfg->seq;
+  const int DK = cfg->kv_rank + cfg->rope_dim, DVL = cfg->kv_rank;
+  size_t o = al(decode_ws_bytes((int)rows, cfg->n_heads, DK, DVL, cfg->seq));
+  *off_o = o;
+  o += al((size_t)rows * cfg->n_heads * cfg->head_dim * 2);
+  *off_lat = o;
+  o += al((size_t)rows * cfg->n_heads * DVL * 2);
+  return o;
+}
+
+static int prefill_check(const mla_recon_cfg* cfg) {
+  int rc = decode_check(cfg, cfg ? cfg->seq : 0);
+  if (rc) return rc;
+  if ((int64_t)cfg->batch * cfg->seq > 65535)
+    return fail(MLA_ERR_UNSUPPORTED, "prefill: at most 65535 tokens per call");
+  return MLA_OK;
+}
+
+size_t mla_recon_prefill_workspace_size(const mla_recon_cfg* cfg) {
+  g_err[0] = 0;
+  if (prefill_check(cfg)) return 0;
+  size_t a, b;
+  return prefill_layout(cfg, &a, &b);
+}
+
+int mla_recon_prefill(const mla_recon_cfg* cfg, const void* q, const void* cache, const void* Wuk,
+                      const void* Wuv, const void* Wo, const void* Wo_folded, void* o, float* A,
+                      void* ws, size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = prefill_check(cfg);
+  if (rc) return rc;
+  if (!q || !cache || !Wuk || !ws) return fail(MLA_ERR_INVALID_ARG, "prefill: NULL pointer argument");
+  if (!o && !A) return fail(MLA_ERR_INVALID_ARG, "prefill: neither o nor A requested");
+  if (o && !Wuv) return fail(MLA_ERR_INVALID_ARG, "prefill: o needs Wuv");
+  if (A && !Wo_folded && !(Wo && Wuv))
+    return fail(MLA_ERR_INVALID_ARG, "prefill: A needs Wo_folded, or Wo and Wuv");
+  if (((uintptr_t)q | (uintptr_t)cache | (uintptr_t)ws | (uintptr_t)(Wuv ? Wuv : q)) % 16)
+    return fail(MLA_ERR_INVALID_ARG, "prefill: q, cache, Wuv and ws must be 16-byte aligned");
+  size_t off_o, off_lat;
+  const size_t need = prefill_layout(cfg, &off_o, &off_lat);
+  if (ws_bytes < need)
+    return fail(MLA_ERR_WORKSPACE, "prefill: workspace too small: %zu < %zu bytes", ws_bytes, need);
+  hipStream_t s = (hipStream_t)hip_stream;
+  const int rows = cfg->batch * cfg->seq, H = cfg->n_heads, D = cfg->hidden;
+  const int dv = cfg->head_dim, rkv = cfg->kv_rank;
+  const bool folded = A && Wo_folded;
+  // rows b T + t: token t of sequence b, against the first t + 1 rows of its cache
+  Decode d = decode_of(cfg, q, cache, cfg->seq, nullptr, Wuk, Wuv, nullptr, ws);
+  d.B = rows;
+  d.tps = cfg->seq;
+  void* obuf = o ? o : (A && !folded ? (void*)at(ws, off_o) : nullptr);
+  d.o = obuf;
+  if (folded) d.lat_out = at(ws, off_lat);
+  HIP_TRY(decode_attention(d, s));
+  if (A) {
+    // A = o W_O^T, or with the folded weights A = latent W_O'^T (K = H r_kv)
+    const int K = folded ? H * rkv : H * dv;
+    HIP_TRY(gemm(mk(rows, D, K, folded ? d.lat_out : obuf, K, true, folded ? Wo_folded : Wo, K, true,
+                    A, D, DT_BF16, DT_F32), nullptr, 0, s));
+  }
+  return MLA_OK;
+}
+
+int mla_recon_fold_uv_into_o(const mla_recon_cfg* cfg, const void* Wo, const void* Wuv,
+                             void* Wo_folded, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (cfg->dtype != MLA_BF16) return fail(MLA_ERR_UNSUPPORTED, "fold_uv_into_o: bf16 only");
+  if (!Wo || !Wuv || !Wo_folded) return fail(MLA_ERR_INVALID_ARG, "fold_uv_into_o: NULL pointer argument");
+  const int H = cfg->n_heads, D = cfg->hidden, dv = cfg->head_dim, rkv = cfg->kv_rank;
+  const int hpg = H / cfg->s_kv_groups;
+  hipStream_t s = (hipStream_t)hip_stream;
+  // head i: W_O'[:, i r_kv + c] = sum_e W_O[:, i d_k + e] W_UV[g(i) d_k + e][c]
+  for (int i = 0; i < H; ++i)
+    HIP_TRY(gemm(mk(D, rkv, dv, (const uint16_t*)Wo + (size_t)i * dv, (int64_t)H * dv, true,
+                    (const uint16_t*)Wuv + (size_t)(i / hpg) * dv * rkv, rkv, false,
+                    (uint16_t*)Wo_folded + (size_t)i * rkv, (int64_t)H * rkv, DT_BF16, DT_BF16),
+                 nullptr, 0, s));
   return MLA_OK;
 }
 

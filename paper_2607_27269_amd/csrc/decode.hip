@@ -76,6 +76,8 @@ struct DecodeDev {
   int64_t seq_stride;   // Lmax * ldc
   int ldc;              // row stride of the cache (elements)
   const int32_t* len;   // [B]
+  int tps;              // prefill: query row b is token b % tps of sequence b / tps and
+                        // attends to that sequence's first b % tps + 1 rows (0: decoding)
   int Lmax, HP, nsplit, chunk;
   float sl2;            // softmax scale * log2(e)
   float* part_o;        // [B][nsplit][HP][DVL]
@@ -183,14 +185,14 @@ __global__ __launch_bounds__(64 * DEC_WAVES) void decode_attn_kernel(DecodeDev a
   const int split = blockIdx.x, b = blockIdx.y, h0 = 32 * blockIdx.z;
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5, col = lane & 31;
-  const int len = min(max(a.len[b], 0), a.Lmax);
+  const int len = a.tps ? b % a.tps + 1 : min(max(a.len[b], 0), a.Lmax);
   const int kbeg = split * a.chunk;
   const int kend = min(len, kbeg + a.chunk);
   const int64_t pbase = ((int64_t)b * a.nsplit + split) * a.HP + h0;
   // this wave's share of the K steps
   const int kk0 = wave * NKK / DEC_WAVES, kk1 = (wave + 1) * NKK / DEC_WAVES;
 
-  const bf16_t* cs = a.cache + (int64_t)b * a.seq_stride;
+  const bf16_t* cs = a.cache + (int64_t)(a.tps ? b / a.tps : b) * a.seq_stride;
   KT kt_copy;
   kt_copy.init();
   // key tile t into stage t % NST; rows past the chunk end repeat its last row (finite,
@@ -327,9 +329,10 @@ __global__ __launch_bounds__(64 * DEC_WAVES) void decode_attn_kernel(DecodeDev a
           f32x4{acc[c][4 * g], acc[c][4 * g + 1], acc[c][4 * g + 2], acc[c][4 * g + 3]};
 }
 
-// lat[b][i][d] = sum_s o_s[d] 2^(m_s - M) / sum_s l_s 2^(m_s - M), splits in order
+// lat[b][i][d] = sum_s o_s[d] 2^(m_s - M) / sum_s l_s 2^(m_s - M), splits in order (bf16:
+// the operand of the W_UV product)
 __global__ void decode_combine_kernel(const float* __restrict__ part_o,
-                                      const float* __restrict__ part_ml, float* __restrict__ lat,
+                                      const float* __restrict__ part_ml, bf16_t* __restrict__ lat,
                                       int H, int HP, int nsplit, int DVL) {
   const int b = blockIdx.y, i = blockIdx.x;
   float M = -INFINITY;
@@ -348,27 +351,37 @@ __global__ void decode_combine_kernel(const float* __restrict__ part_o,
       const float m = part_ml[2 * r];
       if (m != -INFINITY) v += part_o[r * DVL + d] * __builtin_amdgcn_exp2f(m - M);
     }
-    lat[((int64_t)b * H + i) * DVL + d] = v * inv;
+    lat[((int64_t)b * H + i) * DVL + d] = f2bf(v * inv);
   }
 }
 
-// o[b][i][d] = sum_c Wuv[g dv + d][c] lat[b][i][c]: one workgroup per (head, sequence), one
-// thread per output (a W_UV row each, read in 16-byte pieces; the latent row is shared)
-__global__ void uv_proj_kernel(const float* __restrict__ lat, const bf16_t* __restrict__ Wuv,
-                               bf16_t* __restrict__ o, int H, int dv, int rkv, int hpg) {
-  const int b = blockIdx.y, i = blockIdx.x;
-  const float* lr = lat + ((int64_t)b * H + i) * rkv;
-  for (int d = threadIdx.x; d < dv; d += blockDim.x) {
-    const bf16_t* w = Wuv + ((int64_t)(i / hpg) * dv + d) * rkv;
-    float v = 0.f;
-    for (int c = 0; c < rkv; c += 8) {
-      const u32x4 ww = *(const u32x4*)(w + c);
+// o[r][i][e] = sum_c W_UV[g dv + e][c] lat[r][i][c] (g = i / hpg) on the matrix cores: a
+// workgroup owns 32 rows of one head, each of its DV / 32 wavefronts 32 of the head's dv
+// outputs; both operands are K-contiguous rows read straight from memory (16 bytes per
+// lane per K step; the workgroup's wavefronts share the latent rows through L1), fp32
+// accumulation over the r_kv latent dims.  bf16 output.
+template <int DV>
+__global__ __launch_bounds__(64 * (DV / 32)) void uv_mfma_kernel(const bf16_t* __restrict__ lat,
+                                                                  const bf16_t* __restrict__ Wuv,
+                                                                  bf16_t* __restrict__ o, int rows,
+                                                                  int H, int rkv, int hpg) {
+  const int i = blockIdx.y, r0 = 32 * blockIdx.x;
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int half = lane >> 5, col = lane & 31;
+  const int r = min(r0 + col, rows - 1);
+  const bf16_t* ap = lat + ((int64_t)r * H + i) * rkv + 8 * half;
+  const bf16_t* bp = Wuv + ((int64_t)(i / hpg) * DV + 32 * wave + col) * rkv + 8 * half;
+  f32x16 acc;
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        v += lr[c + 2 * k] * __uint_as_float(ww[k] << 16) +
-             lr[c + 2 * k + 1] * __uint_as_float(ww[k] & 0xffff0000u);
-    }
-    o[((int64_t)b * H + i) * dv + d] = f2bf(v);
+  for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+  for (int k = 0; k < rkv; k += 16)
+    acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(*(const bf16x8*)(ap + k), *(const bf16x8*)(bp + k),
+                                                  acc, 0, 0, 0);
+  // acc: row r0 + 8 (e / 4) + 4 half + e % 4, output column 32 wave + col
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int rr = r0 + 8 * (e >> 2) + 4 * half + (e & 3);
+    if (rr < rows) o[((int64_t)rr * H + i) * DV + 32 * wave + col] = f2bf(acc[e]);
   }
 }
 
@@ -396,7 +409,7 @@ size_t decode_ws_bytes(int B, int H, int DK, int DVL, int Lmax) {
   const int nsplit = (Lmax + decode_chunk(Lmax, B) - 1) / decode_chunk(Lmax, B);
   auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
   return al((size_t)B * HP * DK * 2) + al((size_t)B * nsplit * HP * DVL * 4) +
-         al((size_t)B * nsplit * HP * 2 * 4) + al((size_t)B * H * DVL * 4);
+         al((size_t)B * nsplit * HP * 2 * 4) + al((size_t)B * H * DVL * 2);
 }
 
 hipError_t decode_attention(const Decode& d, hipStream_t s) {
@@ -413,16 +426,32 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
   w += al((size_t)d.B * nsplit * HP * DVL * 4);
   float* part_ml = (float*)w;
   w += al((size_t)d.B * nsplit * HP * 2 * 4);
-  float* lat = (float*)w;
+  bf16_t* lat = d.lat_out ? (bf16_t*)d.lat_out : (bf16_t*)w;
 
   prof_begin(KC_ELEM, s);
   const int64_t nq = (int64_t)d.B * HP * DK;
   const int G = d.H / d.hpg;
   const int grow = (d.B * d.hpg + 31) / 32;
   // latent part: q_abs[b][i][:rkv] = q^nope[b][i] W_UK[g]
-  group_gemm_kernel<bf16_t><<<dim3((d.rkv + 31) / 32, grow, G), 256, 0, s>>>(
-      (const bf16_t*)d.q, d.dn + d.dr, (const bf16_t*)d.Wuk, qabs, DK, HP, d.B, d.H, d.hpg, d.dn,
-      d.rkv);
+  if (d.tps == 0 || d.dn % 8 || d.rkv % 32) {
+    group_gemm_kernel<bf16_t><<<dim3((d.rkv + 31) / 32, grow, G), 256, 0, s>>>(
+        (const bf16_t*)d.q, d.dn + d.dr, (const bf16_t*)d.Wuk, qabs, DK, HP, d.B, d.H, d.hpg, d.dn,
+        d.rkv);
+  } else {
+    // many query rows (prefill): one matrix-core product per head, [rows, d_nope] x
+    // W_UK[g] ([d_nope, r_kv], N-contiguous)
+    for (int i = 0; i < d.H; ++i) {
+      Gemm g;
+      g.M = d.B; g.N = d.rkv; g.K = d.dn;
+      g.A = (const bf16_t*)d.q + (int64_t)i * (d.dn + d.dr); g.lda = (int64_t)d.H * (d.dn + d.dr);
+      g.a_kmajor = true;
+      g.B = (const bf16_t*)d.Wuk + (int64_t)(i / d.hpg) * d.dn * d.rkv; g.ldb = d.rkv; g.b_kmajor = false;
+      g.C = qabs + (int64_t)i * DK; g.ldc = (int64_t)HP * DK;
+      g.in_t = DT_BF16; g.c_t = DT_BF16; g.alpha = 1.f; g.beta = 0.f;
+      hipError_t e = gemm(g, nullptr, 0, s);
+      if (e != hipSuccess) return e;
+    }
+  }
   {
     const int64_t nrest = (int64_t)d.B * d.H * d.dr + (int64_t)d.B * (HP - d.H) * DK;
     absorb_rest_kernel<<<(unsigned)((nrest + 255) / 256), 256, 0, s>>>(
@@ -432,7 +461,7 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
 
   DecodeDev a;
   a.qabs = qabs; a.cache = (const bf16_t*)d.cache; a.ldc = d.ldc;
-  a.seq_stride = (int64_t)d.Lmax * d.ldc; a.len = d.len; a.Lmax = d.Lmax; a.HP = HP;
+  a.seq_stride = (int64_t)d.Lmax * d.ldc; a.len = d.len; a.tps = d.tps; a.Lmax = d.Lmax; a.HP = HP;
   a.nsplit = nsplit; a.chunk = chunk; a.sl2 = d.scale * attn::LOG2E;
   a.part_o = part_o; a.part_ml = part_ml;
   const dim3 grid(nsplit, d.B, HP / 32);
@@ -447,9 +476,23 @@ hipError_t decode_attention(const Decode& d, hipStream_t s) {
            (double)d.B * d.Lmax * DK * 2, KLABEL("decode_attn_kernel"));
   prof_begin(KC_ELEM, s);
   decode_combine_kernel<<<dim3(d.H, d.B), 256, 0, s>>>(part_o, part_ml, lat, d.H, HP, nsplit, DVL);
-  uv_proj_kernel<<<dim3(d.H, d.B), 128, 0, s>>>(lat, (const bf16_t*)d.Wuv, (bf16_t*)d.o, d.H,
-                                                 d.dv, d.rkv, d.hpg);
-  prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dv * d.rkv, (double)d.B * d.H * (d.dv * 2 + DVL * 4), KLABEL("decode_combine_kernel + uv_proj_kernel"));
+  prof_end(KC_ELEM, s, 0.0, (double)d.B * nsplit * HP * (DVL + 2) * 4 + (double)d.B * d.H * DVL * 2,
+           KLABEL("decode_combine_kernel"));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || d.o == nullptr) return e;
+  // o = W_UV[g] lat per head (matrix cores)
+  prof_begin(KC_ELEM, s);
+  if (d.dv == 128)
+    uv_mfma_kernel<128><<<dim3((d.B + 31) / 32, d.H), 256, 0, s>>>(lat, (const bf16_t*)d.Wuv,
+                                                                   (bf16_t*)d.o, d.B, d.H, d.rkv, d.hpg);
+  else if (d.dv == 64)
+    uv_mfma_kernel<64><<<dim3((d.B + 31) / 32, d.H), 128, 0, s>>>(lat, (const bf16_t*)d.Wuv,
+                                                                  (bf16_t*)d.o, d.B, d.H, d.rkv, d.hpg);
+  else
+    return hipErrorInvalidValue;
+  prof_end(KC_ELEM, s, 2.0 * d.B * d.H * d.dv * d.rkv,
+           (double)d.B * d.H * (d.dv + DVL) * 2 + (double)d.H / d.hpg * d.dv * d.rkv * 2,
+           KLABEL("uv_mfma_kernel"));
   return hipGetLastError();
 }
 

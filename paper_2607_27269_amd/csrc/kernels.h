@@ -185,8 +185,12 @@ struct Decode {
   const void* Wuk;                 // [G_kv dn][rkv]
   const void* Wuv;                 // [G_kv dv][rkv]
   float scale;
-  void* o;                         // [B][H][dv] bf16
+  void* o;                         // [B][H][dv] bf16, or null (no W_UV product)
   void* ws;                        // decode_ws_bytes
+  // prefill: B counts query rows, row b is token b % tps of sequence b / tps and attends to
+  // that sequence's first b % tps + 1 cache rows (len unused); 0 = decoding
+  int tps = 0;
+  void* lat_out = nullptr;         // optional [B][H][rkv] bf16: the attention-weighted latent
 };
 bool decode_supported(int DK, int DVL);
 size_t decode_ws_bytes(int B, int H, int DK, int DVL, int Lmax);

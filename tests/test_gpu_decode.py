@@ -5,6 +5,7 @@ import numpy as np
 import pytest
 
 from paper_2607_27269_amd import configs, synth
+from parity_util import rel_err
 
 pytestmark = pytest.mark.gpu
 
@@ -115,3 +116,66 @@ def test_decode_fullsize_sampled():
         e = np.linalg.norm(got[b] - ref[j]) / np.linalg.norm(ref[j])
         print(f"[decode] full size seq {b} len {lengths[b]}: vs absorbed {e:.2e}", flush=True)
         assert e <= 1e-2
+
+
+@pytest.mark.parametrize("idx,B,T", [(3, 2, 200), (1, 2, 131), (2, 1, 96)])
+def test_prefill_parity(idx, B, T):
+    """Absorbed-form prefill over the latent cache (mla_recon_prefill) against the naive
+    student block of the oracle on the same weights: the per-head outputs o and the
+    post-W_O output A, both with W_O applied after W_UV and with W_UV folded into W_O
+    (mla_recon_fold_uv_into_o, itself checked against the product of the two matrices)."""
+    import torch
+    import oracle as O
+    from paper_2607_27269_amd import _lib as L
+    print(f"[prefill] cfg{idx} B={B} T={T}", flush=True)
+    cfg = configs.shrink(configs.get(idx), batch=B, seq=T)
+    wl = synth.make_workload(cfg)
+    s = wl.student_weights()
+    A_ref, cache = O.student_forward(wl.h, s["Wdq"], s["Wuq"], s["Wdkv_kr"], s["Wuk"], s["Wuv"],
+                                     wl.Wo, s["inv_freq"], n_heads=cfg.n_heads,
+                                     s_kv_groups=cfg.s_kv_groups, s_rope_groups=cfg.s_rope_groups,
+                                     nope_dim=cfg.nope_dim, rope_dim=cfg.rope_dim,
+                                     scale=cfg.softmax_scale)
+    H, dn, dr, rkv, dv, D = cfg.n_heads, cfg.nope_dim, cfg.rope_dim, cfg.kv_rank, cfg.head_dim, cfg.hidden
+    q = np.stack([cache["seq"][b]["qh"] for b in range(B)])                # [B, T, H, dqk]
+    kv = np.concatenate([np.stack([cache["seq"][b]["ckv"] for b in range(B)]),
+                         np.stack([cache["seq"][b]["kh"][:, 0, dn:] for b in range(B)])], axis=-1)
+    o_ref = np.stack([cache["seq"][b]["o"] for b in range(B)])             # [B, T, H, dv]
+    q, kv = _bf16(q), _bf16(kv)
+    c = L.make_cfg(cfg)
+    wsb = L.mla_recon_prefill_workspace_size(c)
+    assert wsb > 0, L.last_error()
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    tq, tkv = _upload(q), _upload(kv)
+    tuk, tuv, two = _upload(s["Wuk"]), _upload(s["Wuv"]), _upload(wl.Wo)
+    to = torch.full((B, T, H, dv), float("nan"), dtype=torch.bfloat16, device="cuda")
+    tA = torch.full((B, T, D), float("nan"), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    L.mla_recon_prefill(c, tq.data_ptr(), tkv.data_ptr(), tuk.data_ptr(), tuv.data_ptr(),
+                        two.data_ptr(), None, to.data_ptr(), tA.data_ptr(), ws.data_ptr(), wsb, stream)
+    # folded W_UV into W_O
+    tfold = torch.empty(D, H * rkv, dtype=torch.bfloat16, device="cuda")
+    L.mla_recon_fold_uv_into_o(c, two.data_ptr(), tuv.data_ptr(), tfold.data_ptr(), stream)
+    tA2 = torch.full((B, T, D), float("nan"), dtype=torch.float32, device="cuda")
+    L.mla_recon_prefill(c, tq.data_ptr(), tkv.data_ptr(), tuk.data_ptr(), None, None,
+                        tfold.data_ptr(), None, tA2.data_ptr(), ws.data_ptr(), wsb, stream)
+    torch.cuda.synchronize()
+    g = H // cfg.s_kv_groups
+    fold_ref = np.concatenate([wl.Wo[:, i * dv:(i + 1) * dv] @ s["Wuv"][(i // g) * dv:(i // g + 1) * dv]
+                               for i in range(H)], axis=1)
+    e_fold = rel_err(tfold.double().cpu().numpy(), fold_ref)
+    got_o = to.double().cpu().numpy()
+    e_o = rel_err(got_o, o_ref)
+    e_A = rel_err(tA.double().cpu().numpy(), A_ref)
+    e_A2 = rel_err(tA2.double().cpu().numpy(), A_ref)
+    print(f"[prefill] cfg{idx}: fold {e_fold:.2e}, o {e_o:.2e}, A {e_A:.2e}, A folded {e_A2:.2e}",
+          flush=True)
+    assert e_fold <= 4e-3
+    assert np.all(np.isfinite(got_o)) and e_o <= 2e-2
+    assert e_A <= 2e-2 and e_A2 <= 2e-2
+    # per-token tiles and per-head blocks (a defect confined to one tile or head)
+    for b in range(B):
+        for t0 in range(0, T, 64):
+            assert rel_err(got_o[b, t0:t0 + 64], o_ref[b, t0:t0 + 64]) <= 2e-2
+        for i in range(H):
+            assert rel_err(got_o[b, :, i], o_ref[b, :, i]) <= 2e-2
