@@ -48,8 +48,8 @@ constexpr int DQ_TILE = 256;
 // A workgroup owns 256 keys of one (sequence, KV group), 32 per wavefront (8 wavefronts,
 // one workgroup per CU), and walks the group's heads and 32-query blocks.  K and V of the
 // lane's key are B-operand fragments held in registers; only the 32-query Q / dO tiles
-// and their softmax statistics pass through LDS, in a ring of two stages, each block's
-// copy issued one step before its use; the more keys share a copied tile, the fewer
+// and their softmax statistics pass through LDS, in a ring of three stages, each block's
+// copy issued two steps before its use; the more keys share a copied tile, the fewer
 // copies per key.  Every wavefront issues the same number of copies per stage (the block
 // count is padded) and of dS^T stores per step, so one counter wait names exactly the
 // copies that must have landed.
@@ -58,7 +58,7 @@ constexpr int DV_BQ = 32;
 // private LDS tile so that each 16-byte store continues its neighbours' along a key row
 // (4 lanes write a row's 64 bytes)
 constexpr int DS_STORES = DV_BQ * 32 * 2 / (64 * 16);
-constexpr int DV_NST = 2;  // LDS stages: a step's copies are issued one step ahead
+constexpr int DV_NST = 3;  // LDS stages: a step's copies are issued two steps ahead
 constexpr int DV_WAVES = 8;
 constexpr int DV_BKB = 32 * DV_WAVES;  // keys per workgroup
 
@@ -272,15 +272,22 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
   stg.init(w, b);
   // steps walk (query block, head): query blocks in descending order with the group's heads
   // innermost, so that all key blocks of a (sequence, group) stream the same Q/dO tile at
-  // the same time and share it through L2.  (qc, hc) is this step's pair, (qn, hn) the
-  // next one (the last step's "next" re-copies the last pair into the free stage).
+  // the same time and share it through L2.  (qc, hc) is this step's pair, (q1, h1) the next
+  // one, (qn, hn) the one whose copies this step issues (step sn = this step + 2, capped at
+  // the last step: past the end the last pair is copied again into the free stage, so that
+  // every step issues the same number of copies).
   int qc = (nqb - 1) * DV_BQ, hc = i0;
-  int qn = qc, hn = hc;
   auto advance = [&](int& q, int& h) {
     if (++h == i0 + hpg) { h = i0; q -= DV_BQ; }
   };
-  if (niter > 1) advance(qn, hn);
-  auto stage_of = [&](int it) { return smem + (it & 1) * Stage::ELEMS; };
+  int q1 = qc, h1 = hc;
+  if (niter > 1) advance(q1, h1);
+  int qn = q1, hn = h1, sn = niter > 1 ? 1 : 0;
+  if (sn < niter - 1) { advance(qn, hn); ++sn; }
+  // (stage offsets through readfirstlane: uniform, added to one per-lane address)
+  auto stage_of = [&](int it) {
+    return smem + __builtin_amdgcn_readfirstlane((it % DV_NST) * Stage::ELEMS);
+  };
   bf16_t* scratch = w.ds_dummy + 64 * lane;
   // transpose tile: key row r holds 64 bytes (32 queries) as four 16-byte segments, segment
   // s stored at position s ^ ((r / 4) % 4) (the packed writes of 32 rows at one segment
@@ -290,7 +297,8 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
   // reader side: lane handles rows rr + 16 j (j < 2), queries 8 sg .. 8 sg + 7
   const int rr = lane >> 2, sg = lane & 3;
   stg.issue(w, b, hc, qc, stage_of(0));
-  wait_vm<0>();
+  stg.issue(w, b, h1, q1, stage_of(1));
+  wait_vm<D>();
   lds_barrier();
 
   for (int it = 0; it < niter; ++it) {
@@ -300,7 +308,7 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
     const float* st_lse = (const float*)(Qs + Stage::OFF_S);
     const float* st_dl = st_lse + DV_BQ;
     // the stage of step it - 1 is free: every wave passed the barrier after reading it
-    stg.issue(w, b, hn, qn, stage_of(it + 1));
+    stg.issue(w, b, hn, qn, stage_of(it + 2));
 
     // this lane's dS^T store targets for the block: key rows kw0 + rr + 16 j, queries
     // q0 + 8 sg .. + 7; rows past the sequence end go to a scratch row instead, so that every
@@ -378,11 +386,12 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
     }
     // step it + 1's copies have landed; younger are only this step's stores (counters
     // complete in issue order)
-    wait_vm<DS_STORES>();
+    // step it + 1's copies have landed; younger are this step's stores, step it + 2's copies
+    // and (from step 1 on) the previous step's stores (counters complete in issue order)
+    if (it == 0) wait_vm<D + DS_STORES>(); else wait_vm<D + 2 * DS_STORES>();
     lds_barrier();
-    qc = qn;
-    hc = hn;
-    if (it + 2 < niter) advance(qn, hn);
+    advance(qc, hc);
+    if (sn < niter - 1) { advance(qn, hn); ++sn; }
   }
 
   // epilogue: this lane's key; rows d = 32c + 8(e/4) + 4 half + e%4
