@@ -358,6 +358,19 @@ def main():
     stop.record()
     torch.cuda.synchronize()
     ms = start.elapsed_time(stop) / args.steps
+    loss = float(dev.loss_buf[0].cpu())
+
+    # also reported: the relative error on request (mla_recon_rel_error after the step; one
+    # more [B T, H d_k] x [H d_k, D] product), timed alone over the same number of calls
+    dev.rel_error()
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(args.steps):
+        dev.rel_error()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_rel = start.elapsed_time(stop) / args.steps
+    rel = float(dev.loss_buf[1].cpu())
 
     # also reported: the step with the teacher cached (its output depends only on h and the
     # frozen weights, so a training loop can compute it once per minibatch)
@@ -445,7 +458,6 @@ def main():
     for k in classes:
         L.mla_recon_prof_enable(k, False)
 
-    loss = float(dev.loss_buf[0])
     tokens = cfg.tokens
     flops = step_flops(cfg)
     tok_s = tokens / (ms / 1e3)
@@ -517,6 +529,8 @@ def main():
                            "frac": round(ca / cp, 4)},
         "other_configs": others,
         "loss": loss,
+        "rel_error": {"value": rel, "ms_per_call": round(ms_rel, 4),
+                      "call": "mla_recon_rel_error after the step"},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(cfg, wl, min(args.cpu_seq, cfg.seq))

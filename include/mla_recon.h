@@ -154,7 +154,8 @@ int mla_recon_bwd(const mla_recon_cfg *cfg, const void *h, const mla_student_w *
  * (o_s - o_t) W_O^T, the only quantity Eq. 11 and its gradient depend on; the step
  * forms o_s - o_t (storage dtype) and applies W_O to it.  tw->Wo is that shared W_O.
  * mask [B, T] uint8 or NULL (all valid).  Writes loss[0] = L (device fp32; loss[1] = NaN:
- * the relative error needs A_t) and the requested gradients (fp32, overwritten).
+ * the relative error needs sum M A_t^2, which mla_recon_rel_error adds on request) and the
+ * requested gradients (fp32, overwritten).
  * dA: NULL, or [B, T, D] (storage dtype, 16-byte aligned) that receives dL/dA_s.  Without
  * dA (bf16), the backward's dL/do_s = dA W_O is taken as 2 M Y / (D sum M) with
  * Y = (o_s - o_t) W_O^T W_O, and each token's squared error as its row of Y dotted with
@@ -178,6 +179,18 @@ int mla_recon_student_step(const mla_recon_cfg *cfg, const void *h, const mla_st
                            const void *Wo, const uint8_t *mask, float *loss, void *dA,
                            const mla_student_grads *grads, void *ws, size_t ws_bytes,
                            void *hip_stream);
+
+/* The relative error of the single-call step (the diagnostic loss[1] of mla_recon_loss:
+ * sum(M (A_s - A_t))^2 / sum(M A_t)^2, Eq. 11's numerator over the teacher's masked
+ * energy).  Call it after mla_recon_step or mla_recon_student_step, on the same stream,
+ * with the same cfg, mask and ws and before any other call uses ws: it reads the teacher
+ * output o_t and the step's fp64 sum of squared differences that the step left in ws, and
+ * writes loss[1] (device fp32 [2]; loss[0] is not touched).  Wo is the teacher's W_O
+ * [D, H*d_k].  Costs one [B T, H d_k] x [H d_k, D] product (A_t = o_t W_O^T, not stored
+ * in bf16 mode), which is why the step leaves it out.  loss[1] = 0 for an all-invalid
+ * mask, +inf when only sum(M A_t)^2 is 0. */
+int mla_recon_rel_error(const mla_recon_cfg *cfg, const void *Wo, const uint8_t *mask,
+                        float *loss, void *ws, size_t ws_bytes, void *hip_stream);
 
 /* Optimizer step of the reconstruction loop (Sec. 4.1 trains the converter-introduced
  * projections but names no optimizer; this is AdamW: bias-corrected Adam moments, weight

@@ -122,9 +122,11 @@ def lib() -> ctypes.CDLL:
                                       ctypes.c_float, vp]
         L.mla_recon_student_step.argtypes = [P(Cfg), vp, P(StudentW), vp, vp, vp, vp,
                                              P(StudentGrads), vp, sz, vp]
+        L.mla_recon_rel_error.argtypes = [P(Cfg), vp, vp, vp, vp, sz, vp]
         for f in ("mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
                   "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
-                  "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
+                  "mla_recon_student_step", "mla_recon_rel_error", "mla_recon_adamw",
+                  "mla_recon_residual_rmsnorm",
                   "mla_recon_decode", "mla_recon_decode_noalloc", "mla_recon_prefill",
                   "mla_recon_fold_uv_into_o",
                   "mla_recon_prof_enable",
@@ -209,6 +211,11 @@ def mla_recon_student_step(cfg: Cfg, h: int, sw: StudentW, Wo: int, mask: int | 
                            stream: int) -> None:
     _check(lib().mla_recon_student_step(ctypes.byref(cfg), h, ctypes.byref(sw), Wo, mask, loss,
                                         dA, ctypes.byref(grads), ws, ws_bytes, stream))
+
+
+def mla_recon_rel_error(cfg: Cfg, Wo: int, mask: int | None, loss: int, ws: int, ws_bytes: int,
+                        stream: int) -> None:
+    _check(lib().mla_recon_rel_error(ctypes.byref(cfg), Wo, mask, loss, ws, ws_bytes, stream))
 
 
 def mla_recon_adamw(tensors: list, dtype: int, step: int, lr: float, beta1: float, beta2: float,

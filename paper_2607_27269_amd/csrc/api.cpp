@@ -646,6 +646,36 @@ int mla_recon_student_step(const mla_recon_cfg* cfg, const void* h, const mla_st
   return student_step_impl(cfg, L, h, sw, Wo, mask, loss, dA, gr, ws, (hipStream_t)hip_stream);
 }
 
+int mla_recon_rel_error(const mla_recon_cfg* cfg, const void* Wo, const uint8_t* mask,
+                        float* loss, void* ws, size_t ws_bytes, void* hip_stream) {
+  g_err[0] = 0;
+  int rc = check_cfg(cfg);
+  if (rc) return rc;
+  if (!Wo || !loss) return fail(MLA_ERR_INVALID_ARG, "rel_error: NULL pointer argument");
+  Layout L;
+  if ((rc = check_ws(cfg, ws, ws_bytes, &L))) return rc;
+  hipStream_t s = (hipStream_t)hip_stream;
+  const Dims d = dims_of(cfg);
+  const int N = (int)d.N, D = (int)d.D, HV = (int)(d.H * d.dv);
+  void* scr = at(ws, L.l_scr);
+  const void* o_t = at(ws, L.t_o);  // the teacher's attention output, kept by the step
+  if (d.t == DT_BF16) {
+    // sum M A_t^2 with A_t = o_t W_O^T, per output tile of the product (A_t not stored)
+    double* parts = (double*)at(ws, L.l_diff);
+    int nparts = 0;
+    HIP_TRY(loss_prepare(mask, d.N, D, scr, s));
+    HIP_TRY(gemm_masked_sse(mk(N, D, HV, o_t, HV, true, Wo, HV, true, nullptr, D, d.t, d.t),
+                            loss_scale(scr), mask, nullptr, 0, parts, &nparts, s));
+    HIP_TRY(loss_rel_from_parts(parts, nparts, 1, loss, scr, s));
+    return MLA_OK;
+  }
+  // fp32 check mode: A_t formed in ws (l_diff, free after the step)
+  float* A_t = (float*)at(ws, L.l_diff);
+  HIP_TRY(gemm(mk(N, D, HV, o_t, HV, true, Wo, HV, true, A_t, D, d.t, DT_F32), nullptr, 0, s));
+  HIP_TRY(loss_rel_fp32(A_t, mask, d.N, D, loss, scr, s));
+  return MLA_OK;
+}
+
 int mla_recon_adamw(const mla_adamw_tensor* tensors, int32_t count, int32_t dtype, int32_t step,
                     float lr, float beta1, float beta2, float eps, float weight_decay,
                     void* hip_stream) {

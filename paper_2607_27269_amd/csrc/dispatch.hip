@@ -34,7 +34,8 @@ hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mas
                            hipStream_t s) {
   double flops = 2.0 * g.M * g.N * (double)g.K;
   double bytes = ((double)g.M * g.K + (double)g.N * g.K) * dsize(g.in_t) +
-                 (double)g.M * g.N * dsize(g.c_t) * (ref ? 2.0 : 1.0) + (mask ? (double)g.M : 0.0);
+                 (double)g.M * g.N * dsize(g.c_t) * ((ref ? 1.0 : 0.0) + (g.C ? 1.0 : 0.0)) +
+                 (mask ? (double)g.M : 0.0);
   prof_begin(KC_GEMM_NT, s);
   const char* kname = nullptr;
   hipError_t e = gemm_mfma_masked_sse(g, scale, mask, ref, ldref, part, nparts, s, &kname);

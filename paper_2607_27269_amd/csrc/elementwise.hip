@@ -241,7 +241,8 @@ struct LossScratch {
   double count;
   float scale;  // 2 / (D count): dL/dA per unit of masked difference (0 if nothing is valid)
   float pad_f;
-  double pad[30];
+  double sse;   // the last loss's sum of squared masked differences
+  double pad[29];
   double part[2 * LOSS_BLOCKS];
 };
 
@@ -321,7 +322,7 @@ __global__ __launch_bounds__(LOSS_THREADS) void loss_main_kernel(
   }
 }
 
-__global__ __launch_bounds__(256) void loss_final_kernel(const LossScratch* __restrict__ ws,
+__global__ __launch_bounds__(256) void loss_final_kernel(LossScratch* __restrict__ ws,
                                                          int nblocks, int D, bool has_ref,
                                                          float* __restrict__ loss) {
   // thread t sums partials t, t+256, ... in order; then a fixed tree over the 256 threads
@@ -344,6 +345,7 @@ __global__ __launch_bounds__(256) void loss_final_kernel(const LossScratch* __re
   if (threadIdx.x != 0) return;
   s = red[0][0];
   r = red[1][0];
+  ws->sse = s;
   double den = (double)D * ws->count;
   if (den == 0.0) {
     loss[0] = 0.f;
@@ -381,31 +383,73 @@ hipError_t loss_prepare(const uint8_t* mask, int64_t N, int D, void* scratch, hi
 
 const float* loss_scale(const void* scratch) { return &((const LossScratch*)scratch)->scale; }
 
-__global__ __launch_bounds__(256) void loss_parts_kernel(const double* __restrict__ part,
-                                                         int nparts, int D,
-                                                         const LossScratch* __restrict__ ws,
-                                                         float* __restrict__ loss) {
-  // thread t sums parts t, t+256, ... in order; then a fixed tree over the 256 threads
+// the fixed-order sum of part[i * stride], i < n, for a 256-thread block: thread t sums
+// i = t, t+256, ... in order, then a fixed tree over the threads; the total is valid in
+// thread 0
+__device__ double sum_parts_ordered(const double* __restrict__ part, int n, int stride) {
   __shared__ double red[256];
   double v = 0.0;
-  for (int i = threadIdx.x; i < nparts; i += 256) v += part[i];
+  for (int i = threadIdx.x; i < n; i += 256) v += part[(int64_t)i * stride];
   red[threadIdx.x] = v;
   __syncthreads();
   for (int w = 128; w > 0; w >>= 1) {
     if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
     __syncthreads();
   }
+  return red[0];
+}
+
+__global__ __launch_bounds__(256) void loss_parts_kernel(const double* __restrict__ part,
+                                                         int nparts, int D,
+                                                         LossScratch* __restrict__ ws,
+                                                         float* __restrict__ loss) {
+  const double v = sum_parts_ordered(part, nparts, 1);
   if (threadIdx.x != 0) return;
+  ws->sse = v;
   const double den = (double)D * ws->count;
-  loss[0] = den > 0.0 ? (float)(red[0] / den) : 0.f;
+  loss[0] = den > 0.0 ? (float)(v / den) : 0.f;
   loss[1] = NAN;
 }
 
 hipError_t loss_from_parts(const double* part, int nparts, int D, float* loss,
-                           const void* scratch, hipStream_t s) {
+                           void* scratch, hipStream_t s) {
   prof_begin(KC_LOSS, s);
-  loss_parts_kernel<<<1, 256, 0, s>>>(part, nparts, D, (const LossScratch*)scratch, loss);
+  loss_parts_kernel<<<1, 256, 0, s>>>(part, nparts, D, (LossScratch*)scratch, loss);
   prof_end(KC_LOSS, s, 0.0, 8.0 * nparts, KLABEL("loss_parts_kernel"));
+  return hipGetLastError();
+}
+
+// relative error: the kept sum of squared masked differences over sum M A_t^2
+__global__ __launch_bounds__(256) void loss_rel_kernel(const double* __restrict__ part,
+                                                       int nparts, int stride,
+                                                       const LossScratch* __restrict__ ws,
+                                                       float* __restrict__ loss) {
+  const double r = sum_parts_ordered(part, nparts, stride);
+  if (threadIdx.x != 0) return;
+  const double e = ws->sse;
+  loss[1] = ws->count == 0.0 ? 0.f : r > 0.0 ? (float)(e / r) : (e == 0.0 ? 0.f : INFINITY);
+}
+
+hipError_t loss_rel_from_parts(const double* part, int nparts, int stride, float* loss,
+                               const void* scratch, hipStream_t s) {
+  prof_begin(KC_LOSS, s);
+  loss_rel_kernel<<<1, 256, 0, s>>>(part, nparts, stride, (const LossScratch*)scratch, loss);
+  prof_end(KC_LOSS, s, 0.0, 8.0 * nparts, KLABEL("loss_rel_kernel"));
+  return hipGetLastError();
+}
+
+hipError_t loss_rel_fp32(const float* A_t, const uint8_t* mask, int64_t N, int D, float* loss,
+                         void* scratch, hipStream_t s) {
+  LossScratch* ws = (LossScratch*)scratch;
+  const int64_t nvec = N * (int64_t)D / 4;
+  const int blocks = (int)std::min<int64_t>(LOSS_BLOCKS, std::max<int64_t>(1, (nvec + LOSS_THREADS - 1) / LOSS_THREADS));
+  prof_begin(KC_LOSS, s);
+  mask_count_kernel<<<1, 1024, 0, s>>>(mask, N, D, ws);
+  // with no reference, the first partial of each workgroup is its sum of M A_t^2
+  loss_main_kernel<float><<<blocks, LOSS_THREADS, 0, s>>>(A_t, nullptr, mask, N, D, nullptr, ws);
+  loss_rel_kernel<<<1, 256, 0, s>>>(ws->part, blocks, 2, ws, loss);
+  prof_end(KC_LOSS, s, 0.0, (double)N * D * 4.0 + (mask ? N : 0),
+           KLABEL("mask_count_kernel + loss_main_kernel + loss_rel_kernel"));
   return hipGetLastError();
 }
 

@@ -49,8 +49,9 @@ struct GemmDev {
   const bf16_t* B; int64_t ldb;
   void* C; int64_t ldc;
   float* part;        // split-K partials [splits][M][N], or null
-  // masked-loss epilogue (with lpart set): C = lscale[0] mask[m] acc and lpart[tile] = the
-  // sum over the tile of mask[m] acc^2, or of mask[m] acc lref[m, n] when lref is set
+  // masked-loss epilogue (with lpart set): C = lscale[0] mask[m] acc (not stored when C is
+  // NULL) and lpart[tile] = the sum over the tile of mask[m] acc^2, or of mask[m] acc
+  // lref[m, n] when lref is set
   const float* lscale; const uint8_t* lmask; double* lpart;
   const bf16_t* lref; int64_t ldref;
   float alpha, beta;
@@ -440,6 +441,7 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
           }
         }
         sse += v[0] * r[0] + v[1] * r[1] + v[2] * r[2] + v[3] * r[3];
+        if (C == nullptr) continue;  // tile sums only
         v *= lsc;
       }
       if (g.part) {

@@ -146,12 +146,23 @@ hipError_t dkpe_finish(const float* part, void* out, DType t, int64_t out_tok, i
 // Eq. 11 with the masked squared differences summed per GEMM tile (gemm_masked_sse):
 // loss_prepare counts the valid tokens and stores the gradient scale 2 / (D count), which
 // loss_scale points to (device fp32); loss_from_parts then writes loss[0] = L from the
-// tile sums (fixed order) and loss[1] = NaN.
+// tile sums (fixed order) and loss[1] = NaN.  Both loss paths keep the fp64 sum of squared
+// masked differences in the scratch, for loss_rel_from_parts.
 hipError_t loss_prepare(const uint8_t* mask, int64_t N, int D, void* scratch, hipStream_t s);
 const float* loss_scale(const void* scratch);
 hipError_t loss_from_parts(const double* part, int nparts, int D, float* loss,
-                           const void* scratch, hipStream_t s);
-// C = scale[0] mask[m] X[m, n] in C's dtype, X = A B^T, and part[t] = the sum over output
+                           void* scratch, hipStream_t s);
+// The relative error of the last loss computed with this scratch: loss[1] = (its sum of
+// squared masked differences) / ref, ref = the fixed-order sum of part[i * stride],
+// i < nparts (tile sums of M A_t^2).  loss[1] = 0 when nothing is valid or both are 0,
+// +inf when only ref is 0.
+hipError_t loss_rel_from_parts(const double* part, int nparts, int stride, float* loss,
+                               const void* scratch, hipStream_t s);
+// fp32 check mode: the same from A_t [N, D] fp32 (masked sum of squares, fixed order).
+hipError_t loss_rel_fp32(const float* A_t, const uint8_t* mask, int64_t N, int D, float* loss,
+                         void* scratch, hipStream_t s);
+// C = scale[0] mask[m] X[m, n] in C's dtype (C may be NULL: not stored), X = A B^T, and
+// part[t] = the sum over output
 // tile t of mask[m] X[m, n]^2, or of mask[m] X[m, n] ref[m, n] with ref (bf16, row stride
 // ldref) given (bf16 operands, both K-contiguous); *nparts tiles, at most
 // gemm_masked_sse_parts(g).

@@ -120,6 +120,12 @@ class DeviceStep:
                                  _ptr(self.loss_buf), _ptr(self.dA) if with_dA else None, self.sg,
                                  _ptr(self.ws), self.ws_bytes, self.stream)
 
+    def rel_error(self):
+        """loss[1] after fused_step / student_step: the relative error, from the teacher
+        output the step left in the workspace (one more product)."""
+        L.mla_recon_rel_error(self.ccfg, _ptr(self.Wo), _ptr(self.mask), _ptr(self.loss_buf),
+                              _ptr(self.ws), self.ws_bytes, self.stream)
+
     # ---- optimizer (AdamW on the trainable projections, mla_recon_adamw) -----------------
     def init_optimizer(self):
         """fp32 master copies of the trainable weights and zero moments."""

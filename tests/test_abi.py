@@ -29,7 +29,8 @@ def test_exports_every_declared_function():
     names = header_functions()
     assert {"mla_recon_teacher_fwd", "mla_recon_student_fwd", "mla_recon_loss",
             "mla_recon_bwd", "mla_recon_step", "mla_recon_teacher_cache",
-            "mla_recon_student_step", "mla_recon_adamw", "mla_recon_residual_rmsnorm",
+            "mla_recon_student_step", "mla_recon_rel_error", "mla_recon_adamw",
+            "mla_recon_residual_rmsnorm",
             "mla_recon_decode", "mla_recon_decode_workspace_size",
             "mla_recon_workspace_size", "mla_recon_workspace_size_min",
             "mla_recon_last_error"} <= set(names)
@@ -168,6 +169,12 @@ def test_cached_teacher_arguments_validated():
     with pytest.raises(L.MlaError) as e:                                       # no loss
         L.mla_recon_student_step(c, 1, sw, 1, None, None, None, g, 256, ws, None)
     assert e.value.code == L.MLA_ERR_INVALID_ARG
+    for args, code in (((c, None, None, 256, 256, ws, None), L.MLA_ERR_INVALID_ARG),  # no W_O
+                       ((c, 1, None, None, 256, ws, None), L.MLA_ERR_INVALID_ARG),    # no loss
+                       ((c, 1, None, 256, 256, ws - 1, None), L.MLA_ERR_WORKSPACE)):
+        with pytest.raises(L.MlaError) as e:
+            L.mla_recon_rel_error(*args)
+        assert e.value.code == code, args
 
 
 def test_adamw_arguments_validated():

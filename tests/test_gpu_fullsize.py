@@ -147,6 +147,12 @@ def test_fullsize_timed_step_one_sequence(idx):
     errs = compare(out, ref, GRADS, tol, label=f"cfg{idx} timed step: ", cfg=cfg)
     print(f"[fullsize] timed step loss {out['loss']:.6e} grad errs {errs}", flush=True)
     fused_loss = out["loss"]
+    # the relative error on request, from the teacher output the step left in ws
+    dev.rel_error()
+    rel = dev.loss_buf.double().cpu().numpy()
+    print(f"[fullsize] timed step rel {rel[1]:.6e}", flush=True)
+    assert rel[0] == np.float32(fused_loss)
+    assert abs(rel[1] - ref["rel"]) <= LOSS_TOL * abs(ref["rel"]), (rel[1], ref["rel"])
 
     dev.step()
     out = dev.results()

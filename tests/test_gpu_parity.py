@@ -78,6 +78,11 @@ def test_fused_step_parity(name, with_dA):
     errs = compare(out, ref, (("dA",) if with_dA else ()) + GRADS, tol, label=f"fused {name}: ", cfg=cfg)
     assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
     assert math.isnan(out["rel"])
+    # the relative error on request (one more product over the teacher output in ws)
+    dev.rel_error()
+    rel = dev.loss_buf.double().cpu().numpy()
+    assert rel[0] == np.float32(out["loss"])
+    assert abs(rel[1] - ref["rel"]) <= LOSS_TOL * abs(ref["rel"]), (rel[1], ref["rel"])
     # the separate path on the same device state gives the same loss
     dev.step()
     again = dev.results()
@@ -102,6 +107,9 @@ def test_cached_teacher_parity(name):
     dev.student_step(with_dA=True)
     second = dev.results()
     tol = TOL[cfg.dtype]
+    dev.rel_error()
+    rel = float(dev.loss_buf[1].cpu())
+    assert abs(rel - ref["rel"]) <= LOSS_TOL * abs(ref["rel"]), (rel, ref["rel"])
     for out, names in ((first, GRADS), (second, ("dA",) + GRADS)):
         compare(out, ref, names, tol, label=f"cached {name}: ", cfg=cfg)
         assert abs(out["loss"] - ref["loss"]) <= LOSS_TOL * abs(ref["loss"]), (out["loss"], ref["loss"])
