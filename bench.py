@@ -35,6 +35,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-separate", action="store_true",
                    help="skip the reference timing of the four-call step (profiling runs)")
+    p.add_argument("--no-graph", action="store_true",
+                   help="skip the timing of the step replayed as a HIP graph (profiling runs)")
+    p.add_argument("--no-rel", action="store_true",
+                   help="skip the timing of the relative-error call (profiling runs)")
     p.add_argument("--no-cached", action="store_true",
                    help="skip the timing of the cached-teacher step (profiling runs)")
     p.add_argument("--no-train", action="store_true",
@@ -362,15 +366,33 @@ def main():
 
     # also reported: the relative error on request (mla_recon_rel_error after the step; one
     # more [B T, H d_k] x [H d_k, D] product), timed alone over the same number of calls
-    dev.rel_error()
-    torch.cuda.synchronize()
-    start.record()
-    for _ in range(args.steps):
+    # also reported: the same step replayed as a HIP graph (captured once; the replays run
+    # the same kernels on the same buffers without per-launch host work)
+    ms_graph = None
+    if not args.no_graph:
+        graph = dev.capture_fused_step(with_dA=False)
+        for _ in range(args.warmup):
+            graph.replay()
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            graph.replay()
+        stop.record()
+        torch.cuda.synchronize()
+        ms_graph = start.elapsed_time(stop) / args.steps
+        del graph
+
+    ms_rel = rel = None
+    if not args.no_rel:
         dev.rel_error()
-    stop.record()
-    torch.cuda.synchronize()
-    ms_rel = start.elapsed_time(stop) / args.steps
-    rel = float(dev.loss_buf[1].cpu())
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(args.steps):
+            dev.rel_error()
+        stop.record()
+        torch.cuda.synchronize()
+        ms_rel = start.elapsed_time(stop) / args.steps
+        rel = float(dev.loss_buf[1].cpu())
 
     # also reported: the step with the teacher cached (its output depends only on h and the
     # frozen weights, so a training loop can compute it once per minibatch)
@@ -512,6 +534,9 @@ def main():
                    {"ms_per_layer": round(ms_cap, 4),
                     "value": round(tokens / (ms_cap / 1e3), 1), "unit": "tokens/s per layer"},
         "decode_absorbed": decode,
+        "graph_step": None if ms_graph is None else
+                      {"ms_per_step": round(ms_graph, 4),
+                       "value": round(tokens / (ms_graph / 1e3), 1), "unit": "tokens/s"},
         "cached_teacher": None if ms_cached is None else
                           {"ms_per_step": round(ms_cached, 4),
                            "value": round(tokens / (ms_cached / 1e3), 1), "unit": "tokens/s"},
@@ -529,7 +554,8 @@ def main():
                            "frac": round(ca / cp, 4)},
         "other_configs": others,
         "loss": loss,
-        "rel_error": {"value": rel, "ms_per_call": round(ms_rel, 4),
+        "rel_error": None if ms_rel is None else
+                     {"value": rel, "ms_per_call": round(ms_rel, 4),
                       "call": "mla_recon_rel_error after the step"},
     }
     if not args.no_cpu_baseline:

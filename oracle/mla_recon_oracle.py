@@ -212,7 +212,8 @@ def recon_loss(A_s, A_t, mask):
     ref = float(np.sum((M * A_t) ** 2))
     if den == 0.0:
         return 0.0, 0.0, np.zeros_like(A_s)
-    rel = sse / ref if ref > 0 else (0.0 if sse == 0 else np.inf)
+    # a zero teacher energy is the only degenerate denominator; a NaN one propagates
+    rel = (0.0 if sse == 0 else np.inf) if ref == 0 else sse / ref
     return sse / den, rel, 2.0 * E / den
 
 

@@ -353,7 +353,8 @@ __global__ __launch_bounds__(256) void loss_final_kernel(LossScratch* __restrict
     return;
   }
   loss[0] = (float)(s / den);
-  loss[1] = !has_ref ? NAN : r > 0.0 ? (float)(s / r) : (s == 0.0 ? 0.f : INFINITY);
+  // (a zero reference is the only degenerate denominator: a NaN one propagates)
+  loss[1] = !has_ref ? NAN : r == 0.0 ? (s == 0.0 ? 0.f : INFINITY) : (float)(s / r);
 }
 
 hipError_t recon_loss(const float* A_s, const float* A_t, const uint8_t* mask, int64_t N, int D,
@@ -427,7 +428,7 @@ __global__ __launch_bounds__(256) void loss_rel_kernel(const double* __restrict_
   const double r = sum_parts_ordered(part, nparts, stride);
   if (threadIdx.x != 0) return;
   const double e = ws->sse;
-  loss[1] = ws->count == 0.0 ? 0.f : r > 0.0 ? (float)(e / r) : (e == 0.0 ? 0.f : INFINITY);
+  loss[1] = ws->count == 0.0 ? 0.f : r == 0.0 ? (e == 0.0 ? 0.f : INFINITY) : (float)(e / r);
 }
 
 hipError_t loss_rel_from_parts(const double* part, int nparts, int stride, float* loss,

@@ -109,6 +109,20 @@ class DeviceStep:
                          _ptr(self.loss_buf), _ptr(self.dA) if with_dA else None, self.sg,
                          _ptr(self.ws), self.ws_bytes, self.stream)
 
+    def capture_fused_step(self, with_dA: bool = False):
+        """The single-call step recorded once as a HIP graph (torch.cuda.CUDAGraph): replay()
+        launches the same kernels on the same buffers (h, weights, mask, workspace, outputs
+        as they are at replay time) without the per-launch host work.  The library makes
+        no allocation, synchronisation or memset inside a step, so the step is capturable;
+        one eager call first does the library's one-time per-device queries."""
+        self.fused_step(with_dA)
+        torch.cuda.synchronize(self.device)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            self.fused_step(with_dA)
+        torch.cuda.synchronize(self.device)
+        return graph
+
     def teacher_cache(self):
         """Teacher forward up to its attention output (and W_O^T W_O), kept in the workspace."""
         L.mla_recon_teacher_cache(self.ccfg, _ptr(self.h), self.tw, _ptr(self.ws), self.ws_bytes,

@@ -291,6 +291,15 @@ def test_P8_loss_properties():
     # an all-invalid minibatch contributes nothing
     L0, rel0, dA0 = O.recon_loss(A_s, A_t, np.zeros_like(mask))
     assert L0 == 0.0 and not dA0.any()
+    # relative error: a silent teacher on the valid rows is the only degenerate denominator
+    # (0 when the student is silent too, else +inf); a NaN anywhere on a valid row is NaN
+    Az = np.where(mask[..., None] == 1, 0.0, A_t)
+    assert O.recon_loss(A_s, Az, mask)[1] == np.inf
+    assert O.recon_loss(np.where(mask[..., None] == 1, 0.0, A_s), Az, mask)[1] == 0.0
+    An = A_t.copy()
+    An[b, t, 0] = np.nan
+    Ln, reln, _ = O.recon_loss(A_s, An, mask)
+    assert np.isnan(Ln) and np.isnan(reln)
 
 
 # ---------------------------------------------------------------------------
