@@ -334,7 +334,6 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
             *(const bf16x8*)(dOs + col * LDO + 16 * kk + 8 * half), vf[kk], dp, 0, 0, 0);
       // P = 2^(S sl2 - lse2), dS = P (dP - delta); rows q = q0 + 8(e/4) + 4 half + e%4
       // (lse2 = +inf past the sequence end)
-      const bool diag = kw0 + 31 > q0;
 #pragma unroll
       for (int e4 = 0; e4 < 4; ++e4) {
         const int qr = 8 * e4 + 4 * half;
@@ -343,11 +342,21 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int e = 4 * e4 + r;
-          float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sp[e], a.sl2, -l2[r]));
-          if (diag && my_key > q0 + qr + r) p = 0.f;
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sp[e], a.sl2, -l2[r]));
           sp[e] = p;
           dp[e] = p * (dp[e] - dl[r]);
         }
+      }
+      // causal mask, on the diagonal steps only (a real branch: the empty asm keeps the
+      // compiler from selecting per element on every step)
+      if (kw0 + 31 > q0) {
+        asm volatile("");
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (my_key > q0 + 8 * (e >> 2) + 4 * half + (e & 3)) {
+            sp[e] = 0.f;
+            dp[e] = 0.f;
+          }
       }
       // dS^T in bf16: element e is query 8 (e/4) + 4 half + e%4 of key row col, i.e. half
       // h of 16-byte segment e/4; through the transpose tile to row-contiguous stores
