@@ -320,7 +320,10 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
                              q0 + 8 * sg
                        : scratch + 8 * sg;
     };
-    if (kw0 <= min(q0 + DV_BQ - 1, a.T - 1)) {  // wave-uniform: some pair is visible
+    // every step runs the products: a step whose pairs are all masked (keys past every
+    // query of the block) gets zeros from the mask branch below.  (A branch around the
+    // whole step made dV's accumulators live in two register sets, copied every step.)
+    {
       f32x16 sp, dp;
 #pragma unroll
       for (int e = 0; e < 16; ++e) { sp[e] = 0.f; dp[e] = 0.f; }
@@ -347,8 +350,8 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
           dp[e] = p * (dp[e] - dl[r]);
         }
       }
-      // causal mask, on the diagonal steps only (a real branch: the empty asm keeps the
-      // compiler from selecting per element on every step)
+      // causal mask, on the diagonal (and fully masked) steps only (a real branch: the
+      // empty asm keeps the compiler from selecting per element on every step)
       if (kw0 + 31 > q0) {
         asm volatile("");
 #pragma unroll
@@ -388,13 +391,7 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
         st_global16(dst(j), *(const u32x4*)(tr + r * DV_BQ + 8 * (sg ^ ((r >> 2) & 3))));
       }
       asm volatile("" ::: "memory");
-    } else {
-      // every key of this wavefront follows every query of the block: zeros
-#pragma unroll
-      for (int j = 0; j < 2; ++j) st_global16(dst(j), u32x4{0u, 0u, 0u, 0u});
     }
-    // step it + 1's copies have landed; younger are only this step's stores (counters
-    // complete in issue order)
     // step it + 1's copies have landed; younger are this step's stores, step it + 2's copies
     // and (from step 1 on) the previous step's stores (counters complete in issue order)
     if (it == 0) wait_vm<D + DS_STORES>(); else wait_vm<D + 2 * DS_STORES>();
