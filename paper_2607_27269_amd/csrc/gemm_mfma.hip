@@ -94,10 +94,9 @@ struct Loader<true, ROWS, NTHR, BK> {
   static_assert(BK == 32 || BK == 64, "k-major slice depth");
   static __device__ __forceinline__ int swz(int row) { return (row / RPW) % NCH; }
   static constexpr int CHUNKS = ROWS * NCH;
-  static constexpr int PER = CHUNKS / NTHR;
+  static constexpr int PER = (CHUNKS + NTHR - 1) / NTHR;
   using Dma = DmaTile<ROWS, BK, KM_LD, NTHR / 64, true>;
   static constexpr int ELEMS = Dma::ALLOC;  // whole 1 KB blocks, a multiple per wavefront
-  static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
   // the copy that fills LDS position (row, p) fetches k-chunk p ^ swz(row)
   static __device__ __forceinline__ void swizzle(Dma& t) {
 #pragma unroll
@@ -112,7 +111,7 @@ struct Loader<true, ROWS, NTHR, BK> {
       const int c = threadIdx.x + i * NTHR;
       const int row = c / NCH, kc = (c % NCH) * 8;
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (row < rows_valid && k0 + kc < kend)
+      if ((CHUNKS % NTHR == 0 || c < CHUNKS) && row < rows_valid && k0 + kc < kend)
         v = *(const u32x4*)(p + (int64_t)(row0 + row) * ld + k0 + kc);
       r[i] = v;
     }
@@ -122,7 +121,8 @@ struct Loader<true, ROWS, NTHR, BK> {
     for (int i = 0; i < PER; ++i) {
       const int c = threadIdx.x + i * NTHR;
       const int row = c / NCH;
-      *(u32x4*)(lds + row * KM_LD + 8 * ((c % NCH) ^ swz(row))) = r[i];
+      if (CHUNKS % NTHR == 0 || c < CHUNKS)
+        *(u32x4*)(lds + row * KM_LD + 8 * ((c % NCH) ^ swz(row))) = r[i];
     }
   }
   // full k-slice of a full tile straight from HBM into LDS (uniform base + lane offset)
@@ -153,10 +153,9 @@ struct Loader<false, ROWS, NTHR, BK> {
   static constexpr int LD = SWZ ? ROWS : mm_ld(ROWS);
   static constexpr int CPR = ROWS / 8;
   static constexpr int CHUNKS = BK * CPR;
-  static constexpr int PER = CHUNKS / NTHR;
+  static constexpr int PER = (CHUNKS + NTHR - 1) / NTHR;
   using Dma = DmaTile<BK, ROWS, LD, NTHR / 64, true>;
   static constexpr int ELEMS = Dma::ALLOC;  // whole 1 KB blocks, a multiple per wavefront
-  static_assert(CHUNKS % NTHR == 0, "tile / thread mismatch");
   static __device__ __forceinline__ int pos(int k, int c) {
     return !SWZ ? c : SWZ4 ? c ^ (4 * (k & 3)) : c ^ (4 * ((k >> 1) & 1));
   }
@@ -175,7 +174,7 @@ struct Loader<false, ROWS, NTHR, BK> {
       const int c = threadIdx.x + i * NTHR;
       const int kr = c / CPR, rc = (c % CPR) * 8;
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (rc < rows_valid && k0 + kr < kend)
+      if ((CHUNKS % NTHR == 0 || c < CHUNKS) && rc < rows_valid && k0 + kr < kend)
         v = *(const u32x4*)(p + (int64_t)(k0 + kr) * ld + row0 + rc);
       r[i] = v;
     }
@@ -185,7 +184,8 @@ struct Loader<false, ROWS, NTHR, BK> {
     for (int i = 0; i < PER; ++i) {
       const int c = threadIdx.x + i * NTHR;
       const int kr = c / CPR;
-      *(u32x4*)(lds + kr * LD + pos(kr, c % CPR) * 8) = r[i];
+      if (CHUNKS % NTHR == 0 || c < CHUNKS)
+        *(u32x4*)(lds + kr * LD + pos(kr, c % CPR) * 8) = r[i];
     }
   }
   __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
@@ -970,9 +970,12 @@ static void launch_causal(const GemmDev& d, int nbatch, hipStream_t s) {
   const int ntm = (d.M + 255) / 256, ntn = (d.N + BN - 1) / BN;
   const int items = ntm * ntn * nbatch;
   if constexpr (!AK) {
-    // dQ (M-contiguous A; K ranges end at the diagonal): measured 1.3% slower persistent,
-    // so one tile per workgroup, dispatched longest range first
-    attn_ds_gemm_kernel<256, BN, WM, WN, AK, false, TC, 64, 2>
+    // dQ (M-contiguous A; K ranges end at the diagonal): one tile per workgroup, dispatched
+    // longest range first, in 32-deep slices through a ring of four LDS stages.  The
+    // product waits on its copies (the dS^T stream): three slices in flight (84 KB per CU)
+    // instead of one 64-deep slice (56 KB) measured 3-6% faster (five stages, and a
+    // persistent grid of the two-stage ring, were slower)
+    attn_ds_gemm_kernel<256, BN, WM, WN, AK, false, TC, 32, 4>
         <<<dim3(items, 1), 64 * WM * WN, 0, s>>>(d);
   } else {
     // dK (K ranges start at the diagonal): persistent, 2.6% faster; as many workgroups as
