@@ -6,8 +6,8 @@
 //
 // * dV and dS^T: a workgroup owns 256 keys of one (sequence, KV group) and walks the
 //   group's heads and 32-query blocks; it accumulates dV in registers and stores dS^T in
-//   bf16, transposed through LDS so that the stores run along key rows, zeros included
-//   wherever the products below read a masked pair.
+//   bf16 as 32 x 32 tiles ([32 keys][32 queries], 2 KB each; each wavefront writes whole
+//   tiles), zeros included wherever the products below read a masked pair.
 // * dK = scale dS^T Q: a batched causal GEMM per (sequence, group), the group's heads
 //   stacked along K.
 // * dQ = scale dS K: a batched causal GEMM per (sequence, head) over the stored dS^T and
@@ -30,7 +30,7 @@ struct BwdDev {
   const bf16_t* dO;      // [N][H*dv]
   bf16_t* dV; int64_t dv_tok;
   int G;                 // Ka groups
-  bf16_t* dsT;           // [B*H][T][ds_ld]
+  bf16_t* dsT;           // [B*H] planes of ds_ld x ds_ld in 32 x 32 tiles (ds_at)
   int64_t ds_ld;
   bf16_t* ds_dummy;      // scratch rows for stores of lanes past the sequence end
   const float* statT;    // [2][H][B][tpad]: log2-scaled lse, delta
@@ -41,6 +41,14 @@ struct BwdDev {
 // dS^T tile rows a dQ GEMM row tile reads: queries from the start of the 256-query tile
 // that holds the key (the GEMM's row tile) to the end
 constexpr int DQ_TILE = 256;
+
+// element (key, query) of a dS^T plane: 32 x 32 tiles of [32 keys][32 queries], the tiles
+// of a key block in query order (ld / 32 per row of tiles), key blocks in order.  A
+// wavefront's 32 x 32 block is then 2 KB of whole lines, and the products' slices are
+// runs of consecutive tiles.
+__device__ __forceinline__ int64_t ds_at(int64_t key, int64_t q, int64_t ld) {
+  return ((key >> 5) * (ld >> 5) + (q >> 5)) * 1024 + (key & 31) * 32 + (q & 31);
+}
 
 // ---------------------------------------------------------------------------------------
 // dV and dS^T (the path where dK and dQ are GEMMs over the stored dS^T)
@@ -55,8 +63,8 @@ constexpr int DQ_TILE = 256;
 // copies that must have landed.
 constexpr int DV_BQ = 32;
 // dS^T stores per lane per step: a wavefront's 32 x 32 block is transposed through a
-// private LDS tile so that each 16-byte store continues its neighbours' along a key row
-// (4 lanes write a row's 64 bytes)
+// private LDS tile into the [key][query] order of its 2 KB dS^T tile, which two 16-byte
+// stores per lane write whole (1 KB per store instruction)
 constexpr int DS_STORES = DV_BQ * 32 * 2 / (64 * 16);
 constexpr int DV_NST = 3;  // LDS stages: a step's copies are issued two steps ahead
 constexpr int DV_WAVES = 8;
@@ -232,10 +240,10 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
     const int cpr = nz / 8;                        // 16-byte chunks per key row
     const int kr = min(DV_BKB, a.T - k0);
     for (int h = 0; h < hpg; ++h) {
-      bf16_t* plane = w.dsT + ((int64_t)b * a.H + i0 + h) * a.T * w.ds_ld;
+      bf16_t* plane = w.dsT + ((int64_t)b * a.H + i0 + h) * w.ds_ld * w.ds_ld;
       for (int c = threadIdx.x; c < kr * cpr; c += 64 * DV_WAVES) {
         const int r = c / cpr, q = zq0 + (c % cpr) * 8;
-        *(u32x4*)(plane + (int64_t)(k0 + r) * w.ds_ld + q) = u32x4{0u, 0u, 0u, 0u};
+        *(u32x4*)(plane + ds_at(k0 + r, q, w.ds_ld)) = u32x4{0u, 0u, 0u, 0u};
       }
     }
   }
@@ -311,13 +319,15 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
     stg.issue(w, b, hn, qn, stage_of(it + 2));
 
     // this lane's dS^T store targets for the block: key rows kw0 + rr + 16 j, queries
-    // q0 + 8 sg .. + 7; rows past the sequence end go to a scratch row instead, so that every
-    // wavefront issues exactly DS_STORES stores per step
-    // (computed where the stores are issued: short-lived registers)
+    // q0 + 8 sg .. + 7, i.e. 16 bytes at 8 lane + 512 j of the block's tile (kw0 and q0
+    // are multiples of 32): a store instruction writes 1 KB of the tile; rows past the
+    // sequence end go to a scratch row instead, so that every wavefront issues exactly
+    // DS_STORES stores per step (computed where the stores are issued: short-lived
+    // registers)
     auto dst = [&](int j) {
       const int key = kw0 + rr + 16 * j;
-      return key < a.T ? w.dsT + ((int64_t)b * a.H + hc) * a.T * w.ds_ld + (int64_t)key * w.ds_ld +
-                             q0 + 8 * sg
+      return key < a.T ? w.dsT + ((int64_t)b * a.H + hc) * w.ds_ld * w.ds_ld +
+                             ds_at(kw0, q0, w.ds_ld) + 512 * j + 8 * lane
                        : scratch + 8 * sg;
     };
     // every step runs the products: a step whose pairs are all masked (keys past every
@@ -486,7 +496,7 @@ hipError_t bwd_chunk(const AttnBwd& wb, int b0, int nb, hipStream_t s) {
   w.G = wb.n_ka_groups;
   w.dsT = (bf16_t*)wb.dsT;
   w.ds_ld = attn_ds_ld(at.T);
-  w.ds_dummy = w.dsT + (int64_t)at.B * at.H * at.T * w.ds_ld;
+  w.ds_dummy = w.dsT + (int64_t)at.B * at.H * w.ds_ld * w.ds_ld;
   w.statT = wb.statT;
   w.tpad = attn_stats_tpad(at.T);
   w.off32 = (int64_t)at.T * at.Q.tok * 2 < (1ll << 31) &&
@@ -525,7 +535,7 @@ hipError_t bwd_chunk(const AttnBwd& wb, int b0, int nb, hipStream_t s) {
     GemmBatch bt;
     bt.nbatch = at.B * w.G; bt.zdiv = w.G; bt.bdiv = 1; bt.mstore = at.T;
     bt.rev = 1; bt.kgroups = hpg;
-    bt.sA = (int64_t)hpg * at.T * w.ds_ld; bt.sAk = (int64_t)at.T * w.ds_ld;
+    bt.sA = (int64_t)hpg * w.ds_ld * w.ds_ld; bt.sAk = w.ds_ld * w.ds_ld;
     bt.sB1 = (int64_t)at.T * at.Q.tok; bt.sB2 = (int64_t)hpg * at.Q.head; bt.sBk = at.Q.head;
     bt.sC1 = (int64_t)at.T * w.G * DQK; bt.sC2 = DQK;
     prof_begin(KC_ATTN_DK, s);
@@ -557,7 +567,7 @@ hipError_t bwd_chunk(const AttnBwd& wb, int b0, int nb, hipStream_t s) {
   g.in_t = DT_BF16; g.c_t = DT_BF16; g.alpha = at.scale; g.beta = 0.f;
   GemmBatch bt;
   bt.nbatch = at.B * at.H; bt.zdiv = at.H; bt.bdiv = at.H / w.G; bt.mstore = at.T;
-  bt.sA = (int64_t)at.T * w.ds_ld;
+  bt.sA = w.ds_ld * w.ds_ld;
   bt.sB1 = (int64_t)at.T * w.G * DQK; bt.sB2 = DQK;
   bt.sC1 = (int64_t)at.T * at.H * DQK; bt.sC2 = DQK;
   bt.rev = 0; bt.kgroups = 1; bt.sAk = bt.sBk = 0;
@@ -606,8 +616,9 @@ int64_t attn_ds_ld(int T) { return ((int64_t)T + 63) / 64 * 64; }
 int attn_stats_tpad(int T) { return (T + 31) / 32 * 32; }
 size_t attn_stats_bytes(int B, int H, int T) { return 2ull * H * B * attn_stats_tpad(T) * 4; }
 size_t attn_ds_bytes(int B, int H, int T) {
-  // + scratch rows: 64 lanes x 64 elements
-  return (size_t)B * H * (size_t)T * (size_t)attn_ds_ld(T) * 2 + 64 * 64 * 2;
+  // square ds_ld x ds_ld planes (whole 32 x 32 tiles in both directions) + scratch rows:
+  // 64 lanes x 64 elements
+  return (size_t)B * H * (size_t)attn_ds_ld(T) * (size_t)attn_ds_ld(T) * 2 + 64 * 64 * 2;
 }
 
 }  // namespace mla

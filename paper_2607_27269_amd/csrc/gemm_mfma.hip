@@ -78,8 +78,16 @@ constexpr int mm_ld(int rows) {
   }
   return rows + 32;
 }
+// A operand of the batched causal products: dS^T stored in 32 x 32 tiles, element (key r,
+// query c) at ((r / 32) tq + c / 32) 1024 + (r % 32) 32 + c % 32 (tq: tiles per row of
+// tiles), so that each wavefront of the producer writes its 32 x 32 block as 2 KB of
+// whole lines and a slice of 32 keys x 256 queries is 16 KB of consecutive tiles
+__device__ __forceinline__ int64_t tile32_off(int64_t r, int64_t c, int64_t tq) {
+  return ((r >> 5) * tq + (c >> 5)) * 1024 + (r & 31) * 32 + (c & 31);
+}
+
 // ---- global -> register staging -------------------------------------------------------
-template <bool KMAJOR, int ROWS, int NTHR, int BK>
+template <bool KMAJOR, int ROWS, int NTHR, int BK, bool TILED = false>
 struct Loader;
 
 // k-major tile: ROWS x BK, chunk c -> row c / (BK/8), k-chunk c % (BK/8).  Rows are not
@@ -87,7 +95,7 @@ struct Loader;
 // row, so that the 16 rows one operand read covers per LDS cycle (one k-chunk each) fall on
 // 16 distinct 16-byte bank groups (a 256-byte bank window holds 128 / BK rows)
 template <int ROWS, int NTHR, int BK>
-struct Loader<true, ROWS, NTHR, BK> {
+struct Loader<true, ROWS, NTHR, BK, false> {
   static constexpr int KM_LD = BK;
   static constexpr int NCH = BK / 8;    // 16-byte chunks per row
   static constexpr int RPW = 128 / BK;  // rows per 256-byte bank window
@@ -147,7 +155,7 @@ struct Loader<true, ROWS, NTHR, BK> {
 // G ^ (k mod 4); with rows an odd multiple of 128 bytes, odd rows start half a bank
 // window (two groups) later, and group G sits at G ^ ((k / 2) mod 2).  Other widths keep padded rows.
 template <int ROWS, int NTHR, int BK>
-struct Loader<false, ROWS, NTHR, BK> {
+struct Loader<false, ROWS, NTHR, BK, false> {
   static constexpr bool SWZ = ROWS % 64 == 0;
   static constexpr bool SWZ4 = ROWS % 128 == 0;  // else rows are an odd multiple of 128 B
   static constexpr int LD = SWZ ? ROWS : mm_ld(ROWS);
@@ -192,6 +200,7 @@ struct Loader<false, ROWS, NTHR, BK> {
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
     t.issue_s(lds, p + (int64_t)k0 * ld + row0, [&](int r, int c) { return r * (int)ld + c; });
   }
+
   // operand fragment through the transposing read (lds_operand_tr's lane pattern: k-rows
   // klo + lane%16/4 and klo + 4 + lane%16/4, columns row0 + 16 ((lane/16) % 2) + 4 (lane % 4));
   // klo is a multiple of 4, so the swizzle's k mod 4 is the lane's lane%16/4
@@ -202,6 +211,119 @@ struct Loader<false, ROWS, NTHR, BK> {
     const int mc = SWZ ? pos(kq, m >> 3) * 8 + (m & 7) : m;
     const u32x2 lo = lds_read_tr4(lds + (klo + kq) * LD + mc);
     const u32x2 hi = lds_read_tr4(lds + (klo + 4 + kq) * LD + mc);
+    const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
+    return __builtin_bit_cast(bf16x8, w);
+  }
+};
+
+// A of the batched causal products: dS^T in 32 x 32 tiles (tile32_off), ld = the plane's
+// row length (a multiple of 32).  The LDS copy of a slice holds the slice's tiles whole and
+// in order, so that each 1 KB copy instruction moves 1 KB of consecutive global memory.
+//
+// Rows = keys, k = queries (the dK product): the slice's tiles (key tile i, query tile j)
+// at (i NQT + j) 1024 elements; inside a tile, key row r (64 bytes) holds its 16-byte chunk
+// q at position q ^ ((r / 4) % 4), so that the 16 rows one operand read covers per LDS
+// cycle fall on 16 distinct 16-byte bank groups.
+template <int ROWS, int NTHR, int BK>
+struct Loader<true, ROWS, NTHR, BK, true> {
+  static_assert(ROWS % 32 == 0 && BK % 32 == 0, "whole tiles");
+  static constexpr int NQT = BK / 32;   // query tiles per slice
+  static constexpr int NCH = BK / 8;    // 16-byte chunks per row
+  static constexpr int CHUNKS = ROWS * NCH;
+  static constexpr int PER = (CHUNKS + NTHR - 1) / NTHR;
+  using Dma = DmaTile<ROWS * BK / 64, 64, 64, NTHR / 64, true>;  // the slice as flat 1 KB blocks
+  static constexpr int ELEMS = Dma::ALLOC;
+  static __device__ __forceinline__ int sw(int r) { return (r >> 2) & 3; }
+  // LDS element of (row, k) of the slice (k a multiple of 8)
+  static __device__ __forceinline__ int lds_off(int row, int k) {
+    return ((row >> 5) * NQT + (k >> 5)) * 1024 + (row & 31) * 32 + 8 * (((k & 31) >> 3) ^ sw(row & 31));
+  }
+  static __device__ __forceinline__ void swizzle(Dma&) {}
+  u32x4 r[PER];
+  __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
+                                       int rows_valid, int k0, int kend) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NTHR;
+      const int row = c / NCH, kc = (c % NCH) * 8;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if ((CHUNKS % NTHR == 0 || c < CHUNKS) && row < rows_valid && k0 + kc < kend)
+        v = *(const u32x4*)(p + tile32_off(row0 + row, k0 + kc, ld >> 5));
+      r[i] = v;
+    }
+  }
+  __device__ __forceinline__ void store(bf16_t* lds) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NTHR;
+      if (CHUNKS % NTHR == 0 || c < CHUNKS) *(u32x4*)(lds + lds_off(c / NCH, (c % NCH) * 8)) = r[i];
+    }
+  }
+  // LDS element e = 64 r + c of the flat block layout holds tile e / 1024 (key tile i,
+  // query tile j), row (e % 1024) / 32, chunk position (e % 32) / 8; it is copied from the
+  // same row of global tile (i, j), chunk position ^ sw(row)
+  __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
+                                      int row0, int rows_valid, int k0, bf16_t* lds) const {
+    const int tq = (int)(ld >> 5);
+    t.issue_s(lds, p + tile32_off(row0, k0, tq), [&](int r, int c) {
+      const int e = 64 * r + c, tile = e >> 10, w = e & 1023, rr = w >> 5;
+      return ((tile / NQT) * tq + tile % NQT) * 1024 + rr * 32 + 8 * (((w & 31) >> 3) ^ sw(rr));
+    });
+  }
+  // operand fragment: rows row0 + lane%32 (row0 a multiple of 32: one key tile), k = 16 kk +
+  // 8 half + 0..7
+  static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
+    const int lane = threadIdx.x & 63, l = lane & 31;
+    const int c = 2 * kk + (lane >> 5);
+    return *(const bf16x8*)(lds + ((row0 >> 5) * NQT + (c >> 2)) * 1024 + l * 32 + 8 * ((c & 3) ^ sw(l)));
+  }
+};
+
+// k = keys, rows = queries (the dQ product, 32-deep slices: one key tile per slice): the
+// slice's query tiles in order, each a copy of its global tile ([32 keys][32 queries]); the
+// transposing read of 4 key rows x 32 queries is then 256 consecutive bytes
+template <int ROWS, int NTHR, int BK>
+struct Loader<false, ROWS, NTHR, BK, true> {
+  static_assert(BK == 32 && ROWS % 32 == 0, "one key tile per slice");
+  static constexpr int CPR = ROWS / 8;
+  static constexpr int CHUNKS = BK * CPR;
+  static constexpr int PER = (CHUNKS + NTHR - 1) / NTHR;
+  using Dma = DmaTile<BK, ROWS, ROWS, NTHR / 64, true>;
+  static constexpr int ELEMS = Dma::ALLOC;
+  static __device__ __forceinline__ int lds_off(int k, int m) { return (m >> 5) * 1024 + k * 32 + (m & 31); }
+  static __device__ __forceinline__ void swizzle(Dma&) {}
+  u32x4 r[PER];
+  __device__ __forceinline__ void load(const bf16_t* __restrict__ p, int64_t ld, int row0,
+                                       int rows_valid, int k0, int kend) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NTHR;
+      const int kr = c / CPR, rc = (c % CPR) * 8;
+      u32x4 v = {0u, 0u, 0u, 0u};
+      if ((CHUNKS % NTHR == 0 || c < CHUNKS) && rc < rows_valid && k0 + kr < kend)
+        v = *(const u32x4*)(p + tile32_off(k0 + kr, row0 + rc, ld >> 5));
+      r[i] = v;
+    }
+  }
+  __device__ __forceinline__ void store(bf16_t* lds) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NTHR;
+      if (CHUNKS % NTHR == 0 || c < CHUNKS) *(u32x4*)(lds + lds_off(c / CPR, (c % CPR) * 8)) = r[i];
+    }
+  }
+  // LDS element e = ROWS r + c of the flat block layout is element e of the slice's tiles
+  // in global memory (they are consecutive)
+  __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
+                                      int row0, int rows_valid, int k0, bf16_t* lds) const {
+    t.issue_s(lds, p + tile32_off(k0, row0, ld >> 5), [&](int r, int c) { return ROWS * r + c; });
+  }
+  static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
+    const int lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
+    const int klo = 16 * kk + 8 * (lane >> 5), kq = r >> 2;
+    const int m = row0 + 16 * (g & 1) + 4 * (r & 3);
+    const u32x2 lo = lds_read_tr4(lds + lds_off(klo + kq, m));
+    const u32x2 hi = lds_read_tr4(lds + lds_off(klo + 4 + kq, m));
     const u32x4 w = {lo[0], lo[1], hi[0], hi[1]};
     return __builtin_bit_cast(bf16x8, w);
   }
@@ -235,13 +357,14 @@ __device__ __forceinline__ void store4<bf16_t>(bf16_t* p, f32x4 v, float alpha, 
 }
 
 // ---- the kernel --------------------------------------------------------------------------
-template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST>
+template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST,
+          bool ATILE = false>
 __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   constexpr int NTHR = 64 * WM * WN;
   constexpr int TM = BM / WM / 32;  // 32x32 MFMA tiles per wave along M
   constexpr int TN = BN / WN / 32;
   constexpr int KK = BK / 16;       // MFMA k-steps per slice
-  using LA = Loader<AK, BM, NTHR, BK>;
+  using LA = Loader<AK, BM, NTHR, BK, ATILE>;
   using LB = Loader<BKM, BN, NTHR, BK>;
   constexpr int STAGE = LA::ELEMS + LB::ELEMS;
   constexpr int D = LA::Dma::PER + LB::Dma::PER;  // copies per wavefront per slice
@@ -493,12 +616,14 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST,
           bool CAUSAL>
 __device__ __forceinline__ void gemm_persist(const GemmDev& g) {
+  // the causal products read a 32 x 32-tiled A (tile32_off)
+  constexpr bool ATILE = CAUSAL;
   static_assert(NST == 2, "the cross-tile copy assumes a two-stage ring");
   constexpr int NTHR = 64 * WM * WN;
   constexpr int TM = BM / WM / 32;
   constexpr int TN = BN / WN / 32;
   constexpr int KK = BK / 16;
-  using LA = Loader<AK, BM, NTHR, BK>;
+  using LA = Loader<AK, BM, NTHR, BK, ATILE>;
   using LB = Loader<BKM, BN, NTHR, BK>;
   constexpr int STAGE = LA::ELEMS + LB::ELEMS;
   __shared__ __attribute__((aligned(1024))) bf16_t lds[NST * STAGE];
@@ -754,11 +879,11 @@ template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK
 __global__ __launch_bounds__(64 * WM * WN) void gemm_mfma_kernel(GemmDev g) {
   gemm_tile<BM, BN, WM, WN, AK, BKM, TC, BK, NST>(g);
 }
-// the same tile program for the dS products of attention's backward (own name, so that
-// profiles tell them apart)
+// the same tile program for the dS products of attention's backward, on the 32 x 32-tiled
+// dS^T (own name, so that profiles tell them apart)
 template <int BM, int BN, int WM, int WN, bool AK, bool BKM, typename TC, int BK, int NST>
 __global__ __launch_bounds__(64 * WM * WN) void attn_ds_gemm_kernel(GemmDev g) {
-  gemm_tile<BM, BN, WM, WN, AK, BKM, TC, BK, NST>(g);
+  gemm_tile<BM, BN, WM, WN, AK, BKM, TC, BK, NST, true>(g);
 }
 
 // C = alpha * sum_s part[s] + beta * C, summed in split order

@@ -22,6 +22,9 @@ hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t
 // k >= start of m's tile (rev = 1; A K-contiguous, fp32 C), so A must hold zeros for the
 // excluded side of the diagonal inside a tile; that K range is summed kgroups times, the
 // j-th on A + j sAk and B + j sBk.  B is N-contiguous; rows m >= mstore are not written.
+// A (a dS^T plane, key r x query c) is stored in 32 x 32 tiles: element (r, c) at
+// ((r / 32) (lda / 32) + c / 32) 1024 + (r % 32) 32 + c % 32, lda a multiple of 32 (r is
+// the K index for rev = 0 and the M index for rev = 1).
 struct GemmBatch {
   int nbatch, zdiv, bdiv, mstore, rev, kgroups;
   int64_t sA, sB1, sB2, sC1, sC2, sAk, sBk;

@@ -61,7 +61,8 @@ def test_workspace_chunks(idx):
     else for as many sequences as fit; one sequence beyond 16 GiB is unsupported."""
     cfg = configs.get(idx)
     H, T = cfg.n_heads, cfg.seq
-    ds_seq = H * T * ((T + 63) // 64 * 64) * 2
+    ld = (T + 63) // 64 * 64
+    ds_seq = H * ld * ld * 2    # square planes of 32 x 32 tiles
     pref = L.mla_recon_workspace_size(L.make_cfg(cfg))
     lo = L.mla_recon_workspace_size_min(L.make_cfg(cfg))
     assert 0 < lo < pref
