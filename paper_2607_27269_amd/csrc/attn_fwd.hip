@@ -31,7 +31,10 @@ constexpr int FWD_WAVES = 8;
 constexpr int FWD_BQ = 32 * FWD_WAVES;   // queries per workgroup
 constexpr float RESCALE_SLACK = 8.f;     // log2 units the running reference max may lag
 
-template <int DQK, int DV, bool LSE>
+// HG heads that share their keys and values (a KV group) per workgroup: wavefront w works
+// on head i0 + w % HG and queries 32 (w / HG) .. of the workgroup's 256 / HG per head, so
+// that one K/V tile in LDS serves all HG heads (HG = 1: 256 queries of one head)
+template <int DQK, int DV, bool LSE, int HG>
 __device__ __forceinline__ void fwd_tile(const AttnDev& a, int pid, bf16_t* smem) {
   using Stage = KVStage<DQK, DV, FWD_WAVES>;
   constexpr int LDK = Stage::LDK, LDV = Stage::LDV;
@@ -40,16 +43,19 @@ __device__ __forceinline__ void fwd_tile(const AttnDev& a, int pid, bf16_t* smem
   constexpr int NKK = DQK / 16;  // MFMA K-steps of the logits
   constexpr int NC = DV / 32;    // 32-row tiles of O^T
 
-  // work item pid (XCD-aware order: the query blocks of neighbouring heads, which share
-  // K/V, run on one XCD); heavy (late) query blocks first inside each head
+  // work item pid (XCD-aware order: the query blocks of neighbouring head groups, which
+  // share K/V, run on one XCD); heavy (late) query blocks first inside each head group
+  constexpr int BQH = FWD_BQ / HG;  // queries per head
+  const int ngr = a.H / HG;
   const int bh = pid / a.nqb;
   const int qb = a.nqb - 1 - pid % a.nqb;
-  const int b = bh / a.H, i = bh % a.H;
-  const int q0 = qb * FWD_BQ;
+  const int b = bh / ngr, i0 = (bh % ngr) * HG;
+  const int q0 = qb * BQH;
 
   const int lane = threadIdx.x & 63, wave = wave_id();
   const int half = lane >> 5, col = lane & 31;
-  const int qw0 = q0 + wave * 32;
+  const int i = i0 + wave % HG;  // this wavefront's head
+  const int qw0 = q0 + (wave / HG) * 32;
   // this lane's part of a transposing V read (lds_operand_tr's addressing): key row
   // 4 (lane half) + (lane % 16) / 4, column 16 ((lane / 16) % 2) + 4 (lane % 4)
   const int vlane = (4 * half + ((lane & 15) >> 2)) * LDV + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
@@ -102,12 +108,12 @@ __device__ __forceinline__ void fwd_tile(const AttnDev& a, int pid, bf16_t* smem
     for (int e = 0; e < 16; ++e) acc_o[c][e] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
 
-  const int kend = min(a.T, q0 + FWD_BQ);
+  const int kend = min(a.T, q0 + BQH);
   const int nkb = (kend + BKV - 1) / BKV;
   // tiles this wavefront sees (a prefix: the causal diagonal cuts its queries last)
   const int nvis = min(nkb, (qw0 + 31) / BKV + 1);
   Stage st;
-  st.init(a, b, i);
+  st.init(a, b, i0);  // the group's keys and values
   st.issue(0, smem, smem + KS);
   if (nkb > 1) st.issue(BKV, smem + (KS + VS), smem + (KS + VS) + KS);
   wait_all();
@@ -239,56 +245,66 @@ __device__ __forceinline__ void fwd_tile(const AttnDev& a, int pid, bf16_t* smem
 }
 
 // one work item per workgroup
-template <int DQK, int DV, bool LSE>
+template <int DQK, int DV, bool LSE, int HG>
 __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_mfma_kernel(AttnDev a) {
   using Stage = KVStage<DQK, DV, FWD_WAVES>;
   __shared__ __attribute__((aligned(1024))) bf16_t smem[3 * (Stage::KS + Stage::VS)];
-  const int nwork = a.B * a.H * a.nqb;
-  fwd_tile<DQK, DV, LSE>(a, xcd_remap(blockIdx.x, nwork), smem);
+  const int nwork = a.B * (a.H / HG) * a.nqb;
+  fwd_tile<DQK, DV, LSE, HG>(a, xcd_remap(blockIdx.x, nwork), smem);
 }
 
 // persistent: FWD_PCU workgroups per XCD (one per CU) walk that XCD's share of the work
 // items in the same order (rounds of FWD_PCU items), in snake order (forward in even rounds,
 // backward in odd ones), so that heavy and light query blocks of a head pair up on a CU
 constexpr int FWD_PCU = 32;
-template <int DQK, int DV, bool LSE>
+template <int DQK, int DV, bool LSE, int HG>
 __global__ __launch_bounds__(64 * FWD_WAVES) void attn_fwd_persist_kernel(AttnDev a) {
   using Stage = KVStage<DQK, DV, FWD_WAVES>;
   __shared__ __attribute__((aligned(1024))) bf16_t smem[3 * (Stage::KS + Stage::VS)];
-  const int per = a.B * a.H * a.nqb / 8;  // items of one XCD
+  const int per = a.B * (a.H / HG) * a.nqb / 8;  // items of one XCD
   const int x = blockIdx.x % 8, j = blockIdx.x / 8;
   for (int r = 0;; ++r) {
     const int local = r * FWD_PCU + ((r & 1) ? FWD_PCU - 1 - j : j);
     if (local >= per) break;
     if (r > 0) __syncthreads();  // every wavefront is done with the previous item's LDS
-    fwd_tile<DQK, DV, LSE>(a, x * per + local, smem);
+    fwd_tile<DQK, DV, LSE, HG>(a, x * per + local, smem);
   }
 }
 
-template <int DQK, int DV>
-hipError_t fwd_launch(const Attn& at, hipStream_t s, const char** kernel) {
+template <int DQK, int DV, int HG>
+hipError_t fwd_launch_hg(const Attn& at, hipStream_t s, const char** kernel) {
   AttnDev d = to_dev(at);
-  d.nqb = (at.T + FWD_BQ - 1) / FWD_BQ;
-  const int nwork = d.B * d.H * d.nqb;
+  constexpr int BQH = FWD_BQ / HG;
+  d.nqb = (at.T + BQH - 1) / BQH;
+  const int nwork = d.B * (d.H / HG) * d.nqb;
   // the persistent walk needs whole XCD shares of several rounds
   if (nwork % 8 == 0 && nwork / 8 >= 2 * FWD_PCU) {
     if (at.lse) {
-      attn_fwd_persist_kernel<DQK, DV, true><<<8 * FWD_PCU, 64 * FWD_WAVES, 0, s>>>(d);
+      attn_fwd_persist_kernel<DQK, DV, true, HG><<<8 * FWD_PCU, 64 * FWD_WAVES, 0, s>>>(d);
       *kernel = KLABEL("attn_fwd_persist_kernel<%d,%d,lse>", DQK, DV);
     } else {
-      attn_fwd_persist_kernel<DQK, DV, false><<<8 * FWD_PCU, 64 * FWD_WAVES, 0, s>>>(d);
+      attn_fwd_persist_kernel<DQK, DV, false, HG><<<8 * FWD_PCU, 64 * FWD_WAVES, 0, s>>>(d);
       *kernel = KLABEL("attn_fwd_persist_kernel<%d,%d>", DQK, DV);
     }
     return hipGetLastError();
   }
   if (at.lse) {
-    attn_fwd_mfma_kernel<DQK, DV, true><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
+    attn_fwd_mfma_kernel<DQK, DV, true, HG><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
     *kernel = KLABEL("attn_fwd_mfma_kernel<%d,%d,lse>", DQK, DV);
   } else {
-    attn_fwd_mfma_kernel<DQK, DV, false><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
+    attn_fwd_mfma_kernel<DQK, DV, false, HG><<<nwork, 64 * FWD_WAVES, 0, s>>>(d);
     *kernel = KLABEL("attn_fwd_mfma_kernel<%d,%d>", DQK, DV);
   }
   return hipGetLastError();
+}
+
+// four heads per workgroup when they share every key / value source (the head -> group
+// divisors are multiples of 4), else one
+template <int DQK, int DV>
+hipError_t fwd_launch(const Attn& at, hipStream_t s, const char** kernel) {
+  const bool share4 = at.H % 4 == 0 && at.Ka.div % 4 == 0 && at.V.div % 4 == 0 &&
+                      (at.dnope == DQK || at.Kb.div % 4 == 0);
+  return share4 ? fwd_launch_hg<DQK, DV, 4>(at, s, kernel) : fwd_launch_hg<DQK, DV, 1>(at, s, kernel);
 }
 
 
