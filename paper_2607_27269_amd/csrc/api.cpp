@@ -141,7 +141,7 @@ struct Layout {
   size_t b_split_elems;
   // loss scratch; the single-call step's per-tile sums (bf16) or A_s - A_t (fp32), its
   // W_O^T W_O (bf16) and, in fp32, its dA when the caller passes none
-  size_t l_scr, l_diff, l_gram, l_da;
+  size_t l_scr, l_diff, l_gram, l_da, l_dot;
   int chunk;  // sequences per chunk of the backward's dS^T
   size_t total;
 };
@@ -196,6 +196,8 @@ static Layout layout_of(const Dims& d, int chunk) {
                                                                      0, d.t, d.t))) * 8);
   L.l_gram = take(d.t == DT_BF16 ? (size_t)HV * HV * 2 : 0);
   L.l_da = take(d.t == DT_F32 ? N * d.D * 4 : 0);
+  // partial sums of dO . (o_s - o_t) left by the backward's delta pass (single call, bf16)
+  L.l_dot = take(d.t == DT_BF16 ? (size_t)attn_delta_parts((int64_t)N * d.H) * 8 : 0);
   // the backward's dS^T chunk and its per-token scratch
   L.chunk = chunk;
   const size_t ctok = (size_t)chunk * d.T;
@@ -436,7 +438,8 @@ static int check_grads(const mla_recon_cfg* cfg, const mla_student_grads* gr, co
 
 static int bwd_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
                     const mla_student_w* w, const void* Wo, const void* dA,
-                    const mla_student_grads* gr, void* ws, hipStream_t s) {
+                    const mla_student_grads* gr, void* ws, hipStream_t s,
+                    const void* loss_ref = nullptr, double* loss_part = nullptr) {
   const bool need_q = gr->dWuq || gr->dWdq;
   const bool need_kv = gr->dWuk || gr->dWuv || gr->dWdkv_kr;
   if (!need_q && !need_kv) return MLA_OK;
@@ -489,6 +492,8 @@ static int bwd_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
   ab.dk_tmp = L.b_ds_bytes ? (float*)at(ws, L.b_dktmp) : nullptr;
   ab.statT = L.b_ds_bytes ? (float*)at(ws, L.b_statT) : nullptr;
   ab.chunk_seqs = L.chunk;
+  ab.loss_ref = loss_ref;
+  ab.loss_part = loss_part;
   HIP_TRY(attn_bwd(ab, s));
 
   if (need_q) {
@@ -566,6 +571,18 @@ static int student_step_impl(const mla_recon_cfg* cfg, const Layout& L, const vo
     void* dO = at(ws, L.b_do);
     int nparts = 0;
     HIP_TRY(loss_prepare(mask, d.N, D, scr, s));
+    const bool any_grad = gr->dWdq || gr->dWuq || gr->dWdkv_kr || gr->dWuk || gr->dWuv;
+    if (any_grad && d.dv % 8 == 0) {
+      // the product writes dO only; the backward's delta pass, which streams dO anyway,
+      // sums dO . (o_s - o_t) = 2 L (so the product's epilogue does not read o_s - o_t)
+      HIP_TRY(gemm_masked_sse(mk(N, HV, HV, odiff, HV, true, at(ws, L.l_gram), HV, true, dO, HV, d.t, d.t),
+                              loss_scale(scr), mask, nullptr, 0, parts, &nparts, s));
+      double* dot = (double*)at(ws, L.l_dot);
+      int rc = bwd_impl(cfg, L, h, sw, Wo, nullptr, gr, ws, s, odiff, dot);
+      if (rc) return rc;
+      HIP_TRY(loss_from_dot(dot, attn_delta_parts((int64_t)d.N * d.H), D, loss, scr, s));
+      return MLA_OK;
+    }
     HIP_TRY(gemm_masked_sse(mk(N, HV, HV, odiff, HV, true, at(ws, L.l_gram), HV, true, dO, HV, d.t, d.t),
                             loss_scale(scr), mask, odiff, HV, parts, &nparts, s));
     HIP_TRY(loss_from_parts(parts, nparts, D, loss, scr, s));

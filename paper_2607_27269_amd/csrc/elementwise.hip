@@ -253,7 +253,18 @@ __global__ void mask_count_kernel(const uint8_t* __restrict__ mask, int64_t N, i
   __shared__ double red[16];
   double c = 0.0;
   if (mask) {
-    for (int64_t i = threadIdx.x; i < N; i += blockDim.x) c += mask[i] ? 1.0 : 0.0;
+    // 16 mask bytes per thread and step where the mask is 16-byte aligned, the tail byte-wise
+    const int64_t nv = (uintptr_t)mask % 16 == 0 ? N / 16 : 0;
+    int cnt = 0;
+    for (int64_t v = threadIdx.x; v < nv; v += blockDim.x) {
+      const u32x4 w = ((const u32x4*)mask)[v];
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+#pragma unroll
+        for (int b = 0; b < 4; ++b) cnt += ((w[k] >> (8 * b)) & 0xffu) != 0u;
+    }
+    for (int64_t i = nv * 16 + threadIdx.x; i < N; i += blockDim.x) cnt += mask[i] ? 1 : 0;
+    c = (double)cnt;
   } else if (threadIdx.x == 0) {
     c = (double)N;
   }
@@ -417,6 +428,41 @@ hipError_t loss_from_parts(const double* part, int nparts, int D, float* loss,
   prof_begin(KC_LOSS, s);
   loss_parts_kernel<<<1, 256, 0, s>>>(part, nparts, D, (LossScratch*)scratch, loss);
   prof_end(KC_LOSS, s, 0.0, 8.0 * nparts, KLABEL("loss_parts_kernel"));
+  return hipGetLastError();
+}
+
+// Eq. 11 from the partials of sum dO . (o_s - o_t): with dO = 2 M Y / (D sum M), the
+// squared-error sum is sum M Y . (o_s - o_t) = dot D count / 2 and L = dot / 2
+// (tens of thousands of partials: thread t sums the contiguous run t * per .. in order,
+// with independent loads, then a fixed tree over the 1024 threads)
+__global__ __launch_bounds__(1024) void loss_dot_kernel(const double* __restrict__ part,
+                                                        int nparts, int D,
+                                                        LossScratch* __restrict__ ws,
+                                                        float* __restrict__ loss) {
+  __shared__ double red[1024];
+  const int per = (nparts + 1023) / 1024;
+  const int b0 = (int)threadIdx.x * per, b1 = min(nparts, b0 + per);
+  double v = 0.0;
+  for (int i = b0; i < b1; ++i) v += part[i];
+  red[threadIdx.x] = v;
+  __syncthreads();
+  for (int w = 512; w > 0; w >>= 1) {
+    if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+    __syncthreads();
+  }
+  v = red[0];
+  if (threadIdx.x != 0) return;
+  const double cnt = ws->count;
+  ws->sse = cnt > 0.0 ? v * (double)D * cnt / 2.0 : 0.0;
+  loss[0] = cnt > 0.0 ? (float)(v / 2.0) : 0.f;
+  loss[1] = NAN;
+}
+
+hipError_t loss_from_dot(const double* part, int64_t nparts, int D, float* loss, void* scratch,
+                         hipStream_t s) {
+  prof_begin(KC_LOSS, s);
+  loss_dot_kernel<<<1, 1024, 0, s>>>(part, (int)nparts, D, (LossScratch*)scratch, loss);
+  prof_end(KC_LOSS, s, 0.0, 8.0 * nparts, KLABEL("loss_dot_kernel"));
   return hipGetLastError();
 }
 

@@ -97,8 +97,9 @@ struct AttnBwd {
   void* dV;  int64_t dv_tok;   // group g's value grads at dV[n*dv_tok + g*dv]
   float* dkb_part;           // [Gka, N, dqk - dnope] fp32 partial grads of the Kb part per Ka group
   int n_ka_groups;           // number of Ka groups (heads i / f.Ka.div)
-  // Matrix-core path: dS^T is stored in bf16 by the dV kernel as [B'*H][T keys][ds_ld
-  // queries] (ds_ld = T rounded up to 64) for B' = attn_bwd_chunk_seqs sequences at a time;
+  // Matrix-core path: dS^T is stored in bf16 by the dV kernel as B'*H planes of ds_ld x
+  // ds_ld in 32 x 32 tiles (ds_ld = T rounded up to 64) for B' = attn_bwd_chunk_seqs
+  // sequences at a time;
   // dQ = scale dS K is a batched causal GEMM against the keys gathered as kcat
   // [B' T][n_ka_groups][dqk], and dK = scale dS^T Q a GEMM into dk_tmp before the split into
   // dKa and dkb_part.
@@ -107,7 +108,13 @@ struct AttnBwd {
   float* dk_tmp;             // B' T * n_ka_groups * dqk fp32
   float* statT;              // attn_stats_bytes(B', f.H, f.T)
   int chunk_seqs;            // B' (>= 1, at most attn_bwd_chunk_seqs)
+  // optional (bf16, dv % 8 == 0): with loss_ref [N, H*dv] (row stride H*dv) set, the delta
+  // pass also leaves in loss_part[attn_delta_parts(N * H)] the fixed-order partial sums of
+  // dO . loss_ref, one per workgroup
+  const void* loss_ref = nullptr;
+  double* loss_part = nullptr;
 };
+int64_t attn_delta_parts(int64_t rows);
 // Row stride and size of the stored dS^T of the matrix-core backward.
 int64_t attn_ds_ld(int T);
 size_t attn_ds_bytes(int B, int H, int T);
@@ -214,6 +221,12 @@ hipError_t decode_attention(const Decode& d, hipStream_t s);
 // out = a - b elementwise over n elements of dtype t (fp32 arithmetic)
 hipError_t sub_elementwise(const void* a, const void* b, void* out, int64_t n, DType t,
                            hipStream_t s);
+
+// Eq. 11 from dO = 2 M Y / (D sum M) and o_s - o_t: L = sum(dO . (o_s - o_t)) / 2 (the
+// fixed-order sum of the nparts partials of the delta pass); loss[1] = NaN, the squared-error
+// sum kept for loss_rel_from_parts
+hipError_t loss_from_dot(const double* part, int64_t nparts, int D, float* loss, void* scratch,
+                         hipStream_t s);
 
 // Loss (Eq. 11) -------------------------------------------------------------------------
 // scratch: at least loss_scratch_bytes(); loss[0] = L, loss[1] = relative error.  With

@@ -308,30 +308,67 @@ __global__ __launch_bounds__(64) void attn_dkv_simt_kernel(AttnBwd w) {
 }
 
 // bf16 rows of 8-element multiples: each of a row's 16 lanes loads 16-byte pieces (eight
-// consecutive elements) of dO and O, so a row of 128 takes one load per tensor per lane
+// consecutive elements) of dO and O, so a row of 128 takes one load per tensor per lane.
+// With R set, the workgroup also leaves part[blockIdx.x] = the sum over its 16 rows of
+// dO . R (R laid out as dO), in a fixed order.
+// (groups of 16 rows, walked by a fixed grid in a fixed order: block b takes groups b,
+// b + grid, ...; with R its partial sums its groups in that order)
+constexpr int DELTA_MAX_BLOCKS = 2048;
 __global__ void attn_delta_bf16x8_kernel(const bf16_t* __restrict__ dO, const bf16_t* __restrict__ O,
                                          int64_t o_tok, int64_t N, int H, int dv,
-                                         float* __restrict__ delta) {
-  const int64_t row = (int64_t)blockIdx.x * (blockDim.x / 16) + threadIdx.x / 16;
+                                         float* __restrict__ delta, const bf16_t* __restrict__ R,
+                                         double* __restrict__ part) {
+  __shared__ double red[16];
   const int sub = threadIdx.x % 16;
-  const bool ok = row < N * H;
-  const int64_t n = ok ? row / H : 0;
-  const int i = ok ? (int)(row % H) : 0;
-  const bf16_t* g = dO + n * (int64_t)H * dv + (int64_t)i * dv;
-  const bf16_t* o = O + n * o_tok + (int64_t)i * dv;
-  float s = 0.f;
-  if (ok)
-    for (int d = 8 * sub; d < dv; d += 128) {
-      const u32x4 a = *(const u32x4*)(g + d), b = *(const u32x4*)(o + d);
+  auto dot8 = [](u32x4 a, u32x4 b) {
+    float t = 0.f;
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
-        s += __uint_as_float(a[k] << 16) * __uint_as_float(b[k] << 16) +
-             __uint_as_float(a[k] & 0xffff0000u) * __uint_as_float(b[k] & 0xffff0000u);
+    for (int k = 0; k < 4; ++k)
+      t += __uint_as_float(a[k] << 16) * __uint_as_float(b[k] << 16) +
+           __uint_as_float(a[k] & 0xffff0000u) * __uint_as_float(b[k] & 0xffff0000u);
+    return t;
+  };
+  const int64_t groups = (N * H + 15) / 16;
+  double acc = 0.0;  // this lane's (sub == 0) rows of dO . R, in group order
+  for (int64_t grp = blockIdx.x; grp < groups; grp += gridDim.x) {
+    const int64_t row = grp * 16 + threadIdx.x / 16;
+    const bool ok = row < N * H;
+    const int64_t n = ok ? row / H : 0;
+    const int i = ok ? (int)(row % H) : 0;
+    const bf16_t* g = dO + n * (int64_t)H * dv + (int64_t)i * dv;
+    const bf16_t* o = O + n * o_tok + (int64_t)i * dv;
+    float s = 0.f, sr = 0.f;
+    if (ok)
+      for (int d = 8 * sub; d < dv; d += 128) {
+        const u32x4 a = *(const u32x4*)(g + d);
+        s += dot8(a, *(const u32x4*)(o + d));
+        if (R) sr += dot8(a, *(const u32x4*)(R + n * (int64_t)H * dv + (int64_t)i * dv + d));
+      }
+#pragma unroll
+    for (int off = 8; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
+    if (ok && sub == 0) delta[row] = s;
+    if (R) {  // uniform
+#pragma unroll
+      for (int off = 8; off > 0; off >>= 1) sr += __shfl_xor(sr, off, 64);
+      acc += (double)sr;
     }
-#pragma unroll
-  for (int off = 8; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
-  if (ok && sub == 0) delta[row] = s;
+  }
+  if (R) {
+    if (sub == 0) red[threadIdx.x / 16] = acc;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      double t = 0.0;
+      for (int r = 0; r < (int)(blockDim.x / 16); ++r) t += red[r];
+      part[blockIdx.x] = t;
+    }
+  }
 }
+
+static int64_t delta_grid(int64_t rows) {
+  const int64_t g = (rows + 15) / 16;
+  return g < DELTA_MAX_BLOCKS ? g : DELTA_MAX_BLOCKS;
+}
+int64_t attn_delta_parts(int64_t rows) { return delta_grid(rows); }
 
 template <typename T>
 hipError_t delta_launch(const AttnBwd& w, hipStream_t s) {
@@ -339,10 +376,12 @@ hipError_t delta_launch(const AttnBwd& w, hipStream_t s) {
   int64_t rows = (int64_t)a.B * a.T * a.H;
   if (a.t == DT_BF16 && a.dv % 8 == 0 && a.o_tok % 8 == 0 && (uintptr_t)w.dO % 16 == 0 &&
       (uintptr_t)a.O % 16 == 0) {
-    attn_delta_bf16x8_kernel<<<(unsigned)((rows + 15) / 16), 256, 0, s>>>(
-        (const bf16_t*)w.dO, (const bf16_t*)a.O, a.o_tok, (int64_t)a.B * a.T, a.H, a.dv, w.delta);
+    attn_delta_bf16x8_kernel<<<(unsigned)delta_grid(rows), 256, 0, s>>>(
+        (const bf16_t*)w.dO, (const bf16_t*)a.O, a.o_tok, (int64_t)a.B * a.T, a.H, a.dv, w.delta,
+        (const bf16_t*)w.loss_ref, w.loss_part);
     return hipGetLastError();
   }
+  if (w.loss_ref) return hipErrorInvalidValue;  // the dot needs the bf16 row path
   attn_delta_kernel<T><<<(unsigned)((rows + 15) / 16), 256, 0, s>>>(w.dO, a.O, a.o_tok,
                                                                   (int64_t)a.B * a.T, a.H, a.dv,
                                                                   w.delta);
