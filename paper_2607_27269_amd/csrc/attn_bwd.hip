@@ -586,7 +586,8 @@ hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   // delta = rowsum(dO . O) of every token
   prof_begin(KC_ELEM, s);
   hipError_t e = attn_delta(wb, s);
-  prof_end(KC_ELEM, s, 0.0, (double)at.B * at.T * at.H * (2.0 * DV * 2.0 + 4.0),
+  // reads dO and O (and o_s - o_t when it also sums Eq. 11), writes delta
+  prof_end(KC_ELEM, s, 0.0, (double)at.B * at.T * at.H * ((wb.loss_ref ? 3.0 : 2.0) * DV * 2.0 + 4.0),
            KLABEL("attn_delta_bf16x8_kernel"));
   if (e != hipSuccess) return e;
   for (int b0 = 0; b0 < at.B; b0 += chunk) {

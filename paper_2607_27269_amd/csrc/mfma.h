@@ -1,4 +1,4 @@
-// bf16 matrix-core (MFMA) kernels for gfx950; see gemm_mfma.hip and attn_mfma.hip.
+// bf16 matrix-core (MFMA) kernels for gfx950 (gemm_mfma.hip, attn_fwd.hip, attn_bwd.hip).
 #pragma once
 #include "kernels.h"
 
