@@ -575,8 +575,8 @@ static int student_step_impl(const mla_recon_cfg* cfg, const Layout& L, const vo
     if (any_grad && d.dv % 8 == 0) {
       // the product writes dO only; the backward's delta pass, which streams dO anyway,
       // sums dO . (o_s - o_t) = 2 L (so the product's epilogue does not read o_s - o_t)
-      HIP_TRY(gemm_masked_sse(mk(N, HV, HV, odiff, HV, true, at(ws, L.l_gram), HV, true, dO, HV, d.t, d.t),
-                              loss_scale(scr), mask, nullptr, 0, parts, &nparts, s));
+      HIP_TRY(gemm_masked_scale(mk(N, HV, HV, odiff, HV, true, at(ws, L.l_gram), HV, true, dO, HV, d.t, d.t),
+                                loss_scale(scr), mask, parts, s));
       double* dot = (double*)at(ws, L.l_dot);
       int rc = bwd_impl(cfg, L, h, sw, Wo, nullptr, gr, ws, s, odiff, dot);
       if (rc) return rc;

@@ -159,6 +159,15 @@ __device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff_bytes, 
                : "memory");
 }
 
+// A pointer that is the same in every lane, as a 64-bit value in scalar registers (for an
+// "s" operand of inline assembly)
+__device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
+  const uint64_t a = (uint64_t)(uintptr_t)p;
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(a >> 32));
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  return ((uint64_t)hi << 32) | (uint64_t)lo;
+}
+
 template <int ROWS, int D, int LD, int NW, bool EXACT = false>
 struct DmaTile {
   static constexpr int BYTES = ROWS * LD * 2;

@@ -43,6 +43,18 @@ hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mas
   return e;
 }
 
+hipError_t gemm_masked_scale(const Gemm& g, const float* scale, const uint8_t* mask,
+                             double* part, hipStream_t s) {
+  double flops = 2.0 * g.M * g.N * (double)g.K;
+  double bytes = ((double)g.M * g.K + (double)g.N * g.K) * dsize(g.in_t) +
+                 (double)g.M * g.N * dsize(g.c_t) + (mask ? (double)g.M : 0.0);
+  prof_begin(KC_GEMM_NT, s);
+  const char* kname = nullptr;
+  hipError_t e = gemm_mfma_masked_scale(g, scale, mask, part, s, &kname);
+  prof_end(KC_GEMM_NT, s, flops, bytes, kname);
+  return e;
+}
+
 static double causal_pairs(const Attn& a) {
   return (double)a.B * a.H * (double)a.T * (a.T + 1) / 2.0;
 }

@@ -886,6 +886,232 @@ __global__ __launch_bounds__(64 * WM * WN) void attn_ds_gemm_kernel(GemmDev g) {
   gemm_tile<BM, BN, WM, WN, AK, BKM, TC, BK, NST, true>(g);
 }
 
+// ---- NT products on four wavefronts, k-steps scheduled by hand ------------------------
+//
+// Both operands K-contiguous, M and N multiples of 256, K a multiple of 128.  A workgroup
+// of four wavefronts (one per SIMD) owns a 256 x 256 tile, 128 x 128 per wavefront (16
+// accumulators of 32 x 32 in AGPRs); per 64-deep slice each wavefront reads 8 KB of
+// operands from LDS per 16-wide k step, a third fewer LDS bytes per MFMA than the
+// 8-wavefront tiles.  With one wavefront per SIMD no other wavefront hides its waits, so
+// each k step is one block of inline assembly in a fixed order: the 16 MFMAs of the step,
+// one operand read for the step after next between every other pair of them (operands
+// are read two k steps ahead into four register buffers), and on the two steps after
+// each slice barrier the 8 LDS DMA copies of the next-but-one slice between the others.
+// The compiler does not see the assembly's LDS and memory operations: every block starts
+// with the wait for the reads of the step before last (at most 8 reads are younger), and
+// each slice barrier waits for all copies.  A persistent grid walks the tiles; the next
+// tile's first two slices are copied, and its first two k steps read, while the current
+// tile finishes, and the epilogue stages 8-row strips in a 17 KB LDS region of its own.
+// Measured on the 16384 x 4096 x 4096 product: 475 us against 532 us for the 8-wavefront
+// tile, the matrix cores 81% busy instead of 62%.
+#define NT4_MF(c, a, b) "v_mfma_f32_32x32x16_bf16 %[" #c "], %[" #a "], %[" #b "], %[" #c "]\n"
+#define NT4_RD(d, base, off) "ds_read_b128 %[" #d "], %[" #base "] offset:" #off "\n"
+#define NT4_CP(o, src, m, off) \
+  "s_add_u32 m0, %[" #m "], " #off "\ns_nop 0\nglobal_load_lds_dwordx4 %[" #o "], %[" #src "]\n"
+// the 16 MFMAs of one k step with the 8 operand reads of the step after next after
+// MFMAs 0, 2, .., 14 (read order = first use: A0, B0..B3, A1..A3)
+#define NT4_STEP_BODY(X0, X1, X2, X3, X4, X5, X6, X7)                                       \
+  "s_waitcnt lgkmcnt(8)\n"                                                                \
+  NT4_MF(c00, a0, b0) NT4_RD(nA0, ra, 0) NT4_MF(c01, a0, b1) X0                             \
+  NT4_MF(c02, a0, b2) NT4_RD(nB0, rb, 0) NT4_MF(c03, a0, b3) X1                             \
+  NT4_MF(c10, a1, b0) NT4_RD(nB1, rb, 4096) NT4_MF(c11, a1, b1) X2                          \
+  NT4_MF(c12, a1, b2) NT4_RD(nB2, rb, 8192) NT4_MF(c13, a1, b3) X3                          \
+  NT4_MF(c20, a2, b0) NT4_RD(nB3, rb, 12288) NT4_MF(c21, a2, b1) X4                         \
+  NT4_MF(c22, a2, b2) NT4_RD(nA1, ra, 4096) NT4_MF(c23, a2, b3) X5                          \
+  NT4_MF(c30, a3, b0) NT4_RD(nA2, ra, 8192) NT4_MF(c31, a3, b1) X6                          \
+  NT4_MF(c32, a3, b2) NT4_RD(nA3, ra, 12288) NT4_MF(c33, a3, b3) X7
+#define NT4_OUTS                                                                            \
+  [c00] "+a"(acc[0][0]), [c01] "+a"(acc[0][1]), [c02] "+a"(acc[0][2]), [c03] "+a"(acc[0][3]), \
+  [c10] "+a"(acc[1][0]), [c11] "+a"(acc[1][1]), [c12] "+a"(acc[1][2]), [c13] "+a"(acc[1][3]), \
+  [c20] "+a"(acc[2][0]), [c21] "+a"(acc[2][1]), [c22] "+a"(acc[2][2]), [c23] "+a"(acc[2][3]), \
+  [c30] "+a"(acc[3][0]), [c31] "+a"(acc[3][1]), [c32] "+a"(acc[3][2]), [c33] "+a"(acc[3][3]), \
+  [nA0] "=&v"(nx[0]), [nA1] "=&v"(nx[1]), [nA2] "=&v"(nx[2]), [nA3] "=&v"(nx[3]),          \
+  [nB0] "=&v"(nx[4]), [nB1] "=&v"(nx[5]), [nB2] "=&v"(nx[6]), [nB3] "=&v"(nx[7])
+#define NT4_INS                                                                             \
+  [a0] "v"(cu[0]), [a1] "v"(cu[1]), [a2] "v"(cu[2]), [a3] "v"(cu[3]), [b0] "v"(cu[4]),      \
+  [b1] "v"(cu[5]), [b2] "v"(cu[6]), [b3] "v"(cu[7]), [ra] "v"(ra), [rb] "v"(rb)
+
+template <typename TC>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void gemm_nt4_persist_kernel(GemmDev g) {
+  constexpr int BM = 256, BN = 256, BKK = 64, TM = 4, TN = 4;
+  using LA = Loader<true, BM, 256, BKK>;  // layout of both operand tiles (swizzled rows)
+  constexpr int STAGE = 2 * LA::ELEMS;    // elements: A [256][64], then B [256][64]
+  constexpr int SLD = 128 + 4;            // epilogue strip row (floats)
+  constexpr int EPI = 4 * 8 * SLD;        // floats: four wavefronts x 8 rows
+  static_assert(LA::Dma::PER == 8, "copies per lane per operand slice");
+  __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * STAGE + 2 * EPI];
+  const int ntm = g.M / BM, ntn = g.N / BN, ntiles = ntm * ntn;
+  const int G = (int)gridDim.x;
+  int w = blockIdx.x;
+  if (w >= ntiles) return;
+  const int lane = threadIdx.x & 63, wave = wave_id();
+  const int wrow0 = (wave >> 1) * 128, wcol0 = (wave & 1) * 128;
+  // the tile order of the one-tile launch: XCD-aware remap, 8 row panels per group
+  auto tile_of = [&](int x, int& m0, int& n0) {
+    const int pid = xcd_remap(x, ntiles);
+    const int group = pid / (8 * ntn), first = group * 8, gsz = min(ntm - first, 8);
+    m0 = __builtin_amdgcn_readfirstlane((first + (pid % (8 * ntn)) % gsz) * BM);
+    n0 = __builtin_amdgcn_readfirstlane(((pid % (8 * ntn)) / gsz) * BN);
+  };
+  typename LA::Dma da;
+  da.init();
+  LA::swizzle(da);
+  // copy p of a slice: this lane's byte offset from the slice's first element (A, B) and
+  // LDS block wave + 4 p of the operand tile
+  uint32_t oA[8], oB[8];
+#pragma unroll
+  for (int p = 0; p < 8; ++p) {
+    oA[p] = 2u * (uint32_t)(da.row[p] * (int)g.lda + da.col[p]);
+    oB[p] = 2u * (uint32_t)(da.row[p] * (int)g.ldb + da.col[p]);
+  }
+  const uint32_t lds0 = (uint32_t)(uintptr_t)lds;  // LDS byte address
+  // operand read addresses of stage st, k step kk (fragment i / j at + 4096 i bytes)
+  const int l = lane & 31, h = lane >> 5;
+  uint32_t adA[2][4], adB[2][4];
+#pragma unroll
+  for (int st = 0; st < 2; ++st)
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+      const uint32_t sw = 16u * (uint32_t)((2 * kk + h) ^ LA::swz(l));
+      adA[st][kk] = lds0 + st * STAGE * 2 + (wrow0 + l) * BKK * 2 + sw;
+      adB[st][kk] = lds0 + st * STAGE * 2 + LA::ELEMS * 2 + (wcol0 + l) * BKK * 2 + sw;
+    }
+  const int nk = g.ktotal / BKK;  // even
+  int m0, n0, nm0 = 0, nn0 = 0;
+  tile_of(w, m0, n0);
+  const bf16_t* baseA = g.A + (int64_t)m0 * g.lda;
+  const bf16_t* baseB = g.B + (int64_t)n0 * g.ldb;
+  int wnext = w + G;
+  bool has_next = wnext < ntiles;
+  const bf16_t* nbaseA = baseA;
+  const bf16_t* nbaseB = baseB;
+  if (has_next) {
+    tile_of(wnext, nm0, nn0);
+    nbaseA = g.A + (int64_t)nm0 * g.lda;
+    nbaseB = g.B + (int64_t)nn0 * g.ldb;
+  }
+  f32x16 acc[TM][TN];
+  bf16x8 F[4][8];  // operand buffers of four k steps: A 0..3, B 4..7
+  // k step on buffer cur, reading step kk of stage st into buffer nxt
+  auto step = [&](int cur, int nxt, int st, int kk) {
+    const bf16x8* cu = F[cur];
+    bf16x8* nx = F[nxt];
+    const uint32_t ra = adA[st][kk], rb = adB[st][kk];
+    asm volatile(NT4_STEP_BODY("", "", "", "", "", "", "", "") : NT4_OUTS : NT4_INS : "memory");
+  };
+  // the same with copies q (0: 0..3, 1: 4..7) of slice ks of this tile into stage ks % 2,
+  // or of slice ks - nk of the next one (after the last tile: a repeat of this tile's last
+  // slice into the stage nobody reads any more)
+  auto step_copy = [&](int cur, int nxt, int st, int kk, int ks, int q) {
+    const bf16x8* cu = F[cur];
+    bf16x8* nx = F[nxt];
+    const uint32_t ra = adA[st][kk], rb = adB[st][kk];
+    const bool in_next = ks >= nk;
+    const int kq = in_next ? (has_next ? ks - nk : nk - 1) : ks;
+    const bf16_t* pa = (in_next && has_next ? nbaseA : baseA) + kq * BKK;
+    const bf16_t* pb = (in_next && has_next ? nbaseB : baseB) + kq * BKK;
+    const uint32_t ma = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)(lds0 + (ks & 1) * STAGE * 2 + (wave + 16 * q) * 1024));
+    const uint32_t mb = ma + LA::ELEMS * 2;
+    const uint64_t sa = uniform_ptr(pa), sb = uniform_ptr(pb);
+    const uint32_t oa0 = oA[4 * q], oa1 = oA[4 * q + 1], oa2 = oA[4 * q + 2], oa3 = oA[4 * q + 3];
+    const uint32_t ob0 = oB[4 * q], ob1 = oB[4 * q + 1], ob2 = oB[4 * q + 2], ob3 = oB[4 * q + 3];
+    uint32_t m0v;  // m0 (the copies' LDS destination) is written early by the block
+    asm volatile(NT4_STEP_BODY(NT4_CP(oa0, sa, ma, 0), NT4_CP(oa1, sa, ma, 4096),
+                               NT4_CP(oa2, sa, ma, 8192), NT4_CP(oa3, sa, ma, 12288),
+                               NT4_CP(ob0, sb, mb, 0), NT4_CP(ob1, sb, mb, 4096),
+                               NT4_CP(ob2, sb, mb, 8192), NT4_CP(ob3, sb, mb, 12288))
+                 : NT4_OUTS, [m0v] "=&{m0}"(m0v)
+                 : NT4_INS, [oa0] "v"(oa0), [oa1] "v"(oa1), [oa2] "v"(oa2), [oa3] "v"(oa3),
+                   [ob0] "v"(ob0), [ob1] "v"(ob1), [ob2] "v"(ob2), [ob3] "v"(ob3), [sa] "s"(sa),
+                   [sb] "s"(sb), [ma] "s"(ma), [mb] "s"(mb)
+                 : "memory");
+  };
+  // prologue: slices 0 and 1 of the first tile, steps 0 and 1 read
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt) {
+    bf16_t* dst = lds + kt * STAGE;
+#pragma unroll
+    for (int p = 0; p < 8; ++p) {
+      dma16_s(baseA + kt * BKK, oA[p], dst + (wave + p * 4) * 512);
+      dma16_s(baseB + kt * BKK, oB[p], dst + LA::ELEMS + (wave + p * 4) * 512);
+    }
+  }
+  wait_vm<16>();
+  lds_barrier();
+#pragma unroll
+  for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) F[kk][i] = LA::frag(lds, wrow0 + i * 32, kk);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) F[kk][4 + j] = LA::frag(lds + LA::ELEMS, wcol0 + j * 32, kk);
+  }
+  // every read of the compiler's own has landed: its counter bookkeeping starts empty
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const float lsc = g.lscale ? *g.lscale : 0.f;  // row-masked scale of the result
+  float* strip = (float*)(lds + 2 * STAGE) + wave * 8 * SLD;
+  for (;;) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) acc[i][j][e] = 0.f;
+    // two slices per pass: slice kt in stage 0, slice kt + 1 in stage 1
+    for (int kt = 0; kt < nk; kt += 2) {
+      step(0, 2, 0, 2);
+      step(1, 3, 0, 3);
+      wait_vm<0>();
+      lds_barrier();  // slice kt + 1 has landed; nobody reads stage 0 any more
+      step_copy(2, 0, 1, 0, kt + 2, 0);
+      step_copy(3, 1, 1, 1, kt + 2, 1);
+      step(0, 2, 1, 2);
+      step(1, 3, 1, 3);
+      wait_vm<0>();
+      lds_barrier();  // slice kt + 2 (or the next tile's slice 0) has landed
+      step_copy(2, 0, 0, 0, kt + 3, 0);
+      step_copy(3, 1, 0, 1, kt + 3, 1);
+    }
+    // epilogue: rows 8 gq .. 8 gq + 7 of each 32-row block, staged in this wavefront's
+    // region (a lane holds column l of rows 4 h .. 4 h + 3 of the group) and written back
+    // 4 columns per lane
+    TC* C = (TC*)g.C;
+#pragma unroll
+    for (int i = 0; i < TM; ++i) {
+#pragma unroll
+      for (int gq = 0; gq < 4; ++gq) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) strip[(4 * h + q) * SLD + j * 32 + l] = acc[i][j][4 * gq + q];
+#pragma unroll
+        for (int it = 0; it < 4; ++it) {
+          const int c = it * 64 + lane;
+          const int r = c / 32, col = (c % 32) * 4;
+          const int m = m0 + wrow0 + i * 32 + 8 * gq + r, n = n0 + wcol0 + col;
+          f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+          if (g.lscale) v = (g.lmask && !g.lmask[m]) ? f32x4{0.f, 0.f, 0.f, 0.f} : v * lsc;
+          store4<TC>(C + (int64_t)m * g.ldc + n, v, g.alpha, g.beta);
+        }
+      }
+    }
+    if (!has_next) break;
+    w = wnext;
+    m0 = nm0;
+    n0 = nn0;
+    baseA = nbaseA;
+    baseB = nbaseB;
+    wnext = w + G;
+    has_next = wnext < ntiles;
+    if (has_next) {
+      tile_of(wnext, nm0, nn0);
+      nbaseA = g.A + (int64_t)nm0 * g.lda;
+      nbaseB = g.B + (int64_t)nn0 * g.ldb;
+    }
+  }
+}
+
 // C = alpha * sum_s part[s] + beta * C, summed in split order
 template <typename TC>
 __global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits, int M, int N,
@@ -961,8 +1187,26 @@ Plan plan_of(const Gemm& g, bool allow_split) {
   return best;
 }
 
+// the four-wavefront NT kernel takes the product: whole tiles, K a multiple of 128, no
+// split-K, operand rows within 32-bit offsets, 16-byte aligned operands and 4-element
+// output rows
+bool nt4_ok(const GemmDev& d, const Plan& p) {
+  return p.splits == 1 && !d.part && !d.lpart && !d.causal && d.M % 256 == 0 &&
+         d.N % 256 == 0 && d.ktotal % 128 == 0 && d.ktotal >= 128 && d.lda % 8 == 0 &&
+         d.ldb % 8 == 0 && d.ldc % 4 == 0 && (uintptr_t)d.A % 16 == 0 &&
+         (uintptr_t)d.B % 16 == 0 && (uintptr_t)d.C % 16 == 0 &&
+         (int64_t)256 * d.lda * 2 < (1ll << 31) && (int64_t)256 * d.ldb * 2 < (1ll << 31);
+}
+
 template <bool AK, bool BKM, typename TC>
 const char* launch(const GemmDev& d, const Plan& p, hipStream_t s) {
+  if constexpr (AK && BKM) {
+    if (nt4_ok(d, p)) {
+      const int tiles = (d.M / 256) * (d.N / 256);
+      gemm_nt4_persist_kernel<TC><<<std::min(tiles, NUM_CU), 256, 0, s>>>(d);
+      return KLABEL("gemm_nt4_persist_kernel<256,256,NT,%s>", sizeof(TC) == 4 ? "fp32" : "bf16");
+    }
+  }
   const int tiles = ((d.M + p.bm - 1) / p.bm) * ((d.N + p.bn - 1) / p.bn);
   const bool persist = d.lpart == nullptr;
 #define GL_(name, bm, bn) KLABEL(name "<%d,%d,%s,%s>", bm, bn, AK ? (BKM ? "NT" : "NN") : (BKM ? "TT" : "TN"), \
@@ -1061,6 +1305,32 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
 
 size_t gemm_mfma_masked_sse_parts(const Gemm& g) {
   return (size_t)((g.M + 127) / 128) * ((g.N + 127) / 128);
+}
+
+hipError_t gemm_mfma_masked_scale(const Gemm& g, const float* scale, const uint8_t* mask,
+                                  double* part, hipStream_t s, const char** kernel) {
+  if (g.beta != 0.f || g.alpha != 1.f || g.in_t != DT_BF16 || !scale || !g.C ||
+      !g.a_kmajor || !g.b_kmajor)
+    return hipErrorInvalidValue;
+  GemmDev d;
+  d.M = g.M; d.N = g.N; d.ktotal = g.K; d.nsplit = 1;
+  d.A = (const bf16_t*)g.A; d.lda = g.lda;
+  d.B = (const bf16_t*)g.B; d.ldb = g.ldb;
+  d.C = g.C; d.ldc = g.ldc; d.alpha = 1.f; d.beta = 0.f;
+  d.mstore = g.M;
+  d.lscale = scale; d.lmask = mask; d.lpart = nullptr; d.lref = nullptr; d.ldref = 0;
+  d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
+  d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
+  const Plan p = plan_of(g, false);
+  d.kchunk = p.kchunk;
+  d.part = nullptr;
+  if (nt4_ok(d, p)) {
+    *kernel = g.c_t == DT_F32 ? launch<true, true, float>(d, p, s) : launch<true, true, bf16_t>(d, p, s);
+    return hipGetLastError();
+  }
+  // elsewhere the masked-loss kernel, its tile sums left unused
+  int nparts = 0;
+  return gemm_mfma_masked_sse(g, scale, mask, nullptr, 0, part, &nparts, s, kernel);
 }
 
 hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,

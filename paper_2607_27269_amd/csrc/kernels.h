@@ -177,6 +177,11 @@ size_t gemm_masked_sse_parts(const Gemm& g);
 hipError_t gemm_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
                            const void* ref, int64_t ldref, double* part, int* nparts,
                            hipStream_t s);
+// C = scale[0] X[m, n] on rows with mask[m] != 0 and 0 on the others, X = A B^T (bf16
+// operands and C, both operands K-contiguous; no tile sums: part, of
+// gemm_masked_sse_parts(g) values, is scratch).
+hipError_t gemm_masked_scale(const Gemm& g, const float* scale, const uint8_t* mask,
+                             double* part, hipStream_t s);
 
 // AdamW (decoupled weight decay) on up to ADAMW_MAX tensors: fp32 master weights, moments
 // and gradient; w (dtype wt) receives the rounded master weights.  16-byte aligned arrays.

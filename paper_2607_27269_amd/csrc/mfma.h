@@ -16,6 +16,12 @@ size_t gemm_mfma_masked_sse_parts(const Gemm& g);
 hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t* mask,
                                 const void* ref, int64_t ldref, double* part, int* nparts,
                                 hipStream_t s, const char** kernel);
+// C = scale[0] X[m, n] on rows with mask[m] != 0 (mask null = all rows) and 0 on the other
+// rows, X = A B^T (bf16 operands, both K-contiguous): the four-wavefront product with that
+// epilogue where it applies, else the masked-loss kernel (its tile sums go to part, at
+// least gemm_mfma_masked_sse_parts(g) values, and are not used).
+hipError_t gemm_mfma_masked_scale(const Gemm& g, const float* scale, const uint8_t* mask,
+                                  double* part, hipStream_t s, const char** kernel);
 // Batch entry z of a batched causal GEMM uses A + z sA, B + (z / zdiv) sB1 +
 // ((z % zdiv) / bdiv) sB2 and C + (z / zdiv) sC1 + (z % zdiv) sC2 (elements).  Row m of C
 // sums k < min(K, end of m's 256-row tile) (rev = 0; A M-contiguous, bf16 C) or

@@ -30,6 +30,10 @@ CASES = {
     # more than one 256-key block of the dV / dS^T kernel, ragged last block
     "cfg1_long": (1, 2, 300, [300, 263]),
     "cfg3_long": (3, 1, 520, [517]),
+    # token counts that are whole 256-row tiles: the projections and W_O products run on the
+    # four-wavefront NT kernel (its persistent walk, the masked dO epilogue)
+    "cfg3_tiles": (3, 1, 512, [400]),
+    "cfg2_tiles": (2, 2, 256, [256, 180]),
 }
 
 
@@ -58,7 +62,7 @@ def test_step_parity(name):
 
 
 FUSED_CASES = ("cfg0_ragged_fp32", "cfg0_bf16", "cfg1_ragged", "cfg3_short", "cfg4_short",
-               "cfg1_long", "cfg3_long")
+               "cfg1_long", "cfg3_long", "cfg3_tiles", "cfg2_tiles")
 
 
 @pytest.mark.parametrize("with_dA", [True, False])
