@@ -82,8 +82,8 @@ def rocprof_label(name):
                ("false", "true"): "TT"}[(args[4], args[5])]
         tag = fn if fn == "gemm_mfma_persist_kernel" else "gemm_mfma_kernel(masked loss)"
         return f"{tag}<{args[0]},{args[1]},{lay},{ty(args[6])}>"
-    if fn == "gemm_nt4_persist_kernel" and len(args) == 1:
-        return f"{fn}<256,256,NT,{ty(args[0])}>"
+    if fn == "gemm_nt4_persist_kernel" and len(args) == 2:
+        return f"{fn}<256,{args[0]},NT,{ty(args[1])}>"
     if fn in ("attn_ds_gemm_persist_kernel", "attn_ds_gemm_kernel") and len(args) >= 7:
         return f"{fn}<{args[0]},{args[1]},{'dK' if args[4] == 'true' else 'dQ'},{ty(args[6])}>"
     if fn in ("attn_fwd_persist_kernel", "attn_fwd_mfma_kernel") and len(args) >= 3:

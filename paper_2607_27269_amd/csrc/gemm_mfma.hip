@@ -930,23 +930,47 @@ __global__ __launch_bounds__(64 * WM * WN) void attn_ds_gemm_kernel(GemmDev g) {
 #define NT4_INS                                                                             \
   [a0] "v"(cu[0]), [a1] "v"(cu[1]), [a2] "v"(cu[2]), [a3] "v"(cu[3]), [b0] "v"(cu[4]),      \
   [b1] "v"(cu[5]), [b2] "v"(cu[6]), [b3] "v"(cu[7]), [ra] "v"(ra), [rb] "v"(rb)
+// the same for 256 x 192 tiles (128 x 96 per wavefront): 12 MFMAs, 7 reads (A0, B0..B2,
+// A1..A3), up to 7 copies
+#define NT4_STEP_BODY3(X0, X1, X2, X3, X4, X5, X6)                                          \
+  "s_waitcnt lgkmcnt(7)\n"                                                                \
+  NT4_MF(c00, a0, b0) NT4_RD(nA0, ra, 0) NT4_MF(c01, a0, b1) X0                             \
+  NT4_MF(c02, a0, b2) NT4_RD(nB0, rb, 0) NT4_MF(c10, a1, b0) X1                             \
+  NT4_MF(c11, a1, b1) NT4_RD(nB1, rb, 4096) NT4_MF(c12, a1, b2) X2                          \
+  NT4_MF(c20, a2, b0) NT4_RD(nB2, rb, 8192) NT4_MF(c21, a2, b1) X3                          \
+  NT4_MF(c22, a2, b2) NT4_RD(nA1, ra, 4096) NT4_MF(c30, a3, b0) X4                          \
+  NT4_MF(c31, a3, b1) NT4_RD(nA2, ra, 8192) NT4_MF(c32, a3, b2) X5                          \
+  NT4_RD(nA3, ra, 12288) X6
+#define NT4_OUTS3                                                                           \
+  [c00] "+a"(acc[0][0]), [c01] "+a"(acc[0][1]), [c02] "+a"(acc[0][2]), [c10] "+a"(acc[1][0]), \
+  [c11] "+a"(acc[1][1]), [c12] "+a"(acc[1][2]), [c20] "+a"(acc[2][0]), [c21] "+a"(acc[2][1]), \
+  [c22] "+a"(acc[2][2]), [c30] "+a"(acc[3][0]), [c31] "+a"(acc[3][1]), [c32] "+a"(acc[3][2]), \
+  [nA0] "=&v"(nx[0]), [nA1] "=&v"(nx[1]), [nA2] "=&v"(nx[2]), [nA3] "=&v"(nx[3]),          \
+  [nB0] "=&v"(nx[4]), [nB1] "=&v"(nx[5]), [nB2] "=&v"(nx[6])
+#define NT4_INS3                                                                            \
+  [a0] "v"(cu[0]), [a1] "v"(cu[1]), [a2] "v"(cu[2]), [a3] "v"(cu[3]), [b0] "v"(cu[4]),      \
+  [b1] "v"(cu[5]), [b2] "v"(cu[6]), [ra] "v"(ra), [rb] "v"(rb)
 
-template <typename TC>
+template <int BN, typename TC>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void gemm_nt4_persist_kernel(GemmDev g) {
-  constexpr int BM = 256, BN = 256, BKK = 64, TM = 4, TN = 4;
-  using LA = Loader<true, BM, 256, BKK>;  // layout of both operand tiles (swizzled rows)
-  constexpr int STAGE = 2 * LA::ELEMS;    // elements: A [256][64], then B [256][64]
-  constexpr int SLD = 128 + 4;            // epilogue strip row (floats)
-  constexpr int EPI = 4 * 8 * SLD;        // floats: four wavefronts x 8 rows
-  static_assert(LA::Dma::PER == 8, "copies per lane per operand slice");
+  constexpr int BM = 256, BKK = 64, TM = 4, TN = BN / 64;  // 4 or 3 fragments of B
+  constexpr int WTN = BN / 2;                              // columns per wavefront
+  using LA = Loader<true, BM, 256, BKK>;  // operand tile layouts (swizzled rows)
+  using LB = Loader<true, BN, 256, BKK>;
+  constexpr int STAGE = LA::ELEMS + LB::ELEMS;  // elements: A [256][64], then B [BN][64]
+  constexpr int SLD = WTN + 4;                  // epilogue strip row (floats)
+  constexpr int EPI = 4 * 8 * SLD;              // floats: four wavefronts x 8 rows
+  constexpr int PB = LB::Dma::PER;              // B copies per lane per slice: 8 or 6
+  static_assert(BN == 256 || BN == 192, "tile widths");
+  static_assert(LA::Dma::PER == 8 && PB == TN * 2, "copies per lane per operand slice");
   __shared__ __attribute__((aligned(1024))) bf16_t lds[2 * STAGE + 2 * EPI];
   const int ntm = g.M / BM, ntn = g.N / BN, ntiles = ntm * ntn;
   const int G = (int)gridDim.x;
   int w = blockIdx.x;
   if (w >= ntiles) return;
   const int lane = threadIdx.x & 63, wave = wave_id();
-  const int wrow0 = (wave >> 1) * 128, wcol0 = (wave & 1) * 128;
+  const int wrow0 = (wave >> 1) * 128, wcol0 = (wave & 1) * WTN;
   // the tile order of the one-tile launch: XCD-aware remap, 8 row panels per group
   auto tile_of = [&](int x, int& m0, int& n0) {
     const int pid = xcd_remap(x, ntiles);
@@ -955,16 +979,18 @@ void gemm_nt4_persist_kernel(GemmDev g) {
     n0 = __builtin_amdgcn_readfirstlane(((pid % (8 * ntn)) / gsz) * BN);
   };
   typename LA::Dma da;
+  typename LB::Dma db;
   da.init();
+  db.init();
   LA::swizzle(da);
+  LB::swizzle(db);
   // copy p of a slice: this lane's byte offset from the slice's first element (A, B) and
   // LDS block wave + 4 p of the operand tile
   uint32_t oA[8], oB[8];
 #pragma unroll
-  for (int p = 0; p < 8; ++p) {
-    oA[p] = 2u * (uint32_t)(da.row[p] * (int)g.lda + da.col[p]);
-    oB[p] = 2u * (uint32_t)(da.row[p] * (int)g.ldb + da.col[p]);
-  }
+  for (int p = 0; p < 8; ++p) oA[p] = 2u * (uint32_t)(da.row[p] * (int)g.lda + da.col[p]);
+#pragma unroll
+  for (int p = 0; p < PB; ++p) oB[p] = 2u * (uint32_t)(db.row[p] * (int)g.ldb + db.col[p]);
   const uint32_t lds0 = (uint32_t)(uintptr_t)lds;  // LDS byte address
   // operand read addresses of stage st, k step kk (fragment i / j at + 4096 i bytes)
   const int l = lane & 31, h = lane >> 5;
@@ -975,7 +1001,8 @@ void gemm_nt4_persist_kernel(GemmDev g) {
     for (int kk = 0; kk < 4; ++kk) {
       const uint32_t sw = 16u * (uint32_t)((2 * kk + h) ^ LA::swz(l));
       adA[st][kk] = lds0 + st * STAGE * 2 + (wrow0 + l) * BKK * 2 + sw;
-      adB[st][kk] = lds0 + st * STAGE * 2 + LA::ELEMS * 2 + (wcol0 + l) * BKK * 2 + sw;
+      adB[st][kk] = lds0 + st * STAGE * 2 + LA::ELEMS * 2 + (wcol0 + l) * BKK * 2 +
+                    16u * (uint32_t)((2 * kk + h) ^ LB::swz(l));
     }
   const int nk = g.ktotal / BKK;  // even
   int m0, n0, nm0 = 0, nn0 = 0;
@@ -998,7 +1025,10 @@ void gemm_nt4_persist_kernel(GemmDev g) {
     const bf16x8* cu = F[cur];
     bf16x8* nx = F[nxt];
     const uint32_t ra = adA[st][kk], rb = adB[st][kk];
-    asm volatile(NT4_STEP_BODY("", "", "", "", "", "", "", "") : NT4_OUTS : NT4_INS : "memory");
+    if constexpr (TN == 4)
+      asm volatile(NT4_STEP_BODY("", "", "", "", "", "", "", "") : NT4_OUTS : NT4_INS : "memory");
+    else
+      asm volatile(NT4_STEP_BODY3("", "", "", "", "", "", "") : NT4_OUTS3 : NT4_INS3 : "memory");
   };
   // the same with copies q (0: 0..3, 1: 4..7) of slice ks of this tile into stage ks % 2,
   // or of slice ks - nk of the next one (after the last tile: a repeat of this tile's last
@@ -1011,41 +1041,54 @@ void gemm_nt4_persist_kernel(GemmDev g) {
     const int kq = in_next ? (has_next ? ks - nk : nk - 1) : ks;
     const bf16_t* pa = (in_next && has_next ? nbaseA : baseA) + kq * BKK;
     const bf16_t* pb = (in_next && has_next ? nbaseB : baseB) + kq * BKK;
-    const uint32_t ma = (uint32_t)__builtin_amdgcn_readfirstlane(
-        (int)(lds0 + (ks & 1) * STAGE * 2 + (wave + 16 * q) * 1024));
-    const uint32_t mb = ma + LA::ELEMS * 2;
+    // copies q of A: blocks wave + 4 p, p = 4 q .. 4 q + 3; of B: p = (PB / 2) q + u
+    const uint32_t stg = lds0 + (ks & 1) * STAGE * 2 + wave * 1024;
+    const uint32_t ma = (uint32_t)__builtin_amdgcn_readfirstlane((int)(stg + 16384 * q));
+    const uint32_t mb = (uint32_t)__builtin_amdgcn_readfirstlane(
+        (int)(stg + LA::ELEMS * 2 + 4096 * (PB / 2) * q));
     const uint64_t sa = uniform_ptr(pa), sb = uniform_ptr(pb);
     const uint32_t oa0 = oA[4 * q], oa1 = oA[4 * q + 1], oa2 = oA[4 * q + 2], oa3 = oA[4 * q + 3];
-    const uint32_t ob0 = oB[4 * q], ob1 = oB[4 * q + 1], ob2 = oB[4 * q + 2], ob3 = oB[4 * q + 3];
+    const int qb = (PB / 2) * q;
+    const uint32_t ob0 = oB[qb], ob1 = oB[qb + 1], ob2 = oB[qb + 2], ob3 = oB[PB == 8 ? qb + 3 : qb];
     uint32_t m0v;  // m0 (the copies' LDS destination) is written early by the block
-    asm volatile(NT4_STEP_BODY(NT4_CP(oa0, sa, ma, 0), NT4_CP(oa1, sa, ma, 4096),
-                               NT4_CP(oa2, sa, ma, 8192), NT4_CP(oa3, sa, ma, 12288),
-                               NT4_CP(ob0, sb, mb, 0), NT4_CP(ob1, sb, mb, 4096),
-                               NT4_CP(ob2, sb, mb, 8192), NT4_CP(ob3, sb, mb, 12288))
-                 : NT4_OUTS, [m0v] "=&{m0}"(m0v)
-                 : NT4_INS, [oa0] "v"(oa0), [oa1] "v"(oa1), [oa2] "v"(oa2), [oa3] "v"(oa3),
-                   [ob0] "v"(ob0), [ob1] "v"(ob1), [ob2] "v"(ob2), [ob3] "v"(ob3), [sa] "s"(sa),
-                   [sb] "s"(sb), [ma] "s"(ma), [mb] "s"(mb)
-                 : "memory");
+    if constexpr (TN == 4)
+      asm volatile(NT4_STEP_BODY(NT4_CP(oa0, sa, ma, 0), NT4_CP(oa1, sa, ma, 4096),
+                                 NT4_CP(oa2, sa, ma, 8192), NT4_CP(oa3, sa, ma, 12288),
+                                 NT4_CP(ob0, sb, mb, 0), NT4_CP(ob1, sb, mb, 4096),
+                                 NT4_CP(ob2, sb, mb, 8192), NT4_CP(ob3, sb, mb, 12288))
+                   : NT4_OUTS, [m0v] "=&{m0}"(m0v)
+                   : NT4_INS, [oa0] "v"(oa0), [oa1] "v"(oa1), [oa2] "v"(oa2), [oa3] "v"(oa3),
+                     [ob0] "v"(ob0), [ob1] "v"(ob1), [ob2] "v"(ob2), [ob3] "v"(ob3), [sa] "s"(sa),
+                     [sb] "s"(sb), [ma] "s"(ma), [mb] "s"(mb)
+                   : "memory");
+    else
+      asm volatile(NT4_STEP_BODY3(NT4_CP(oa0, sa, ma, 0), NT4_CP(oa1, sa, ma, 4096),
+                                  NT4_CP(oa2, sa, ma, 8192), NT4_CP(oa3, sa, ma, 12288),
+                                  NT4_CP(ob0, sb, mb, 0), NT4_CP(ob1, sb, mb, 4096),
+                                  NT4_CP(ob2, sb, mb, 8192))
+                   : NT4_OUTS3, [m0v] "=&{m0}"(m0v)
+                   : NT4_INS3, [oa0] "v"(oa0), [oa1] "v"(oa1), [oa2] "v"(oa2), [oa3] "v"(oa3),
+                     [ob0] "v"(ob0), [ob1] "v"(ob1), [ob2] "v"(ob2), [sa] "s"(sa), [sb] "s"(sb),
+                     [ma] "s"(ma), [mb] "s"(mb)
+                   : "memory");
   };
   // prologue: slices 0 and 1 of the first tile, steps 0 and 1 read
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt) {
     bf16_t* dst = lds + kt * STAGE;
 #pragma unroll
-    for (int p = 0; p < 8; ++p) {
-      dma16_s(baseA + kt * BKK, oA[p], dst + (wave + p * 4) * 512);
-      dma16_s(baseB + kt * BKK, oB[p], dst + LA::ELEMS + (wave + p * 4) * 512);
-    }
+    for (int p = 0; p < 8; ++p) dma16_s(baseA + kt * BKK, oA[p], dst + (wave + p * 4) * 512);
+#pragma unroll
+    for (int p = 0; p < PB; ++p) dma16_s(baseB + kt * BKK, oB[p], dst + LA::ELEMS + (wave + p * 4) * 512);
   }
-  wait_vm<16>();
+  wait_vm<8 + PB>();
   lds_barrier();
 #pragma unroll
   for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) F[kk][i] = LA::frag(lds, wrow0 + i * 32, kk);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) F[kk][4 + j] = LA::frag(lds + LA::ELEMS, wcol0 + j * 32, kk);
+    for (int j = 0; j < TN; ++j) F[kk][4 + j] = LB::frag(lds + LA::ELEMS, wcol0 + j * 32, kk);
   }
   // every read of the compiler's own has landed: its counter bookkeeping starts empty
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
@@ -1086,9 +1129,9 @@ void gemm_nt4_persist_kernel(GemmDev g) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) strip[(4 * h + q) * SLD + j * 32 + l] = acc[i][j][4 * gq + q];
 #pragma unroll
-        for (int it = 0; it < 4; ++it) {
+        for (int it = 0; it < TN; ++it) {
           const int c = it * 64 + lane;
-          const int r = c / 32, col = (c % 32) * 4;
+          const int r = c / (WTN / 4), col = (c % (WTN / 4)) * 4;
           const int m = m0 + wrow0 + i * 32 + 8 * gq + r, n = n0 + wcol0 + col;
           f32x4 v = *(const f32x4*)(strip + r * SLD + col);
           if (g.lscale) v = (g.lmask && !g.lmask[m]) ? f32x4{0.f, 0.f, 0.f, 0.f} : v * lsc;
@@ -1187,24 +1230,39 @@ Plan plan_of(const Gemm& g, bool allow_split) {
   return best;
 }
 
-// the four-wavefront NT kernel takes the product: whole tiles, K a multiple of 128, no
-// split-K, operand rows within 32-bit offsets, 16-byte aligned operands and 4-element
-// output rows
-bool nt4_ok(const GemmDev& d, const Plan& p) {
-  return p.splits == 1 && !d.part && !d.lpart && !d.causal && d.M % 256 == 0 &&
-         d.N % 256 == 0 && d.ktotal % 128 == 0 && d.ktotal >= 128 && d.lda % 8 == 0 &&
-         d.ldb % 8 == 0 && d.ldc % 4 == 0 && (uintptr_t)d.A % 16 == 0 &&
-         (uintptr_t)d.B % 16 == 0 && (uintptr_t)d.C % 16 == 0 &&
-         (int64_t)256 * d.lda * 2 < (1ll << 31) && (int64_t)256 * d.ldb * 2 < (1ll << 31);
+// Tile width of the four-wavefront NT kernel for this product: 256 or 192, or 0 where it
+// does not apply (it needs whole tiles, K a multiple of 128, no split-K, operand rows
+// within 32-bit offsets, 16-byte aligned operands and 4-element output rows).  Of the two
+// widths, the one with fewer rounds x tile width (rounds of one tile per CU).
+int nt4_bn(const GemmDev& d, const Plan& p) {
+  const bool ok = p.splits == 1 && !d.part && !d.lpart && !d.causal && d.M % 256 == 0 &&
+                  d.ktotal % 128 == 0 && d.ktotal >= 128 && d.lda % 8 == 0 && d.ldb % 8 == 0 &&
+                  d.ldc % 4 == 0 && (uintptr_t)d.A % 16 == 0 && (uintptr_t)d.B % 16 == 0 &&
+                  (uintptr_t)d.C % 16 == 0 && (int64_t)256 * d.lda * 2 < (1ll << 31) &&
+                  (int64_t)256 * d.ldb * 2 < (1ll << 31);
+  if (!ok) return 0;
+  auto cost = [&](int bn) {
+    const int64_t tiles = (int64_t)(d.M / 256) * (d.N / bn);
+    return (double)((tiles + NUM_CU - 1) / NUM_CU) * bn;
+  };
+  const bool w256 = d.N % 256 == 0, w192 = d.N % 192 == 0;
+  if (w256 && (!w192 || cost(256) <= cost(192))) return 256;
+  return w192 ? 192 : 0;
 }
 
 template <bool AK, bool BKM, typename TC>
 const char* launch(const GemmDev& d, const Plan& p, hipStream_t s) {
   if constexpr (AK && BKM) {
-    if (nt4_ok(d, p)) {
+    const int bn = nt4_bn(d, p);
+    if (bn == 256) {
       const int tiles = (d.M / 256) * (d.N / 256);
-      gemm_nt4_persist_kernel<TC><<<std::min(tiles, NUM_CU), 256, 0, s>>>(d);
+      gemm_nt4_persist_kernel<256, TC><<<std::min(tiles, NUM_CU), 256, 0, s>>>(d);
       return KLABEL("gemm_nt4_persist_kernel<256,256,NT,%s>", sizeof(TC) == 4 ? "fp32" : "bf16");
+    }
+    if (bn == 192) {
+      const int tiles = (d.M / 256) * (d.N / 192);
+      gemm_nt4_persist_kernel<192, TC><<<std::min(tiles, NUM_CU), 256, 0, s>>>(d);
+      return KLABEL("gemm_nt4_persist_kernel<256,192,NT,%s>", sizeof(TC) == 4 ? "fp32" : "bf16");
     }
   }
   const int tiles = ((d.M + p.bm - 1) / p.bm) * ((d.N + p.bn - 1) / p.bn);
@@ -1324,7 +1382,7 @@ hipError_t gemm_mfma_masked_scale(const Gemm& g, const float* scale, const uint8
   const Plan p = plan_of(g, false);
   d.kchunk = p.kchunk;
   d.part = nullptr;
-  if (nt4_ok(d, p)) {
+  if (nt4_bn(d, p)) {
     *kernel = g.c_t == DT_F32 ? launch<true, true, float>(d, p, s) : launch<true, true, bf16_t>(d, p, s);
     return hipGetLastError();
   }

@@ -12,10 +12,10 @@ def test_rocprof_label_per_kernel_family():
     import bench
     ns = "void mla::(anonymous namespace)::"
     cases = {
-        ns + "gemm_nt4_persist_kernel<unsigned short>(mla::(anonymous namespace)::GemmDev)":
+        ns + "gemm_nt4_persist_kernel<256, unsigned short>(mla::(anonymous namespace)::GemmDev)":
             "gemm_nt4_persist_kernel<256,256,NT,bf16>",
-        ns + "gemm_nt4_persist_kernel<float>(mla::(anonymous namespace)::GemmDev)":
-            "gemm_nt4_persist_kernel<256,256,NT,fp32>",
+        ns + "gemm_nt4_persist_kernel<192, float>(mla::(anonymous namespace)::GemmDev)":
+            "gemm_nt4_persist_kernel<256,192,NT,fp32>",
         ns + "gemm_mfma_persist_kernel<256, 256, 2, 4, false, false, float, 64, 2>(GemmDev)":
             "gemm_mfma_persist_kernel<256,256,TN,fp32>",
         ns + "gemm_mfma_persist_kernel<256, 192, 4, 2, true, false, unsigned short, 64, 2>(GemmDev)":
