@@ -398,7 +398,7 @@ __global__ __launch_bounds__(64 * DV_WAVES, 8 / DV_WAVES) void attn_dv_mfma_kern
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const int r = rr + 16 * j;
-        st_global16(dst(j), *(const u32x4*)(tr + r * DV_BQ + 8 * (sg ^ ((r >> 2) & 3))));
+        st_global16_nt(dst(j), *(const u32x4*)(tr + r * DV_BQ + 8 * (sg ^ ((r >> 2) & 3))));
       }
       asm volatile("" ::: "memory");
     }

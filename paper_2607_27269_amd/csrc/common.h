@@ -144,6 +144,9 @@ __device__ __forceinline__ void dma16(const bf16_t* gsrc, bf16_t* lds_dst) {
 // Same copy with the global address split into a wave-uniform base (SGPRs) and a per-lane
 // 32-bit byte offset: the per-lane part is usually loop-invariant, so a copy costs no
 // 64-bit address arithmetic.  sbase must be the same in every lane.
+// NT: the non-temporal cache policy, for data streamed once (it then displaces less of what
+// the caches hold for other operands).
+template <bool NT = false>
 __device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff_bytes, bf16_t* lds_dst) {
   const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds_dst);
   // the base is uniform by contract; reading it from the first lane puts it in SGPRs (the
@@ -155,8 +158,12 @@ __device__ __forceinline__ void dma16_s(const void* sbase, uint32_t voff_bytes, 
   // s_nop 4: five wait states between a VALU write of the base SGPRs (the readfirstlane
   // above) and their read by the memory instruction, which the compiler cannot see inside
   // the asm; this also covers the m0 write before the LDS copy
-  asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff_bytes), "s"(su), "{m0}"(l)
-               : "memory");
+  if constexpr (NT)
+    asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1 nt" : : "v"(voff_bytes), "s"(su), "{m0}"(l)
+                 : "memory");
+  else
+    asm volatile("s_nop 4\n\tglobal_load_lds_dwordx4 %0, %1" : : "v"(voff_bytes), "s"(su), "{m0}"(l)
+                 : "memory");
 }
 
 // A pointer that is the same in every lane, as a 64-bit value in scalar registers (for an
@@ -202,14 +209,14 @@ struct DmaTile {
     }
   }
   // off(row, col) -> element offset of the chunk from sbase (uniform), below 2^31 bytes
-  template <class F>
+  template <bool NT = false, class F>
   __device__ __forceinline__ void issue_s(bf16_t* lds, const bf16_t* sbase, F off) const {
     const int wave = wave_id();
 #pragma unroll
     for (int p = 0; p < PER; ++p) {
       const int b = wave + p * NW;
       if (NBLK % NW == 0 || b < NBLK)
-        dma16_s(sbase, 2u * (uint32_t)off(row[p], col[p]), lds + b * 512);
+        dma16_s<NT>(sbase, 2u * (uint32_t)off(row[p], col[p]), lds + b * 512);
     }
   }
 };
@@ -222,6 +229,11 @@ __device__ __forceinline__ void st_global8(bf16_t* p, u32x2 v) {
 // 16-byte store through an explicitly global pointer
 __device__ __forceinline__ void st_global16(bf16_t* p, u32x4 v) {
   *(__attribute__((address_space(1))) u32x4*)p = v;
+}
+
+// the same with the non-temporal cache policy (data read back once, by a later launch)
+__device__ __forceinline__ void st_global16_nt(bf16_t* p, u32x4 v) {
+  __builtin_nontemporal_store(v, (__attribute__((address_space(1))) u32x4*)p);
 }
 
 // at most N vector-memory operations of this wavefront (e.g. LDS DMA copies of later

@@ -265,7 +265,9 @@ struct Loader<true, ROWS, NTHR, BK, true> {
   __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
     const int tq = (int)(ld >> 5);
-    t.issue_s(lds, p + tile32_off(row0, k0, tq), [&](int r, int c) {
+    // dS^T is streamed once per product: non-temporal, so that it displaces less of the
+    // B operand (Q) the caches keep between the row tiles of a batch entry
+    t.template issue_s<true>(lds, p + tile32_off(row0, k0, tq), [&](int r, int c) {
       const int e = 64 * r + c, tile = e >> 10, w = e & 1023, rr = w >> 5;
       return ((tile / NQT) * tq + tile % NQT) * 1024 + rr * 32 + 8 * (((w & 31) >> 3) ^ sw(rr));
     });
@@ -316,7 +318,9 @@ struct Loader<false, ROWS, NTHR, BK, true> {
   // in global memory (they are consecutive)
   __device__ __forceinline__ void dma(const Dma& t, const bf16_t* __restrict__ p, int64_t ld,
                                       int row0, int rows_valid, int k0, bf16_t* lds) const {
-    t.issue_s(lds, p + tile32_off(k0, row0, ld >> 5), [&](int r, int c) { return ROWS * r + c; });
+    // dS^T streamed once: non-temporal (the keys stay cached between row tiles)
+    t.template issue_s<true>(lds, p + tile32_off(k0, row0, ld >> 5),
+                             [&](int r, int c) { return ROWS * r + c; });
   }
   static __device__ __forceinline__ bf16x8 frag(const bf16_t* lds, int row0, int kk) {
     const int lane = threadIdx.x & 63, g = lane >> 4, r = lane & 15;
