@@ -341,8 +341,9 @@ __global__ void attn_delta_bf16x8_kernel(const bf16_t* __restrict__ dO, const bf
     if (ok)
       for (int d = 8 * sub; d < dv; d += 128) {
         const u32x4 a = *(const u32x4*)(g + d);
-        s += dot8(a, *(const u32x4*)(o + d));
-        if (R) sr += dot8(a, *(const u32x4*)(R + n * (int64_t)H * dv + (int64_t)i * dv + d));
+        // O and o_s - o_t are not read again: non-temporal loads
+        s += dot8(a, __builtin_nontemporal_load((const u32x4*)(o + d)));
+        if (R) sr += dot8(a, __builtin_nontemporal_load((const u32x4*)(R + n * (int64_t)H * dv + (int64_t)i * dv + d)));
       }
 #pragma unroll
     for (int off = 8; off > 0; off >>= 1) s += __shfl_xor(s, off, 64);
