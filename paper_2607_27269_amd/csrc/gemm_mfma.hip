@@ -1194,7 +1194,7 @@ __global__ void splitk_reduce4_kernel(const float* __restrict__ part, int splits
 // rounds x (work of one workgroup) / (relative matrix-core rate of its tile), plus the
 // split-K partials' traffic, over tile shapes and split factors.
 struct Plan {
-  int kind;  // 0: 256 x 256, 1: 256 x 192, 2: 128 x 128
+  int kind;  // 0: 256 x 256, 1: 256 x 192, 2: 128 x 128, 3: 192 x 256 (weight gradients)
   int bm, bn, splits, kchunk;
 };
 
@@ -1205,12 +1205,16 @@ Plan plan_of(const Gemm& g, bool allow_split) {
   // relative per-CU rates (fitted to timings of the step's shapes): the narrower tile reads
   // more LDS bytes per matrix op (much more so with an M-contiguous A); two 4-wavefront
   // workgroups share one CU
+  // 192-row tiles for the weight gradients whose rows are a multiple of 192 but not of 256
+  // (e.g. the 576 rows of [W_DKV; W_KR]): no ragged row tile
+  const bool tn192 = !g.a_kmajor && !g.b_kmajor && g.M % 192 == 0 && g.M % 256 != 0;
   const Cand cands[] = {{0, 256, 256, 1, 1.0}, {1, 256, 192, 1, g.a_kmajor ? 0.93 : 0.7},
-                        {2, 128, 128, 2, 0.62}};
+                        {2, 128, 128, 2, 0.62}, {3, 192, 256, 1, 0.9}};
   Plan best{2, 128, 128, 1, 0};
   double best_t = 1e300;
   const int kslices = (g.K + BK - 1) / BK;
   for (const Cand& c : cands) {
+    if (c.kind == 3 && !tn192) continue;
     const int64_t tiles = (int64_t)((g.M + c.bm - 1) / c.bm) * ((g.N + c.bn - 1) / c.bn);
     const int max_s = allow_split && g.K >= 8 * BK * 8 ? std::max(1, kslices / 8) : 1;
     for (int sp = 1; sp <= std::min(max_s, 64); ++sp) {
@@ -1284,6 +1288,11 @@ const char* launch(const GemmDev& d, const Plan& p, hipStream_t s) {
     } else if (p.kind == 1) {
       gemm_mfma_persist_kernel<256, 192, 4, 2, AK, BKM, TC, GBK, GNST><<<grid, 512, 0, s>>>(e);
       return GL_("gemm_mfma_persist_kernel", 256, 192);
+    } else if (p.kind == 3) {
+      if constexpr (!AK && !BKM) {
+        gemm_mfma_persist_kernel<192, 256, 2, 4, AK, BKM, TC, GBK, GNST><<<grid, 512, 0, s>>>(e);
+        return GL_("gemm_mfma_persist_kernel", 192, 256);
+      }
     }
     gemm_mfma_persist_kernel<128, 128, 2, 2, AK, BKM, TC, 64, 2><<<grid, 256, 0, s>>>(e);
     return GL_("gemm_mfma_persist_kernel", 128, 128);
