@@ -1205,11 +1205,11 @@ Plan plan_of(const Gemm& g, bool allow_split) {
   // relative per-CU rates (fitted to timings of the step's shapes): the narrower tile reads
   // more LDS bytes per matrix op (much more so with an M-contiguous A); two 4-wavefront
   // workgroups share one CU
-  // 192-row tiles for the weight gradients whose rows are a multiple of 192 but not of 256
-  // (e.g. the 576 rows of [W_DKV; W_KR]): no ragged row tile
-  const bool tn192 = !g.a_kmajor && !g.b_kmajor && g.M % 192 == 0 && g.M % 256 != 0;
+  // 192-row tiles for the weight gradients whose rows are a multiple of 192 (the 576 rows
+  // of [W_DKV; W_KR] without a ragged row tile; fewer rounds or splits for others)
+  const bool tn192 = !g.a_kmajor && !g.b_kmajor && g.M % 192 == 0;
   const Cand cands[] = {{0, 256, 256, 1, 1.0}, {1, 256, 192, 1, g.a_kmajor ? 0.93 : 0.7},
-                        {2, 128, 128, 2, 0.62}, {3, 192, 256, 1, 0.9}};
+                        {2, 128, 128, 2, 0.62}, {3, 192, 256, 1, 0.8}};
   Plan best{2, 128, 128, 1, 0};
   double best_t = 1e300;
   const int kslices = (g.K + BK - 1) / BK;
