@@ -24,7 +24,8 @@
 // ids are remapped so that neighbouring tiles (sharing A row panels or B column panels)
 // run on one XCD and hit its L2.  Weight gradients reduce over all tokens (K up to 1e5)
 // and have few output tiles: they are split along K into fp32 partials that a second
-// kernel sums in a fixed order (deterministic).
+// kernel sums in a fixed order (deterministic).  NT products of whole tiles run on a
+// four-wavefront kernel whose k steps are scheduled by hand (below, gemm_nt4_persist_kernel).
 #include <atomic>
 
 #include "common.h"
@@ -892,11 +893,11 @@ __global__ __launch_bounds__(64 * WM * WN) void attn_ds_gemm_kernel(GemmDev g) {
 
 // ---- NT products on four wavefronts, k-steps scheduled by hand ------------------------
 //
-// Both operands K-contiguous, M and N multiples of 256, K a multiple of 128.  A workgroup
-// of four wavefronts (one per SIMD) owns a 256 x 256 tile, 128 x 128 per wavefront (16
-// accumulators of 32 x 32 in AGPRs); per 64-deep slice each wavefront reads 8 KB of
-// operands from LDS per 16-wide k step, a third fewer LDS bytes per MFMA than the
-// 8-wavefront tiles.  With one wavefront per SIMD no other wavefront hides its waits, so
+// Both operands K-contiguous, M a multiple of 256, N of the tile width (256 or 192), K a
+// multiple of 128.  A workgroup of four wavefronts (one per SIMD) owns a 256 x 256 tile,
+// 128 x 128 per wavefront (16 accumulators of 32 x 32 in AGPRs; 256 x 192 tiles: 128 x 96,
+// 12 accumulators); per 16-wide k step each wavefront reads 8 KB of operands from LDS,
+// a third fewer LDS bytes per MFMA than the 8-wavefront tiles.  With one wavefront per SIMD no other wavefront hides its waits, so
 // each k step is one block of inline assembly in a fixed order: the 16 MFMAs of the step,
 // one operand read for the step after next between every other pair of them (operands
 // are read two k steps ahead into four register buffers), and on the two steps after
@@ -907,7 +908,9 @@ __global__ __launch_bounds__(64 * WM * WN) void attn_ds_gemm_kernel(GemmDev g) {
 // tile's first two slices are copied, and its first two k steps read, while the current
 // tile finishes, and the epilogue stages 8-row strips in a 17 KB LDS region of its own.
 // Measured on the 16384 x 4096 x 4096 product: 475 us against 532 us for the 8-wavefront
-// tile, the matrix cores 81% busy instead of 62%.
+// tile, the matrix cores 81% busy instead of 62%.  (The other operand layouts read one
+// operand with the transposing LDS read, 8 bytes of a fragment per instruction; inline
+// assembly cannot name the halves of a 128-bit operand, so they stay compiler-scheduled.)
 #define NT4_MF(c, a, b) "v_mfma_f32_32x32x16_bf16 %[" #c "], %[" #a "], %[" #b "], %[" #c "]\n"
 #define NT4_RD(d, base, off) "ds_read_b128 %[" #d "], %[" #base "] offset:" #off "\n"
 #define NT4_CP(o, src, m, off) \
