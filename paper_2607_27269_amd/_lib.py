@@ -39,7 +39,7 @@ KCLASS_KERNELS = {"gemm_nt": "gemm_mfma_persist_kernel<..., true, true, ...> (an
                   "attn_bwd_dk": "attn_ds_gemm_persist_kernel<..., true, false, float>",
                   "loss": "mask_count_kernel + loss_main_kernel + loss_final_kernel",
                   "elementwise": "rope_table_kernel, rope_apply_kernel, attn_delta_kernel, dkpe_finish_kernel, "
-                                 "kcat_kernel, dk_split_kernel"}
+                                 "kcat_kernel, attn_stats_t_kernel"}
 
 
 class MlaError(RuntimeError):

@@ -135,7 +135,7 @@ struct Layout {
   // student state kept from student_fwd to bwd
   size_t s_cos, s_sin, s_cq, s_q, s_ckv, s_knope, s_v, s_o, s_lse;
   // backward scratch
-  size_t b_do, b_delta, b_dqacc, b_dq, b_dkv, b_dkpe, b_dckv, b_dcq, b_split, b_ds, b_kcat, b_dktmp;
+  size_t b_do, b_delta, b_dqacc, b_dq, b_dkv, b_dkpe, b_dckv, b_dcq, b_split, b_ds, b_kcat;
   size_t b_statT;
   size_t b_ds_bytes;
   size_t b_split_elems;
@@ -204,7 +204,6 @@ static Layout layout_of(const Dims& d, int chunk) {
   L.b_ds_bytes = chunk ? attn_ds_bytes(chunk, (int)d.H, (int)d.T) : 0;
   L.b_ds = take(L.b_ds_bytes);
   L.b_kcat = take(ctok * d.Gkv * d.dqk * ts);
-  L.b_dktmp = take(ctok * d.Gkv * d.dqk * 4);
   L.b_statT = take(chunk ? attn_stats_bytes(chunk, (int)d.H, (int)d.T) : 0);
   L.total = o;
   return L;
@@ -489,7 +488,6 @@ static int bwd_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
   ab.dkb_part = dkpe; ab.n_ka_groups = Gkv;
   ab.dsT = L.b_ds_bytes ? at(ws, L.b_ds) : nullptr;
   ab.kcat = L.b_ds_bytes ? at(ws, L.b_kcat) : nullptr;
-  ab.dk_tmp = L.b_ds_bytes ? (float*)at(ws, L.b_dktmp) : nullptr;
   ab.statT = L.b_ds_bytes ? (float*)at(ws, L.b_statT) : nullptr;
   ab.chunk_seqs = L.chunk;
   ab.loss_ref = loss_ref;

@@ -441,27 +441,6 @@ __global__ void kcat_kernel(AttnDev a, int G, int DQK, bf16_t* __restrict__ out)
   *(u32x4*)(out + ng * DQK + d) = *(const u32x4*)src;
 }
 
-// dK of the GEMM ([N][G][DQK] fp32) split into the layouts the caller expects: the first
-// dnope dims in bf16 at dKa[n*dka_tok + g*dnope + d], the rest as the per-group fp32
-// partials dkb_part[g*gstride + n*(DQK - dnope) + d - dnope]; 4 elements per thread
-__global__ void dk_split_kernel(const float* __restrict__ dk, int64_t N, int G, int DQK,
-                                int dnope, bf16_t* __restrict__ dKa, int64_t dka_tok,
-                                float* __restrict__ dkb_part, int64_t gstride) {
-  const int cpr = DQK / 4;
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= N * G * cpr) return;
-  const int d = (int)(c % cpr) * 4;
-  const int64_t ng = c / cpr;
-  const int g = (int)(ng % G);
-  const int64_t n = ng / G;
-  const f32x4 v = *(const f32x4*)(dk + ng * DQK + d);
-  if (d < dnope) {
-    *(u32x2*)(dKa + n * dka_tok + (int64_t)g * dnope + d) = u32x2{pack2bf(v[0], v[1]), pack2bf(v[2], v[3])};
-  } else {
-    *(f32x4*)(dkb_part + (int64_t)g * gstride + n * (DQK - dnope) + (d - dnope)) = v;
-  }
-}
-
 // The attention of sequences b0 .. b0 + nb - 1 as a problem of its own (token-major views
 // shifted by b0 T tokens)
 static Attn seq_slice(const Attn& a, int b0, int nb) {
@@ -530,25 +509,22 @@ hipError_t bwd_chunk(const AttnBwd& wb, int b0, int nb, hipStream_t s) {
     g.M = at.T; g.N = DQK; g.K = at.T;
     g.A = wb.dsT; g.lda = w.ds_ld; g.a_kmajor = true;
     g.B = at.Q.p; g.ldb = at.Q.tok; g.b_kmajor = false;
-    g.C = wb.dk_tmp; g.ldc = (int64_t)w.G * DQK;
+    // written split: dk^nope in bf16 into dKa, the dk^PE partials (fp32) into dkb
+    g.C = dkb; g.ldc = dr;
     g.in_t = DT_BF16; g.c_t = DT_F32; g.alpha = at.scale; g.beta = 0.f;
     GemmBatch bt;
     bt.nbatch = at.B * w.G; bt.zdiv = w.G; bt.bdiv = 1; bt.mstore = at.T;
     bt.rev = 1; bt.kgroups = hpg;
     bt.sA = (int64_t)hpg * w.ds_ld * w.ds_ld; bt.sAk = w.ds_ld * w.ds_ld;
     bt.sB1 = (int64_t)at.T * at.Q.tok; bt.sB2 = (int64_t)hpg * at.Q.head; bt.sBk = at.Q.head;
-    bt.sC1 = (int64_t)at.T * w.G * DQK; bt.sC2 = DQK;
+    bt.sC1 = (int64_t)at.T * dr; bt.sC2 = Ntot * dr;
+    bt.split_n = at.dnope; bt.c_lo = dKa;
+    bt.ldc_lo = wb.dka_tok; bt.sC1_lo = (int64_t)at.T * wb.dka_tok; bt.sC2_lo = at.dnope;
     prof_begin(KC_ATTN_DK, s);
     e = gemm_mfma_causal(g, bt, s);
-    prof_end(KC_ATTN_DK, s, 2.0 * pairs * DQK, pairs * 2.0 + N * at.H * DQK * 2.0 + N * w.G * DQK * 4.0,
+    prof_end(KC_ATTN_DK, s, 2.0 * pairs * DQK,
+             pairs * 2.0 + N * at.H * DQK * 2.0 + N * w.G * (at.dnope * 2.0 + dr * 4.0),
              KLABEL("attn_ds_gemm_persist_kernel<256,%d,dK,fp32>", DQK));
-    if (e != hipSuccess) return e;
-    prof_begin(KC_ELEM, s);
-    const int64_t chunks = (int64_t)at.B * at.T * w.G * (DQK / 4);
-    dk_split_kernel<<<(unsigned)((chunks + 255) / 256), 256, 0, s>>>(
-        wb.dk_tmp, (int64_t)at.B * at.T, w.G, DQK, at.dnope, dKa, wb.dka_tok, dkb, Ntot * dr);
-    prof_end(KC_ELEM, s, 0.0, N * w.G * DQK * 4.0 * 2.0, KLABEL("dk_split_kernel"));
-    e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   // keys of each group gathered into one operand, then dQ = scale dS K per (sequence,
@@ -582,7 +558,7 @@ template <int DQK, int DV>
 hipError_t bwd_launch(const AttnBwd& wb, hipStream_t s) {
   const Attn& at = wb.f;
   const int chunk = wb.chunk_seqs;
-  if (chunk < 1 || chunk > attn_bwd_chunk_seqs(at.B, at.H, at.T, at.dqk, at.dv, at.t) || !wb.dsT || !wb.kcat || !wb.dk_tmp || !wb.statT) return hipErrorInvalidValue;
+  if (chunk < 1 || chunk > attn_bwd_chunk_seqs(at.B, at.H, at.T, at.dqk, at.dv, at.t) || !wb.dsT || !wb.kcat || !wb.statT) return hipErrorInvalidValue;
   // delta = rowsum(dO . O) of every token
   prof_begin(KC_ELEM, s);
   hipError_t e = attn_delta(wb, s);

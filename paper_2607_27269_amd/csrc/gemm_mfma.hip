@@ -67,6 +67,11 @@ struct GemmDev {
   // j-th time on A + j sAk and B + j sBk (a sum over stacked operands)
   int causal, rev, nbatch, zdiv, bdiv, kgroups;
   int64_t sA, sB1, sB2, sC1, sC2, sAk, sBk;
+  // split output of the persistent causal k-major product (dK), when split_n > 0: columns
+  // n < split_n in bf16 at c_lo + z1 sC1_lo + z2 sC2_lo + m ldc_lo + n, the rest (fp32) at C
+  // with the strides above, column n - split_n
+  int split_n;
+  bf16_t* c_lo; int64_t ldc_lo, sC1_lo, sC2_lo;
 };
 
 // row stride (elements) of an m-major [k][ROWS] tile, read only through the transposing
@@ -655,11 +660,11 @@ __device__ __forceinline__ void gemm_persist(const GemmDev& g) {
   LB::swizzle(db);
 
   // nkg: slices of one operand group (the causal products walk kgroups stacked operands)
-  struct Item { int m0, n0, split, kbeg, kend, nk, nkg, nfull; int64_t aoff, boff, coff; };
+  struct Item { int m0, n0, split, kbeg, kend, nk, nkg, nfull; int64_t aoff, boff, coff, coff_lo; };
   auto item = [&](int it) {
     Item t;
     int tm, tn;
-    t.aoff = t.boff = t.coff = 0;
+    t.aoff = t.boff = t.coff = t.coff_lo = 0;
     if constexpr (CAUSAL) {
       // the one-tile launch's order: row tiles by K range, longest first; inside one, batch
       // entries that share their B panel on one XCD
@@ -676,6 +681,7 @@ __device__ __forceinline__ void gemm_persist(const GemmDev& g) {
       t.aoff = z * g.sA;
       t.boff = z1 * g.sB1 + (z2 / g.bdiv) * g.sB2;
       t.coff = z1 * g.sC1 + z2 * g.sC2;
+      if constexpr (AK) t.coff_lo = z1 * g.sC1_lo + z2 * g.sC2_lo;
       t.split = 0;
     } else {
       const int x = it % ntiles;
@@ -849,6 +855,18 @@ __device__ __forceinline__ void gemm_persist(const GemmDev& g) {
               for (int q = 0; q < 4 && n + q < g.N; ++q) p[q] = v[q];
             }
             continue;
+          }
+          if constexpr (CAUSAL && AK) {
+            if (g.split_n > 0) {  // uniform; whole 4-column groups (split_n % 4 == 0)
+              if (n < g.split_n) {
+                const f32x4 o = v * g.alpha;
+                *(u32x2*)(g.c_lo + cur.coff_lo + (int64_t)m * g.ldc_lo + n) =
+                    u32x2{pack2bf(o[0], o[1]), pack2bf(o[2], o[3])};
+              } else {
+                *(f32x4*)((float*)g.C + cur.coff + (int64_t)m * g.ldc + (n - g.split_n)) = v * g.alpha;
+              }
+              continue;
+            }
           }
           TC* p = C + cur.coff + (int64_t)m * g.ldc + n;
           if (vec && n + 4 <= g.N) {
@@ -1333,6 +1351,7 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   d.lscale = nullptr; d.lmask = nullptr; d.lpart = nullptr; d.lref = nullptr; d.ldref = 0;
   d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
   d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
+  d.split_n = 0; d.c_lo = nullptr; d.ldc_lo = d.sC1_lo = d.sC2_lo = 0;
   Plan p = plan_of(g, true);
   if (p.splits > 1 && (scratch == nullptr || scratch_elems < (size_t)p.splits * g.M * g.N))
     p = plan_of(g, false);
@@ -1395,6 +1414,7 @@ hipError_t gemm_mfma_masked_scale(const Gemm& g, const float* scale, const uint8
   d.lscale = scale; d.lmask = mask; d.lpart = nullptr; d.lref = nullptr; d.ldref = 0;
   d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
   d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
+  d.split_n = 0; d.c_lo = nullptr; d.ldc_lo = d.sC1_lo = d.sC2_lo = 0;
   const Plan p = plan_of(g, false);
   d.kchunk = p.kchunk;
   d.part = nullptr;
@@ -1421,6 +1441,7 @@ hipError_t gemm_mfma_masked_sse(const Gemm& g, const float* scale, const uint8_t
   d.lref = (const bf16_t*)ref; d.ldref = ldref;
   d.causal = 0; d.rev = 0; d.nbatch = 1; d.zdiv = 1; d.bdiv = 1; d.kgroups = 1;
   d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
+  d.split_n = 0; d.c_lo = nullptr; d.ldc_lo = d.sC1_lo = d.sC2_lo = 0;
   const Plan p = plan_of(g, false);
   d.kchunk = p.kchunk;
   d.part = nullptr;
@@ -1485,7 +1506,12 @@ hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s) {
                   (g.a_kmajor || g.M % 8 == 0) &&
                   g.N % 32 == 0 && g.lda % 8 == 0 && g.ldb % 8 == 0 && bt.mstore <= g.M &&
                   bt.kgroups >= 1 && (g.a_kmajor ? (bt.rev && g.c_t == DT_F32)
-                                                 : (!bt.rev && g.c_t == DT_BF16));
+                                                 : (!bt.rev && g.c_t == DT_BF16)) &&
+                  (bt.split_n == 0 || (g.a_kmajor && bt.split_n % 4 == 0 && bt.split_n <= g.N &&
+                                       bt.c_lo && bt.ldc_lo % 4 == 0 && bt.sC1_lo % 4 == 0 &&
+                                       bt.sC2_lo % 4 == 0 && (uintptr_t)bt.c_lo % 8 == 0 &&
+                                       g.ldc % 4 == 0 && bt.sC1 % 4 == 0 && bt.sC2 % 4 == 0 &&
+                                       (uintptr_t)g.C % 16 == 0));
   if (!ok) return hipErrorInvalidValue;
   GemmDev d;
   d.M = g.M; d.N = g.N; d.ktotal = g.K; d.nsplit = 1;
@@ -1500,6 +1526,8 @@ hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s) {
   d.kgroups = bt.kgroups;
   d.sA = bt.sA; d.sB1 = bt.sB1; d.sB2 = bt.sB2; d.sC1 = bt.sC1; d.sC2 = bt.sC2;
   d.sAk = bt.sAk; d.sBk = bt.sBk;
+  d.split_n = bt.split_n; d.c_lo = (bf16_t*)bt.c_lo;
+  d.ldc_lo = bt.ldc_lo; d.sC1_lo = bt.sC1_lo; d.sC2_lo = bt.sC2_lo;
   return g.a_kmajor ? dispatch_causal<true, float>(d, bt.nbatch, s)
                     : dispatch_causal<false, bf16_t>(d, bt.nbatch, s);
 }

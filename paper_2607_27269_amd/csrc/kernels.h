@@ -101,11 +101,10 @@ struct AttnBwd {
   // ds_ld in 32 x 32 tiles (ds_ld = T rounded up to 64) for B' = attn_bwd_chunk_seqs
   // sequences at a time;
   // dQ = scale dS K is a batched causal GEMM against the keys gathered as kcat
-  // [B' T][n_ka_groups][dqk], and dK = scale dS^T Q a GEMM into dk_tmp before the split into
-  // dKa and dkb_part.
+  // [B' T][n_ka_groups][dqk], and dK = scale dS^T Q a GEMM whose epilogue writes dKa (bf16)
+  // and dkb_part (fp32) directly.
   void* dsT;                 // attn_ds_bytes(B', f.H, f.T) bytes
   void* kcat;                // B' T * n_ka_groups * dqk bf16
-  float* dk_tmp;             // B' T * n_ka_groups * dqk fp32
   float* statT;              // attn_stats_bytes(B', f.H, f.T)
   int chunk_seqs;            // B' (>= 1, at most attn_bwd_chunk_seqs)
   // optional (bf16, dv % 8 == 0): with loss_ref [N, H*dv] (row stride H*dv) set, the delta

@@ -34,6 +34,11 @@ hipError_t gemm_mfma_masked_scale(const Gemm& g, const float* scale, const uint8
 struct GemmBatch {
   int nbatch, zdiv, bdiv, mstore, rev, kgroups;
   int64_t sA, sB1, sB2, sC1, sC2, sAk, sBk;
+  // k-major A only: columns n < split_n go to c_lo in bf16 (row stride ldc_lo, batch
+  // strides sC1_lo, sC2_lo), the others to C in fp32 at column n - split_n (0: plain C)
+  int split_n = 0;
+  void* c_lo = nullptr;
+  int64_t ldc_lo = 0, sC1_lo = 0, sC2_lo = 0;
 };
 hipError_t gemm_mfma_causal(const Gemm& g, const GemmBatch& bt, hipStream_t s);
 bool attn_mfma_supported(int dqk, int dv);
