@@ -254,6 +254,11 @@ static std::vector<Gemm> bwd_gemm_shapes(const Dims& d) {
   const int N = (int)d.N;
   v.push_back(mk((int)(d.Gkv * d.dn), (int)d.rkv, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
   v.push_back(mk((int)(d.Gkv * d.dv), (int)d.rkv, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
+  // dW_UK and dW_UV as one product (rows of both), summed into the two outputs
+  v.push_back(mk((int)(d.Gkv * (d.dn + d.dv)), (int)d.rkv, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
+  v.back().C2 = reinterpret_cast<void*>(uintptr_t{256});  // any non-null pointer: the
+                                                           // two-output form (always partials)
+  v.back().m2 = (int)(d.Gkv * d.dn);
   v.push_back(mk((int)d.kv_out, (int)d.D, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
   v.push_back(mk((int)(d.H * d.dqk), (int)(d.rq ? d.rq : d.D), N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
   if (d.rq) v.push_back(mk((int)d.rq, (int)d.D, N, 0, 0, false, 0, 0, false, 0, 0, d.t, DT_F32));
@@ -507,11 +512,22 @@ static int bwd_impl(const mla_recon_cfg* cfg, const Layout& L, const void* h,
     }
   }
   if (need_kv) {
-    // Eq. 5 backward: dW_UK = dk^nope^T c^KV, dW_UV = dv^T c^KV
-    if (gr->dWuk && dn > 0)
-      HIP_TRY(gemm(mk(Gkv * dn, rkv, N, dkv, ld_dkv, false, ckv, kv_out, false, gr->dWuk, rkv, t, DT_F32), split, se, s));
-    if (gr->dWuv)
-      HIP_TRY(gemm(mk(Gkv * dv, rkv, N, dkv + (size_t)Gkv * dn * ts, ld_dkv, false, ckv, kv_out, false, gr->dWuv, rkv, t, DT_F32), split, se, s));
+    // Eq. 5 backward: dW_UK = dk^nope^T c^KV, dW_UV = dv^T c^KV.  In bf16 both are one
+    // product over the adjacent [dk^nope | dv] columns of dkv, its split-K sum written to the
+    // two outputs (one launch pair instead of two for these short, wide-K products)
+    Gemm both = mk(Gkv * (dn + dv), rkv, N, dkv, ld_dkv, false, ckv, kv_out, false, gr->dWuk, rkv, t, DT_F32);
+    both.C2 = gr->dWuv;
+    both.m2 = Gkv * dn;
+    if (t == DT_BF16 && gr->dWuk && gr->dWuv && dn > 0 && rkv % 4 == 0 &&
+        (uintptr_t)gr->dWuk % 16 == 0 && (uintptr_t)gr->dWuv % 16 == 0 &&
+        gemm_scratch_elems(both) <= se) {
+      HIP_TRY(gemm(both, split, se, s));
+    } else {
+      if (gr->dWuk && dn > 0)
+        HIP_TRY(gemm(mk(Gkv * dn, rkv, N, dkv, ld_dkv, false, ckv, kv_out, false, gr->dWuk, rkv, t, DT_F32), split, se, s));
+      if (gr->dWuv)
+        HIP_TRY(gemm(mk(Gkv * dv, rkv, N, dkv + (size_t)Gkv * dn * ts, ld_dkv, false, ckv, kv_out, false, gr->dWuv, rkv, t, DT_F32), split, se, s));
+    }
     if (gr->dWdkv_kr) {
       // dc^KV = dk^nope W_UK + dv W_UV; dk^PE = R^T sum of the head partials
       if (dn > 0)

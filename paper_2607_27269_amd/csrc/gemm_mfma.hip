@@ -1180,16 +1180,18 @@ void gemm_nt4_persist_kernel(GemmDev g) {
   }
 }
 
-// C = alpha * sum_s part[s] + beta * C, summed in split order
+// C = alpha * sum_s part[s] + beta * C, summed in split order (split s of the M x N block at
+// part + s * sstride)
 template <typename TC>
-__global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits, int M, int N,
-                                     TC* __restrict__ C, int64_t ldc, float alpha, float beta) {
+__global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits, int64_t sstride,
+                                     int M, int N, TC* __restrict__ C, int64_t ldc, float alpha,
+                                     float beta) {
   int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int64_t total = (int64_t)M * N;
   if (idx >= total) return;
   int m = (int)(idx / N), n = (int)(idx % N);
   float s = 0.f;
-  for (int z = 0; z < splits; ++z) s += part[(int64_t)z * total + idx];
+  for (int z = 0; z < splits; ++z) s += part[(int64_t)z * sstride + idx];
   TC* c = C + (int64_t)m * ldc + n;
   float v = alpha * s;
   if (beta != 0.f) v += beta * ld(c);
@@ -1198,14 +1200,15 @@ __global__ void splitk_reduce_kernel(const float* __restrict__ part, int splits,
 
 // the same, four consecutive outputs per thread (N and ldc multiples of 4)
 template <typename TC>
-__global__ void splitk_reduce4_kernel(const float* __restrict__ part, int splits, int M, int N,
-                                      TC* __restrict__ C, int64_t ldc, float alpha, float beta) {
+__global__ void splitk_reduce4_kernel(const float* __restrict__ part, int splits, int64_t sstride,
+                                      int M, int N, TC* __restrict__ C, int64_t ldc, float alpha,
+                                      float beta) {
   const int64_t idx = 4 * ((int64_t)blockIdx.x * blockDim.x + threadIdx.x);
   const int64_t total = (int64_t)M * N;
   if (idx >= total) return;
   const int m = (int)(idx / N), n = (int)(idx % N);
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-  for (int z = 0; z < splits; ++z) acc += *(const f32x4*)(part + (int64_t)z * total + idx);
+  for (int z = 0; z < splits; ++z) acc += *(const f32x4*)(part + (int64_t)z * sstride + idx);
   store4<TC>(C + (int64_t)m * ldc + n, acc, alpha, beta);
 }
 
@@ -1337,7 +1340,7 @@ const char* launch(const GemmDev& d, const Plan& p, hipStream_t s) {
 
 size_t gemm_mfma_scratch_elems(const Gemm& g) {
   Plan p = plan_of(g, true);
-  return p.splits > 1 ? (size_t)p.splits * g.M * g.N : 0;
+  return p.splits > 1 || g.C2 ? (size_t)p.splits * g.M * g.N : 0;
 }
 
 hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStream_t s, int kc,
@@ -1353,10 +1356,17 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
   d.sA = d.sB1 = d.sB2 = d.sC1 = d.sC2 = d.sAk = d.sBk = 0;
   d.split_n = 0; d.c_lo = nullptr; d.ldc_lo = d.sC1_lo = d.sC2_lo = 0;
   Plan p = plan_of(g, true);
-  if (p.splits > 1 && (scratch == nullptr || scratch_elems < (size_t)p.splits * g.M * g.N))
+  // two outputs: always through the partials (also unsplit), summed into C and C2
+  const bool two = g.C2 != nullptr;
+  if (two && (g.beta != 0.f || g.m2 <= 0 || g.m2 >= g.M || g.N % 4 || g.ldc % 4 ||
+              (uintptr_t)g.C % 16 || (uintptr_t)g.C2 % 16 || g.c_t != DT_F32))
+    return hipErrorInvalidValue;
+  if ((p.splits > 1 || two) && (scratch == nullptr || scratch_elems < (size_t)p.splits * g.M * g.N)) {
+    if (two) return hipErrorInvalidValue;
     p = plan_of(g, false);
+  }
   d.kchunk = p.kchunk;
-  d.part = p.splits > 1 ? scratch : nullptr;
+  d.part = p.splits > 1 || two ? scratch : nullptr;
   const bool f32 = g.c_t == DT_F32;
   const char* kname = nullptr;
   prof_begin(kc, s);
@@ -1369,29 +1379,38 @@ hipError_t gemm_mfma(const Gemm& g, float* scratch, size_t scratch_elems, hipStr
 #undef L_
   prof_end(kc, s, flops, bytes, kname);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || p.splits == 1) return e;
+  if (e != hipSuccess || (p.splits == 1 && !two)) return e;
   // the split-K partials summed in a fixed order (an elementwise launch of its own)
   int64_t total = (int64_t)g.M * g.N;
   unsigned grid = (unsigned)((total + 255) / 256);
   const double rbytes = (double)total * (4.0 * p.splits + (f32 ? 4.0 : 2.0) * (g.beta != 0.f ? 2.0 : 1.0));
   prof_begin(KC_ELEM, s);
+  if (two) {  // rows [0, m2) into C, [m2, M) into C2 (f32, 4-aligned: checked above)
+    const int64_t t1 = (int64_t)g.m2 * g.N, t2 = total - t1;
+    splitk_reduce4_kernel<float><<<(unsigned)((t1 / 4 + 255) / 256), 256, 0, s>>>(
+        scratch, p.splits, total, g.m2, g.N, (float*)g.C, g.ldc, g.alpha, 0.f);
+    splitk_reduce4_kernel<float><<<(unsigned)((t2 / 4 + 255) / 256), 256, 0, s>>>(
+        scratch + t1, p.splits, total, g.M - g.m2, g.N, (float*)g.C2, g.ldc, g.alpha, 0.f);
+    prof_end(KC_ELEM, s, 0.0, rbytes, KLABEL("splitk_reduce4_kernel"));
+    return hipGetLastError();
+  }
   if (g.N % 4 == 0 && g.ldc % 4 == 0 && (uintptr_t)g.C % (f32 ? 16 : 8) == 0) {
     const unsigned grid4 = (unsigned)((total / 4 + 255) / 256);
     if (f32)
-      splitk_reduce4_kernel<float><<<grid4, 256, 0, s>>>(scratch, p.splits, g.M, g.N,
+      splitk_reduce4_kernel<float><<<grid4, 256, 0, s>>>(scratch, p.splits, total, g.M, g.N,
                                                          (float*)g.C, g.ldc, g.alpha, g.beta);
     else
-      splitk_reduce4_kernel<bf16_t><<<grid4, 256, 0, s>>>(scratch, p.splits, g.M, g.N,
+      splitk_reduce4_kernel<bf16_t><<<grid4, 256, 0, s>>>(scratch, p.splits, total, g.M, g.N,
                                                           (bf16_t*)g.C, g.ldc, g.alpha, g.beta);
     prof_end(KC_ELEM, s, 0.0, rbytes, KLABEL("splitk_reduce4_kernel"));
     return hipGetLastError();
   }
   if (f32)
-    splitk_reduce_kernel<float><<<grid, 256, 0, s>>>(scratch, p.splits, g.M, g.N, (float*)g.C,
-                                                     g.ldc, g.alpha, g.beta);
+    splitk_reduce_kernel<float><<<grid, 256, 0, s>>>(scratch, p.splits, total, g.M, g.N,
+                                                     (float*)g.C, g.ldc, g.alpha, g.beta);
   else
-    splitk_reduce_kernel<bf16_t><<<grid, 256, 0, s>>>(scratch, p.splits, g.M, g.N, (bf16_t*)g.C,
-                                                      g.ldc, g.alpha, g.beta);
+    splitk_reduce_kernel<bf16_t><<<grid, 256, 0, s>>>(scratch, p.splits, total, g.M, g.N,
+                                                      (bf16_t*)g.C, g.ldc, g.alpha, g.beta);
   prof_end(KC_ELEM, s, 0.0, rbytes, KLABEL("splitk_reduce_kernel"));
   return hipGetLastError();
 }

@@ -51,6 +51,10 @@ struct Gemm {
   void* C; int64_t ldc;
   DType in_t, c_t;
   float alpha, beta;
+  // optional second output: rows m >= m2 are stored at C2 + (m - m2) * ldc instead (bf16
+  // operands, beta = 0; the product then always goes through the split-K partials)
+  void* C2 = nullptr;
+  int m2 = 0;
 };
 // Scratch (fp32 elements) a GEMM of this shape needs for split-K partials.
 size_t gemm_scratch_elems(const Gemm& g);
