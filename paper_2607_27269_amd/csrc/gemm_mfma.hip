@@ -27,6 +27,7 @@
 // kernel sums in a fixed order (deterministic).  NT products of whole tiles run on a
 // four-wavefront kernel whose k steps are scheduled by hand (below, gemm_nt4_persist_kernel).
 #include <atomic>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -542,6 +543,9 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   const bool lmode = g.lpart != nullptr;  // uniform
   const float lsc = lmode ? *g.lscale : 0.f;
   float sse = 0.f;
+  // two copies, as in the persistent epilogue: with beta = 0 no C is read
+  auto epilogue = [&](auto with_beta) {
+  constexpr bool WB = decltype(with_beta)::value;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -588,16 +592,20 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
       }
       TC* p = C + (int64_t)m * g.ldc + n;
       if (vec && n + 4 <= g.N) {
-        store4<TC>(p, v, g.alpha, g.beta);
+        store4<TC>(p, v, g.alpha, WB ? g.beta : 0.f);
       } else {
         for (int q = 0; q < 4 && n + q < g.N; ++q) {
           float x = g.alpha * v[q];
-          if (g.beta != 0.f) x += g.beta * ld(p + q);
+          if (WB && g.beta != 0.f) x += g.beta * ld(p + q);
           store_out<TC>(p + q, x);
         }
       }
     }
   }
+  };
+  // (the dS^T products never accumulate into C: beta = 0 is checked at their launch)
+  if constexpr (ATILE) epilogue(std::false_type{});
+  else if (g.beta != 0.f) epilogue(std::true_type{}); else epilogue(std::false_type{});
   if (lmode) {
     // the tile's sum in a fixed order: lanes (fixed tree), then wavefronts in order
     // (the last bytes of the operand LDS, past every wavefront's strip)
@@ -829,6 +837,11 @@ __device__ __forceinline__ void gemm_persist(const GemmDev& g) {
     int el = lane;
     asm volatile("" : "+v"(el));
     float* strip = (float*)(lds + es * STAGE) + wave * 16 * SLD;
+    // two copies: with beta = 0 the epilogue reads no C, so the compiler has no loads to
+    // wait for before each store (a wait that would also cover the next tile's copy and
+    // every earlier store)
+    auto epilogue = [&](auto with_beta) {
+    constexpr bool WB = decltype(with_beta)::value;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -870,17 +883,21 @@ __device__ __forceinline__ void gemm_persist(const GemmDev& g) {
           }
           TC* p = C + cur.coff + (int64_t)m * g.ldc + n;
           if (vec && n + 4 <= g.N) {
-            store4<TC>(p, v, g.alpha, g.beta);
+            store4<TC>(p, v, g.alpha, WB ? g.beta : 0.f);
           } else {
             for (int q = 0; q < 4 && n + q < g.N; ++q) {
               float x = g.alpha * v[q];
-              if (g.beta != 0.f) x += g.beta * ld(p + q);
+              if (WB && g.beta != 0.f) x += g.beta * ld(p + q);
               store_out<TC>(p + q, x);
             }
           }
         }
       }
     }
+    };
+    // (the causal products never accumulate into C: beta = 0 is checked at their launch)
+    if constexpr (CAUSAL) epilogue(std::false_type{});
+    else if (g.beta != 0.f) epilogue(std::true_type{}); else epilogue(std::false_type{});
     if (!has_next) break;
     rb = (rb + cur.nk) & 1;
     issued = pre;
@@ -1117,7 +1134,16 @@ void gemm_nt4_persist_kernel(GemmDev g) {
   }
   // every read of the compiler's own has landed: its counter bookkeeping starts empty
   asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  const float lsc = g.lscale ? *g.lscale : 0.f;  // row-masked scale of the result
+  // row-masked scale of the result, through a scalar load: a vector load would leave the
+  // compiler counting it as outstanding in the tile loop, where its waits would also wait
+  // for the copies in flight
+  float lsc = 0.f;
+  if (g.lscale) {  // uniform
+    const uint64_t pl = uniform_ptr(g.lscale);
+    uint32_t u;
+    asm volatile("s_load_dword %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(u) : "s"(pl) : "memory");
+    lsc = __uint_as_float(u);
+  }
   float* strip = (float*)(lds + 2 * STAGE) + wave * 8 * SLD;
   for (;;) {
 #pragma unroll
@@ -1143,10 +1169,23 @@ void gemm_nt4_persist_kernel(GemmDev g) {
     }
     // epilogue: rows 8 gq .. 8 gq + 7 of each 32-row block, staged in this wavefront's
     // region (a lane holds column l of rows 4 h .. 4 h + 3 of the group) and written back
-    // 4 columns per lane
+    // 4 columns per lane.  Two copies: with beta = 0 (every product of the step) the
+    // epilogue reads no C, so the compiler has no loads to wait for before each store (it
+    // would otherwise wait for every memory operation in flight, the next tile's copies
+    // included)
     TC* C = (TC*)g.C;
+    auto epilogue = [&](auto with_beta) {
+    constexpr bool WB = decltype(with_beta)::value;
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
+      // the row mask of this 32-row block through one scalar load (the launcher checks its
+      // 4-byte alignment): a vector load here would wait, in order, for the next tile's
+      // copies already in flight
+      u32x8 mk = {1u, 1u, 1u, 1u, 1u, 1u, 1u, 1u};
+      if (g.lscale && g.lmask) {  // uniform
+        const uint64_t pa = uniform_ptr(g.lmask + m0 + wrow0 + i * 32);
+        asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(mk) : "s"(pa) : "memory");
+      }
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
 #pragma unroll
@@ -1159,11 +1198,16 @@ void gemm_nt4_persist_kernel(GemmDev g) {
           const int r = c / (WTN / 4), col = (c % (WTN / 4)) * 4;
           const int m = m0 + wrow0 + i * 32 + 8 * gq + r, n = n0 + wcol0 + col;
           f32x4 v = *(const f32x4*)(strip + r * SLD + col);
-          if (g.lscale) v = (g.lmask && !g.lmask[m]) ? f32x4{0.f, 0.f, 0.f, 0.f} : v * lsc;
-          store4<TC>(C + (int64_t)m * g.ldc + n, v, g.alpha, g.beta);
+          if (g.lscale) {  // row r of the block's 8-row group gq: byte 8 gq + r of mk
+            const uint32_t dw = r >= 4 ? mk[2 * gq + 1] : mk[2 * gq];
+            v = ((dw >> (8 * (r & 3))) & 0xffu) == 0u ? f32x4{0.f, 0.f, 0.f, 0.f} : v * lsc;
+          }
+          store4<TC>(C + (int64_t)m * g.ldc + n, v, g.alpha, WB ? g.beta : 0.f);
         }
       }
     }
+    };
+    if (g.beta != 0.f) epilogue(std::true_type{}); else epilogue(std::false_type{});
     if (!has_next) break;
     w = wnext;
     m0 = nm0;
@@ -1437,7 +1481,8 @@ hipError_t gemm_mfma_masked_scale(const Gemm& g, const float* scale, const uint8
   const Plan p = plan_of(g, false);
   d.kchunk = p.kchunk;
   d.part = nullptr;
-  if (nt4_bn(d, p)) {
+  // (the four-wavefront kernel reads the row mask with 32-byte scalar loads: 4-byte aligned)
+  if (nt4_bn(d, p) && (uintptr_t)mask % 4 == 0) {
     *kernel = g.c_t == DT_F32 ? launch<true, true, float>(d, p, s) : launch<true, true, bf16_t>(d, p, s);
     return hipGetLastError();
   }
