@@ -225,6 +225,15 @@ __device__ __forceinline__ void fwd_tile(const AttnDev& a, int pid, bf16_t* smem
   const float inv = 1.f / l;
   const int64_t ooff = ((int64_t)b * a.T + my_q) * a.o_tok + (int64_t)i * DV + 4 * half;
   bf16_t* op = a.O + ooff;
+  // the reference rows first, all loads before any store: interleaved, each load would
+  // wait (one in-order memory counter) for every store issued before it
+  u32x2 rf[NC][4];
+  if (a.Odiff) {  // uniform
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) rf[c][g] = *(const u32x2*)(a.Oref + ooff + 32 * c + 8 * g);
+  }
 #pragma unroll
   for (int c = 0; c < NC; ++c)
 #pragma unroll
@@ -233,7 +242,7 @@ __device__ __forceinline__ void fwd_tile(const AttnDev& a, int pid, bf16_t* smem
                  pack2bf(acc_o[c][4 * g + 2] * inv, acc_o[c][4 * g + 3] * inv)};
       *(u32x2*)(op + 32 * c + 8 * g) = w;
       if (a.Odiff) {  // uniform
-        const u32x2 r = *(const u32x2*)(a.Oref + ooff + 32 * c + 8 * g);
+        const u32x2 r = rf[c][g];
         auto lo = [](uint32_t x) { return __uint_as_float(x << 16); };
         auto hi = [](uint32_t x) { return __uint_as_float(x & 0xffff0000u); };
         *(u32x2*)(a.Odiff + ooff + 32 * c + 8 * g) =
