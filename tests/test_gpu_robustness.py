@@ -46,6 +46,35 @@ def test_step_bitwise_reproducible(idx, B, T, lengths):
         assert np.array_equal(runs[0][n], runs[1][n]), f"four calls: {n} differs between runs"
 
 
+def test_unaligned_mask_matches_aligned():
+    """The mask has no alignment requirement: at a 1-byte offset the masked dO product
+    leaves the four-wavefront kernel (which reads the mask with 32-byte scalar loads) for
+    the 8-wavefront one; both give the same loss and gradients up to accumulation order."""
+    import torch
+    from paper_2607_27269_amd.step import DeviceStep
+    print("[robust] unaligned mask cfg3 B=1 T=512", flush=True)
+    cfg, wl = _case(3, 1, 512, [401])
+    dev = DeviceStep(wl)
+    dev.fused_step(with_dA=False)
+    ref = dev.results()
+    n = dev.mask.numel()
+    buf = torch.zeros(n + 16, dtype=torch.uint8, device=dev.mask.device)
+    buf[1:1 + n].copy_(dev.mask)
+    aligned = dev.mask
+    dev.mask = buf[1:1 + n]
+    assert dev.mask.data_ptr() % 4 != 0
+    try:
+        dev.fused_step(with_dA=False)
+        out = dev.results()
+    finally:
+        dev.mask = aligned
+    assert abs(out["loss"] - ref["loss"]) <= 1e-3 * abs(ref["loss"]), (out["loss"], ref["loss"])
+    for g in GRADS:
+        if g in ref:
+            err = np.linalg.norm(out[g] - ref[g]) / np.linalg.norm(ref[g])
+            assert err <= 1e-2, (g, err)
+
+
 def test_nan_in_valid_token_reaches_loss_and_gradients():
     import torch
     from paper_2607_27269_amd.step import DeviceStep
