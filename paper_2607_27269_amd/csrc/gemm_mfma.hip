@@ -545,63 +545,63 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
   float sse = 0.f;
   // two copies, as in the persistent epilogue: with beta = 0 no C is read
   auto epilogue = [&](auto with_beta) {
-  constexpr bool WB = decltype(with_beta)::value;
+    constexpr bool WB = decltype(with_beta)::value;
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+    for (int i = 0; i < TM; ++i) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j)
+      for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int e = 0; e < 16; ++e)
-        strip[((e >> 2) * 8 + (lane >> 5) * 4 + (e & 3)) * SLD + j * 32 + (lane & 31)] =
-            acc[i][j][e];
-    constexpr int CPR = WTN / 4;            // float4 chunks per strip row
+        for (int e = 0; e < 16; ++e)
+          strip[((e >> 2) * 8 + (lane >> 5) * 4 + (e & 3)) * SLD + j * 32 + (lane & 31)] =
+              acc[i][j][e];
+      constexpr int CPR = WTN / 4;            // float4 chunks per strip row
 #pragma unroll
-    for (int it = 0; it < 32 * CPR / 64; ++it) {
-      const int c = it * 64 + lane;
-      const int r = c / CPR, col = (c % CPR) * 4;
-      const int m = m0 + wrow0 + i * 32 + r, n = n0 + wcol0 + col;
-      if (m >= g.mstore || n >= g.N) continue;
-      f32x4 v = *(const f32x4*)(strip + r * SLD + col);
-      if (lmode) {
-        if (n + 4 > g.N) v = f32x4{v[0], n + 1 < g.N ? v[1] : 0.f, n + 2 < g.N ? v[2] : 0.f, 0.f};
-        if (g.lmask && !g.lmask[m]) v = f32x4{0.f, 0.f, 0.f, 0.f};
-        f32x4 r = v;
-        if (g.lref) {
-          const bf16_t* rp = g.lref + (int64_t)m * g.ldref + n;
-          if (n + 4 <= g.N && (g.ldref & 3) == 0) {
-            const u32x2 w = *(const u32x2*)rp;
-            r = f32x4{__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
-                      __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u)};
-          } else {
-            r = f32x4{bf2f(rp[0]), n + 1 < g.N ? bf2f(rp[1]) : 0.f,
-                      n + 2 < g.N ? bf2f(rp[2]) : 0.f, n + 3 < g.N ? bf2f(rp[3]) : 0.f};
+      for (int it = 0; it < 32 * CPR / 64; ++it) {
+        const int c = it * 64 + lane;
+        const int r = c / CPR, col = (c % CPR) * 4;
+        const int m = m0 + wrow0 + i * 32 + r, n = n0 + wcol0 + col;
+        if (m >= g.mstore || n >= g.N) continue;
+        f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+        if (lmode) {
+          if (n + 4 > g.N) v = f32x4{v[0], n + 1 < g.N ? v[1] : 0.f, n + 2 < g.N ? v[2] : 0.f, 0.f};
+          if (g.lmask && !g.lmask[m]) v = f32x4{0.f, 0.f, 0.f, 0.f};
+          f32x4 r = v;
+          if (g.lref) {
+            const bf16_t* rp = g.lref + (int64_t)m * g.ldref + n;
+            if (n + 4 <= g.N && (g.ldref & 3) == 0) {
+              const u32x2 w = *(const u32x2*)rp;
+              r = f32x4{__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
+                        __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u)};
+            } else {
+              r = f32x4{bf2f(rp[0]), n + 1 < g.N ? bf2f(rp[1]) : 0.f,
+                        n + 2 < g.N ? bf2f(rp[2]) : 0.f, n + 3 < g.N ? bf2f(rp[3]) : 0.f};
+            }
           }
+          sse += v[0] * r[0] + v[1] * r[1] + v[2] * r[2] + v[3] * r[3];
+          if (C == nullptr) continue;  // tile sums only
+          v *= lsc;
         }
-        sse += v[0] * r[0] + v[1] * r[1] + v[2] * r[2] + v[3] * r[3];
-        if (C == nullptr) continue;  // tile sums only
-        v *= lsc;
-      }
-      if (g.part) {
-        float* p = g.part + ((int64_t)split * g.M + m) * g.N + n;
-        if (n + 4 <= g.N && (g.N % 4) == 0) {
-          *(f32x4*)p = v;
+        if (g.part) {
+          float* p = g.part + ((int64_t)split * g.M + m) * g.N + n;
+          if (n + 4 <= g.N && (g.N % 4) == 0) {
+            *(f32x4*)p = v;
+          } else {
+            for (int q = 0; q < 4 && n + q < g.N; ++q) p[q] = v[q];
+          }
+          continue;
+        }
+        TC* p = C + (int64_t)m * g.ldc + n;
+        if (vec && n + 4 <= g.N) {
+          store4<TC>(p, v, g.alpha, WB ? g.beta : 0.f);
         } else {
-          for (int q = 0; q < 4 && n + q < g.N; ++q) p[q] = v[q];
-        }
-        continue;
-      }
-      TC* p = C + (int64_t)m * g.ldc + n;
-      if (vec && n + 4 <= g.N) {
-        store4<TC>(p, v, g.alpha, WB ? g.beta : 0.f);
-      } else {
-        for (int q = 0; q < 4 && n + q < g.N; ++q) {
-          float x = g.alpha * v[q];
-          if (WB && g.beta != 0.f) x += g.beta * ld(p + q);
-          store_out<TC>(p + q, x);
+          for (int q = 0; q < 4 && n + q < g.N; ++q) {
+            float x = g.alpha * v[q];
+            if (WB && g.beta != 0.f) x += g.beta * ld(p + q);
+            store_out<TC>(p + q, x);
+          }
         }
       }
     }
-  }
   };
   // (the dS^T products never accumulate into C: beta = 0 is checked at their launch)
   if constexpr (ATILE) epilogue(std::false_type{});
@@ -841,59 +841,59 @@ __device__ __forceinline__ void gemm_persist(const GemmDev& g) {
     // wait for before each store (a wait that would also cover the next tile's copy and
     // every earlier store)
     auto epilogue = [&](auto with_beta) {
-    constexpr bool WB = decltype(with_beta)::value;
+      constexpr bool WB = decltype(with_beta)::value;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
+      for (int i = 0; i < TM; ++i) {
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
+        for (int h = 0; h < 2; ++h) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+          for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int e = 8 * h; e < 8 * h + 8; ++e)
-            strip[(((e >> 2) & 1) * 8 + (el >> 5) * 4 + (e & 3)) * SLD + j * 32 + (el & 31)] =
-                acc[i][j][e];
-        constexpr int CPR = WTN / 4;
+            for (int e = 8 * h; e < 8 * h + 8; ++e)
+              strip[(((e >> 2) & 1) * 8 + (el >> 5) * 4 + (e & 3)) * SLD + j * 32 + (el & 31)] =
+                  acc[i][j][e];
+          constexpr int CPR = WTN / 4;
 #pragma unroll
-        for (int it = 0; it < 16 * CPR / 64; ++it) {
-          const int c = it * 64 + el;
-          const int r = c / CPR, col = (c % CPR) * 4;
-          const int m = cur.m0 + wrow0 + i * 32 + 16 * h + r, n = cur.n0 + wcol0 + col;
-          if (m >= g.mstore || n >= g.N) continue;
-          const f32x4 v = *(const f32x4*)(strip + r * SLD + col);
-          if (g.part) {
-            float* p = g.part + ((int64_t)cur.split * g.M + m) * g.N + n;
-            if (n + 4 <= g.N && (g.N % 4) == 0) {
-              *(f32x4*)p = v;
-            } else {
-              for (int q = 0; q < 4 && n + q < g.N; ++q) p[q] = v[q];
-            }
-            continue;
-          }
-          if constexpr (CAUSAL && AK) {
-            if (g.split_n > 0) {  // uniform; whole 4-column groups (split_n % 4 == 0)
-              if (n < g.split_n) {
-                const f32x4 o = v * g.alpha;
-                *(u32x2*)(g.c_lo + cur.coff_lo + (int64_t)m * g.ldc_lo + n) =
-                    u32x2{pack2bf(o[0], o[1]), pack2bf(o[2], o[3])};
+          for (int it = 0; it < 16 * CPR / 64; ++it) {
+            const int c = it * 64 + el;
+            const int r = c / CPR, col = (c % CPR) * 4;
+            const int m = cur.m0 + wrow0 + i * 32 + 16 * h + r, n = cur.n0 + wcol0 + col;
+            if (m >= g.mstore || n >= g.N) continue;
+            const f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+            if (g.part) {
+              float* p = g.part + ((int64_t)cur.split * g.M + m) * g.N + n;
+              if (n + 4 <= g.N && (g.N % 4) == 0) {
+                *(f32x4*)p = v;
               } else {
-                *(f32x4*)((float*)g.C + cur.coff + (int64_t)m * g.ldc + (n - g.split_n)) = v * g.alpha;
+                for (int q = 0; q < 4 && n + q < g.N; ++q) p[q] = v[q];
               }
               continue;
             }
-          }
-          TC* p = C + cur.coff + (int64_t)m * g.ldc + n;
-          if (vec && n + 4 <= g.N) {
-            store4<TC>(p, v, g.alpha, WB ? g.beta : 0.f);
-          } else {
-            for (int q = 0; q < 4 && n + q < g.N; ++q) {
-              float x = g.alpha * v[q];
-              if (WB && g.beta != 0.f) x += g.beta * ld(p + q);
-              store_out<TC>(p + q, x);
+            if constexpr (CAUSAL && AK) {
+              if (g.split_n > 0) {  // uniform; whole 4-column groups (split_n % 4 == 0)
+                if (n < g.split_n) {
+                  const f32x4 o = v * g.alpha;
+                  *(u32x2*)(g.c_lo + cur.coff_lo + (int64_t)m * g.ldc_lo + n) =
+                      u32x2{pack2bf(o[0], o[1]), pack2bf(o[2], o[3])};
+                } else {
+                  *(f32x4*)((float*)g.C + cur.coff + (int64_t)m * g.ldc + (n - g.split_n)) = v * g.alpha;
+                }
+                continue;
+              }
+            }
+            TC* p = C + cur.coff + (int64_t)m * g.ldc + n;
+            if (vec && n + 4 <= g.N) {
+              store4<TC>(p, v, g.alpha, WB ? g.beta : 0.f);
+            } else {
+              for (int q = 0; q < 4 && n + q < g.N; ++q) {
+                float x = g.alpha * v[q];
+                if (WB && g.beta != 0.f) x += g.beta * ld(p + q);
+                store_out<TC>(p + q, x);
+              }
             }
           }
         }
       }
-    }
     };
     // (the causal products never accumulate into C: beta = 0 is checked at their launch)
     if constexpr (CAUSAL) epilogue(std::false_type{});
@@ -1175,37 +1175,37 @@ void gemm_nt4_persist_kernel(GemmDev g) {
     // included)
     TC* C = (TC*)g.C;
     auto epilogue = [&](auto with_beta) {
-    constexpr bool WB = decltype(with_beta)::value;
+      constexpr bool WB = decltype(with_beta)::value;
 #pragma unroll
-    for (int i = 0; i < TM; ++i) {
-      // the row mask of this 32-row block through one scalar load (the launcher checks its
-      // 4-byte alignment): a vector load here would wait, in order, for the next tile's
-      // copies already in flight
-      u32x8 mk = {1u, 1u, 1u, 1u, 1u, 1u, 1u, 1u};
-      if (g.lscale && g.lmask) {  // uniform
-        const uint64_t pa = uniform_ptr(g.lmask + m0 + wrow0 + i * 32);
-        asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(mk) : "s"(pa) : "memory");
-      }
+      for (int i = 0; i < TM; ++i) {
+        // the row mask of this 32-row block through one scalar load (the launcher checks its
+        // 4-byte alignment): a vector load here would wait, in order, for the next tile's
+        // copies already in flight
+        u32x8 mk = {1u, 1u, 1u, 1u, 1u, 1u, 1u, 1u};
+        if (g.lscale && g.lmask) {  // uniform
+          const uint64_t pa = uniform_ptr(g.lmask + m0 + wrow0 + i * 32);
+          asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(mk) : "s"(pa) : "memory");
+        }
 #pragma unroll
-      for (int gq = 0; gq < 4; ++gq) {
+        for (int gq = 0; gq < 4; ++gq) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j)
+          for (int j = 0; j < TN; ++j)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) strip[(4 * h + q) * SLD + j * 32 + l] = acc[i][j][4 * gq + q];
+            for (int q = 0; q < 4; ++q) strip[(4 * h + q) * SLD + j * 32 + l] = acc[i][j][4 * gq + q];
 #pragma unroll
-        for (int it = 0; it < TN; ++it) {
-          const int c = it * 64 + lane;
-          const int r = c / (WTN / 4), col = (c % (WTN / 4)) * 4;
-          const int m = m0 + wrow0 + i * 32 + 8 * gq + r, n = n0 + wcol0 + col;
-          f32x4 v = *(const f32x4*)(strip + r * SLD + col);
-          if (g.lscale) {  // row r of the block's 8-row group gq: byte 8 gq + r of mk
-            const uint32_t dw = r >= 4 ? mk[2 * gq + 1] : mk[2 * gq];
-            v = ((dw >> (8 * (r & 3))) & 0xffu) == 0u ? f32x4{0.f, 0.f, 0.f, 0.f} : v * lsc;
+          for (int it = 0; it < TN; ++it) {
+            const int c = it * 64 + lane;
+            const int r = c / (WTN / 4), col = (c % (WTN / 4)) * 4;
+            const int m = m0 + wrow0 + i * 32 + 8 * gq + r, n = n0 + wcol0 + col;
+            f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+            if (g.lscale) {  // row r of the block's 8-row group gq: byte 8 gq + r of mk
+              const uint32_t dw = r >= 4 ? mk[2 * gq + 1] : mk[2 * gq];
+              v = ((dw >> (8 * (r & 3))) & 0xffu) == 0u ? f32x4{0.f, 0.f, 0.f, 0.f} : v * lsc;
+            }
+            store4<TC>(C + (int64_t)m * g.ldc + n, v, g.alpha, WB ? g.beta : 0.f);
           }
-          store4<TC>(C + (int64_t)m * g.ldc + n, v, g.alpha, WB ? g.beta : 0.f);
         }
       }
-    }
     };
     if (g.beta != 0.f) epilogue(std::true_type{}); else epilogue(std::false_type{});
     if (!has_next) break;
