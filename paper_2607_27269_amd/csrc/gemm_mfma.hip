@@ -555,13 +555,21 @@ __device__ __forceinline__ void gemm_tile(const GemmDev& g) {
           strip[((e >> 2) * 8 + (lane >> 5) * 4 + (e & 3)) * SLD + j * 32 + (lane & 31)] =
               acc[i][j][e];
       constexpr int CPR = WTN / 4;            // float4 chunks per strip row
+      constexpr int NIT = 32 * CPR / 64;
+      // the strip's reads first (all inside the strip), then the stores
+      f32x4 vv[NIT];
 #pragma unroll
-      for (int it = 0; it < 32 * CPR / 64; ++it) {
+      for (int it = 0; it < NIT; ++it) {
+        const int c = it * 64 + lane;
+        vv[it] = *(const f32x4*)(strip + (c / CPR) * SLD + (c % CPR) * 4);
+      }
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) {
         const int c = it * 64 + lane;
         const int r = c / CPR, col = (c % CPR) * 4;
         const int m = m0 + wrow0 + i * 32 + r, n = n0 + wcol0 + col;
         if (m >= g.mstore || n >= g.N) continue;
-        f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+        f32x4 v = vv[it];
         if (lmode) {
           if (n + 4 > g.N) v = f32x4{v[0], n + 1 < g.N ? v[1] : 0.f, n + 2 < g.N ? v[2] : 0.f, 0.f};
           if (g.lmask && !g.lmask[m]) v = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -853,13 +861,28 @@ __device__ __forceinline__ void gemm_persist(const GemmDev& g) {
               strip[(((e >> 2) & 1) * 8 + (el >> 5) * 4 + (e & 3)) * SLD + j * 32 + (el & 31)] =
                   acc[i][j][e];
           constexpr int CPR = WTN / 4;
+          constexpr int NIT = 16 * CPR / 64;
+          // the strip's reads first (all inside the strip), then the stores: the reads go
+          // out together instead of one wait per store (not for the causal products, where
+          // reading as it stores measured faster)
+          constexpr bool BATCH = !CAUSAL;
+          f32x4 vv[BATCH ? NIT : 1];
+          if constexpr (BATCH) {
 #pragma unroll
-          for (int it = 0; it < 16 * CPR / 64; ++it) {
+            for (int it = 0; it < NIT; ++it) {
+              const int c = it * 64 + el;
+              vv[it] = *(const f32x4*)(strip + (c / CPR) * SLD + (c % CPR) * 4);
+            }
+          }
+#pragma unroll
+          for (int it = 0; it < NIT; ++it) {
             const int c = it * 64 + el;
             const int r = c / CPR, col = (c % CPR) * 4;
             const int m = cur.m0 + wrow0 + i * 32 + 16 * h + r, n = cur.n0 + wcol0 + col;
             if (m >= g.mstore || n >= g.N) continue;
-            const f32x4 v = *(const f32x4*)(strip + r * SLD + col);
+            f32x4 v;
+            if constexpr (BATCH) v = vv[it];
+            else v = *(const f32x4*)(strip + r * SLD + col);
             if (g.part) {
               float* p = g.part + ((int64_t)cur.split * g.M + m) * g.N + n;
               if (n + 4 <= g.N && (g.N % 4) == 0) {
@@ -1174,15 +1197,18 @@ void gemm_nt4_persist_kernel(GemmDev g) {
     // would otherwise wait for every memory operation in flight, the next tile's copies
     // included)
     TC* C = (TC*)g.C;
-    auto epilogue = [&](auto with_beta) {
+    // (beta and the masked scale are compile-time in each copy: with no branch inside, the
+    // four strip reads of a row group are issued together, then converted and stored)
+    auto epilogue = [&](auto with_beta, auto with_scale) {
       constexpr bool WB = decltype(with_beta)::value;
+      constexpr bool LS = decltype(with_scale)::value;
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         // the row mask of this 32-row block through one scalar load (the launcher checks its
         // 4-byte alignment): a vector load here would wait, in order, for the next tile's
         // copies already in flight
         u32x8 mk = {1u, 1u, 1u, 1u, 1u, 1u, 1u, 1u};
-        if (g.lscale && g.lmask) {  // uniform
+        if (LS && g.lmask) {  // uniform
           const uint64_t pa = uniform_ptr(g.lmask + m0 + wrow0 + i * 32);
           asm volatile("s_load_dwordx8 %0, %1, 0x0\n\ts_waitcnt lgkmcnt(0)" : "=s"(mk) : "s"(pa) : "memory");
         }
@@ -1192,22 +1218,36 @@ void gemm_nt4_persist_kernel(GemmDev g) {
           for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int q = 0; q < 4; ++q) strip[(4 * h + q) * SLD + j * 32 + l] = acc[i][j][4 * gq + q];
+          f32x4 v[TN];
+#pragma unroll
+          for (int it = 0; it < TN; ++it) {
+            const int c = it * 64 + lane;
+            v[it] = *(const f32x4*)(strip + (c / (WTN / 4)) * SLD + (c % (WTN / 4)) * 4);
+          }
 #pragma unroll
           for (int it = 0; it < TN; ++it) {
             const int c = it * 64 + lane;
             const int r = c / (WTN / 4), col = (c % (WTN / 4)) * 4;
             const int m = m0 + wrow0 + i * 32 + 8 * gq + r, n = n0 + wcol0 + col;
-            f32x4 v = *(const f32x4*)(strip + r * SLD + col);
-            if (g.lscale) {  // row r of the block's 8-row group gq: byte 8 gq + r of mk
+            f32x4 o = v[it];
+            if constexpr (LS) {  // row r of the block's 8-row group gq: byte 8 gq + r of mk
               const uint32_t dw = r >= 4 ? mk[2 * gq + 1] : mk[2 * gq];
-              v = ((dw >> (8 * (r & 3))) & 0xffu) == 0u ? f32x4{0.f, 0.f, 0.f, 0.f} : v * lsc;
+              const bool keep = ((dw >> (8 * (r & 3))) & 0xffu) != 0u;
+              const f32x4 so = o * lsc;  // masked rows exactly 0 (also where o is not finite)
+              o = f32x4{keep ? so[0] : 0.f, keep ? so[1] : 0.f, keep ? so[2] : 0.f, keep ? so[3] : 0.f};
             }
-            store4<TC>(C + (int64_t)m * g.ldc + n, v, g.alpha, WB ? g.beta : 0.f);
+            store4<TC>(C + (int64_t)m * g.ldc + n, o, g.alpha, WB ? g.beta : 0.f);
           }
         }
       }
     };
-    if (g.beta != 0.f) epilogue(std::true_type{}); else epilogue(std::false_type{});
+    if (g.lscale) {  // the masked dO product (beta = 0)
+      if (g.beta != 0.f) epilogue(std::true_type{}, std::true_type{});
+      else epilogue(std::false_type{}, std::true_type{});
+    } else {
+      if (g.beta != 0.f) epilogue(std::true_type{}, std::false_type{});
+      else epilogue(std::false_type{}, std::false_type{});
+    }
     if (!has_next) break;
     w = wnext;
     m0 = nm0;
